@@ -1,0 +1,351 @@
+"""Benchmark of the RSLM IVF hot path on one MI355X.
+
+Workload (default): a text-embedding shaped collection of N = 10,000,000
+float32 vectors of dimension 768 (anisotropic Gaussian, power-law variance
+spectrum with exponent 1, shared mean offset, not normalised), nlist = 4096
+Euclidean k-means partitions (10 iterations on 256 points per centre),
+4-bit RSLM codes with global scaling and SQ8 codes of the second residual for
+rescoring; 10,000 queries from the same distribution in batches of 256,
+nprobe = 64, top-100 from the scan, rescored to top-10.
+
+A step is one pass of the whole path over one batch: query rotation,
+probing, scan + top-k, rescoring, and the encoding of 65,536 new vectors.
+``value`` is the number of scored (query, candidate) pairs per second of
+whole-step time, inputs resident in HBM.  The JSON line also carries the
+roofline of the scan kernel, per-stage times, encode throughput and the CPU
+oracle's throughput on a bounded sample of the same workload.
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "scored candidates/sec + achieved HBM GB/s, 4-bit d=768 IVF scan, 1 GPU"
+HBM_PEAK_GBPS = 8000.0
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--n", type=int, default=10_000_000)
+    ap.add_argument("--dim", type=int, default=768)
+    ap.add_argument("--nlist", type=int, default=4096)
+    ap.add_argument("--nprobe", type=int, default=64)
+    ap.add_argument("--batch", type=int, default=256)
+    ap.add_argument("--nq", type=int, default=10_000)
+    ap.add_argument("--k", type=int, default=100)
+    ap.add_argument("--k-out", type=int, default=10)
+    ap.add_argument("--bits", type=int, default=4)
+    ap.add_argument("--kmeans-iters", type=int, default=10)
+    ap.add_argument("--encode-chunk", type=int, default=65536)
+    ap.add_argument("--cpu-seconds", type=float, default=20.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calib", action="store_true",
+                    help="only run a 1 GiB device copy (counter calibration) and exit")
+    return ap.parse_args()
+
+
+def csrc_hash():
+    h = hashlib.sha256()
+    d = os.path.join(ROOT, "paper_2608_30384_amd", "csrc")
+    for f in sorted(os.listdir(d)):
+        with open(os.path.join(d, f), "rb") as fh:
+            h.update(f.encode() + fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_from_profiles(streamed_records_per_launch):
+    """HBM bytes per scan launch from committed rocprofv3 counters, if they
+    were taken on the current kernel sources; else None."""
+    p = os.path.join(ROOT, "profiles", "scan_traffic_text768.json")
+    if not os.path.exists(p):
+        return None
+    with open(p) as f:
+        t = json.load(f)
+    if t.get("csrc_sha") != csrc_hash():
+        return None
+    return t.get("hbm_bytes_per_launch")
+
+
+# ------------------------------------------------------------------ CPU baseline
+_CPU = {}
+
+
+def _cpu_query(i):
+    import oracle
+    d = _CPU
+    i = i % len(d["pid"])
+    t0 = time.perf_counter()
+    all_s, all_i = [], []
+    pairs = 0
+    for j, L in enumerate(d["pid"][i]):
+        rec = d["lists"][L]
+        s = oracle.scan_scores_lut(d["qrot"][i], d["pdot"][i, j], rec["codes"], rec["s_hat"],
+                                   rec["g_hat"], d["C"])
+        all_s.append(s)
+        all_i.append(rec["ids"])
+        pairs += len(s)
+    oracle.topk(np.concatenate(all_s), np.concatenate(all_i), d["k"])
+    return pairs, time.perf_counter() - t0
+
+
+def cpu_baseline(R, plan, index, qrot, pid, pdot, k, budget_s):
+    """The oracle's LUT-route scan + top-k on the host cores, bounded sample."""
+    import multiprocessing as mp
+
+    import oracle
+    import synth
+
+    workers = max(1, min(16, os.cpu_count() or 1))
+    nq_max = min(qrot.shape[0], 8)      # queries whose probed lists are unpacked to the host
+    pid_h = pid[:nq_max].cpu().numpy()
+    need = sorted(set(pid_h.reshape(-1).tolist()))
+    offs = index.list_offsets.cpu().numpy()
+    sizes = index.list_sizes.cpu().numpy()
+    ids_all = index.ids
+    K, g = oracle.codec_shape(plan.bits)
+    n_sub = -(-plan.dim // g)
+    lists = {}
+    for L in need:
+        o, s = int(offs[L]), int(sizes[L])
+        if s == 0:
+            lists[L] = {"codes": np.zeros((0, n_sub), np.uint8), "s_hat": np.zeros(0),
+                        "g_hat": np.zeros(0), "ids": np.zeros(0, np.int64)}
+            continue
+        tiles = index.codes[(o // 16) * plan.tile_bytes:(o // 16 + (s + 15) // 16) * plan.tile_bytes]
+        canon = R.rslm_unpack_codes(plan, tiles.contiguous(), s).cpu().numpy()
+        sc = index.scales[o:o + s].cpu().numpy().astype(np.uint32)
+        lists[L] = {"codes": oracle.unpack_canonical(canon, plan.bits, n_sub).astype(np.uint8),
+                    "s_hat": np.array([oracle.dec_ue7m9(int(v) & 0xFFFF) for v in sc]),
+                    "g_hat": np.array([oracle.dec_ue4m12(int(v) >> 16) for v in sc]),
+                    "ids": ids_all[o:o + s].cpu().numpy().astype(np.int64)}
+    _CPU.update(pid=pid_h, pdot=pdot[:nq_max].cpu().numpy().astype(np.float64),
+                qrot=qrot[:nq_max].cpu().numpy().astype(np.float64), lists=lists,
+                C=synth.codebook(plan.bits), k=k)
+    # calibrate on one query, then size the sample to ~budget_s of wall time;
+    # the tasks cycle over the unpacked queries
+    p1, t1 = _cpu_query(0)
+    nq = int(workers * max(1, budget_s // max(t1, 1e-3)))
+    os.environ.setdefault("OMP_NUM_THREADS", "1")
+    ctx = mp.get_context("fork")
+    t0 = time.perf_counter()
+    with ctx.Pool(workers) as pool:
+        res = pool.map(_cpu_query, range(nq), chunksize=1)
+    wall = time.perf_counter() - t0
+    pairs = sum(r[0] for r in res)
+    return {"value": pairs / wall, "unit": "scored candidates/s", "cores": workers,
+            "kind": "oracle",
+            "sample": (f"oracle LUT-route scan + top-{k} (float64 NumPy), {nq} query scans cycling "
+                       f"over the first {nq_max} queries of the first batch and their probed "
+                       f"{plan.dim}-d {plan.bits}-bit lists ({pairs} pairs, {wall:.1f} s wall, "
+                       f"{workers} worker processes)")}
+
+
+# ------------------------------------------------------------------ main
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build measures one GPU only; run with --gpus 1"}))
+        sys.exit(2)
+    import torch
+
+    import synth
+    import paper_2608_30384_amd as R
+    from paper_2608_30384_amd import _lib as LL
+    from paper_2608_30384_amd import ivf
+
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+    if args.copy_calib:
+        a = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        a.fill_(1.0)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calib_bytes": a.numel() * 4}))
+        return
+
+    N, D, nlist = args.n, args.dim, args.nlist
+    t_setup = time.time()
+    log(f"generating {N} x {D} vectors on device")
+    x = synth.aniso_torch(N, D, alpha=1.0, seed=100, device=dev)
+    q_all = torch.from_numpy(synth.queries_like("aniso", args.nq, D, data_seed=100,
+                                                query_seed=200)).to(dev)
+    torch.cuda.synchronize()
+    log(f"k-means: {nlist} lists, {args.kmeans_iters} iterations on {min(N, 256 * nlist)} points")
+    t0 = time.time()
+    cen = ivf.kmeans(x, nlist, iters=args.kmeans_iters, seed=0, sample=256 * nlist)
+    torch.cuda.synchronize()
+    log(f"k-means done in {time.time() - t0:.1f} s")
+    plan = R.Plan(D, args.bits, passes=-1, scale_mode="global")
+    resid = torch.empty_like(x)
+    t0 = time.time()
+    index, crot, assign = ivf.build_index(plan, x, cen, resid_rot=resid)
+    torch.cuda.synchronize()
+    log(f"assign + layout + encode of {N} vectors: {time.time() - t0:.1f} s; "
+        f"max list {index.max_list_size}, records {index.ids.numel()}")
+    codes2, lo, hi = ivf.build_sq8(resid)
+    del resid
+    torch.cuda.synchronize()
+    # a chunk of new vectors for the per-step encode (row a7)
+    xe = synth.aniso_torch(args.encode_chunk, D, alpha=1.0, seed=300, device=dev)
+    ae, _ = R.ivf_assign_probe(xe, cen, 1, R.IVF_ASSIGN_L2)
+    codes_e = torch.empty(plan.code_bytes(args.encode_chunk), dtype=torch.uint8, device=dev)
+    scales_e = torch.empty(args.encode_chunk, dtype=torch.int32, device=dev)
+    resid_e = torch.empty_like(xe)
+    log(f"setup {time.time() - t_setup:.1f} s")
+
+    batches = [q_all[i:i + args.batch].contiguous() for i in range(0, args.nq, args.batch)]
+    sizes = index.list_sizes.long()
+    rec_bytes = D * args.bits // 8 + 4
+    # per-batch work, computed outside the timed region from the probe result
+    work = []
+    for qb in batches:
+        pid, _ = R.ivf_assign_probe(qb, cen, args.nprobe, R.IVF_PROBE_IP)
+        pl = pid.long().reshape(-1)
+        pairs = int(sizes[pl].sum().item())
+        m = torch.bincount(pl, minlength=nlist)
+        groups = (m + 7) // 8
+        streamed = int((groups * sizes).sum().item())
+        work.append((pairs, streamed))
+
+    ws_scan = torch.empty(R.rslm_scan_topk_workspace(plan, index, args.batch, args.nprobe, args.k),
+                          dtype=torch.uint8, device=dev)
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+
+    def step(b, timers):
+        qb = batches[b % len(batches)]
+        e = timers
+        e[0].record()
+        qrot = R.rslm_fwht(plan, qb)
+        e[1].record()
+        pid, pdot = R.ivf_assign_probe(qb, cen, args.nprobe, R.IVF_PROBE_IP)
+        e[2].record()
+        s1, i1 = R.rslm_scan_topk(plan, index, qrot, pid, pdot, args.k, ws=ws_scan)
+        e[3].record()
+        R.rslm_rescore(codes2, lo, hi, qrot, s1, i1, args.k_out)
+        e[4].record()
+        R.rslm_encode(plan, xe, codes_e, scales_e, rec_list=ae, centroids=cen, centroids_rot=crot,
+                      resid_rot=resid_e)
+        e[5].record()
+        return qrot, pid, pdot
+
+    lib = LL.lib()
+    for w in range(args.warmup):
+        step(w, [ev() for _ in range(6)])
+    torch.cuda.synchronize()
+    all_ev, scan_ev = [], []
+    for s in range(args.steps):
+        all_ev.append([ev() for _ in range(6)])
+        scan_ev.append([ev() for _ in range(4)])
+        for e in scan_ev[-1]:
+            e.record()          # materialise the HIP events before handing them over
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        se = scan_ev[s]
+        lib.rslm_set_timer(0, se[0]._as_parameter_, se[1]._as_parameter_)
+        lib.rslm_set_timer(1, se[2]._as_parameter_, se[3]._as_parameter_)
+        step(args.warmup + s, all_ev[s])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    lib.rslm_set_timer(0, None, None)
+    lib.rslm_set_timer(1, None, None)
+
+    names = ["rotate", "probe", "scan_topk", "rescore", "encode"]
+    stage = {n: 0.0 for n in names}
+    for e in all_ev:
+        for i, n in enumerate(names):
+            stage[n] += e[i].elapsed_time(e[i + 1])
+    t_scan = sum(se[0].elapsed_time(se[1]) for se in scan_ev) / args.steps
+    t_topk = sum(se[2].elapsed_time(se[3]) for se in scan_ev) / args.steps
+    steps_b = [(args.warmup + s) % len(batches) for s in range(args.steps)]
+    pairs_total = sum(work[b][0] for b in steps_b)
+    streamed_avg = sum(work[b][1] for b in steps_b) / args.steps
+    pairs_avg = pairs_total / args.steps
+    ms_per_step = wall * 1e3 / args.steps
+    value = pairs_total / wall
+    achieved = streamed_avg * rec_bytes / (t_scan * 1e-3) / 1e9
+    traffic = traffic_from_profiles(streamed_avg)
+    enc_ms = stage["encode"] / args.steps
+    enc_bytes = args.encode_chunk * (4 * D + rec_bytes + 4 * D)
+
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "scored candidates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"text-embedding shaped IVF scan: N={N:,} x d={D} anisotropic Gaussian "
+                         f"(power-law spectrum, exponent 1, mean offset, unnormalised), "
+                         f"nlist={nlist}, {args.bits}-bit RSLM global scale + SQ8 rescore, "
+                         f"batches of {args.batch} queries, nprobe={args.nprobe}, "
+                         f"top-{args.k} -> top-{args.k_out}; each step also encodes "
+                         f"{args.encode_chunk:,} vectors"),
+            "N": N, "dim": D, "nlist": nlist, "nprobe": args.nprobe, "batch": args.batch,
+            "k": args.k, "k_out": args.k_out, "bits": args.bits, "passes": plan.passes,
+        },
+        "hbm_GBps": achieved,
+        "roofline": {
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBPS,
+            "traffic": traffic,
+            "kernel": f"k_scan<{args.bits},{min(32, max(4, -(-plan.d_pad // 32)))}>",
+            "algorithmic_bytes_per_launch": streamed_avg * rec_bytes,
+            "kernel_ms": t_scan,
+        },
+        "scan": {
+            "pairs_per_step": pairs_avg,
+            "streamed_records_per_step": streamed_avg,
+            "record_bytes": rec_bytes,
+            "candidates_per_s_scan_kernel": pairs_avg / (t_scan * 1e-3),
+            "pair_equivalent_GBps": pairs_avg * rec_bytes / (t_scan * 1e-3) / 1e9,
+            "topk_kernel_ms": t_topk,
+        },
+        "stages_ms": {n: stage[n] / args.steps for n in names},
+        "encode": {
+            "vectors": args.encode_chunk,
+            "ms": enc_ms,
+            "vectors_per_s": args.encode_chunk / (enc_ms * 1e-3),
+            "GBps": enc_bytes / (enc_ms * 1e-3) / 1e9,
+        },
+        "kernel_sources": csrc_hash(),
+    }
+    if not args.no_cpu_baseline:
+        log("CPU oracle baseline")
+        qb = batches[0]
+        qrot, pid, pdot = step(0, [ev() for _ in range(6)])
+        torch.cuda.synchronize()
+        out["cpu_baseline"] = cpu_baseline(R, plan, index, qrot, pid, pdot, args.k,
+                                           args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

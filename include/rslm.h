@@ -1,0 +1,254 @@
+/*
+ * rslm.h -- C ABI of librslm, an MI355X (gfx950) implementation of the RSLM
+ * (Rotated Scaled Lloyd-Max) IVF second-stage scan and bulk encoder.
+ *
+ * Method: "RSLM: Training-Free Vector Quantization for Approximate Nearest
+ * Neighbor Search" (arXiv 2608.30384).  Each entry point cites the section of
+ * the paper that defines the operation.
+ *
+ * Conventions shared by every call
+ *   - Array arguments are DEVICE pointers owned by the caller, row-major and
+ *     contiguous, unless a comment says "host".  The library never frees or
+ *     retains caller memory; only rslm_plan_create allocates (the plan's own
+ *     device tables, released by rslm_plan_destroy).
+ *   - Scratch memory is a caller-provided workspace ("ws", "ws_bytes") whose
+ *     size comes from the matching *_workspace function.
+ *   - "stream" is a hipStream_t passed as void* (NULL = the null stream).
+ *     Every call is asynchronous on that stream; results are ready after the
+ *     caller synchronises the stream.
+ *   - Every call returns an rslm_status.  Arguments are validated before any
+ *     launch; on a non-zero status nothing was launched and outputs are
+ *     untouched.  RSLM_ERR_HIP means a launch failed (the HIP error is
+ *     retrievable with rslm_last_hip_error).  Faults during kernel execution
+ *     surface at the caller's next synchronisation.
+ *   - Calls on distinct streams are thread-safe; a plan may be shared.
+ *   - Vector ids are int32 (collections of up to 2^31 - 1 vectors).
+ */
+#ifndef RSLM_H
+#define RSLM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum rslm_status {
+  RSLM_OK = 0,
+  RSLM_ERR_INVALID_ARG = 1,   /* null pointer, size or enum out of range */
+  RSLM_ERR_UNSUPPORTED = 2,   /* valid request this build does not implement */
+  RSLM_ERR_HIP = 3,           /* a HIP launch or runtime call failed */
+  RSLM_ERR_WORKSPACE = 4,     /* ws_bytes smaller than the *_workspace size */
+  RSLM_ERR_NO_DEVICE = 5      /* no usable gfx950 device is current */
+} rslm_status;
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char *rslm_status_string(int status);
+/* The hipError_t recorded by the last RSLM_ERR_HIP on this thread. */
+int rslm_last_hip_error(void);
+/* Library version, "major.minor.patch" (static string). */
+const char *rslm_version(void);
+
+/* ------------------------------------------------------------------------
+ * Codec plan.  Section "Rslm codec family": the block-wise cascaded FWHT
+ * ("Pre-Quantization Transformations"), the fixed Lloyd-Max codebooks
+ * ("Quantization Using Lloyd-Max Codebook", table tab:rslm_codecs), the
+ * norm-correcting scale ("Norm Correction", "Scale Encoding") and the
+ * local/global relative modes ("Relative Quantization").
+ * ------------------------------------------------------------------------ */
+typedef struct rslm_plan rslm_plan;
+
+typedef struct rslm_plan_desc {
+  int32_t dim;            /* D, 1 <= D <= 4096 */
+  int32_t bits;           /* 1, 2, 3 or 4 bits per dimension: (g, K) = (4,16),
+                             (2,16), (1,8), (1,16) */
+  int32_t passes;         /* rotation passes: 0 (none), 1, 2, or -1 for the
+                             paper's rule (1 iff bits == 4 and D <= 256) */
+  int32_t scale_mode;     /* 0 local (second scale fixed to 1.0),
+                             1 global (second scale ||x|| / ||a + r~||) */
+  const int8_t *signs;    /* host, 256 entries, each +1 or -1 (S1) */
+  const int32_t *perm;    /* host, 128 entries, a permutation of 0..127 (P) */
+  const float *codebook;  /* host, K*g floats, centroid k at [k*g, k*g+g);
+                             every value exactly representable in float16;
+                             for g == 1 strictly ascending */
+} rslm_plan_desc;
+
+typedef struct rslm_plan_info {
+  int32_t dim, bits, passes, scale_mode;
+  int32_t K, g;            /* centroids and sub-vector size */
+  int32_t block;           /* FWHT block size B */
+  int32_t n_full_blocks;   /* floor(D / B); an overlap block follows iff D % B */
+  int32_t d_pad;           /* D rounded up to a multiple of 32 (scan layout) */
+  int32_t canon_bytes;     /* canonical code bytes per record */
+  int32_t tile_records;    /* records per scan tile (16) */
+  int32_t tile_bytes;      /* bytes of one tile of packed codes */
+  double emax;             /* E_max(D) = E[max_i |Z_i|], Z_i ~ N(0,1) i.i.d. */
+} rslm_plan_info;
+
+/* Creates a plan on the current HIP device; copies the host tables.
+ * Status INVALID_ARG for out-of-range fields or tables, NO_DEVICE when the
+ * current device is not gfx950. */
+int rslm_plan_create(const rslm_plan_desc *desc, rslm_plan **out);
+int rslm_plan_destroy(rslm_plan *plan);
+int rslm_plan_get_info(const rslm_plan *plan, rslm_plan_info *info);
+
+/* ------------------------------------------------------------------------
+ * rslm_fwht -- the cascaded rotation R (Sections "Fast Walsh Hadamard
+ * Transform", "Sign Flips and Dimension Permutation", "Cascaded Rotation
+ * Pipeline"); used for Precompute-Query (Section "Performance Impact and
+ * Memory Savings": rotate a query once, score in the rotated space).
+ *   x, y   : n x D float32 (y may equal x).
+ *   inverse: 0 -> y = R x;  1 -> y = R^T x (blocks in reverse order).
+ * ------------------------------------------------------------------------ */
+int rslm_fwht(const rslm_plan *plan, const float *x, float *y, int64_t n,
+              int inverse, void *stream);
+
+/* ------------------------------------------------------------------------
+ * rslm_encode -- bulk RSLM encoding of records (Sections "Quantization Using
+ * Lloyd-Max Codebook", "Norm Correction", "Scale Encoding", "Relative
+ * Quantization"; the IVF residual of Section "End-to-End Comparison": the
+ * residual is taken against the record's partition centre).
+ * For record r (0 <= r < n_records):
+ *   row  = src_row ? src_row[r] : r        (row of x; < 0 marks a padding
+ *                                            record, which is skipped)
+ *   c    = centroids ? centroids[rec_list[r]] : 0
+ *   z    = R (x[row] - c);  u = z * E_max(D) / max|z|
+ *   code = nearest centroid per g-sub-vector (lower index on ties)
+ *   s^   = UE7M9(||x - c|| / ||C[code]||)
+ *   g^   = UE4M12(||x|| / ||c + R^T s^ C[code]||) (global) or 1.0 (local)
+ * Outputs:
+ *   codes     : scan tile layout, ceil(n_records/16) * tile_bytes bytes
+ *               (record r is in tile r/16; see rslm_pack_codes)
+ *   scales    : n_records uint32, lo16 = s^ (UE7M9), hi16 = g^ (UE4M12)
+ *   resid_rot : n_rows x D float32 or NULL: row `row` of record r receives
+ *               the rotated second residual R x - g^ (R c + s^ C[code]) for a
+ *               rescoring codec (rows not referenced are left untouched)
+ * centroids_rot (nlist x D, = R c) is required when centroids is given.
+ * x has n_rows rows (bounds for src_row); centroids has nlist rows.
+ * ------------------------------------------------------------------------ */
+int rslm_encode(const rslm_plan *plan, const float *x, int64_t n_rows,
+                const int64_t *src_row, const int32_t *rec_list,
+                int64_t n_records, const float *centroids,
+                const float *centroids_rot, int32_t nlist, uint8_t *codes,
+                uint32_t *scales, float *resid_rot, void *stream);
+
+/* Canonical <-> scan layout of packed codes (Section "Codecs Description":
+ * codes are a packed bit stream, code j of a record at bits [w j, w j + w),
+ * w = log2 K, little-endian).  canon: n x canon_bytes; tiles: ceil(n/16) *
+ * tile_bytes.  Padding records of the last tile are zero-filled. */
+int rslm_pack_codes(const rslm_plan *plan, const uint8_t *canon, int64_t n,
+                    uint8_t *tiles, void *stream);
+int rslm_unpack_codes(const rslm_plan *plan, const uint8_t *tiles, int64_t n,
+                      uint8_t *canon, void *stream);
+
+/* ------------------------------------------------------------------------
+ * ivf_assign_probe -- IVF routing (Section "End-to-End Comparison", Setup):
+ *   IVF_ASSIGN_L2: out_ids[i] = argmin_p ||x_i - c_p||^2 (lowest p on ties),
+ *                  out_scores[i] = that squared distance (may be NULL);
+ *                  nprobe must be 1.
+ *   IVF_PROBE_IP : the nprobe partitions with the largest <x_i, c_p>,
+ *                  ordered by (dot desc, p asc): out_ids / out_scores are
+ *                  n x nprobe (out_scores = the dots).
+ *   x: n x dim, centroids: nlist x dim (float32).  nlist <= 65536,
+ *   nprobe <= min(nlist, 1024).
+ * ------------------------------------------------------------------------ */
+#define IVF_ASSIGN_L2 0
+#define IVF_PROBE_IP 1
+size_t ivf_assign_probe_workspace(int64_t n, int32_t dim, int32_t nlist,
+                                  int32_t nprobe, int mode);
+int ivf_assign_probe(const float *x, int64_t n, int32_t dim,
+                     const float *centroids, int32_t nlist, int32_t nprobe,
+                     int mode, int32_t *out_ids, float *out_scores, void *ws,
+                     size_t ws_bytes, void *stream);
+
+/* ------------------------------------------------------------------------
+ * IVF index of RSLM records (caller-owned device arrays).  List L holds
+ * list_sizes[L] records starting at record list_offsets[L] (a multiple of
+ * 16, the tile size); record r has id ids[r], packed codes in tile r/16 and
+ * scales[r].
+ * ------------------------------------------------------------------------ */
+typedef struct rslm_index {
+  int32_t nlist;
+  int32_t max_list_size;        /* host value: max_L list_sizes[L] */
+  const int64_t *list_offsets;  /* nlist */
+  const int32_t *list_sizes;    /* nlist */
+  const int32_t *ids;           /* per record */
+  const uint8_t *codes;         /* scan tile layout */
+  const uint32_t *scales;       /* per record: lo16 s^ | hi16 g^ */
+} rslm_index;
+
+/* ------------------------------------------------------------------------
+ * rslm_scan_topk -- second-stage scan and per-query top-k (Sections
+ * "Relative Quantization" and "End-to-End Comparison"): for every query q
+ * and every candidate x of its probed lists (probe_ids, from IVF_PROBE_IP),
+ *   score = g^_x (<q, c_p> + s^_x sum_j <q_rot[j g:(j+1) g], C[code_x,j]>)
+ * with <q, c_p> = probe_dots; then the k best by (score desc, id asc),
+ * padded with (-inf, -1).
+ *   q_rot: Q x D rotated queries (rslm_fwht); probe_ids / probe_dots:
+ *   Q x nprobe; out_scores / out_ids: Q x k.  1 <= k <= 1024.
+ * ------------------------------------------------------------------------ */
+size_t rslm_scan_topk_workspace(const rslm_plan *plan, const rslm_index *index,
+                                int32_t Q, int32_t nprobe, int32_t k);
+int rslm_scan_topk(const rslm_plan *plan, const rslm_index *index,
+                   const float *q_rot, int32_t Q, const int32_t *probe_ids,
+                   const float *probe_dots, int32_t nprobe, int32_t k,
+                   float *out_scores, int32_t *out_ids, void *ws,
+                   size_t ws_bytes, void *stream);
+
+/* ------------------------------------------------------------------------
+ * 8-bit rescoring codec: SQ8 (Section "Background and Related Work": scalar
+ * quantisation to 2^8 levels with a per-dimension range) applied to the
+ * rotated second residual, used relatively with local scaling ("RelApprox-
+ * SQ8", tab:recall_eval_relative).
+ *   rslm_sq8_fit   : lo[d] / hi[d] = min / max over the n rows of v (n x dim);
+ *                    accumulate != 0 folds into the existing lo / hi.
+ *   rslm_sq8_encode: codes[dest_row[i] or i] = clamp(rne((v - lo) / step),
+ *                    0, 255), step = (hi - lo) / 255 (a zero step gives 0).
+ * ------------------------------------------------------------------------ */
+int rslm_sq8_fit(const float *v, int64_t n, int32_t dim, float *lo, float *hi,
+                 int accumulate, void *stream);
+int rslm_sq8_encode(const float *v, int64_t n, int32_t dim, const float *lo,
+                    const float *hi, const int32_t *dest_row, int64_t n_dest,
+                    uint8_t *codes, void *stream);
+
+/* ------------------------------------------------------------------------
+ * rslm_rescore -- second stage of two-stage retrieval (Sections "Background
+ * and Related Work" and "Relative Quantization"): for each shortlisted
+ * candidate, score2 = score1 + <q_rot, r~2> where r~2 decodes the
+ * candidate's rescoring record; then the k_out best by (score2 desc, id asc).
+ *   codec kind RSLM_RESCORE_SQ8: codes is n_vectors x dim uint8 indexed by
+ *   id, lo / hi the SQ8 ranges.  cand_ids < 0 are empty slots.
+ *   cand_scores / cand_ids: Q x k_in; out_*: Q x k_out; k_out <= k_in <= 1024.
+ * ------------------------------------------------------------------------ */
+#define RSLM_RESCORE_SQ8 0
+typedef struct rslm_rescore_codec {
+  int32_t kind;
+  int32_t dim;
+  int64_t n_vectors;
+  const uint8_t *codes;
+  const float *lo;
+  const float *hi;
+} rslm_rescore_codec;
+
+int rslm_rescore(const rslm_rescore_codec *codec, const float *q_rot,
+                 int32_t Q, const float *cand_scores, const int32_t *cand_ids,
+                 int32_t k_in, int32_t k_out, float *out_scores,
+                 int32_t *out_ids, void *stream);
+
+/* ------------------------------------------------------------------------
+ * Profiling hook (not part of the method): later rslm_scan_topk calls record
+ * ev_begin / ev_end (hipEvent_t passed as void*, created by the caller) on
+ * their stream immediately before and after one of their kernels:
+ *   RSLM_TIMER_SCAN: the scan kernel;  RSLM_TIMER_TOPK: the top-k kernel.
+ * Both NULL disables.  The setting is process-wide and not synchronised:
+ * set it from one thread while no rslm_scan_topk call is in flight.
+ * ------------------------------------------------------------------------ */
+#define RSLM_TIMER_SCAN 0
+#define RSLM_TIMER_TOPK 1
+int rslm_set_timer(int which, void *ev_begin, void *ev_end);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* RSLM_H */

@@ -1,0 +1,233 @@
+// Plan objects, status handling and the E_max constant.
+#include <cmath>
+#include <cstring>
+#include <new>
+
+#include "rslm_internal.h"
+
+namespace rslm {
+
+static thread_local int g_last_hip = 0;
+
+int set_hip_error(hipError_t e) {
+  g_last_hip = int(e);
+  return RSLM_ERR_HIP;
+}
+
+int check_launch() {
+  hipError_t e = hipGetLastError();
+  return e == hipSuccess ? RSLM_OK : set_hip_error(e);
+}
+
+bool device_ok() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return false;
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return false;
+  return std::strncmp(prop.gcnArchName, "gfx950", 6) == 0;
+}
+
+// E_max(D) = E[max_{i<=D} |Z_i|] for i.i.d. standard normal Z_i
+//          = integral_0^inf P(max |Z_i| > t) dt = integral_0^inf 1 - (1 - erfc(t/sqrt2))^D dt.
+// Composite Simpson on [0, 16] (the tail beyond is below D * 1e-57).
+static double emax_of(int D) {
+  const int n = 1 << 18;
+  const double a = 0.0, b = 16.0, h = (b - a) / n;
+  auto f = [D](double t) {
+    double q = std::erfc(t / std::sqrt(2.0));          // P(|Z| > t)
+    return -std::expm1(double(D) * std::log1p(-q));    // 1 - (1 - q)^D
+  };
+  double s = f(a) + f(b);
+  for (int i = 1; i < n; ++i) s += f(a + i * h) * ((i & 1) ? 4.0 : 2.0);
+  return s * h / 3.0;
+}
+
+static bool f16_exact(float v) {
+  _Float16 h = static_cast<_Float16>(v);
+  return static_cast<float>(h) == v;
+}
+
+static uint16_t f16_bits(float v) {
+  _Float16 h = static_cast<_Float16>(v);
+  uint16_t b;
+  std::memcpy(&b, &h, 2);
+  return b;
+}
+
+}  // namespace rslm
+
+using namespace rslm;
+
+extern "C" {
+
+const char *rslm_status_string(int s) {
+  switch (s) {
+    case RSLM_OK: return "ok";
+    case RSLM_ERR_INVALID_ARG: return "invalid argument";
+    case RSLM_ERR_UNSUPPORTED: return "unsupported";
+    case RSLM_ERR_HIP: return "HIP error";
+    case RSLM_ERR_WORKSPACE: return "workspace too small";
+    case RSLM_ERR_NO_DEVICE: return "no gfx950 device";
+    default: return "unknown status";
+  }
+}
+
+int rslm_last_hip_error(void) { return g_last_hip; }
+
+const char *rslm_version(void) { return "0.1.0"; }
+
+int rslm_plan_create(const rslm_plan_desc *d, rslm_plan **out) {
+  if (!d || !out || !d->signs || !d->perm || !d->codebook) return RSLM_ERR_INVALID_ARG;
+  if (d->dim < 1 || d->dim > kMaxDim) return RSLM_ERR_INVALID_ARG;
+  if (d->bits < 1 || d->bits > 4) return RSLM_ERR_INVALID_ARG;
+  if (d->passes < -1 || d->passes > 2) return RSLM_ERR_INVALID_ARG;
+  if (d->scale_mode != 0 && d->scale_mode != 1) return RSLM_ERR_INVALID_ARG;
+  for (int i = 0; i < 256; ++i)
+    if (d->signs[i] != 1 && d->signs[i] != -1) return RSLM_ERR_INVALID_ARG;
+  {
+    bool seen[128] = {};
+    for (int i = 0; i < 128; ++i) {
+      int p = d->perm[i];
+      if (p < 0 || p >= 128 || seen[p]) return RSLM_ERR_INVALID_ARG;
+      seen[p] = true;
+    }
+  }
+  const int D = d->dim, bits = d->bits;
+  static const int kK[5] = {0, 16, 16, 8, 16};
+  static const int kG[5] = {0, 4, 2, 1, 1};
+  const int K = kK[bits], g = kG[bits];
+  for (int i = 0; i < K * g; ++i) {
+    float v = d->codebook[i];
+    if (!std::isfinite(v) || !f16_exact(v)) return RSLM_ERR_INVALID_ARG;
+  }
+  if (g == 1)
+    for (int k = 0; k + 1 < K; ++k)
+      if (!(d->codebook[k] < d->codebook[k + 1])) return RSLM_ERR_INVALID_ARG;
+  if (!device_ok()) return RSLM_ERR_NO_DEVICE;
+
+  rslm_plan *p = new (std::nothrow) rslm_plan();
+  if (!p) return RSLM_ERR_HIP;
+  (void)hipGetDevice(&p->device);
+  std::memcpy(p->signs, d->signs, 256);
+  std::memcpy(p->perm, d->perm, 128 * sizeof(int32_t));
+
+  // --- rotation parameters (block size, full blocks, overlap block, passes)
+  RotParams &r = p->rot;
+  r.D = D;
+  r.B = (D >= 128) ? 128 : (1 << (31 - __builtin_clz(unsigned(D))));
+  r.logB = 31 - __builtin_clz(unsigned(r.B));
+  r.n_full = D / r.B;
+  r.overlap = (D % r.B) != 0;
+  r.passes = (d->passes >= 0) ? d->passes : ((bits == 4 && D <= 256) ? 1 : 2);
+  r.inv_sqrt_b = float(1.0 / std::sqrt(double(r.B)));
+
+  // --- codec parameters
+  CodecParams &c = p->codec;
+  c.D = D;
+  c.bits = bits;
+  c.K = K;
+  c.g = g;
+  c.w = (K == 16) ? 4 : 3;
+  c.n_sub = (D + g - 1) / g;
+  c.d_pad = (D + 31) / 32 * 32;
+  c.n_chunks = c.d_pad / 32;
+  c.lane_bytes = (c.n_chunks * bits + 15) / 16 * 16;
+  c.tile_bytes = 64 * c.lane_bytes;
+  c.canon_bytes = (c.n_sub * c.w + 7) / 8;
+  c.global = d->scale_mode;
+  p->emax = emax_of(D);
+  c.emax = float(p->emax);
+  for (int i = 0; i < 64; ++i) c.cb[i] = (i < K * g) ? d->codebook[i] : 0.0f;
+  for (int k = 0; k < 16; ++k)
+    c.thr[k] = (g == 1 && k + 1 < K) ? 0.5f * (d->codebook[k] + d->codebook[k + 1]) : 0.0f;
+
+  // --- device tables: signs, intra-block permutation, compact decode table
+  float s1f[256];
+  for (int i = 0; i < 256; ++i) s1f[i] = float(d->signs[i]);
+  int16_t pi[128];
+  for (int k = 0; k < r.B; ++k) {
+    if (r.B == 128) {
+      pi[k] = int16_t(d->perm[k]);
+    } else {
+      int v = 0;
+      for (int t = 0; t < r.logB; ++t)
+        if ((k >> t) & 1) v |= 1 << (r.logB - 1 - t);
+      pi[k] = int16_t(v);
+    }
+  }
+  // Decode table: symbol -> the float16 centroid values it stands for.
+  //   bits 4: symbol = a byte (two 1-D codes), entry = half2(C[lo], C[hi])
+  //   bits 3: symbol = 6 bits (two 3-bit codes), entry = half2
+  //   bits 2: symbol = a nibble (one 2-D centroid), entry = half2
+  //   bits 1: symbol = a nibble (one 4-D centroid), entry = half4
+  uint32_t tab[512];
+  int entries = 0, words = 1;
+  auto h = [&](int k, int j) { return uint32_t(f16_bits(d->codebook[k * g + j])); };
+  if (bits == 4) {
+    entries = 256;
+    for (int s = 0; s < 256; ++s) tab[s] = h(s & 15, 0) | (h(s >> 4, 0) << 16);
+  } else if (bits == 3) {
+    entries = 64;
+    for (int s = 0; s < 64; ++s) tab[s] = h(s & 7, 0) | (h(s >> 3, 0) << 16);
+  } else if (bits == 2) {
+    entries = 16;
+    for (int s = 0; s < 16; ++s) tab[s] = h(s, 0) | (h(s, 1) << 16);
+  } else {
+    entries = 16;
+    words = 2;
+    for (int s = 0; s < 16; ++s) {
+      tab[2 * s] = h(s, 0) | (h(s, 1) << 16);
+      tab[2 * s + 1] = h(s, 2) | (h(s, 3) << 16);
+    }
+  }
+  p->dtab_entries = entries;
+  p->dtab_words = words;
+
+  hipError_t e;
+  if ((e = hipMalloc(&p->d_s1, sizeof(s1f))) != hipSuccess ||
+      (e = hipMalloc(&p->d_pi, sizeof(pi))) != hipSuccess ||
+      (e = hipMalloc(&p->d_dtab, sizeof(uint32_t) * entries * words)) != hipSuccess) {
+    rslm_plan_destroy(p);
+    return set_hip_error(e);
+  }
+  if ((e = hipMemcpy(p->d_s1, s1f, sizeof(s1f), hipMemcpyHostToDevice)) != hipSuccess ||
+      (e = hipMemcpy(p->d_pi, pi, sizeof(pi), hipMemcpyHostToDevice)) != hipSuccess ||
+      (e = hipMemcpy(p->d_dtab, tab, sizeof(uint32_t) * entries * words,
+                     hipMemcpyHostToDevice)) != hipSuccess) {
+    rslm_plan_destroy(p);
+    return set_hip_error(e);
+  }
+  r.s1 = p->d_s1;
+  r.pi = p->d_pi;
+  *out = p;
+  return RSLM_OK;
+}
+
+int rslm_plan_destroy(rslm_plan *p) {
+  if (!p) return RSLM_ERR_INVALID_ARG;
+  if (p->d_s1) (void)hipFree(p->d_s1);
+  if (p->d_pi) (void)hipFree(p->d_pi);
+  if (p->d_dtab) (void)hipFree(p->d_dtab);
+  delete p;
+  return RSLM_OK;
+}
+
+int rslm_plan_get_info(const rslm_plan *p, rslm_plan_info *info) {
+  if (!p || !info) return RSLM_ERR_INVALID_ARG;
+  info->dim = p->rot.D;
+  info->bits = p->codec.bits;
+  info->passes = p->rot.passes;
+  info->scale_mode = p->codec.global;
+  info->K = p->codec.K;
+  info->g = p->codec.g;
+  info->block = p->rot.B;
+  info->n_full_blocks = p->rot.n_full;
+  info->d_pad = p->codec.d_pad;
+  info->canon_bytes = p->codec.canon_bytes;
+  info->tile_records = kTileRecords;
+  info->tile_bytes = p->codec.tile_bytes;
+  info->emax = p->emax;
+  return RSLM_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,238 @@
+// IVF routing: assignment of vectors to their nearest partition centre and
+// probing of the partitions with the largest dot product with a query
+// (paper, Section "End-to-End Comparison", Setup: Euclidean partitions,
+// routing by the dot product with the centres).
+//
+// Both modes are a dense [n x D] x [D x nlist] contraction in float32.  A
+// 64x64 output tile per 256-thread workgroup, 4x4 outputs per thread, K
+// staged through LDS in slices of 16.  Assignment keeps a running
+// (distance, id) minimum per row across all column tiles and never writes the
+// product; probing writes the dots and selects the top-nprobe per row.
+#include "rslm_internal.h"
+#include "select_dev.h"
+
+namespace rslm {
+
+constexpr int kTM = 64, kTN = 64, kTK = 16;
+
+__global__ void k_row_norms(const float *__restrict__ c, int n, int D, float *__restrict__ out) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+  if (row >= n) return;
+  float s = 0.f;
+  for (int i = lane; i < D; i += 64) {
+    const float v = c[int64_t(row) * D + i];
+    s += v * v;
+  }
+  s = wave_sum(s);
+  if (lane == 0) out[row] = s;
+}
+
+// Loads a 64-row x 16-column slice of a row-major matrix (rows r0.., cols
+// k0..) transposed into lds[16][64 + 4] (zero outside the matrix).
+__device__ __forceinline__ void load_slice(const float *__restrict__ m, int64_t rows, int D,
+                                           int64_t r0, int k0, float (*lds)[kTM + 4]) {
+  // 256 threads x 4 elements
+  const int t = threadIdx.x;
+  const int r = t >> 2;          // 0..63
+  const int kk = (t & 3) * 4;    // 0,4,8,12
+  const int64_t gr = r0 + r;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int gk = k0 + kk + e;
+    float v = 0.f;
+    if (gr < rows && gk < D) v = m[gr * D + gk];
+    lds[kk + e][r] = v;
+  }
+}
+
+// acc[i][j] = sum_k A[r0 + ty*4 + i][k] * B[c0 + tx*4 + j][k]
+__device__ __forceinline__ void tile_product(const float *__restrict__ A, int64_t n,
+                                             const float *__restrict__ Bm, int nb, int D,
+                                             int64_t r0, int c0, float (*As)[kTM + 4],
+                                             float (*Bs)[kTM + 4], float acc[4][4]) {
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = 0.f;
+  for (int k0 = 0; k0 < D; k0 += kTK) {
+    load_slice(A, n, D, r0, k0, As);
+    load_slice(Bm, nb, D, c0, k0, Bs);
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < kTK; ++kk) {
+      float a[4], b[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) a[i] = As[kk][ty * 4 + i];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) b[j] = Bs[kk][tx * 4 + j];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] += a[i] * b[j];
+    }
+    __syncthreads();
+  }
+}
+
+__global__ void __launch_bounds__(256) k_assign(const float *__restrict__ x, int64_t n, int D,
+                                                const float *__restrict__ cen, int nlist,
+                                                const float *__restrict__ cnorm,
+                                                int32_t *__restrict__ out_ids,
+                                                float *__restrict__ out_d) {
+  __shared__ float As[kTK][kTM + 4];
+  __shared__ float Bs[kTK][kTM + 4];
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  const int64_t r0 = int64_t(blockIdx.x) * kTM;
+  float best[4];
+  int bid[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    best[i] = 3.4e38f;
+    bid[i] = 0x7fffffff;
+  }
+  float acc[4][4];
+  for (int c0 = 0; c0 < nlist; c0 += kTN) {
+    tile_product(x, n, cen, nlist, D, r0, c0, As, Bs, acc);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int c = c0 + tx * 4 + j;
+      if (c < nlist) {
+        const float cn = cnorm[c];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float v = cn - 2.f * acc[i][j];   // ||c||^2 - 2 <x, c>
+          if (v < best[i]) {                      // columns visited in increasing order
+            best[i] = v;
+            bid[i] = c;
+          }
+        }
+      }
+    }
+  }
+  // reduce over the 16 threads (tx) sharing each row: lexicographic (value, id)
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    for (int off = 8; off >= 1; off >>= 1) {
+      const float ov = __shfl_xor(best[i], off, 64);
+      const int oi = __shfl_xor(bid[i], off, 64);
+      if (ov < best[i] || (ov == best[i] && oi < bid[i])) {
+        best[i] = ov;
+        bid[i] = oi;
+      }
+    }
+  }
+  if (tx == 0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t r = r0 + ty * 4 + i;
+      if (r < n) {
+        out_ids[r] = bid[i];
+        if (out_d) {
+          float xx = 0.f;
+          for (int k = 0; k < D; ++k) {
+            const float v = x[r * D + k];
+            xx += v * v;
+          }
+          out_d[r] = xx + best[i];
+        }
+      }
+    }
+  }
+}
+
+__global__ void __launch_bounds__(256) k_dots(const float *__restrict__ x, int64_t n, int D,
+                                              const float *__restrict__ cen, int nlist,
+                                              float *__restrict__ dots) {
+  __shared__ float As[kTK][kTM + 4];
+  __shared__ float Bs[kTK][kTM + 4];
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  const int64_t r0 = int64_t(blockIdx.y) * kTM;
+  const int c0 = blockIdx.x * kTN;
+  float acc[4][4];
+  tile_product(x, n, cen, nlist, D, r0, c0, As, Bs, acc);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int64_t r = r0 + ty * 4 + i;
+    if (r >= n) continue;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int c = c0 + tx * 4 + j;
+      if (c < nlist) dots[r * nlist + c] = acc[i][j];
+    }
+  }
+}
+
+struct IdentityId {
+  __device__ int32_t operator()(int i) const { return i; }
+};
+
+__global__ void __launch_bounds__(kSelThreads) k_probe_select(const float *__restrict__ dots,
+                                                              int nlist, int nprobe,
+                                                              int32_t *__restrict__ out_ids,
+                                                              float *__restrict__ out_s) {
+  __shared__ SelectSmem sm;
+  const int64_t row = blockIdx.x;
+  block_topk(dots + row * nlist, nlist, nprobe, IdentityId(), out_s + row * nprobe,
+             out_ids + row * nprobe, sm);
+}
+
+}  // namespace rslm
+
+using namespace rslm;
+
+extern "C" {
+
+size_t ivf_assign_probe_workspace(int64_t n, int32_t dim, int32_t nlist, int32_t nprobe,
+                                  int mode) {
+  (void)dim;
+  (void)nprobe;
+  if (n < 0 || nlist < 1) return 0;
+  const size_t norms = (size_t(nlist) * sizeof(float) + 255) / 256 * 256;
+  if (mode == IVF_ASSIGN_L2) return norms;
+  const size_t dots = size_t(n) * size_t(nlist) * sizeof(float);
+  return norms + (dots + 255) / 256 * 256;
+}
+
+int ivf_assign_probe(const float *x, int64_t n, int32_t dim, const float *centroids,
+                     int32_t nlist, int32_t nprobe, int mode, int32_t *out_ids,
+                     float *out_scores, void *ws, size_t ws_bytes, void *stream) {
+  if (n < 0 || dim < 1 || nlist < 1 || nlist > 65536) return RSLM_ERR_INVALID_ARG;
+  if (mode != IVF_ASSIGN_L2 && mode != IVF_PROBE_IP) return RSLM_ERR_INVALID_ARG;
+  if (mode == IVF_ASSIGN_L2 && nprobe != 1) return RSLM_ERR_INVALID_ARG;
+  if (mode == IVF_PROBE_IP && (nprobe < 1 || nprobe > nlist || nprobe > kMaxNprobe))
+    return RSLM_ERR_INVALID_ARG;
+  if (n == 0) return RSLM_OK;
+  if (!x || !centroids || !out_ids || (mode == IVF_PROBE_IP && !out_scores))
+    return RSLM_ERR_INVALID_ARG;
+  if (!ws || ws_bytes < ivf_assign_probe_workspace(n, dim, nlist, nprobe, mode))
+    return RSLM_ERR_WORKSPACE;
+  hipStream_t s = as_stream(stream);
+  if (mode == IVF_ASSIGN_L2) {
+    float *cnorm = static_cast<float *>(ws);
+    hipLaunchKernelGGL(k_row_norms, dim3((nlist + 3) / 4), dim3(256), 0, s, centroids, nlist,
+                       dim, cnorm);
+    int st = check_launch();
+    if (st) return st;
+    const int64_t grid = (n + kTM - 1) / kTM;
+    if (grid > 0x7fffffff) return RSLM_ERR_INVALID_ARG;
+    hipLaunchKernelGGL(k_assign, dim3(unsigned(grid)), dim3(256), 0, s, x, n, dim, centroids,
+                       nlist, cnorm, out_ids, out_scores);
+    return check_launch();
+  }
+  const size_t norms = (size_t(nlist) * sizeof(float) + 255) / 256 * 256;
+  float *dots = reinterpret_cast<float *>(static_cast<char *>(ws) + norms);
+  const int64_t gy = (n + kTM - 1) / kTM;
+  if (gy > 65535) return RSLM_ERR_INVALID_ARG;   // gridDim.y limit: n <= 4,194,240
+  hipLaunchKernelGGL(k_dots, dim3((nlist + kTN - 1) / kTN, unsigned(gy)), dim3(256), 0, s, x, n,
+                     dim, centroids, nlist, dots);
+  int st = check_launch();
+  if (st) return st;
+  if (n > 0x7fffffff) return RSLM_ERR_INVALID_ARG;
+  hipLaunchKernelGGL(k_probe_select, dim3(unsigned(n)), dim3(kSelThreads), 0, s, dots, nlist,
+                     nprobe, out_ids, out_scores);
+  return check_launch();
+}
+
+}  // extern "C"

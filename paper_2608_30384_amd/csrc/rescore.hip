@@ -1,0 +1,200 @@
+// Rescoring stage: the 8-bit SQ8 codec on the rotated second residual and
+// the rescoring of a shortlist (paper, Section "Background and Related Work":
+// low-bit scoring produces a shortlist that a higher-fidelity representation
+// rescores; SQ8 as a per-dimension 256-level scalar quantiser; Section
+// "Relative Quantization": <q, a + r~2> = <q, a> + <q, r~2> reuses the
+// first-stage score <q, a>).
+//
+// Rescoring gathers one record per shortlisted candidate (random access, the
+// paper's "LargePool" pattern); a workgroup per query decodes and scores its
+// candidates (lanes across coordinates, one wavefront per candidate) and
+// sorts them in LDS.
+#include "rslm_internal.h"
+
+namespace rslm {
+
+__global__ void k_keys_init(uint32_t *lo, uint32_t *hi, int dim, int from_floats) {
+  const int d = blockIdx.x * blockDim.x + threadIdx.x;
+  if (d >= dim) return;
+  if (from_floats) {
+    lo[d] = order_key(__uint_as_float(lo[d]));
+    hi[d] = order_key(__uint_as_float(hi[d]));
+  } else {
+    lo[d] = 0xffffffffu;
+    hi[d] = 0u;
+  }
+}
+
+__global__ void k_keys_to_float(uint32_t *lo, uint32_t *hi, int dim) {
+  const int d = blockIdx.x * blockDim.x + threadIdx.x;
+  if (d >= dim) return;
+  lo[d] = __float_as_uint(key_to_float(lo[d]));
+  hi[d] = __float_as_uint(key_to_float(hi[d]));
+}
+
+// grid.x covers dimensions (256 per block), grid.y splits the rows
+__global__ void k_sq8_minmax(const float *__restrict__ v, int64_t n, int dim, int64_t rows_per,
+                             uint32_t *lo, uint32_t *hi) {
+  const int d = blockIdx.x * blockDim.x + threadIdx.x;
+  if (d >= dim) return;
+  const int64_t r0 = int64_t(blockIdx.y) * rows_per;
+  const int64_t r1 = min(n, r0 + rows_per);
+  if (r0 >= r1) return;
+  float mn = 3.4e38f, mx = -3.4e38f;
+  for (int64_t r = r0; r < r1; ++r) {
+    const float x = v[r * dim + d];
+    mn = fminf(mn, x);
+    mx = fmaxf(mx, x);
+  }
+  atomicMin(&lo[d], order_key(mn));
+  atomicMax(&hi[d], order_key(mx));
+}
+
+__global__ void k_sq8_encode(const float *__restrict__ v, int64_t n, int dim,
+                             const float *__restrict__ lo, const float *__restrict__ hi,
+                             const int32_t *__restrict__ dest, int64_t n_dest,
+                             uint8_t *__restrict__ codes) {
+  const int64_t total = n * dim;
+  for (int64_t t = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; t < total;
+       t += int64_t(gridDim.x) * blockDim.x) {
+    const int64_t r = t / dim;
+    const int d = int(t - r * dim);
+    const int64_t o = dest ? int64_t(dest[r]) : r;
+    if (o < 0 || o >= n_dest) continue;
+    const float step = (hi[d] - lo[d]) / 255.f;
+    float c = 0.f;
+    if (step > 0.f) c = fminf(fmaxf(rintf((v[t] - lo[d]) / step), 0.f), 255.f);
+    codes[o * dim + d] = uint8_t(c);
+  }
+}
+
+constexpr int kRescoreThreads = 256;
+
+__global__ void __launch_bounds__(kRescoreThreads) k_rescore_sq8(
+    const uint8_t *__restrict__ codes, int64_t n_vec, int dim, const float *__restrict__ lo,
+    const float *__restrict__ hi, const float *__restrict__ q_rot,
+    const float *__restrict__ cand_s, const int32_t *__restrict__ cand_i, int k_in, int k_out,
+    float *__restrict__ out_s, int32_t *__restrict__ out_i) {
+  extern __shared__ float qs[];   // dim floats: q_d * step_d
+  __shared__ uint64_t buf[kMaxK];
+  __shared__ float red[kRescoreThreads / 64];
+  __shared__ uint32_t count;
+  const int q = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const float *qr = q_rot + int64_t(q) * dim;
+  float part = 0.f;
+  for (int d = tid; d < dim; d += kRescoreThreads) {
+    const float step = (hi[d] - lo[d]) / 255.f;
+    qs[d] = qr[d] * step;
+    part += qr[d] * lo[d];
+  }
+  part = wave_sum(part);
+  if (lane == 0) red[wave] = part;
+  if (tid == 0) count = 0;
+  __syncthreads();
+  float qlo = 0.f;
+  for (int w = 0; w < kRescoreThreads / 64; ++w) qlo += red[w];
+  for (int j = wave; j < k_in; j += kRescoreThreads / 64) {
+    const int32_t id = cand_i[int64_t(q) * k_in + j];
+    if (id < 0 || id >= n_vec) continue;   // empty slot
+    const uint8_t *cr = codes + int64_t(id) * dim;
+    float dot = 0.f;
+    for (int d = lane; d < dim; d += 64) dot += qs[d] * float(cr[d]);
+    dot = wave_sum(dot);
+    if (lane == 0) {
+      const float s2 = cand_s[int64_t(q) * k_in + j] + (qlo + dot);
+      const uint32_t pos = atomicAdd(&count, 1u);
+      buf[pos] = (uint64_t(order_key(s2)) << 32) | uint64_t(0xffffffffu - uint32_t(id));
+    }
+  }
+  __syncthreads();
+  const int n = int(count);
+  int p2 = 1;
+  while (p2 < n) p2 <<= 1;
+  for (int i = n + tid; i < p2; i += kRescoreThreads) buf[i] = 0ull;
+  __syncthreads();
+  for (int size = 2; size <= p2; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int i = tid; i < p2 / 2; i += kRescoreThreads) {
+        const int a0 = 2 * i - (i & (stride - 1));
+        const int a1 = a0 + stride;
+        const bool desc = ((a0 & size) == 0);
+        const uint64_t x = buf[a0], y = buf[a1];
+        if ((x < y) == desc) {
+          buf[a0] = y;
+          buf[a1] = x;
+        }
+      }
+      __syncthreads();
+    }
+  }
+  for (int j = tid; j < k_out; j += kRescoreThreads) {
+    if (j < n) {
+      out_s[int64_t(q) * k_out + j] = key_to_float(uint32_t(buf[j] >> 32));
+      out_i[int64_t(q) * k_out + j] = int32_t(0xffffffffu - uint32_t(buf[j] & 0xffffffffu));
+    } else {
+      out_s[int64_t(q) * k_out + j] = -__builtin_inff();
+      out_i[int64_t(q) * k_out + j] = -1;
+    }
+  }
+}
+
+}  // namespace rslm
+
+using namespace rslm;
+
+extern "C" {
+
+int rslm_sq8_fit(const float *v, int64_t n, int32_t dim, float *lo, float *hi, int accumulate,
+                 void *stream) {
+  if (n < 0 || dim < 1 || !lo || !hi || (n > 0 && !v)) return RSLM_ERR_INVALID_ARG;
+  hipStream_t s = as_stream(stream);
+  uint32_t *klo = reinterpret_cast<uint32_t *>(lo), *khi = reinterpret_cast<uint32_t *>(hi);
+  const dim3 gd((dim + 255) / 256);
+  hipLaunchKernelGGL(k_keys_init, gd, dim3(256), 0, s, klo, khi, dim, accumulate ? 1 : 0);
+  int st = check_launch();
+  if (st) return st;
+  if (n > 0) {
+    int64_t splits = (n + 4095) / 4096;
+    if (splits > 4096) splits = 4096;
+    const int64_t rows_per = (n + splits - 1) / splits;
+    hipLaunchKernelGGL(k_sq8_minmax, dim3(gd.x, unsigned(splits)), dim3(256), 0, s, v, n, dim,
+                       rows_per, klo, khi);
+    if ((st = check_launch())) return st;
+  }
+  hipLaunchKernelGGL(k_keys_to_float, gd, dim3(256), 0, s, klo, khi, dim);
+  return check_launch();
+}
+
+int rslm_sq8_encode(const float *v, int64_t n, int32_t dim, const float *lo, const float *hi,
+                    const int32_t *dest_row, int64_t n_dest, uint8_t *codes, void *stream) {
+  if (n < 0 || dim < 1 || n_dest < 0) return RSLM_ERR_INVALID_ARG;
+  if (n == 0) return RSLM_OK;
+  if (!v || !lo || !hi || !codes) return RSLM_ERR_INVALID_ARG;
+  if (!dest_row && n > n_dest) return RSLM_ERR_INVALID_ARG;
+  int64_t grid = (n * dim + 255) / 256;
+  if (grid > 1 << 20) grid = 1 << 20;
+  hipLaunchKernelGGL(k_sq8_encode, dim3(unsigned(grid)), dim3(256), 0, as_stream(stream), v, n,
+                     dim, lo, hi, dest_row, n_dest, codes);
+  return check_launch();
+}
+
+int rslm_rescore(const rslm_rescore_codec *c, const float *q_rot, int32_t Q,
+                 const float *cand_scores, const int32_t *cand_ids, int32_t k_in, int32_t k_out,
+                 float *out_scores, int32_t *out_ids, void *stream) {
+  if (!c || Q < 0 || k_in < 1 || k_in > kMaxK || k_out < 1 || k_out > k_in)
+    return RSLM_ERR_INVALID_ARG;
+  if (c->kind != RSLM_RESCORE_SQ8) return RSLM_ERR_UNSUPPORTED;
+  if (c->dim < 1 || c->dim > kMaxDim || c->n_vectors < 0) return RSLM_ERR_INVALID_ARG;
+  if (Q == 0) return RSLM_OK;
+  if (!c->codes || !c->lo || !c->hi || !q_rot || !cand_scores || !cand_ids || !out_scores ||
+      !out_ids)
+    return RSLM_ERR_INVALID_ARG;
+  hipLaunchKernelGGL(k_rescore_sq8, dim3(unsigned(Q)), dim3(kRescoreThreads),
+                     size_t(c->dim) * sizeof(float), as_stream(stream), c->codes, c->n_vectors,
+                     c->dim, c->lo, c->hi, q_rot, cand_scores, cand_ids, k_in, k_out, out_scores,
+                     out_ids);
+  return check_launch();
+}
+
+}  // extern "C"

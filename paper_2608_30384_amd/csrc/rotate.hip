@@ -1,0 +1,428 @@
+// Block-wise cascaded Walsh-Hadamard rotation and the fused RSLM encoder.
+//
+// Rotation (paper, Section "Pre-Quantization Transformations"): signs S1,
+// orthonormal FWHT on blocks of B (full blocks, then one block overlapping
+// the previous one and ending at D), then for two passes the in-block
+// permutation with the strided transpose x'[k M + b] = x[b B + P(k)], signs
+// S2 = S1 offset by 127, and the block FWHT again.
+//
+// GPU mapping: one wavefront per vector; the vector lives in LDS and each
+// radix-8 round loads 8 elements per lane, runs three butterfly stages in
+// registers and stores them back, so a 128-block needs three LDS round
+// trips (3 + 3 + 1 stages).  The encoder fuses residual, rotation, EVT
+// scale, Lloyd-Max assignment, norm correction, both 16-bit scales, packing
+// into the scan tile layout and the rotated second residual.
+#include "rslm_internal.h"
+
+namespace rslm {
+
+template <int R>
+__device__ __forceinline__ void fwht_round(float *v, int off, int nblk, int B, int s,
+                                           bool last, float scale, int lane) {
+  constexpr int G = 1 << R;
+  const int h = 1 << s;
+  const int gpb = B >> R;  // groups per block (power of two)
+  const int total = nblk * gpb;
+  for (int gi = lane; gi < total; gi += kWave) {
+    const int blk = gi / gpb;
+    const int t = gi - blk * gpb;
+    const int low = t & (h - 1);
+    const int high = t >> s;
+    const int base = off + blk * B + ((high << (s + R)) | low);
+    float e[G];
+#pragma unroll
+    for (int m = 0; m < G; ++m) e[m] = v[base + m * h];
+#pragma unroll
+    for (int st = 0; st < R; ++st) {
+#pragma unroll
+      for (int m = 0; m < G; ++m) {
+        if (!(m & (1 << st))) {
+          const float a = e[m], b = e[m | (1 << st)];
+          e[m] = a + b;
+          e[m | (1 << st)] = a - b;
+        }
+      }
+    }
+    if (last) {
+#pragma unroll
+      for (int m = 0; m < G; ++m) e[m] *= scale;
+    }
+#pragma unroll
+    for (int m = 0; m < G; ++m) v[base + m * h] = e[m];
+  }
+}
+
+// Orthonormal FWHT of nblk adjacent blocks of size B starting at off.
+// Every thread of the block must call this (it contains barriers).
+__device__ __forceinline__ void fwht_blocks(float *v, int off, int nblk, const RotParams &rp,
+                                            int lane, bool active) {
+  const int B = rp.B, logB = rp.logB;
+  if (logB == 0) return;  // B == 1: identity
+  for (int s = 0; s < logB; s += 3) {
+    const int R = (logB - s) < 3 ? (logB - s) : 3;
+    const bool last = (s + R) == logB;
+    if (active) {
+      if (R == 3) fwht_round<3>(v, off, nblk, B, s, last, rp.inv_sqrt_b, lane);
+      else if (R == 2) fwht_round<2>(v, off, nblk, B, s, last, rp.inv_sqrt_b, lane);
+      else fwht_round<1>(v, off, nblk, B, s, last, rp.inv_sqrt_b, lane);
+    }
+    __syncthreads();
+  }
+}
+
+// One pass of block transforms.  Forward: full blocks, then the overlap
+// block.  Reverse (inverse rotation): overlap block first.
+__device__ __forceinline__ void fwht_pass(float *v, const RotParams &rp, int lane, bool active,
+                                          bool reverse) {
+  if (!reverse) {
+    if (rp.n_full) fwht_blocks(v, 0, rp.n_full, rp, lane, active);
+    if (rp.overlap) fwht_blocks(v, rp.D - rp.B, 1, rp, lane, active);
+  } else {
+    if (rp.overlap) fwht_blocks(v, rp.D - rp.B, 1, rp, lane, active);
+    if (rp.n_full) fwht_blocks(v, 0, rp.n_full, rp, lane, active);
+  }
+}
+
+__device__ __forceinline__ int transpose_src(int o, const RotParams &rp) {
+  const int MB = rp.n_full * rp.B;
+  if (o >= MB) return o;
+  const int M = rp.n_full;
+  const int k = o / M;
+  const int b = o - k * M;
+  return b * rp.B + int(rp.pi[k]);
+}
+
+// Forward rotation of the vector held in v (already multiplied by S1 when
+// passes > 0).  Returns the buffer holding the result (v or w).
+__device__ float *rotate_forward(float *v, float *w, const RotParams &rp, int lane, bool active) {
+  if (rp.passes == 0) return v;
+  fwht_pass(v, rp, lane, active, false);
+  if (rp.passes == 1) return v;
+  if (active) {
+    for (int o = lane; o < rp.D; o += kWave)
+      w[o] = v[transpose_src(o, rp)] * rp.s1[(o + 127) & 255];
+  }
+  __syncthreads();
+  fwht_pass(w, rp, lane, active, false);
+  return w;
+}
+
+// Inverse rotation R^T of the vector in v; the result excludes the final S1
+// multiplication, which the caller applies on output.
+__device__ float *rotate_inverse(float *v, float *w, const RotParams &rp, int lane, bool active) {
+  if (rp.passes == 0) return v;
+  if (rp.passes == 1) {
+    fwht_pass(v, rp, lane, active, true);
+    return v;
+  }
+  fwht_pass(v, rp, lane, active, true);
+  if (active) {
+    for (int o = lane; o < rp.D; o += kWave)
+      w[transpose_src(o, rp)] = v[o] * rp.s1[(o + 127) & 255];
+  }
+  __syncthreads();
+  fwht_pass(w, rp, lane, active, true);
+  return w;
+}
+
+// ---------------------------------------------------------------- rslm_fwht
+__global__ void __launch_bounds__(256) k_rotate(const float *__restrict__ x, float *y, int64_t n,
+                                                RotParams rp, int inverse, int dstride) {
+  extern __shared__ float lds[];
+  const int lane = threadIdx.x & 63;
+  const int wid = threadIdx.x >> 6;
+  const int64_t row = int64_t(blockIdx.x) * (blockDim.x >> 6) + wid;
+  const bool active = row < n;
+  float *v = lds + wid * 2 * dstride;
+  float *w = v + dstride;
+  const int D = rp.D;
+  if (active) {
+    const float *xr = x + row * D;
+    for (int i = lane; i < D; i += kWave) {
+      float t = xr[i];
+      v[i] = (!inverse && rp.passes > 0) ? t * rp.s1[i & 255] : t;
+    }
+  }
+  __syncthreads();
+  float *res = inverse ? rotate_inverse(v, w, rp, lane, active)
+                       : rotate_forward(v, w, rp, lane, active);
+  if (active) {
+    float *yr = y + row * D;
+    for (int i = lane; i < D; i += kWave) {
+      float t = res[i];
+      yr[i] = (inverse && rp.passes > 0) ? t * rp.s1[i & 255] : t;
+    }
+  }
+}
+
+// --------------------------------------------------------------- rslm_encode
+// Byte address inside the scan tile layout of the bits of coordinates
+// [8G, 8G + 8) of record rec: the tile holds 16 records; lane l = r * 16 + n
+// (n = record within the tile, r = G mod 4) owns a stream of lane_bytes
+// bytes stored as 16-byte units interleaved across the 64 lanes; chunk
+// c = G / 4 contributes `bits` bytes at stream offset c * bits.
+__device__ __forceinline__ int64_t tile_byte_addr(int64_t rec, int G, int t, const CodecParams &cp) {
+  const int64_t tile = rec >> 4;
+  const int n = int(rec & 15);
+  const int c = G >> 2, r = G & 3;
+  const int lane_id = r * 16 + n;
+  const int off = c * cp.bits + t;
+  return tile * cp.tile_bytes + int64_t((off >> 4) * 64 + lane_id) * 16 + (off & 15);
+}
+
+__device__ __forceinline__ void store_group(uint8_t *codes, int64_t rec, int G, uint32_t val,
+                                            const CodecParams &cp) {
+  const int b = cp.bits;
+  if (b == 4) {
+    *reinterpret_cast<uint32_t *>(codes + tile_byte_addr(rec, G, 0, cp)) = val;
+  } else if (b == 2) {
+    *reinterpret_cast<uint16_t *>(codes + tile_byte_addr(rec, G, 0, cp)) = uint16_t(val);
+  } else if (b == 1) {
+    codes[tile_byte_addr(rec, G, 0, cp)] = uint8_t(val);
+  } else {
+    for (int t = 0; t < 3; ++t) codes[tile_byte_addr(rec, G, t, cp)] = uint8_t(val >> (8 * t));
+  }
+}
+
+__global__ void __launch_bounds__(256) k_encode(
+    const float *__restrict__ x, int64_t n_rows, const int64_t *__restrict__ src_row,
+    const int32_t *__restrict__ rec_list, int64_t n_records, const float *__restrict__ cen,
+    const float *__restrict__ cen_rot, int nlist, uint8_t *__restrict__ codes,
+    uint32_t *__restrict__ scales, float *__restrict__ resid, RotParams rp, CodecParams cp,
+    int dstride) {
+  extern __shared__ float lds[];
+  __shared__ float cbs[64];
+  const int lane = threadIdx.x & 63;
+  const int wid = threadIdx.x >> 6;
+  const int nw = blockDim.x >> 6;
+  if (threadIdx.x < 64) cbs[threadIdx.x] = cp.cb[threadIdx.x];
+  const int64_t rec = int64_t(blockIdx.x) * nw + wid;
+  int64_t row = -1;
+  int L = -1;
+  if (rec < n_records) {
+    row = src_row ? src_row[rec] : rec;
+    if (row >= n_rows) row = -1;
+    if (cen && row >= 0) {
+      L = rec_list[rec];
+      if (L < 0 || L >= nlist) row = -1;
+    }
+  }
+  const bool active = row >= 0;
+  float *v = lds + wid * 2 * dstride;
+  float *w = v + dstride;
+  uint8_t *cl = reinterpret_cast<uint8_t *>(lds + nw * 2 * dstride) + wid * (dstride / 1);
+  const int D = rp.D;
+  float xx = 0.f, rr = 0.f, cc = 0.f;
+  if (active) {
+    const float *xr = x + row * D;
+    const float *cr = (L >= 0) ? cen + int64_t(L) * D : nullptr;
+    for (int i = lane; i < D; i += kWave) {
+      const float xv = xr[i];
+      const float cv = cr ? cr[i] : 0.f;
+      const float r = xv - cv;
+      xx += xv * xv;
+      rr += r * r;
+      cc += cv * cv;
+      v[i] = (rp.passes > 0) ? r * rp.s1[i & 255] : r;
+    }
+  }
+  __syncthreads();
+  const float *z = rotate_forward(v, w, rp, lane, active);
+  if (!active) return;  // no barriers below
+
+  float m = 0.f;
+  for (int i = lane; i < D; i += kWave) m = fmaxf(m, fabsf(z[i]));
+  m = wave_max(m);
+  const float inv_s0 = (m > 0.f) ? cp.emax / m : 0.f;
+  const float *rc = (L >= 0 && cen_rot) ? cen_rot + int64_t(L) * D : nullptr;
+  const int g = cp.g;
+  float cn2 = 0.f, rcd = 0.f;
+  for (int j = lane; j < cp.n_sub; j += kWave) {
+    int code = 0;
+    if (m > 0.f) {
+      if (g == 1) {
+        const float u = z[j] * inv_s0;
+        for (int k = 0; k + 1 < cp.K; ++k) code += (u > cp.thr[k]) ? 1 : 0;
+      } else {
+        float u[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const int i = j * g + t;
+          u[t] = (t < g && i < D) ? z[i] * inv_s0 : 0.f;
+        }
+        float best = 3.4e38f;
+        for (int k = 0; k < 16; ++k) {
+          float d = 0.f;
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            if (t < g) {
+              const float e = u[t] - cp.cb[k * g + t];
+              d += e * e;
+            }
+          }
+          if (d < best) {
+            best = d;
+            code = k;
+          }
+        }
+      }
+      for (int t = 0; t < g; ++t) {
+        const int i = j * g + t;
+        if (i < D) {
+          const float cv = cbs[code * g + t];
+          cn2 += cv * cv;
+          if (rc) rcd += rc[i] * cv;
+        }
+      }
+    }
+    cl[j] = uint8_t(code);
+  }
+  xx = wave_sum(xx);
+  rr = wave_sum(rr);
+  cc = wave_sum(cc);
+  cn2 = wave_sum(cn2);
+  rcd = wave_sum(rcd);
+  const float s = (m > 0.f && cn2 > 0.f) ? sqrtf(rr / cn2) : 0.f;
+  const uint32_t su = enc_ue7m9(s);
+  const float sh = dec_ue7m9(su);
+  uint32_t gu = 0x7000u;
+  if (cp.global) {
+    const float den2 = cc + 2.f * sh * rcd + sh * sh * cn2;
+    const float gv = (den2 > 0.f) ? sqrtf(xx / den2) : 0.f;
+    gu = enc_ue4m12(gv);
+  }
+  if (lane == 0) scales[rec] = su | (gu << 16);
+  __builtin_amdgcn_wave_barrier();  // codes in cl are written by other lanes
+
+  // pack: group G covers coordinates [8G, 8G + 8) = sub-vectors [8G/g, 8G/g + 8/g)
+  const int n_groups = cp.d_pad >> 3;
+  const int per = 8 / g;
+  for (int G = lane; G < n_groups; G += kWave) {
+    uint32_t val = 0;
+    for (int t = 0; t < per; ++t) {
+      const int j = G * per + t;
+      const uint32_t code = (j < cp.n_sub) ? cl[j] : 0u;
+      val |= code << (cp.w * t);
+    }
+    store_group(codes, rec, G, val, cp);
+  }
+  if (resid) {
+    const float gh = dec_ue4m12(gu);
+    float *out = resid + row * D;   // indexed by source row
+    for (int i = lane; i < D; i += kWave) {
+      const int code = cl[i / g];
+      const float cv = (m > 0.f) ? cbs[code * g + (i % g)] : 0.f;
+      const float rcv = rc ? rc[i] : 0.f;
+      out[i] = z[i] + rcv - gh * (rcv + sh * cv);
+    }
+  }
+}
+
+// --------------------------------------------------------- pack / unpack
+// Group G of a record is the `bits` canonical bytes [G bits, G bits + bits).
+__global__ void k_pack(const uint8_t *__restrict__ canon, int64_t n, uint8_t *__restrict__ tiles,
+                       CodecParams cp) {
+  const int n_groups = cp.d_pad >> 3;
+  const int64_t total = ((n + 15) >> 4) * 16 * n_groups;
+  for (int64_t t = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; t < total;
+       t += int64_t(gridDim.x) * blockDim.x) {
+    const int64_t rec = t / n_groups;
+    const int G = int(t - rec * n_groups);
+    for (int b = 0; b < cp.bits; ++b) {
+      const int cb = G * cp.bits + b;
+      tiles[tile_byte_addr(rec, G, b, cp)] =
+          (rec < n && cb < cp.canon_bytes) ? canon[rec * cp.canon_bytes + cb] : uint8_t(0);
+    }
+  }
+}
+
+__global__ void k_unpack(const uint8_t *__restrict__ tiles, int64_t n, uint8_t *__restrict__ canon,
+                         CodecParams cp) {
+  const int n_groups = cp.d_pad >> 3;
+  const int64_t total = n * n_groups;
+  for (int64_t t = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; t < total;
+       t += int64_t(gridDim.x) * blockDim.x) {
+    const int64_t rec = t / n_groups;
+    const int G = int(t - rec * n_groups);
+    for (int b = 0; b < cp.bits; ++b) {
+      const int cb = G * cp.bits + b;
+      if (cb < cp.canon_bytes) canon[rec * cp.canon_bytes + cb] = tiles[tile_byte_addr(rec, G, b, cp)];
+    }
+  }
+}
+
+static int lds_floats(int D) { return (D + 31) / 32 * 32 + 4; }
+
+}  // namespace rslm
+
+using namespace rslm;
+
+extern "C" {
+
+int rslm_fwht(const rslm_plan *p, const float *x, float *y, int64_t n, int inverse, void *stream) {
+  if (!p || (!x && n) || (!y && n) || n < 0 || (inverse != 0 && inverse != 1))
+    return RSLM_ERR_INVALID_ARG;
+  if (n == 0) return RSLM_OK;
+  const int D = p->rot.D;
+  const int dstride = lds_floats(D);
+  int waves = 4;
+  while (waves > 1 && size_t(waves) * 2 * dstride * 4 > 65536) waves >>= 1;
+  const size_t shm = size_t(waves) * 2 * dstride * sizeof(float);
+  const int64_t grid = (n + waves - 1) / waves;
+  if (grid > 0x7fffffff) return RSLM_ERR_INVALID_ARG;
+  hipLaunchKernelGGL(k_rotate, dim3(unsigned(grid)), dim3(64 * waves), shm, as_stream(stream), x,
+                     y, n, p->rot, inverse, dstride);
+  return check_launch();
+}
+
+int rslm_encode(const rslm_plan *p, const float *x, int64_t n_rows, const int64_t *src_row,
+                const int32_t *rec_list, int64_t n_records, const float *centroids,
+                const float *centroids_rot, int32_t nlist, uint8_t *codes, uint32_t *scales,
+                float *resid_rot, void *stream) {
+  if (!p || n_records < 0 || n_rows < 0) return RSLM_ERR_INVALID_ARG;
+  if (n_records == 0) return RSLM_OK;
+  if (!x || !codes || !scales) return RSLM_ERR_INVALID_ARG;
+  if (centroids && (!rec_list || !centroids_rot || nlist < 1)) return RSLM_ERR_INVALID_ARG;
+  if (!src_row && n_records > n_rows) return RSLM_ERR_INVALID_ARG;
+  const int D = p->rot.D;
+  const int dstride = lds_floats(D);
+  int waves = 4;
+  // two float buffers plus one byte per sub-vector (<= dstride bytes) per wave
+  while (waves > 1 && size_t(waves) * (2 * dstride * 4 + dstride) > 65536) waves >>= 1;
+  const size_t shm = size_t(waves) * (2 * dstride * 4 + dstride);
+  const int64_t grid = (n_records + waves - 1) / waves;
+  if (grid > 0x7fffffff) return RSLM_ERR_INVALID_ARG;
+  hipLaunchKernelGGL(k_encode, dim3(unsigned(grid)), dim3(64 * waves), shm, as_stream(stream), x,
+                     n_rows, src_row, rec_list, n_records, centroids, centroids_rot, nlist, codes,
+                     scales, resid_rot, p->rot, p->codec, dstride);
+  return check_launch();
+}
+
+static int64_t pack_grid(int64_t total) {
+  int64_t grid = (total + 255) / 256;
+  return grid > 65536 ? 65536 : (grid < 1 ? 1 : grid);
+}
+
+int rslm_pack_codes(const rslm_plan *p, const uint8_t *canon, int64_t n, uint8_t *tiles,
+                    void *stream) {
+  if (!p || n < 0) return RSLM_ERR_INVALID_ARG;
+  if (n == 0) return RSLM_OK;
+  if (!canon || !tiles) return RSLM_ERR_INVALID_ARG;
+  const int64_t total = (n + 15) / 16 * 16 * (p->codec.d_pad / 8);
+  hipLaunchKernelGGL(k_pack, dim3(unsigned(pack_grid(total))), dim3(256), 0, as_stream(stream),
+                     canon, n, tiles, p->codec);
+  return check_launch();
+}
+
+int rslm_unpack_codes(const rslm_plan *p, const uint8_t *tiles, int64_t n, uint8_t *canon,
+                      void *stream) {
+  if (!p || n < 0) return RSLM_ERR_INVALID_ARG;
+  if (n == 0) return RSLM_OK;
+  if (!canon || !tiles) return RSLM_ERR_INVALID_ARG;
+  const int64_t total = n * (p->codec.d_pad / 8);
+  hipLaunchKernelGGL(k_unpack, dim3(unsigned(pack_grid(total))), dim3(256), 0, as_stream(stream),
+                     tiles, n, canon, p->codec);
+  return check_launch();
+}
+
+}  // extern "C"

@@ -1,0 +1,130 @@
+// Internal definitions of librslm: the plan object, launch helpers and small
+// device utilities shared by the kernels.  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/rslm.h"
+
+namespace rslm {
+
+constexpr int kWave = 64;
+constexpr int kTileRecords = 16;        // records per scan tile (MFMA N)
+constexpr int kMaxDim = 4096;
+constexpr int kMaxK = 1024;             // top-k bound
+constexpr int kMaxNprobe = 1024;
+
+// Per-plan parameters needed on the device, passed by value to kernels.
+struct RotParams {
+  int D;          // dimension
+  int B;          // FWHT block size
+  int logB;
+  int n_full;     // floor(D / B)
+  int overlap;    // 1 iff D % B != 0
+  int passes;     // 0, 1, 2
+  float inv_sqrt_b;
+  const float *s1;     // device, 256 signs (+1/-1) as float
+  const int16_t *pi;   // device, intra-block permutation of size B
+};
+
+struct CodecParams {
+  int D, bits, K, g, w;       // w = log2 K
+  int n_sub;                  // ceil(D / g)
+  int d_pad;                  // multiple of 32
+  int n_chunks;               // d_pad / 32
+  int lane_bytes;             // bytes of one lane's stream in a tile
+  int tile_bytes;             // 64 * lane_bytes
+  int canon_bytes;
+  int global;                 // scale mode
+  float emax;                 // E_max(D) as float
+  float cb[64];               // codebook, K*g values
+  float thr[16];              // 1-D decision thresholds (K-1 used)
+};
+
+}  // namespace rslm
+
+struct rslm_plan {
+  int device;
+  rslm::RotParams rot;
+  rslm::CodecParams codec;
+  double emax;
+  int8_t signs[256];
+  int32_t perm[128];
+  // device allocations owned by the plan
+  float *d_s1 = nullptr;
+  int16_t *d_pi = nullptr;
+  uint32_t *d_dtab = nullptr;   // compact decode table (see scan.hip)
+  int dtab_entries = 0;
+  int dtab_words = 0;           // 32-bit words per entry
+};
+
+namespace rslm {
+
+int set_hip_error(hipError_t e);     // records e, returns RSLM_ERR_HIP
+int check_launch();                  // hipGetLastError -> status
+bool device_ok();                    // current device is gfx950
+
+inline hipStream_t as_stream(void *s) { return reinterpret_cast<hipStream_t>(s); }
+
+// ---- device helpers ------------------------------------------------------
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
+  return v;
+}
+
+// UE7M9: u = e << 9 | m encodes 2^(e-63) (1 + m/512), e in [1,127]; u = 0 is 0.
+// Round to nearest even on 10 significant bits from float32, saturate on
+// overflow, flush values below 2^-62 to 0.
+__device__ __forceinline__ uint32_t enc_ue7m9(float s) {
+  if (!(s > 0.0f)) return 0u;
+  uint32_t b = __float_as_uint(s);
+  if (b >= 0x7f800000u) return (127u << 9) | 511u;
+  b += 0x1fffu + ((b >> 14) & 1u);
+  b >>= 14;                             // (fp32 exponent << 9) | mantissa9
+  int e = int(b >> 9) - 64;
+  if (e < 1) return 0u;
+  if (e > 127) return (127u << 9) | 511u;
+  return (uint32_t(e) << 9) | (b & 511u);
+}
+
+__device__ __forceinline__ float dec_ue7m9(uint32_t u) {
+  return u ? __uint_as_float((u << 14) + (64u << 23)) : 0.0f;
+}
+
+// UE4M12: u = e << 12 | m encodes 2^(e-7) (1 + m/4096), e in [1,15].
+__device__ __forceinline__ uint32_t enc_ue4m12(float s) {
+  if (!(s > 0.0f)) return 0u;
+  uint32_t b = __float_as_uint(s);
+  if (b >= 0x7f800000u) return (15u << 12) | 4095u;
+  b += 0x3ffu + ((b >> 11) & 1u);
+  b >>= 11;
+  int e = int(b >> 12) - 120;
+  if (e < 1) return 0u;
+  if (e > 15) return (15u << 12) | 4095u;
+  return (uint32_t(e) << 12) | (b & 4095u);
+}
+
+__device__ __forceinline__ float dec_ue4m12(uint32_t u) {
+  return u ? __uint_as_float((u << 11) + (120u << 23)) : 0.0f;
+}
+
+// Float -> uint32 whose unsigned order equals the float order.
+__device__ __forceinline__ uint32_t order_key(float f) {
+  uint32_t b = __float_as_uint(f);
+  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+__device__ __forceinline__ float key_to_float(uint32_t k) {
+  uint32_t b = (k & 0x80000000u) ? (k & 0x7fffffffu) : ~k;
+  return __uint_as_float(b);
+}
+
+}  // namespace rslm

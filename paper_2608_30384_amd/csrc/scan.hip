@@ -1,0 +1,553 @@
+// Second-stage IVF scan with per-query top-k.
+//
+// Scoring (paper, Section "Relative Quantization", local/global scaling, and
+// Section "Performance Impact and Memory Savings", scoring in the rotated
+// space): for query q and candidate x of probed list p
+//   score = g^_x (<q, c_p> + s^_x sum_j <q_rot[j g:(j+1) g], C[code_{x,j}]>).
+//
+// GPU design.  All (query, list) pairs of a batch are grouped by list, so a
+// list is streamed from HBM once per group of up to 8 queries instead of once
+// per query.  For such a group the residual term is a dense contraction
+// [8 queries x D] . [D x candidates] once the codes are decoded to their
+// centroid values, so it runs on the matrix cores: v_mfma_f32_16x16x32_f16
+// with the 16 A rows = 8 queries x (hi, lo) float16 halves of the rotated
+// query (hi + lo carries ~22 significant bits), and B = 16 candidates x 32
+// coordinates of decoded centroids.  Centroids are float16-exact, so the
+// products are exact and accumulate in float32.  Codes are decoded through
+// an LDS table indexed by a whole code symbol (a byte = two 4-bit codes for
+// 4-bit codecs), replicated once per lane so the 64 lanes of a read always
+// hit 64 different banks.  The code layout in HBM ("tiles" of 16 records)
+// is arranged so that each lane's share of a tile is contiguous in 16-byte
+// units and a wavefront's load is 1 KiB contiguous.
+//
+// Scores of every candidate are written to a per-query region of the
+// workspace; a second kernel selects each query's top-k exactly (radix
+// select, then a bitonic sort of the survivors) and maps positions to ids.
+#include "rslm_internal.h"
+#include "select_dev.h"
+
+namespace rslm {
+
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+constexpr int kChunkCands = 1024;   // candidates per work item
+constexpr int kGroupQ = 8;          // queries per work item (16 MFMA rows / 2)
+constexpr int kScanThreads = 256;
+
+static size_t align256(size_t b) { return (b + 255) / 256 * 256; }
+
+struct ScanWs {
+  _Float16 *qh, *ql;
+  float *qinv;
+  int32_t *counts, *cursor, *pair_off, *item_off;
+  int32_t *pairs, *prefix, *totals;
+  float *scores;
+  int64_t stride;
+  size_t bytes;
+};
+
+static ScanWs scan_ws_layout(void *base, int Q, int nprobe, int nlist, int d_pad,
+                             int max_list) {
+  ScanWs w{};
+  char *p = static_cast<char *>(base);
+  size_t off = 0;
+  auto take = [&](size_t b) {
+    char *r = p ? p + off : nullptr;
+    off += align256(b);
+    return r;
+  };
+  w.qh = reinterpret_cast<_Float16 *>(take(size_t(Q) * d_pad * 2));
+  w.ql = reinterpret_cast<_Float16 *>(take(size_t(Q) * d_pad * 2));
+  w.qinv = reinterpret_cast<float *>(take(size_t(Q) * 4));
+  w.counts = reinterpret_cast<int32_t *>(take(size_t(nlist) * 4));
+  w.cursor = reinterpret_cast<int32_t *>(take(size_t(nlist) * 4));
+  w.pair_off = reinterpret_cast<int32_t *>(take(size_t(nlist + 1) * 4));
+  w.item_off = reinterpret_cast<int32_t *>(take(size_t(nlist + 1) * 4));
+  w.pairs = reinterpret_cast<int32_t *>(take(size_t(Q) * nprobe * 4));
+  w.prefix = reinterpret_cast<int32_t *>(take(size_t(Q) * nprobe * 4));
+  w.totals = reinterpret_cast<int32_t *>(take(size_t(Q) * 4));
+  w.stride = (int64_t(nprobe) * max_list + 63) / 64 * 64;
+  w.scores = reinterpret_cast<float *>(take(size_t(Q) * size_t(w.stride) * 4));
+  w.bytes = off;
+  return w;
+}
+
+// ------------------------------------------------------------- query prep
+// q_rot (Q x D) -> per-query power-of-two scale so that max |q| * scale lies
+// in [2^14, 2^15), then float16 hi = rne(q * scale), lo = rne(q * scale - hi).
+__global__ void k_prep_queries(const float *__restrict__ q, int Q, int D, int d_pad,
+                               _Float16 *__restrict__ qh, _Float16 *__restrict__ ql,
+                               float *__restrict__ qinv) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+  if (row >= Q) return;
+  const float *qr = q + int64_t(row) * D;
+  float m = 0.f;
+  for (int i = lane; i < D; i += 64) m = fmaxf(m, fabsf(qr[i]));
+  m = wave_max(m);
+  float scale = 1.f;
+  if (m > 0.f) {
+    const int e = ilogbf(m) + 1;  // m in [2^(e-1), 2^e)
+    scale = ldexpf(1.f, 15 - e);
+  }
+  for (int i = lane; i < d_pad; i += 64) {
+    const float v = (i < D) ? qr[i] * scale : 0.f;
+    const _Float16 h = static_cast<_Float16>(v);
+    const _Float16 l = static_cast<_Float16>(v - static_cast<float>(h));
+    qh[int64_t(row) * d_pad + i] = h;
+    ql[int64_t(row) * d_pad + i] = l;
+  }
+  if (lane == 0) qinv[row] = 1.f / scale;
+}
+
+// ------------------------------------------------------------- planning
+__global__ void k_fill_i32(int32_t *a, int n, int32_t v) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) a[i] = v;
+}
+
+__global__ void k_plan_count(const int32_t *__restrict__ probe_ids, int npairs, int nlist,
+                             int32_t *__restrict__ counts) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= npairs) return;
+  const int L = probe_ids[i];
+  if (L >= 0 && L < nlist) atomicAdd(&counts[L], 1);
+}
+
+__global__ void k_plan_prefix(const int32_t *__restrict__ probe_ids, int Q, int nprobe, int nlist,
+                              const int32_t *__restrict__ sizes, int max_list,
+                              int32_t *__restrict__ prefix, int32_t *__restrict__ totals) {
+  const int q = blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= Q) return;
+  int run = 0;
+  for (int p = 0; p < nprobe; ++p) {
+    const int L = probe_ids[int64_t(q) * nprobe + p];
+    prefix[int64_t(q) * nprobe + p] = run;
+    if (L >= 0 && L < nlist) run += max(0, min(sizes[L], max_list));
+  }
+  totals[q] = run;
+}
+
+// Single workgroup: exclusive scans over lists of the pair counts and of the
+// work-item counts (groups of <= 8 queries x chunks of candidates).
+__global__ void __launch_bounds__(1024) k_plan_lists(const int32_t *__restrict__ counts,
+                                                     const int32_t *__restrict__ sizes, int nlist,
+                                                     int max_list,
+                                                     int32_t *__restrict__ pair_off,
+                                                     int32_t *__restrict__ item_off,
+                                                     int32_t *__restrict__ cursor) {
+  __shared__ int32_t s_pairs[1024], s_items[1024];
+  __shared__ int32_t carry[2];
+  const int t = threadIdx.x;
+  if (t == 0) carry[0] = carry[1] = 0;
+  __syncthreads();
+  for (int base = 0; base < nlist; base += 1024) {
+    const int L = base + t;
+    int cp = 0, ci = 0;
+    if (L < nlist) {
+      cp = counts[L];
+      const int sz = max(0, min(sizes[L], max_list));
+      ci = (cp > 0 && sz > 0) ? ((cp + kGroupQ - 1) / kGroupQ) * ((sz + kChunkCands - 1) / kChunkCands) : 0;
+      cursor[L] = 0;
+    }
+    s_pairs[t] = cp;
+    s_items[t] = ci;
+    __syncthreads();
+    for (int off = 1; off < 1024; off <<= 1) {  // Hillis-Steele inclusive scan
+      const int a = (t >= off) ? s_pairs[t - off] : 0;
+      const int b = (t >= off) ? s_items[t - off] : 0;
+      __syncthreads();
+      s_pairs[t] += a;
+      s_items[t] += b;
+      __syncthreads();
+    }
+    if (L < nlist) {
+      pair_off[L] = carry[0] + s_pairs[t] - cp;
+      item_off[L] = carry[1] + s_items[t] - ci;
+    }
+    __syncthreads();
+    if (t == 1023) {
+      carry[0] += s_pairs[1023];
+      carry[1] += s_items[1023];
+    }
+    __syncthreads();
+  }
+  if (t == 0) {
+    pair_off[nlist] = carry[0];
+    item_off[nlist] = carry[1];
+  }
+}
+
+__global__ void k_plan_fill(const int32_t *__restrict__ probe_ids, int npairs, int nlist,
+                            const int32_t *__restrict__ pair_off, int32_t *__restrict__ cursor,
+                            int32_t *__restrict__ pairs) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= npairs) return;
+  const int L = probe_ids[i];
+  if (L < 0 || L >= nlist) return;
+  const int pos = atomicAdd(&cursor[L], 1);
+  pairs[pair_off[L] + pos] = i;
+}
+
+// ------------------------------------------------------------- scan kernel
+struct ScanArgs {
+  const int64_t *list_offsets;
+  const int32_t *list_sizes;
+  const uint8_t *codes;
+  const uint32_t *scales;
+  const uint32_t *dtab;       // compact decode table
+  const _Float16 *qh, *ql;
+  const float *qinv;
+  const float *probe_dots;
+  const int32_t *counts, *pair_off, *item_off, *pairs, *prefix;
+  float *scores;
+  int64_t stride;
+  int nlist, nprobe, d_pad, n_chunks, tile_bytes, lane_units, max_list;
+};
+
+template <int BITS> struct DecodeTab {
+  static constexpr int kEntries = BITS == 4 ? 256 : BITS == 3 ? 64 : 16;
+  static constexpr int kWords = BITS == 1 ? 2 : 1;
+};
+
+__device__ __forceinline__ uint32_t lds_word(const uint32_t *tab, uint32_t byte_addr) {
+  return *reinterpret_cast<const uint32_t *>(reinterpret_cast<const char *>(tab) + byte_addr);
+}
+__device__ __forceinline__ uint2 lds_dword2(const uint32_t *tab, uint32_t byte_addr) {
+  return *reinterpret_cast<const uint2 *>(reinterpret_cast<const char *>(tab) + byte_addr);
+}
+
+// Bits of chunk c (8 coordinates of this lane) from the lane's stream words.
+template <int BITS>
+__device__ __forceinline__ uint32_t chunk_bits(const uint32_t *sw, int c) {
+  if (BITS == 4) return sw[c];
+  if (BITS == 2) return (sw[c >> 1] >> (16 * (c & 1))) & 0xffffu;
+  if (BITS == 1) return (sw[c >> 2] >> (8 * (c & 3))) & 0xffu;
+  // BITS == 3: 24 bits at bit offset 24 c
+  const int bo = 24 * c;
+  const int wi = bo >> 5, sh = bo & 31;
+  uint64_t v = sw[wi];
+  if (sh > 8) v |= uint64_t(sw[wi + 1]) << 32;
+  return uint32_t(v >> sh) & 0xffffffu;
+}
+
+template <int BITS>
+__device__ __forceinline__ half8 decode8(const uint32_t *tab, uint32_t bits, uint32_t lane4) {
+  union {
+    uint32_t u[4];
+    half8 h;
+  } r;
+  if (BITS == 4) {
+    // symbol = byte i; LDS byte address = byte * 256 + lane * 4 (one v_perm)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      r.u[i] = lds_word(tab, __builtin_amdgcn_perm(bits, lane4, 0x0c0c0400u | ((4u + i) << 8)));
+  } else if (BITS == 2) {
+    const uint32_t t = bits & 0x0f0fu, u = (bits >> 4) & 0x0f0fu;
+    r.u[0] = lds_word(tab, __builtin_amdgcn_perm(t, lane4, 0x0c0c0400u));
+    r.u[1] = lds_word(tab, __builtin_amdgcn_perm(u, lane4, 0x0c0c0400u));
+    r.u[2] = lds_word(tab, __builtin_amdgcn_perm(t, lane4, 0x0c0c0500u));
+    r.u[3] = lds_word(tab, __builtin_amdgcn_perm(u, lane4, 0x0c0c0500u));
+  } else if (BITS == 1) {
+    const uint32_t a0 = __builtin_amdgcn_perm(bits & 0xfu, lane4, 0x0c0c0400u) << 1;
+    const uint32_t a1 = __builtin_amdgcn_perm(bits >> 4, lane4, 0x0c0c0400u) << 1;
+    const uint2 e0 = lds_dword2(tab, a0), e1 = lds_dword2(tab, a1);
+    r.u[0] = e0.x;
+    r.u[1] = e0.y;
+    r.u[2] = e1.x;
+    r.u[3] = e1.y;
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t sym = (bits >> (6 * i)) & 63u;
+      r.u[i] = lds_word(tab, (sym << 8) | lane4);
+    }
+  }
+  return r.h;
+}
+
+template <int BITS, int NC>
+__global__ void __launch_bounds__(kScanThreads) k_scan(ScanArgs a) {
+  using T = DecodeTab<BITS>;
+  __shared__ uint32_t dtab[T::kEntries * 64 * T::kWords];
+  constexpr int kWordsPerLane = ((NC * BITS + 15) / 16) * 4;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int nwaves = kScanThreads / 64;
+  const uint32_t lane4 = uint32_t(lane) * 4u;
+
+  // replicate the compact table once per lane: entry e of lane l at
+  // word (e * 64 + l) * kWords
+  for (int idx = tid; idx < T::kEntries * 64; idx += kScanThreads) {
+    const int e = idx >> 6;
+#pragma unroll
+    for (int w = 0; w < T::kWords; ++w) dtab[idx * T::kWords + w] = a.dtab[e * T::kWords + w];
+  }
+  __syncthreads();
+
+  const int n_items = a.item_off[a.nlist];
+  const int m = lane & 15;           // A row / B column of this lane
+  const int kq = lane >> 4;          // k-quarter: coordinates 8 kq .. 8 kq + 7 of a chunk
+  for (int item = blockIdx.x; item < n_items; item += gridDim.x) {
+    // list of this item: last L with item_off[L] <= item
+    int lo = 0, hi = a.nlist;
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (a.item_off[mid] <= item) lo = mid;
+      else hi = mid;
+    }
+    const int L = lo;
+    const int local = item - a.item_off[L];
+    const int size = max(0, min(a.list_sizes[L], a.max_list));
+    const int nch = (size + kChunkCands - 1) / kChunkCands;
+    const int gi = local / nch;
+    const int ci = local - gi * nch;
+    const int npair = a.counts[L];
+    const int G = min(kGroupQ, npair - gi * kGroupQ);
+    const int cand0 = ci * kChunkCands;
+    const int cand1 = min(size, cand0 + kChunkCands);
+    const int pbase = a.pair_off[L] + gi * kGroupQ;
+
+    // A operands: row m = 2 * slot + part (part 0 = hi, 1 = lo)
+    half8 av[NC];
+    {
+      const int slot = m >> 1;
+      if (slot < G) {
+        const int pr = a.pairs[pbase + slot];
+        const int q = pr / a.nprobe;
+        const _Float16 *src = ((m & 1) ? a.ql : a.qh) + int64_t(q) * a.d_pad + 8 * kq;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+          if (c < a.n_chunks) av[c] = *reinterpret_cast<const half8 *>(src + 32 * c);
+          else av[c] = half8{};
+        }
+      } else {
+#pragma unroll
+        for (int c = 0; c < NC; ++c) av[c] = half8{};
+      }
+    }
+    // epilogue parameters of the two query slots this lane outputs
+    float qc[2], qi[2];
+    int64_t obase[2];
+    bool ok[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int slot = 2 * kq + i;
+      ok[i] = slot < G;
+      qc[i] = 0.f;
+      qi[i] = 0.f;
+      obase[i] = 0;
+      if (ok[i]) {
+        const int pr = a.pairs[pbase + slot];
+        const int q = pr / a.nprobe;
+        qc[i] = a.probe_dots[pr];
+        qi[i] = a.qinv[q];
+        obase[i] = int64_t(q) * a.stride + a.prefix[pr];
+      }
+    }
+    const int64_t rec_base = a.list_offsets[L];
+    for (int t = cand0 / 16 + wave; t * 16 < cand1; t += nwaves) {
+      const int64_t rec0 = rec_base + int64_t(t) * 16;
+      const uint8_t *tp = a.codes + (rec0 >> 4) * a.tile_bytes + lane * 16;
+      uint32_t sw[kWordsPerLane];
+#pragma unroll
+      for (int u = 0; u < kWordsPerLane / 4; ++u) {
+        // units beyond this plan's lane stream belong to the next tile
+        const uint4 v = (u < a.lane_units) ? *reinterpret_cast<const uint4 *>(tp + u * 1024)
+                                           : uint4{0u, 0u, 0u, 0u};
+        sw[4 * u + 0] = v.x;
+        sw[4 * u + 1] = v.y;
+        sw[4 * u + 2] = v.z;
+        sw[4 * u + 3] = v.w;
+      }
+      floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        if (c < a.n_chunks) {
+          const half8 bv = decode8<BITS>(dtab, chunk_bits<BITS>(sw, c), lane4);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(av[c], bv, acc, 0, 0, 0);
+        }
+      }
+      // lane holds rows 4 kq + {0,1,2,3} of column m: slots 2 kq (hi, lo), 2 kq + 1 (hi, lo)
+      const int cand = t * 16 + m;
+      if (cand < cand1) {
+        const uint32_t sc = a.scales[rec0 + m];
+        const float sh = dec_ue7m9(sc & 0xffffu);
+        const float gh = dec_ue4m12(sc >> 16);
+        if (ok[0]) a.scores[obase[0] + cand] = gh * (qc[0] + sh * ((acc[0] + acc[1]) * qi[0]));
+        if (ok[1]) a.scores[obase[1] + cand] = gh * (qc[1] + sh * ((acc[2] + acc[3]) * qi[1]));
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------- top-k
+struct ScanId {
+  const int32_t *prefix;       // nprobe entries of this query
+  const int32_t *probe_ids;    // nprobe entries of this query
+  const int64_t *list_offsets;
+  const int32_t *ids;
+  int nprobe;
+  __device__ int32_t operator()(int i) const {
+    int lo = 0, hi = nprobe;  // last p with prefix[p] <= i
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (prefix[mid] <= i) lo = mid;
+      else hi = mid;
+    }
+    const int L = probe_ids[lo];
+    return ids[list_offsets[L] + (i - prefix[lo])];
+  }
+};
+
+__global__ void __launch_bounds__(kSelThreads) k_scan_topk(
+    const float *__restrict__ scores, int64_t stride, const int32_t *__restrict__ totals,
+    const int32_t *__restrict__ prefix, const int32_t *__restrict__ probe_ids, int nprobe,
+    const int64_t *__restrict__ list_offsets, const int32_t *__restrict__ ids, int k,
+    float *__restrict__ out_s, int32_t *__restrict__ out_i) {
+  __shared__ SelectSmem sm;
+  const int q = blockIdx.x;
+  ScanId f{prefix + int64_t(q) * nprobe, probe_ids + int64_t(q) * nprobe, list_offsets, ids, nprobe};
+  block_topk(scores + int64_t(q) * stride, totals[q], k, f, out_s + int64_t(q) * k,
+             out_i + int64_t(q) * k, sm);
+}
+
+// Profiling hook: events recorded around the scan kernel (0) and the top-k
+// kernel (1) of later rslm_scan_topk calls.
+static void *g_timer[2][2] = {{nullptr, nullptr}, {nullptr, nullptr}};
+
+static int record_timer(int which, int end, hipStream_t s) {
+  void *ev = g_timer[which][end];
+  if (!ev) return RSLM_OK;
+  hipError_t e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev), s);
+  return e == hipSuccess ? RSLM_OK : set_hip_error(e);
+}
+
+static int cu_count() {
+  static int cached[64] = {0};
+  int dev = 0;
+  (void)hipGetDevice(&dev);
+  if (dev < 0 || dev >= 64) return 256;
+  if (!cached[dev]) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
+
+template <int BITS>
+static void launch_scan_bits(int nc, dim3 grid, hipStream_t s, const ScanArgs &a) {
+  if (nc <= 4) hipLaunchKernelGGL((k_scan<BITS, 4>), grid, dim3(kScanThreads), 0, s, a);
+  else if (nc <= 8) hipLaunchKernelGGL((k_scan<BITS, 8>), grid, dim3(kScanThreads), 0, s, a);
+  else if (nc <= 16) hipLaunchKernelGGL((k_scan<BITS, 16>), grid, dim3(kScanThreads), 0, s, a);
+  else if (nc <= 24) hipLaunchKernelGGL((k_scan<BITS, 24>), grid, dim3(kScanThreads), 0, s, a);
+  else hipLaunchKernelGGL((k_scan<BITS, 32>), grid, dim3(kScanThreads), 0, s, a);
+}
+
+}  // namespace rslm
+
+using namespace rslm;
+
+extern "C" {
+
+size_t rslm_scan_topk_workspace(const rslm_plan *p, const rslm_index *idx, int32_t Q,
+                                int32_t nprobe, int32_t k) {
+  (void)k;
+  if (!p || !idx || Q < 0 || nprobe < 1 || idx->nlist < 1 || idx->max_list_size < 0) return 0;
+  return scan_ws_layout(nullptr, Q, nprobe, idx->nlist, p->codec.d_pad, idx->max_list_size).bytes;
+}
+
+int rslm_scan_topk(const rslm_plan *p, const rslm_index *idx, const float *q_rot, int32_t Q,
+                   const int32_t *probe_ids, const float *probe_dots, int32_t nprobe, int32_t k,
+                   float *out_scores, int32_t *out_ids, void *ws, size_t ws_bytes,
+                   void *stream) {
+  if (!p || !idx || Q < 0 || nprobe < 1 || nprobe > kMaxNprobe || k < 1 || k > kMaxK)
+    return RSLM_ERR_INVALID_ARG;
+  if (idx->nlist < 1 || idx->nlist > 65536 || nprobe > idx->nlist || idx->max_list_size < 0)
+    return RSLM_ERR_INVALID_ARG;
+  if (int64_t(nprobe) * idx->max_list_size >= (int64_t(1) << 31)) return RSLM_ERR_INVALID_ARG;
+  if (Q == 0) return RSLM_OK;
+  if (!q_rot || !probe_ids || !probe_dots || !out_scores || !out_ids || !idx->list_offsets ||
+      !idx->list_sizes || !idx->ids || !idx->codes || !idx->scales)
+    return RSLM_ERR_INVALID_ARG;
+  if (p->codec.n_chunks > 32) return RSLM_ERR_UNSUPPORTED;   // D > 1024
+  const size_t need = rslm_scan_topk_workspace(p, idx, Q, nprobe, k);
+  if (!ws || ws_bytes < need) return RSLM_ERR_WORKSPACE;
+  const int nlist = idx->nlist;
+  const int d_pad = p->codec.d_pad;
+  ScanWs w = scan_ws_layout(ws, Q, nprobe, nlist, d_pad, idx->max_list_size);
+  hipStream_t s = as_stream(stream);
+  const int npairs = Q * nprobe;
+  int st;
+  hipLaunchKernelGGL(k_prep_queries, dim3((Q + 3) / 4), dim3(256), 0, s, q_rot, Q, p->rot.D, d_pad,
+                     w.qh, w.ql, w.qinv);
+  if ((st = check_launch())) return st;
+  hipLaunchKernelGGL(k_fill_i32, dim3((nlist + 255) / 256), dim3(256), 0, s, w.counts, nlist, 0);
+  if ((st = check_launch())) return st;
+  hipLaunchKernelGGL(k_plan_count, dim3((npairs + 255) / 256), dim3(256), 0, s, probe_ids, npairs,
+                     nlist, w.counts);
+  if ((st = check_launch())) return st;
+  hipLaunchKernelGGL(k_plan_prefix, dim3((Q + 255) / 256), dim3(256), 0, s, probe_ids, Q, nprobe,
+                     nlist, idx->list_sizes, idx->max_list_size, w.prefix, w.totals);
+  if ((st = check_launch())) return st;
+  hipLaunchKernelGGL(k_plan_lists, dim3(1), dim3(1024), 0, s, w.counts, idx->list_sizes, nlist,
+                     idx->max_list_size, w.pair_off, w.item_off, w.cursor);
+  if ((st = check_launch())) return st;
+  hipLaunchKernelGGL(k_plan_fill, dim3((npairs + 255) / 256), dim3(256), 0, s, probe_ids, npairs,
+                     nlist, w.pair_off, w.cursor, w.pairs);
+  if ((st = check_launch())) return st;
+
+  ScanArgs a;
+  a.list_offsets = idx->list_offsets;
+  a.list_sizes = idx->list_sizes;
+  a.codes = idx->codes;
+  a.scales = idx->scales;
+  a.dtab = p->d_dtab;
+  a.qh = w.qh;
+  a.ql = w.ql;
+  a.qinv = w.qinv;
+  a.probe_dots = probe_dots;
+  a.counts = w.counts;
+  a.pair_off = w.pair_off;
+  a.item_off = w.item_off;
+  a.pairs = w.pairs;
+  a.prefix = w.prefix;
+  a.scores = w.scores;
+  a.stride = w.stride;
+  a.nlist = nlist;
+  a.nprobe = nprobe;
+  a.d_pad = d_pad;
+  a.n_chunks = p->codec.n_chunks;
+  a.tile_bytes = p->codec.tile_bytes;
+  a.lane_units = p->codec.lane_bytes / 16;
+  a.max_list = idx->max_list_size;
+  const int wg_per_cu = (p->codec.bits == 4) ? 2 : 4;
+  const dim3 grid(unsigned(cu_count() * wg_per_cu));
+  if ((st = record_timer(0, 0, s))) return st;
+  switch (p->codec.bits) {
+    case 4: launch_scan_bits<4>(a.n_chunks, grid, s, a); break;
+    case 3: launch_scan_bits<3>(a.n_chunks, grid, s, a); break;
+    case 2: launch_scan_bits<2>(a.n_chunks, grid, s, a); break;
+    default: launch_scan_bits<1>(a.n_chunks, grid, s, a); break;
+  }
+  if ((st = check_launch())) return st;
+  if ((st = record_timer(0, 1, s))) return st;
+  if ((st = record_timer(1, 0, s))) return st;
+  hipLaunchKernelGGL(k_scan_topk, dim3(unsigned(Q)), dim3(kSelThreads), 0, s, w.scores, w.stride,
+                     w.totals, w.prefix, probe_ids, nprobe, idx->list_offsets, idx->ids, k,
+                     out_scores, out_ids);
+  if ((st = check_launch())) return st;
+  return record_timer(1, 1, s);
+}
+
+int rslm_set_timer(int which, void *ev_begin, void *ev_end) {
+  if (which < 0 || which > 1 || (!ev_begin) != (!ev_end)) return RSLM_ERR_INVALID_ARG;
+  g_timer[which][0] = ev_begin;
+  g_timer[which][1] = ev_end;
+  return RSLM_OK;
+}
+
+}  // extern "C"

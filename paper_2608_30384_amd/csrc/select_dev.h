@@ -1,0 +1,201 @@
+// Block-wide exact top-k of a float array in global memory, ordered by
+// (value desc, id asc), with ids produced on demand by a functor (so ids are
+// only looked up for survivors).
+//
+// Method: MSB radix select on order-preserving 32-bit keys.  Each pass
+// histograms the next digit of the keys that still share the boundary
+// prefix; as soon as the elements at or above the boundary bin fit in the
+// LDS buffer they are collected with their ids and bitonic-sorted on the
+// 64-bit composite (key << 32 | ~id).  If more than the buffer's capacity
+// share one exact key, the smallest ids among them are chosen by a second
+// radix select over the ids.  Every pass is a full read of the array.
+#pragma once
+
+#include "rslm_internal.h"
+
+namespace rslm {
+
+constexpr int kSelCap = 4096;       // LDS sort buffer entries
+constexpr int kSelThreads = 1024;
+
+struct SelectSmem {
+  uint32_t hist[4096];
+  uint64_t buf[kSelCap];
+  uint32_t bcast[8];
+  uint32_t count;
+};
+
+// Find, in hist[0..nb), the highest bin bb with above + sum(hist[bb..]) >= k.
+// Writes bb and the count strictly above it (plus `above`) to sm.bcast[0..1].
+__device__ __forceinline__ void find_boundary(SelectSmem &sm, int nb, uint32_t above, uint32_t k) {
+  __syncthreads();
+  if (threadIdx.x < 64) {
+    const int lane = threadIdx.x;
+    const int per = nb / 64;
+    // lane 0 owns the highest bins
+    const int hi = nb - lane * per;  // bins [hi - per, hi)
+    uint32_t s = 0;
+    for (int b = hi - per; b < hi; ++b) s += sm.hist[b];
+    // inclusive prefix over lanes (from the top)
+    uint32_t incl = s;
+    for (int off = 1; off < 64; off <<= 1) {
+      uint32_t t = __shfl_up(incl, off, 64);
+      if (lane >= off) incl += t;
+    }
+    const uint32_t excl = incl - s;
+    const bool crosses = (above + excl < k) && (above + incl >= k);
+    const uint64_t mask = __ballot(crosses);
+    int owner = mask ? __ffsll((unsigned long long)mask) - 1 : 63;
+    if (lane == owner) {
+      uint32_t acc = above + excl;
+      int bb = hi - per;
+      for (int b = hi - 1; b >= hi - per; --b) {
+        if (acc + sm.hist[b] >= k) {
+          bb = b;
+          break;
+        }
+        acc += sm.hist[b];
+      }
+      sm.bcast[0] = uint32_t(bb);
+      sm.bcast[1] = acc;  // count strictly above bin bb
+    }
+  }
+  __syncthreads();
+}
+
+// Bitonic sort of sm.buf[0..n) descending; n <= kSelCap.
+__device__ __forceinline__ void sort_desc(SelectSmem &sm, int n) {
+  int p2 = 1;
+  while (p2 < n) p2 <<= 1;
+  for (int i = n + threadIdx.x; i < p2; i += blockDim.x) sm.buf[i] = 0ull;
+  __syncthreads();
+  for (int size = 2; size <= p2; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int i = threadIdx.x; i < p2 / 2; i += blockDim.x) {
+        const int lo = 2 * i - (i & (stride - 1));
+        const int hi = lo + stride;
+        const bool desc = ((lo & size) == 0);
+        const uint64_t a = sm.buf[lo], b = sm.buf[hi];
+        if ((a < b) == desc) {
+          sm.buf[lo] = b;
+          sm.buf[hi] = a;
+        }
+      }
+      __syncthreads();
+    }
+  }
+}
+
+__device__ __forceinline__ uint64_t composite(uint32_t key, int32_t id) {
+  return (uint64_t(key) << 32) | uint64_t(0xffffffffu - uint32_t(id));
+}
+
+template <class IdFn>
+__device__ void block_topk(const float *__restrict__ vals, int n, int k, IdFn idfn,
+                           float *__restrict__ out_s, int32_t *__restrict__ out_i,
+                           SelectSmem &sm) {
+  const int tid = threadIdx.x, nt = blockDim.x;
+  uint32_t lo_key = 0;         // collect keys >= lo_key (when not tie mode)
+  bool tie_mode = false;
+  uint32_t tie_key = 0, id_limit = 0;
+  if (n > kSelCap) {
+    uint32_t prefix = 0, above = 0;
+    int pbits = 0;
+    const int digits[3] = {12, 12, 8};
+    bool fits = false;
+    for (int di = 0; di < 3 && !fits; ++di) {
+      const int d = digits[di];
+      const int nb = 1 << d;
+      const int shift = 32 - pbits - d;
+      for (int b = tid; b < nb; b += nt) sm.hist[b] = 0;
+      __syncthreads();
+      for (int i = tid; i < n; i += nt) {
+        const uint32_t key = order_key(vals[i]);
+        if (pbits == 0 || (key >> (32 - pbits)) == prefix)
+          atomicAdd(&sm.hist[(key >> shift) & (nb - 1)], 1u);
+      }
+      find_boundary(sm, nb, above, uint32_t(k));
+      const uint32_t bb = sm.bcast[0];
+      const uint32_t cnt_b = sm.hist[bb];
+      above = sm.bcast[1];
+      prefix = (prefix << d) | bb;
+      pbits += d;
+      if (above + cnt_b <= uint32_t(kSelCap)) fits = true;
+      __syncthreads();
+    }
+    if (fits) {
+      lo_key = prefix << (32 - pbits);
+    } else {
+      // > capacity elements share the exact key `prefix`: pick the smallest
+      // ids among them by a radix select over the 31-bit id.
+      tie_mode = true;
+      tie_key = prefix;
+      const uint32_t need = uint32_t(k) - above;
+      uint32_t ip = 0, iabove = 0;   // here "above" counts smaller ids
+      int ibits = 1;                 // ids are < 2^31: top bit is 0
+      const int idig[3] = {11, 10, 10};
+      for (int di = 0; di < 3; ++di) {
+        const int d = idig[di];
+        const int nb = 1 << d;
+        const int shift = 32 - ibits - d;
+        for (int b = tid; b < nb; b += nt) sm.hist[b] = 0;
+        __syncthreads();
+        for (int i = tid; i < n; i += nt) {
+          if (order_key(vals[i]) != tie_key) continue;
+          const uint32_t id = uint32_t(idfn(i));
+          // reverse the order so that "highest bin" means smallest id
+          const uint32_t rid = 0x7fffffffu - id;
+          if ((rid >> (32 - ibits)) == ip) atomicAdd(&sm.hist[(rid >> shift) & (nb - 1)], 1u);
+        }
+        find_boundary(sm, nb, iabove, need);
+        const uint32_t bb = sm.bcast[0];
+        iabove = sm.bcast[1];
+        ip = (ip << d) | bb;
+        ibits += d;
+        __syncthreads();
+      }
+      id_limit = 0x7fffffffu - ip;   // collect ties with id <= id_limit
+    }
+  }
+  // collect
+  if (tid == 0) sm.count = 0;
+  __syncthreads();
+  for (int i = tid; i < n; i += nt) {
+    const uint32_t key = order_key(vals[i]);
+    bool take;
+    int32_t id = 0;
+    if (n <= kSelCap) {
+      take = true;
+    } else if (!tie_mode) {
+      take = key >= lo_key;
+    } else if (key > tie_key) {
+      take = true;
+    } else if (key == tie_key) {
+      id = idfn(i);
+      take = uint32_t(id) <= id_limit;
+    } else {
+      take = false;
+    }
+    if (take) {
+      if (!(tie_mode && key == tie_key)) id = idfn(i);
+      const uint32_t pos = atomicAdd(&sm.count, 1u);
+      if (pos < uint32_t(kSelCap)) sm.buf[pos] = composite(key, id);
+    }
+  }
+  __syncthreads();
+  int cnt = int(sm.count);
+  if (cnt > kSelCap) cnt = kSelCap;  // cannot happen: the selection above bounds it
+  sort_desc(sm, cnt);
+  for (int j = tid; j < k; j += nt) {
+    if (j < cnt) {
+      const uint64_t c = sm.buf[j];
+      out_s[j] = key_to_float(uint32_t(c >> 32));
+      out_i[j] = int32_t(0xffffffffu - uint32_t(c & 0xffffffffu));
+    } else {
+      out_s[j] = -__builtin_inff();
+      out_i[j] = -1;
+    }
+  }
+}
+
+}  // namespace rslm

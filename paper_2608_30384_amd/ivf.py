@@ -1,0 +1,82 @@
+"""IVF index construction around the librslm kernels.
+
+Build-time bookkeeping (partition training, the record layout of the
+inverted lists) uses torch tensor operations for counting, sorting and
+means; every step of the codec itself (assignment, rotation, encoding, SQ8)
+runs in librslm.  The paper's partitioning (Section "End-to-End
+Comparison", Setup) is Euclidean k-means with random initialisation on a
+sample of about 256 points per centre.
+"""
+
+import torch
+
+from . import _lib as L
+from .api import Index, ivf_assign_probe, rslm_encode, rslm_fwht, rslm_sq8_encode, rslm_sq8_fit
+
+
+def kmeans(x, nlist, iters=10, seed=0, sample=None):
+    """Euclidean k-means on device; assignment by ``ivf_assign_probe``."""
+    n = x.shape[0]
+    gen = torch.Generator(device=x.device)
+    gen.manual_seed(int(seed))
+    if sample is not None and sample < n:
+        xs = x[torch.randperm(n, generator=gen, device=x.device)[:sample]].contiguous()
+    else:
+        xs = x
+    c = xs[torch.randperm(xs.shape[0], generator=gen, device=x.device)[:nlist]].clone()
+    for _ in range(iters):
+        a, _ = ivf_assign_probe(xs, c, 1, L.IVF_ASSIGN_L2)
+        a = a.long()
+        sums = torch.zeros_like(c).index_add_(0, a, xs)
+        cnt = torch.bincount(a, minlength=nlist).to(c.dtype)
+        nz = cnt > 0
+        c[nz] = sums[nz] / cnt[nz, None]
+    return c.contiguous()
+
+
+def layout(assign, nlist, tile=16):
+    """Inverted-list record layout: lists padded to whole tiles of 16.
+
+    Returns (list_offsets int64, list_sizes int32, src_row int64 per record
+    (-1 = padding), rec_list int32 per record, ids int32 per record, total).
+    Within a list, vectors keep their original order.
+    """
+    a = assign.long()
+    n = a.numel()
+    dev = a.device
+    counts = torch.bincount(a, minlength=nlist)
+    padded = (counts + tile - 1) // tile * tile
+    offsets = torch.cumsum(padded, 0) - padded
+    total = int(padded.sum().item())
+    order = torch.argsort(a, stable=True)
+    sl = a[order]
+    starts = torch.cumsum(counts, 0) - counts
+    rank = torch.arange(n, device=dev) - starts[sl]
+    rec = offsets[sl] + rank
+    src_row = torch.full((total,), -1, dtype=torch.int64, device=dev)
+    src_row[rec] = order
+    rec_list = torch.repeat_interleave(torch.arange(nlist, device=dev, dtype=torch.int32), padded)
+    ids = torch.full((total,), -1, dtype=torch.int32, device=dev)
+    ids[rec] = order.to(torch.int32)
+    return offsets, counts.to(torch.int32), src_row, rec_list.contiguous(), ids, total
+
+
+def build_index(plan, x, centroids, assign=None, resid_rot=None):
+    """Assign, lay out and encode a collection; returns (Index, R c, assign)."""
+    nlist = centroids.shape[0]
+    if assign is None:
+        assign, _ = ivf_assign_probe(x, centroids, 1, L.IVF_ASSIGN_L2)
+    cen_rot = rslm_fwht(plan, centroids)
+    offsets, sizes, src_row, rec_list, ids, total = layout(assign, nlist)
+    codes = torch.zeros(plan.code_bytes(total), dtype=torch.uint8, device=x.device)
+    scales = torch.zeros(total, dtype=torch.int32, device=x.device)
+    rslm_encode(plan, x, codes, scales, n_records=total, src_row=src_row, rec_list=rec_list,
+                centroids=centroids, centroids_rot=cen_rot, resid_rot=resid_rot)
+    return Index(offsets, sizes, ids, codes, scales), cen_rot, assign
+
+
+def build_sq8(resid_rot):
+    """SQ8 rescoring codes of the rotated second residuals (row = vector id)."""
+    lo, hi = rslm_sq8_fit(resid_rot)
+    codes2 = rslm_sq8_encode(resid_rot, lo, hi)
+    return codes2, lo, hi
