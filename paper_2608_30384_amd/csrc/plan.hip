@@ -129,8 +129,21 @@ int rslm_plan_create(const rslm_plan_desc *d, rslm_plan **out) {
   c.g = g;
   c.w = (K == 16) ? 4 : 3;
   c.n_sub = (D + g - 1) / g;
-  c.d_pad = (D + 31) / 32 * 32;
-  c.n_chunks = c.d_pad / 32;
+  // The scan kernel is instantiated for these chunk counts (32 coordinates
+  // each); the padded dimension is rounded up to the next one so that the
+  // kernel's chunk loop is fully static.  Padding coordinates carry code 0
+  // and meet zero query coordinates.
+  {
+    static const int kInst[] = {1, 2, 3, 4, 6, 8, 12, 16, 24, 32};
+    int nc = (D + 31) / 32;
+    for (int v : kInst)
+      if (v >= nc) {
+        nc = v;
+        break;
+      }
+    c.n_chunks = nc;
+    c.d_pad = nc * 32;
+  }
   c.lane_bytes = (c.n_chunks * bits + 15) / 16 * 16;
   c.tile_bytes = 64 * c.lane_bytes;
   c.canon_bytes = (c.n_sub * c.w + 7) / 8;

@@ -266,6 +266,54 @@ __device__ __forceinline__ half8 decode8(const uint32_t *tab, uint32_t bits, uin
   return r.h;
 }
 
+template <int W>
+__device__ __forceinline__ void load_tile(uint32_t (&sw)[W], const ScanArgs &a, int64_t rec_base,
+                                          int t, int lane) {
+  const int64_t rec0 = rec_base + int64_t(t) * 16;
+  const uint8_t *tp = a.codes + (rec0 >> 4) * a.tile_bytes + lane * 16;
+#pragma unroll
+  for (int u = 0; u < W / 4; ++u) {
+    const uint4 v = *reinterpret_cast<const uint4 *>(tp + u * 1024);
+    sw[4 * u + 0] = v.x;
+    sw[4 * u + 1] = v.y;
+    sw[4 * u + 2] = v.z;
+    sw[4 * u + 3] = v.w;
+  }
+}
+
+// Decode one tile (16 candidates) and multiply it with the item's queries;
+// lane (kq, m) ends with rows 4 kq + {0,1,2,3} of candidate column m, i.e.
+// query slots 2 kq (hi, lo) and 2 kq + 1 (hi, lo).
+template <int BITS, int NC, int W>
+__device__ __forceinline__ void score_tile(const uint32_t (&sw)[W], const half8 (&av)[NC],
+                                           const uint32_t *dtab, uint32_t lane4,
+                                           const ScanArgs &a, int64_t rec_base, int t, int cand1,
+                                           int m, const bool (&ok)[2], const float (&qc)[2],
+                                           const float (&qi)[2], const int64_t (&obase)[2]) {
+  // Decoding runs two chunks ahead of the matrix multiply so that the LDS
+  // latency of chunk c + 2 overlaps the MFMAs of chunks c and c + 1; even and
+  // odd chunks accumulate separately to halve the dependent MFMA chain.
+  floatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+  half8 b[3];
+  b[0] = decode8<BITS>(dtab, chunk_bits<BITS>(sw, 0), lane4);
+  if (NC > 1) b[1] = decode8<BITS>(dtab, chunk_bits<BITS>(sw, NC > 1 ? 1 : 0), lane4);
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    if (c + 2 < NC) b[(c + 2) % 3] = decode8<BITS>(dtab, chunk_bits<BITS>(sw, c + 2 < NC ? c + 2 : 0), lane4);
+    if (c & 1) acc1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(av[c], b[c % 3], acc1, 0, 0, 0);
+    else acc0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(av[c], b[c % 3], acc0, 0, 0, 0);
+  }
+  const floatx4 acc = acc0 + acc1;
+  const int cand = t * 16 + m;
+  if (cand < cand1) {
+    const uint32_t sc = a.scales[rec_base + int64_t(t) * 16 + m];
+    const float sh = dec_ue7m9(sc & 0xffffu);
+    const float gh = dec_ue4m12(sc >> 16);
+    if (ok[0]) a.scores[obase[0] + cand] = gh * (qc[0] + sh * ((acc[0] + acc[1]) * qi[0]));
+    if (ok[1]) a.scores[obase[1] + cand] = gh * (qc[1] + sh * ((acc[2] + acc[3]) * qi[1]));
+  }
+}
+
 template <int BITS, int NC>
 __global__ void __launch_bounds__(kScanThreads) k_scan(ScanArgs a) {
   using T = DecodeTab<BITS>;
@@ -318,10 +366,7 @@ __global__ void __launch_bounds__(kScanThreads) k_scan(ScanArgs a) {
         const int q = pr / a.nprobe;
         const _Float16 *src = ((m & 1) ? a.ql : a.qh) + int64_t(q) * a.d_pad + 8 * kq;
 #pragma unroll
-        for (int c = 0; c < NC; ++c) {
-          if (c < a.n_chunks) av[c] = *reinterpret_cast<const half8 *>(src + 32 * c);
-          else av[c] = half8{};
-        }
+        for (int c = 0; c < NC; ++c) av[c] = *reinterpret_cast<const half8 *>(src + 32 * c);
       } else {
 #pragma unroll
         for (int c = 0; c < NC; ++c) av[c] = half8{};
@@ -347,37 +392,21 @@ __global__ void __launch_bounds__(kScanThreads) k_scan(ScanArgs a) {
       }
     }
     const int64_t rec_base = a.list_offsets[L];
-    for (int t = cand0 / 16 + wave; t * 16 < cand1; t += nwaves) {
-      const int64_t rec0 = rec_base + int64_t(t) * 16;
-      const uint8_t *tp = a.codes + (rec0 >> 4) * a.tile_bytes + lane * 16;
-      uint32_t sw[kWordsPerLane];
-#pragma unroll
-      for (int u = 0; u < kWordsPerLane / 4; ++u) {
-        // units beyond this plan's lane stream belong to the next tile
-        const uint4 v = (u < a.lane_units) ? *reinterpret_cast<const uint4 *>(tp + u * 1024)
-                                           : uint4{0u, 0u, 0u, 0u};
-        sw[4 * u + 0] = v.x;
-        sw[4 * u + 1] = v.y;
-        sw[4 * u + 2] = v.z;
-        sw[4 * u + 3] = v.w;
-      }
-      floatx4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int c = 0; c < NC; ++c) {
-        if (c < a.n_chunks) {
-          const half8 bv = decode8<BITS>(dtab, chunk_bits<BITS>(sw, c), lane4);
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(av[c], bv, acc, 0, 0, 0);
-        }
-      }
-      // lane holds rows 4 kq + {0,1,2,3} of column m: slots 2 kq (hi, lo), 2 kq + 1 (hi, lo)
-      const int cand = t * 16 + m;
-      if (cand < cand1) {
-        const uint32_t sc = a.scales[rec0 + m];
-        const float sh = dec_ue7m9(sc & 0xffffu);
-        const float gh = dec_ue4m12(sc >> 16);
-        if (ok[0]) a.scores[obase[0] + cand] = gh * (qc[0] + sh * ((acc[0] + acc[1]) * qi[0]));
-        if (ok[1]) a.scores[obase[1] + cand] = gh * (qc[1] + sh * ((acc[2] + acc[3]) * qi[1]));
-      }
+    const int t_end = (cand1 + 15) / 16;
+    // Software pipeline: the codes of the wave's next tile are in flight
+    // while the current tile is decoded and multiplied.
+    uint32_t bufA[kWordsPerLane], bufB[kWordsPerLane];
+    int t = cand0 / 16 + wave;
+    if (t < t_end) load_tile<kWordsPerLane>(bufA, a, rec_base, t, lane);
+    while (t < t_end) {
+      const int t1 = t + nwaves;
+      if (t1 < t_end) load_tile<kWordsPerLane>(bufB, a, rec_base, t1, lane);
+      score_tile<BITS, NC>(bufA, av, dtab, lane4, a, rec_base, t, cand1, m, ok, qc, qi, obase);
+      if (t1 >= t_end) break;
+      const int t2 = t1 + nwaves;
+      if (t2 < t_end) load_tile<kWordsPerLane>(bufA, a, rec_base, t2, lane);
+      score_tile<BITS, NC>(bufB, av, dtab, lane4, a, rec_base, t1, cand1, m, ok, qc, qi, obase);
+      t = t2;
     }
   }
 }
@@ -440,11 +469,18 @@ static int cu_count() {
 
 template <int BITS>
 static void launch_scan_bits(int nc, dim3 grid, hipStream_t s, const ScanArgs &a) {
-  if (nc <= 4) hipLaunchKernelGGL((k_scan<BITS, 4>), grid, dim3(kScanThreads), 0, s, a);
-  else if (nc <= 8) hipLaunchKernelGGL((k_scan<BITS, 8>), grid, dim3(kScanThreads), 0, s, a);
-  else if (nc <= 16) hipLaunchKernelGGL((k_scan<BITS, 16>), grid, dim3(kScanThreads), 0, s, a);
-  else if (nc <= 24) hipLaunchKernelGGL((k_scan<BITS, 24>), grid, dim3(kScanThreads), 0, s, a);
-  else hipLaunchKernelGGL((k_scan<BITS, 32>), grid, dim3(kScanThreads), 0, s, a);
+  switch (nc) {
+    case 1: hipLaunchKernelGGL((k_scan<BITS, 1>), grid, dim3(kScanThreads), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((k_scan<BITS, 2>), grid, dim3(kScanThreads), 0, s, a); break;
+    case 3: hipLaunchKernelGGL((k_scan<BITS, 3>), grid, dim3(kScanThreads), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((k_scan<BITS, 4>), grid, dim3(kScanThreads), 0, s, a); break;
+    case 6: hipLaunchKernelGGL((k_scan<BITS, 6>), grid, dim3(kScanThreads), 0, s, a); break;
+    case 8: hipLaunchKernelGGL((k_scan<BITS, 8>), grid, dim3(kScanThreads), 0, s, a); break;
+    case 12: hipLaunchKernelGGL((k_scan<BITS, 12>), grid, dim3(kScanThreads), 0, s, a); break;
+    case 16: hipLaunchKernelGGL((k_scan<BITS, 16>), grid, dim3(kScanThreads), 0, s, a); break;
+    case 24: hipLaunchKernelGGL((k_scan<BITS, 24>), grid, dim3(kScanThreads), 0, s, a); break;
+    default: hipLaunchKernelGGL((k_scan<BITS, 32>), grid, dim3(kScanThreads), 0, s, a); break;
+  }
 }
 
 }  // namespace rslm
