@@ -212,6 +212,12 @@ int rslm_plan_create(const rslm_plan_desc *d, rslm_plan **out) {
   }
   r.s1 = p->d_s1;
   r.pi = p->d_pi;
+  for (int w = 0; w < 8; ++w) {
+    uint32_t m = 0;
+    for (int b = 0; b < 32; ++b)
+      if (d->signs[w * 32 + b] < 0) m |= 1u << b;
+    r.s1mask[w] = m;
+  }
   *out = p;
   return RSLM_OK;
 }

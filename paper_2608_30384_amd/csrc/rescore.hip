@@ -7,7 +7,7 @@
 //
 // Rescoring gathers one record per shortlisted candidate (random access, the
 // paper's "LargePool" pattern); a workgroup per query decodes and scores its
-// candidates (lanes across coordinates, one wavefront per candidate) and
+// candidates (16 lanes per candidate, dword loads across coordinates) and
 // sorts them in LDS.
 #include "rslm_internal.h"
 
@@ -94,14 +94,36 @@ __global__ void __launch_bounds__(kRescoreThreads) k_rescore_sq8(
   __syncthreads();
   float qlo = 0.f;
   for (int w = 0; w < kRescoreThreads / 64; ++w) qlo += red[w];
-  for (int j = wave; j < k_in; j += kRescoreThreads / 64) {
-    const int32_t id = cand_i[int64_t(q) * k_in + j];
-    if (id < 0 || id >= n_vec) continue;   // empty slot
-    const uint8_t *cr = codes + int64_t(id) * dim;
+  // 16 lanes per candidate, four candidates per wavefront; lane j of a group
+  // takes dwords j, j + 16, ... of the candidate's codes.
+  __syncthreads();   // qs complete
+  const int grp = lane >> 4, gl = lane & 15;
+  const int ngroups = (kRescoreThreads / 64) * 4;
+  const int nd4 = dim >> 2;
+  for (int j0 = wave * 4; j0 < k_in; j0 += ngroups) {
+    const int j = j0 + grp;
+    int32_t id = -1;
+    if (j < k_in) id = cand_i[int64_t(q) * k_in + j];
+    const bool valid = id >= 0 && id < n_vec;
     float dot = 0.f;
-    for (int d = lane; d < dim; d += 64) dot += qs[d] * float(cr[d]);
-    dot = wave_sum(dot);
-    if (lane == 0) {
+    if (valid) {
+      const uint8_t *cr = codes + int64_t(id) * dim;
+      if ((dim & 3) == 0) {
+        const uint32_t *cw = reinterpret_cast<const uint32_t *>(cr);
+#pragma unroll 4
+        for (int d4 = gl; d4 < nd4; d4 += 16) {
+          const uint32_t w = cw[d4];
+          const float4 qv = *reinterpret_cast<const float4 *>(qs + 4 * d4);
+          dot += qv.x * float(w & 0xffu) + qv.y * float((w >> 8) & 0xffu) +
+                 qv.z * float((w >> 16) & 0xffu) + qv.w * float(w >> 24);
+        }
+      } else {
+        for (int d = gl; d < dim; d += 16) dot += qs[d] * float(cr[d]);
+      }
+    }
+#pragma unroll
+    for (int off = 8; off >= 1; off >>= 1) dot += __shfl_xor(dot, off, 64);
+    if (valid && gl == 0) {
       const float s2 = cand_s[int64_t(q) * k_in + j] + (qlo + dot);
       const uint32_t pos = atomicAdd(&count, 1u);
       buf[pos] = (uint64_t(order_key(s2)) << 32) | uint64_t(0xffffffffu - uint32_t(id));

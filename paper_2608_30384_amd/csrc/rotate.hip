@@ -16,6 +16,20 @@
 
 namespace rslm {
 
+// LDS index of vector element i: one pad word per 32 elements so that the
+// strided butterfly accesses of a round fall into distinct banks.
+__device__ __forceinline__ int px(int i) { return i + (i >> 5); }
+__host__ __device__ constexpr int padded_len(int n) { return n + (n >> 5) + 1; }
+
+// Each wavefront owns its vector, and LDS operations of one wavefront take
+// effect in issue order, so a wavefront-scope fence (a compiler ordering
+// point) is all the synchronisation the rotation needs.
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 template <int R>
 __device__ __forceinline__ void fwht_round(float *v, int off, int nblk, int B, int s,
                                            bool last, float scale, int lane) {
@@ -31,7 +45,7 @@ __device__ __forceinline__ void fwht_round(float *v, int off, int nblk, int B, i
     const int base = off + blk * B + ((high << (s + R)) | low);
     float e[G];
 #pragma unroll
-    for (int m = 0; m < G; ++m) e[m] = v[base + m * h];
+    for (int m = 0; m < G; ++m) e[m] = v[px(base + m * h)];
 #pragma unroll
     for (int st = 0; st < R; ++st) {
 #pragma unroll
@@ -48,80 +62,85 @@ __device__ __forceinline__ void fwht_round(float *v, int off, int nblk, int B, i
       for (int m = 0; m < G; ++m) e[m] *= scale;
     }
 #pragma unroll
-    for (int m = 0; m < G; ++m) v[base + m * h] = e[m];
+    for (int m = 0; m < G; ++m) v[px(base + m * h)] = e[m];
   }
 }
 
-// Orthonormal FWHT of nblk adjacent blocks of size B starting at off.
-// Every thread of the block must call this (it contains barriers).
+// Orthonormal FWHT of nblk adjacent blocks of size B starting at off, by the
+// calling wavefront.
 __device__ __forceinline__ void fwht_blocks(float *v, int off, int nblk, const RotParams &rp,
-                                            int lane, bool active) {
+                                            int lane) {
   const int B = rp.B, logB = rp.logB;
   if (logB == 0) return;  // B == 1: identity
   for (int s = 0; s < logB; s += 3) {
     const int R = (logB - s) < 3 ? (logB - s) : 3;
     const bool last = (s + R) == logB;
-    if (active) {
-      if (R == 3) fwht_round<3>(v, off, nblk, B, s, last, rp.inv_sqrt_b, lane);
-      else if (R == 2) fwht_round<2>(v, off, nblk, B, s, last, rp.inv_sqrt_b, lane);
-      else fwht_round<1>(v, off, nblk, B, s, last, rp.inv_sqrt_b, lane);
-    }
-    __syncthreads();
+    if (R == 3) fwht_round<3>(v, off, nblk, B, s, last, rp.inv_sqrt_b, lane);
+    else if (R == 2) fwht_round<2>(v, off, nblk, B, s, last, rp.inv_sqrt_b, lane);
+    else fwht_round<1>(v, off, nblk, B, s, last, rp.inv_sqrt_b, lane);
+    wave_sync();
   }
 }
 
 // One pass of block transforms.  Forward: full blocks, then the overlap
 // block.  Reverse (inverse rotation): overlap block first.
-__device__ __forceinline__ void fwht_pass(float *v, const RotParams &rp, int lane, bool active,
-                                          bool reverse) {
+__device__ __forceinline__ void fwht_pass(float *v, const RotParams &rp, int lane, bool reverse) {
   if (!reverse) {
-    if (rp.n_full) fwht_blocks(v, 0, rp.n_full, rp, lane, active);
-    if (rp.overlap) fwht_blocks(v, rp.D - rp.B, 1, rp, lane, active);
+    if (rp.n_full) fwht_blocks(v, 0, rp.n_full, rp, lane);
+    if (rp.overlap) fwht_blocks(v, rp.D - rp.B, 1, rp, lane);
   } else {
-    if (rp.overlap) fwht_blocks(v, rp.D - rp.B, 1, rp, lane, active);
-    if (rp.n_full) fwht_blocks(v, 0, rp.n_full, rp, lane, active);
+    if (rp.overlap) fwht_blocks(v, rp.D - rp.B, 1, rp, lane);
+    if (rp.n_full) fwht_blocks(v, 0, rp.n_full, rp, lane);
   }
 }
 
-__device__ __forceinline__ int transpose_src(int o, const RotParams &rp) {
+// Source of output o of the strided transpose; pi is the workgroup's LDS
+// copy of the intra-block permutation.
+__device__ __forceinline__ int transpose_src(int o, const RotParams &rp, const int16_t *pi) {
   const int MB = rp.n_full * rp.B;
   if (o >= MB) return o;
   const int M = rp.n_full;
   const int k = o / M;
   const int b = o - k * M;
-  return b * rp.B + int(rp.pi[k]);
+  return b * rp.B + int(pi[k]);
+}
+
+// Workgroup prologue: LDS copy of the permutation (all threads must call).
+__device__ __forceinline__ void load_perm(const RotParams &rp, int16_t *pi) {
+  for (int k = threadIdx.x; k < rp.B; k += blockDim.x) pi[k] = rp.pi[k];
+  __syncthreads();
 }
 
 // Forward rotation of the vector held in v (already multiplied by S1 when
-// passes > 0).  Returns the buffer holding the result (v or w).
-__device__ float *rotate_forward(float *v, float *w, const RotParams &rp, int lane, bool active) {
+// passes > 0; element i at v[px(i)]).  Returns the buffer holding the result.
+__device__ float *rotate_forward(float *v, float *w, const RotParams &rp, const int16_t *pi,
+                                 uint32_t s2bits, int lane) {
   if (rp.passes == 0) return v;
-  fwht_pass(v, rp, lane, active, false);
+  fwht_pass(v, rp, lane, false);
   if (rp.passes == 1) return v;
-  if (active) {
-    for (int o = lane; o < rp.D; o += kWave)
-      w[o] = v[transpose_src(o, rp)] * rp.s1[(o + 127) & 255];
-  }
-  __syncthreads();
-  fwht_pass(w, rp, lane, active, false);
+#pragma unroll 4
+  for (int o = lane, t = 0; o < rp.D; o += kWave, ++t)
+    w[px(o)] = flip(v[px(transpose_src(o, rp, pi))], s2bits, t);
+  wave_sync();
+  fwht_pass(w, rp, lane, false);
   return w;
 }
 
 // Inverse rotation R^T of the vector in v; the result excludes the final S1
 // multiplication, which the caller applies on output.
-__device__ float *rotate_inverse(float *v, float *w, const RotParams &rp, int lane, bool active) {
+__device__ float *rotate_inverse(float *v, float *w, const RotParams &rp, const int16_t *pi,
+                                 uint32_t s2bits, int lane) {
   if (rp.passes == 0) return v;
   if (rp.passes == 1) {
-    fwht_pass(v, rp, lane, active, true);
+    fwht_pass(v, rp, lane, true);
     return v;
   }
-  fwht_pass(v, rp, lane, active, true);
-  if (active) {
-    for (int o = lane; o < rp.D; o += kWave)
-      w[transpose_src(o, rp)] = v[o] * rp.s1[(o + 127) & 255];
-  }
-  __syncthreads();
-  fwht_pass(w, rp, lane, active, true);
+  fwht_pass(v, rp, lane, true);
+#pragma unroll 4
+  for (int o = lane, t = 0; o < rp.D; o += kWave, ++t)
+    w[px(transpose_src(o, rp, pi))] = flip(v[px(o)], s2bits, t);
+  wave_sync();
+  fwht_pass(w, rp, lane, true);
   return w;
 }
 
@@ -129,30 +148,27 @@ __device__ float *rotate_inverse(float *v, float *w, const RotParams &rp, int la
 __global__ void __launch_bounds__(256) k_rotate(const float *__restrict__ x, float *y, int64_t n,
                                                 RotParams rp, int inverse, int dstride) {
   extern __shared__ float lds[];
+  __shared__ int16_t pi[128];
+  load_perm(rp, pi);
   const int lane = threadIdx.x & 63;
   const int wid = threadIdx.x >> 6;
   const int64_t row = int64_t(blockIdx.x) * (blockDim.x >> 6) + wid;
-  const bool active = row < n;
+  if (row >= n) return;   // no workgroup barriers below
   float *v = lds + wid * 2 * dstride;
   float *w = v + dstride;
   const int D = rp.D;
-  if (active) {
-    const float *xr = x + row * D;
-    for (int i = lane; i < D; i += kWave) {
-      float t = xr[i];
-      v[i] = (!inverse && rp.passes > 0) ? t * rp.s1[i & 255] : t;
-    }
-  }
-  __syncthreads();
-  float *res = inverse ? rotate_inverse(v, w, rp, lane, active)
-                       : rotate_forward(v, w, rp, lane, active);
-  if (active) {
-    float *yr = y + row * D;
-    for (int i = lane; i < D; i += kWave) {
-      float t = res[i];
-      yr[i] = (inverse && rp.passes > 0) ? t * rp.s1[i & 255] : t;
-    }
-  }
+  const uint2 sm = lane_sign_masks(rp, lane);
+  const uint32_t s1in = (!inverse && rp.passes > 0) ? sm.x : 0u;
+  const uint32_t s1out = (inverse && rp.passes > 0) ? sm.x : 0u;
+  const float *xr = x + row * D;
+#pragma unroll 4
+  for (int i = lane, t = 0; i < D; i += kWave, ++t) v[px(i)] = flip(xr[i], s1in, t);
+  wave_sync();
+  const float *res = inverse ? rotate_inverse(v, w, rp, pi, sm.y, lane)
+                             : rotate_forward(v, w, rp, pi, sm.y, lane);
+  float *yr = y + row * D;
+#pragma unroll 4
+  for (int i = lane, t = 0; i < D; i += kWave, ++t) yr[i] = flip(res[px(i)], s1out, t);
 }
 
 // --------------------------------------------------------------- rslm_encode
@@ -192,10 +208,12 @@ __global__ void __launch_bounds__(256) k_encode(
     int dstride) {
   extern __shared__ float lds[];
   __shared__ float cbs[64];
+  __shared__ int16_t pi[128];
   const int lane = threadIdx.x & 63;
   const int wid = threadIdx.x >> 6;
   const int nw = blockDim.x >> 6;
   if (threadIdx.x < 64) cbs[threadIdx.x] = cp.cb[threadIdx.x];
+  load_perm(rp, pi);
   const int64_t rec = int64_t(blockIdx.x) * nw + wid;
   int64_t row = -1;
   int L = -1;
@@ -207,48 +225,57 @@ __global__ void __launch_bounds__(256) k_encode(
       if (L < 0 || L >= nlist) row = -1;
     }
   }
-  const bool active = row >= 0;
+  if (row < 0) return;   // no workgroup barriers below
   float *v = lds + wid * 2 * dstride;
   float *w = v + dstride;
   uint8_t *cl = reinterpret_cast<uint8_t *>(lds + nw * 2 * dstride) + wid * (dstride / 1);
   const int D = rp.D;
   float xx = 0.f, rr = 0.f, cc = 0.f;
-  if (active) {
+  const uint2 sm = lane_sign_masks(rp, lane);
+  const uint32_t s1in = (rp.passes > 0) ? sm.x : 0u;
+  {
     const float *xr = x + row * D;
-    const float *cr = (L >= 0) ? cen + int64_t(L) * D : nullptr;
-    for (int i = lane; i < D; i += kWave) {
+    // branch-free loads: without a centre read x's row and weight it by 0
+    const float *cr = (L >= 0) ? cen + int64_t(L) * D : xr;
+    const float cw = (L >= 0) ? 1.f : 0.f;
+  #pragma unroll 4
+    for (int i = lane, t = 0; i < D; i += kWave, ++t) {
       const float xv = xr[i];
-      const float cv = cr ? cr[i] : 0.f;
+      const float cv = cr[i] * cw;
       const float r = xv - cv;
       xx += xv * xv;
       rr += r * r;
       cc += cv * cv;
-      v[i] = (rp.passes > 0) ? r * rp.s1[i & 255] : r;
+      v[px(i)] = flip(r, s1in, t);
     }
   }
-  __syncthreads();
-  const float *z = rotate_forward(v, w, rp, lane, active);
-  if (!active) return;  // no barriers below
+  wave_sync();
+  const float *z = rotate_forward(v, w, rp, pi, sm.y, lane);
 
   float m = 0.f;
-  for (int i = lane; i < D; i += kWave) m = fmaxf(m, fabsf(z[i]));
+#pragma unroll 4
+  for (int i = lane; i < D; i += kWave) m = fmaxf(m, fabsf(z[px(i)]));
   m = wave_max(m);
   const float inv_s0 = (m > 0.f) ? cp.emax / m : 0.f;
-  const float *rc = (L >= 0 && cen_rot) ? cen_rot + int64_t(L) * D : nullptr;
+  const bool has_rc = L >= 0 && cen_rot;
+  const float *rc = has_rc ? cen_rot + int64_t(L) * D : x + row * D;   // any valid row
+  const float rcw = has_rc ? 1.f : 0.f;
   const int g = cp.g;
   float cn2 = 0.f, rcd = 0.f;
+#pragma unroll 4
   for (int j = lane; j < cp.n_sub; j += kWave) {
     int code = 0;
     if (m > 0.f) {
       if (g == 1) {
-        const float u = z[j] * inv_s0;
-        for (int k = 0; k + 1 < cp.K; ++k) code += (u > cp.thr[k]) ? 1 : 0;
+        const float u = z[px(j)] * inv_s0;
+#pragma unroll
+        for (int k = 0; k < 15; ++k) code += (k + 1 < cp.K && u > cp.thr[k]) ? 1 : 0;
       } else {
         float u[4];
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
           const int i = j * g + t;
-          u[t] = (t < g && i < D) ? z[i] * inv_s0 : 0.f;
+          u[t] = (t < g && i < D) ? z[px(i)] * inv_s0 : 0.f;
         }
         float best = 3.4e38f;
         for (int k = 0; k < 16; ++k) {
@@ -268,11 +295,9 @@ __global__ void __launch_bounds__(256) k_encode(
       }
       for (int t = 0; t < g; ++t) {
         const int i = j * g + t;
-        if (i < D) {
-          const float cv = cbs[code * g + t];
-          cn2 += cv * cv;
-          if (rc) rcd += rc[i] * cv;
-        }
+        const float cv = (i < D) ? cbs[code * g + t] : 0.f;
+        cn2 += cv * cv;
+        rcd += rc[i < D ? i : 0] * rcw * cv;
       }
     }
     cl[j] = uint8_t(code);
@@ -309,11 +334,12 @@ __global__ void __launch_bounds__(256) k_encode(
   if (resid) {
     const float gh = dec_ue4m12(gu);
     float *out = resid + row * D;   // indexed by source row
+  #pragma unroll 4
     for (int i = lane; i < D; i += kWave) {
       const int code = cl[i / g];
       const float cv = (m > 0.f) ? cbs[code * g + (i % g)] : 0.f;
-      const float rcv = rc ? rc[i] : 0.f;
-      out[i] = z[i] + rcv - gh * (rcv + sh * cv);
+      const float rcv = rc[i] * rcw;
+      out[i] = z[px(i)] + rcv - gh * (rcv + sh * cv);
     }
   }
 }
@@ -351,7 +377,7 @@ __global__ void k_unpack(const uint8_t *__restrict__ tiles, int64_t n, uint8_t *
   }
 }
 
-static int lds_floats(int D) { return (D + 31) / 32 * 32 + 4; }
+static int lds_floats(int D) { return (padded_len((D + 31) / 32 * 32) + 3) / 4 * 4; }
 
 }  // namespace rslm
 

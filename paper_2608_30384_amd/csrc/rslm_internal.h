@@ -26,7 +26,36 @@ struct RotParams {
   float inv_sqrt_b;
   const float *s1;     // device, 256 signs (+1/-1) as float
   const int16_t *pi;   // device, intra-block permutation of size B
+  uint32_t s1mask[8];  // bit i set <=> S1[i] = -1
 };
+
+// Sign bit of S1[j & 255] from the plan's mask with a branch-free select
+// chain (the word index is per lane).
+__device__ __forceinline__ uint32_t sign_bit(const uint32_t (&m)[8], int j) {
+  j &= 255;
+  const int w = j >> 5;
+  uint32_t word = m[0];
+#pragma unroll
+  for (int i = 1; i < 8; ++i) word = (w == i) ? m[i] : word;
+  return (word >> (j & 31)) & 1u;
+}
+
+// Per-lane sign masks for elements i = lane + 64 t: bit (t mod 4) of the
+// first word is S1[i mod 256], of the second S2[i] = S1[(i + 127) mod 256]
+// (the index pattern repeats every 4 steps of 64).
+__device__ __forceinline__ uint2 lane_sign_masks(const RotParams &rp, int lane) {
+  uint32_t a = 0, b = 0;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    a |= sign_bit(rp.s1mask, lane + 64 * t) << t;
+    b |= sign_bit(rp.s1mask, lane + 64 * t + 127) << t;
+  }
+  return make_uint2(a, b);
+}
+
+__device__ __forceinline__ float flip(float v, uint32_t mask, int t) {
+  return __uint_as_float(__float_as_uint(v) ^ (((mask >> (t & 3)) & 1u) << 31));
+}
 
 struct CodecParams {
   int D, bits, K, g, w;       // w = log2 K

@@ -90,11 +90,87 @@ __device__ __forceinline__ uint64_t composite(uint32_t key, int32_t id) {
   return (uint64_t(key) << 32) | uint64_t(0xffffffffu - uint32_t(id));
 }
 
+// Calls f(key, i) for every element; each thread first loads U keys with
+// branch-free (clamped) loads so that U global loads are in flight at once.
+template <int U, class F>
+__device__ __forceinline__ void for_each_key(const float *__restrict__ vals, int n, F f) {
+  const int nt = blockDim.x;
+  for (int base = threadIdx.x; base < n; base += nt * U) {
+    uint32_t key[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int i = base + u * nt;
+      key[u] = order_key(vals[i < n ? i : n - 1]);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int i = base + u * nt;
+      if (i < n) f(key[u], i);
+    }
+  }
+}
+
+// Sorts the collected survivors and writes the k best (padding when fewer).
+__device__ __forceinline__ void emit_sorted(SelectSmem &sm, int cnt, int k, float *__restrict__ out_s,
+                                            int32_t *__restrict__ out_i) {
+  sort_desc(sm, cnt);
+  for (int j = threadIdx.x; j < k; j += blockDim.x) {
+    if (j < cnt) {
+      const uint64_t c = sm.buf[j];
+      out_s[j] = key_to_float(uint32_t(c >> 32));
+      out_i[j] = int32_t(0xffffffffu - uint32_t(c & 0xffffffffu));
+    } else {
+      out_s[j] = -__builtin_inff();
+      out_i[j] = -1;
+    }
+  }
+}
+
+// Threshold from a strided sample: the key that about 8 k elements of the
+// array exceed.  Collecting every element at or above it is exact whenever
+// at least k and at most kSelCap elements qualify; the caller checks.
+__device__ __forceinline__ uint32_t sample_threshold(const float *__restrict__ vals, int n, int k,
+                                                     SelectSmem &sm) {
+  constexpr int S = 1024;
+  for (int i = threadIdx.x; i < S; i += blockDim.x) {
+    const int idx = int((int64_t(i) * n) / S);
+    sm.buf[i] = uint64_t(order_key(vals[idx]));
+  }
+  __syncthreads();
+  sort_desc(sm, S);
+  int64_t r = (int64_t(8) * k * S + n - 1) / n;
+  if (r < 1) r = 1;
+  if (r > S) r = S;
+  const uint32_t t = uint32_t(sm.buf[r - 1]);
+  __syncthreads();
+  return t;
+}
+
 template <class IdFn>
 __device__ void block_topk(const float *__restrict__ vals, int n, int k, IdFn idfn,
                            float *__restrict__ out_s, int32_t *__restrict__ out_i,
                            SelectSmem &sm) {
   const int tid = threadIdx.x, nt = blockDim.x;
+  if (n > kSelCap && int64_t(8) * k * 4 <= n) {
+    // fast path: one pass collecting the elements above a sampled threshold
+    const uint32_t thr = sample_threshold(vals, n, k, sm);
+    if (tid == 0) sm.count = 0;
+    __syncthreads();
+    for_each_key<8>(vals, n, [&](uint32_t key, int i) {
+      if (key >= thr) {
+        const uint32_t pos = atomicAdd(&sm.count, 1u);
+        if (pos < uint32_t(kSelCap)) sm.buf[pos] = composite(key, idfn(i));
+      }
+    });
+    __syncthreads();
+    const uint32_t cnt = sm.count;
+    __syncthreads();
+    if (cnt >= uint32_t(k) && cnt <= uint32_t(kSelCap)) {
+      emit_sorted(sm, int(cnt), k, out_s, out_i);
+      return;
+    }
+    // otherwise fall through to the exact radix selection
+  }
   uint32_t lo_key = 0;         // collect keys >= lo_key (when not tie mode)
   bool tie_mode = false;
   uint32_t tie_key = 0, id_limit = 0;
@@ -109,11 +185,10 @@ __device__ void block_topk(const float *__restrict__ vals, int n, int k, IdFn id
       const int shift = 32 - pbits - d;
       for (int b = tid; b < nb; b += nt) sm.hist[b] = 0;
       __syncthreads();
-      for (int i = tid; i < n; i += nt) {
-        const uint32_t key = order_key(vals[i]);
+      for_each_key<8>(vals, n, [&](uint32_t key, int) {
         if (pbits == 0 || (key >> (32 - pbits)) == prefix)
           atomicAdd(&sm.hist[(key >> shift) & (nb - 1)], 1u);
-      }
+      });
       find_boundary(sm, nb, above, uint32_t(k));
       const uint32_t bb = sm.bcast[0];
       const uint32_t cnt_b = sm.hist[bb];
@@ -140,13 +215,12 @@ __device__ void block_topk(const float *__restrict__ vals, int n, int k, IdFn id
         const int shift = 32 - ibits - d;
         for (int b = tid; b < nb; b += nt) sm.hist[b] = 0;
         __syncthreads();
-        for (int i = tid; i < n; i += nt) {
-          if (order_key(vals[i]) != tie_key) continue;
-          const uint32_t id = uint32_t(idfn(i));
+        for_each_key<8>(vals, n, [&](uint32_t key, int i) {
+          if (key != tie_key) return;
           // reverse the order so that "highest bin" means smallest id
-          const uint32_t rid = 0x7fffffffu - id;
+          const uint32_t rid = 0x7fffffffu - uint32_t(idfn(i));
           if ((rid >> (32 - ibits)) == ip) atomicAdd(&sm.hist[(rid >> shift) & (nb - 1)], 1u);
-        }
+        });
         find_boundary(sm, nb, iabove, need);
         const uint32_t bb = sm.bcast[0];
         iabove = sm.bcast[1];
@@ -160,8 +234,7 @@ __device__ void block_topk(const float *__restrict__ vals, int n, int k, IdFn id
   // collect
   if (tid == 0) sm.count = 0;
   __syncthreads();
-  for (int i = tid; i < n; i += nt) {
-    const uint32_t key = order_key(vals[i]);
+  for_each_key<8>(vals, n, [&](uint32_t key, int i) {
     bool take;
     int32_t id = 0;
     if (n <= kSelCap) {
@@ -181,21 +254,11 @@ __device__ void block_topk(const float *__restrict__ vals, int n, int k, IdFn id
       const uint32_t pos = atomicAdd(&sm.count, 1u);
       if (pos < uint32_t(kSelCap)) sm.buf[pos] = composite(key, id);
     }
-  }
+  });
   __syncthreads();
   int cnt = int(sm.count);
   if (cnt > kSelCap) cnt = kSelCap;  // cannot happen: the selection above bounds it
-  sort_desc(sm, cnt);
-  for (int j = tid; j < k; j += nt) {
-    if (j < cnt) {
-      const uint64_t c = sm.buf[j];
-      out_s[j] = key_to_float(uint32_t(c >> 32));
-      out_i[j] = int32_t(0xffffffffu - uint32_t(c & 0xffffffffu));
-    } else {
-      out_s[j] = -__builtin_inff();
-      out_i[j] = -1;
-    }
-  }
+  emit_sorted(sm, cnt, k, out_s, out_i);
 }
 
 }  // namespace rslm

@@ -386,3 +386,55 @@ def test_end_to_end_tiny_config(R):
         tol = H.score_tol(exact, np.linalg.norm(q[i]), np.linalg.norm(xt_o[gi[i]], axis=1))
         viol += int(np.sum(np.abs(gs[i] - exact) > tol))
     assert viol <= 0.01 * Q * k
+
+
+# ------------------------------------------------------------------ large / tied top-k
+def _scan_vs_oracle(R, D, bits, passes, x, cen, assign, q, nprobe, k):
+    Rm = H.rot(D, passes)
+    C = synth.codebook(bits)
+    enc = oracle.encode(x, Rm, C, bits, centroids=cen[assign], scale_mode="global")
+    nlist = len(cen)
+    plan = R.Plan(D, bits, passes=passes, scale_mode="global")
+    index = _device_index(R, plan, enc, assign, nlist, bits)
+    qr = q.astype(np.float64) @ Rm.T
+    lists = _oracle_lists(enc, assign, nlist)
+    ref_s, ref_i, pid = oracle.ivf_search(q, qr, cen, lists, C, nprobe, k)
+    pdot = (q.astype(np.float64) @ cen.T)[np.arange(len(q))[:, None], pid]
+    gs, gi = R.rslm_scan_topk(plan, index, _t(qr.astype(np.float32)), _t(pid, torch.int32),
+                              _t(pdot.astype(np.float32)), k)
+    return gs.cpu().numpy(), gi.cpu().numpy(), ref_s, ref_i, enc, Rm, C
+
+
+def test_scan_topk_large_candidate_sets(R):
+    """~70,000 candidates per query: the sampled-threshold selection."""
+    D, bits, n, nlist, Q, nprobe, k = 64, 4, 90000, 9, 6, 7, 100
+    x = synth.gmix(n, D, 12, seed=77)
+    rng = np.random.default_rng(77)
+    cen = x[rng.choice(n, nlist, replace=False)].astype(np.float64)
+    assign, _ = oracle.assign_l2(x, cen)
+    q = synth.queries_like("gmix", Q, D, data_seed=77, n_comp=12)
+    gs, gi, ref_s, ref_i, enc, Rm, C = _scan_vs_oracle(R, D, bits, 2, x, cen, assign, q, nprobe, k)
+    xt = oracle.reconstruct(enc["codes"], enc["s_code"], enc["g_code"], C, Rm, cen[assign])
+    xn = np.linalg.norm(xt, axis=1).max()
+    diffs = sum(H.check_topk(gs[i], gi[i], ref_s[i], ref_i[i],
+                             H.score_tol(ref_s[i], np.linalg.norm(q[i]), xn)) for i in range(Q))
+    assert diffs <= 1
+
+
+def test_scan_topk_exact_ties(R):
+    """6,000 identical top candidates: the k lowest ids must win (radix
+    selection with the id tie-break, since the tied set exceeds the buffer)."""
+    D, bits, nlist, Q, nprobe, k = 64, 4, 4, 3, 4, 100
+    base = synth.gmix(8000, D, 6, seed=91)
+    q = synth.queries_like("gmix", Q, D, data_seed=91, n_comp=6)
+    star = q[0] / np.linalg.norm(q[0]) * 3.0          # far above every other candidate for q0
+    x = base.copy()
+    dup = np.random.default_rng(91).choice(8000, 6000, replace=False)
+    x[dup] = star.astype(np.float32)
+    rng = np.random.default_rng(91)
+    cen = np.vstack([x[rng.choice(8000, nlist - 1, replace=False)], star[None]]).astype(np.float64)
+    assign, _ = oracle.assign_l2(x, cen)
+    gs, gi, ref_s, ref_i, *_ = _scan_vs_oracle(R, D, bits, 2, x, cen, assign, q, nprobe, k)
+    assert np.array_equal(gi[0], np.sort(dup)[:k])
+    assert np.array_equal(ref_i[0], gi[0])
+    assert np.all(gs[0] == gs[0][0])
