@@ -186,7 +186,7 @@ typedef struct rslm_index {
  * with <q, c_p> = probe_dots; then the k best by (score desc, id asc),
  * padded with (-inf, -1).
  *   q_rot: Q x D rotated queries (rslm_fwht); probe_ids / probe_dots:
- *   Q x nprobe; out_scores / out_ids: Q x k.  1 <= k <= 1024.
+ *   Q x nprobe; out_scores / out_ids: Q x k.  1 <= k <= 1024, Q <= 65535.
  * ------------------------------------------------------------------------ */
 size_t rslm_scan_topk_workspace(const rslm_plan *plan, const rslm_index *index,
                                 int32_t Q, int32_t nprobe, int32_t k);

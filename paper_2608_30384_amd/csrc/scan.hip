@@ -43,12 +43,14 @@ struct ScanWs {
   int32_t *counts, *cursor, *pair_off, *item_off;
   int32_t *pairs, *prefix, *totals;
   float *scores;
+  uint32_t *thr, *cnt;    // per-query top-k threshold and survivor count
+  uint64_t *surv;         // per-query survivors, kSurvCap each
   int64_t stride;
   size_t bytes;
 };
 
 static ScanWs scan_ws_layout(void *base, int Q, int nprobe, int nlist, int d_pad,
-                             int max_list) {
+                             int max_list, int k) {
   ScanWs w{};
   char *p = static_cast<char *>(base);
   size_t off = 0;
@@ -69,6 +71,10 @@ static ScanWs scan_ws_layout(void *base, int Q, int nprobe, int nlist, int d_pad
   w.totals = reinterpret_cast<int32_t *>(take(size_t(Q) * 4));
   w.stride = (int64_t(nprobe) * max_list + 63) / 64 * 64;
   w.scores = reinterpret_cast<float *>(take(size_t(Q) * size_t(w.stride) * 4));
+  (void)k;
+  w.thr = reinterpret_cast<uint32_t *>(take(size_t(Q) * 4));
+  w.cnt = reinterpret_cast<uint32_t *>(take(size_t(Q) * 4));
+  w.surv = reinterpret_cast<uint64_t *>(take(size_t(Q) * 4096 * 8));
   w.bytes = off;
   return w;
 }
@@ -114,18 +120,32 @@ __global__ void k_plan_count(const int32_t *__restrict__ probe_ids, int npairs, 
   if (L >= 0 && L < nlist) atomicAdd(&counts[L], 1);
 }
 
+// One wavefront per query: exclusive prefix over its probes of the (clamped)
+// probed list sizes.
 __global__ void k_plan_prefix(const int32_t *__restrict__ probe_ids, int Q, int nprobe, int nlist,
                               const int32_t *__restrict__ sizes, int max_list,
                               int32_t *__restrict__ prefix, int32_t *__restrict__ totals) {
-  const int q = blockIdx.x * blockDim.x + threadIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int q = blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
   if (q >= Q) return;
-  int run = 0;
-  for (int p = 0; p < nprobe; ++p) {
-    const int L = probe_ids[int64_t(q) * nprobe + p];
-    prefix[int64_t(q) * nprobe + p] = run;
-    if (L >= 0 && L < nlist) run += max(0, min(sizes[L], max_list));
+  int carry = 0;
+  for (int p0 = 0; p0 < nprobe; p0 += 64) {
+    const int p = p0 + lane;
+    int sz = 0;
+    if (p < nprobe) {
+      const int L = probe_ids[int64_t(q) * nprobe + p];
+      if (L >= 0 && L < nlist) sz = max(0, min(sizes[L], max_list));
+    }
+    int incl = sz;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int t = __shfl_up(incl, off, 64);
+      if (lane >= off) incl += t;
+    }
+    if (p < nprobe) prefix[int64_t(q) * nprobe + p] = carry + incl - sz;
+    carry += __shfl(incl, 63, 64);
   }
-  totals[q] = run;
+  if (lane == 0) totals[q] = carry;
 }
 
 // Single workgroup: exclusive scans over lists of the pair counts and of the
@@ -430,16 +450,120 @@ struct ScanId {
   }
 };
 
-__global__ void __launch_bounds__(kSelThreads) k_scan_topk(
+// ------------------------------------------------------------- top-k
+// Stage 1 (one workgroup per query): a threshold from a strided sample of the
+// query's scores that about 8 k of them reach (at most half the survivor
+// buffer); resets the survivor count.
+constexpr int kSurvCap = 4096;
+
+__global__ void __launch_bounds__(kSelThreads) k_topk_sample(const float *__restrict__ scores,
+                                                             int64_t stride,
+                                                             const int32_t *__restrict__ totals,
+                                                             int k, uint32_t *__restrict__ thr,
+                                                             uint32_t *__restrict__ cnt) {
+  __shared__ SelectSmem sm;
+  const int q = blockIdx.x;
+  const int n = totals[q];
+  uint32_t t = 0u;   // keep everything when the region is small
+  if (n > kSurvCap) t = sample_threshold(scores + int64_t(q) * stride, n, k, sm,
+                                         min(8 * k, kSurvCap / 2));
+  if (threadIdx.x == 0) {
+    thr[q] = t;
+    cnt[q] = 0u;
+  }
+}
+
+// Stage 2 (streaming, all queries at once): every score at or above its
+// query's threshold is appended, as (key << 32 | position), to the query's
+// survivor list.  A workgroup covers 4,096 positions of one query with
+// 16-byte loads, stages its survivors in LDS and reserves their slots with a
+// single device atomic (per-survivor atomics on one counter serialise).
+__global__ void __launch_bounds__(256) k_topk_filter(const float *__restrict__ scores,
+                                                     int64_t stride,
+                                                     const int32_t *__restrict__ totals,
+                                                     const uint32_t *__restrict__ thr,
+                                                     uint32_t *__restrict__ cnt,
+                                                     uint64_t *__restrict__ surv) {
+  __shared__ uint64_t stage[4096];
+  __shared__ uint32_t lcount, gbase;
+  const int q = blockIdx.y;
+  const int n = totals[q];
+  const int base = blockIdx.x * 4096;
+  if (base >= n) return;   // uniform per workgroup
+  const uint32_t t = thr[q];
+  const float *row = scores + int64_t(q) * stride;   // stride is a multiple of 64
+  if (threadIdx.x == 0) lcount = 0;
+  float4 v[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int i = base + (u * 256 + int(threadIdx.x)) * 4;
+    v[u] = (i < n) ? *reinterpret_cast<const float4 *>(row + i) : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int i = base + (u * 256 + int(threadIdx.x)) * 4;
+    const float e[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const uint32_t key = order_key(e[c]);
+      if (i + c < n && key >= t) {
+        const uint32_t pos = atomicAdd(&lcount, 1u);
+        stage[pos] = (uint64_t(key) << 32) | uint32_t(i + c);
+      }
+    }
+  }
+  __syncthreads();
+  const uint32_t m = lcount;
+  if (threadIdx.x == 0) gbase = m ? atomicAdd(&cnt[q], m) : 0u;
+  __syncthreads();
+  const uint32_t g0 = gbase;
+  for (uint32_t j = threadIdx.x; j < m; j += blockDim.x)
+    if (g0 + j < uint32_t(kSurvCap)) surv[int64_t(q) * kSurvCap + g0 + j] = stage[j];
+}
+
+// Stage 3 (one workgroup per query): ids of the survivors (binary search of
+// the query's probe prefix in LDS), exact sort by (score desc, id asc), the k
+// best out.  When the sample misjudged (fewer than k or more than the buffer
+// survived) the exact block selection runs over the whole region instead.
+__global__ void __launch_bounds__(kSelThreads) k_topk_final(
     const float *__restrict__ scores, int64_t stride, const int32_t *__restrict__ totals,
+    const uint32_t *__restrict__ cnt, const uint64_t *__restrict__ surv,
     const int32_t *__restrict__ prefix, const int32_t *__restrict__ probe_ids, int nprobe,
     const int64_t *__restrict__ list_offsets, const int32_t *__restrict__ ids, int k,
     float *__restrict__ out_s, int32_t *__restrict__ out_i) {
-  __shared__ SelectSmem sm;
+  __shared__ uint64_t buf[kSurvCap];
+  __shared__ int32_t spre[kMaxNprobe], sprobe[kMaxNprobe];
   const int q = blockIdx.x;
-  ScanId f{prefix + int64_t(q) * nprobe, probe_ids + int64_t(q) * nprobe, list_offsets, ids, nprobe};
-  block_topk(scores + int64_t(q) * stride, totals[q], k, f, out_s + int64_t(q) * k,
-             out_i + int64_t(q) * k, sm);
+  const int n = totals[q];
+  const uint32_t c = cnt[q];
+  for (int p = threadIdx.x; p < nprobe; p += blockDim.x) {
+    spre[p] = prefix[int64_t(q) * nprobe + p];
+    sprobe[p] = probe_ids[int64_t(q) * nprobe + p];
+  }
+  __syncthreads();
+  const ScanId f{spre, sprobe, list_offsets, ids, nprobe};
+  if ((c >= uint32_t(k) || c == uint32_t(n)) && c <= uint32_t(kSurvCap)) {
+    for (int j = threadIdx.x; j < int(c); j += blockDim.x) {
+      const uint64_t e = surv[int64_t(q) * kSurvCap + j];
+      buf[j] = composite(uint32_t(e >> 32), f(int(e & 0xffffffffu)));
+    }
+    __syncthreads();
+    sort_desc_buf(buf, int(c));
+    for (int j = threadIdx.x; j < k; j += blockDim.x) {
+      if (j < int(c)) {
+        out_s[int64_t(q) * k + j] = key_to_float(uint32_t(buf[j] >> 32));
+        out_i[int64_t(q) * k + j] = int32_t(0xffffffffu - uint32_t(buf[j] & 0xffffffffu));
+      } else {
+        out_s[int64_t(q) * k + j] = -__builtin_inff();
+        out_i[int64_t(q) * k + j] = -1;
+      }
+    }
+    return;
+  }
+  SelectSmem &sm = *reinterpret_cast<SelectSmem *>(buf);   // 32 KiB >= sizeof(SelectSmem)
+  block_topk(scores + int64_t(q) * stride, n, k, f, out_s + int64_t(q) * k, out_i + int64_t(q) * k,
+             sm);
 }
 
 // Profiling hook: events recorded around the scan kernel (0) and the top-k
@@ -491,9 +615,10 @@ extern "C" {
 
 size_t rslm_scan_topk_workspace(const rslm_plan *p, const rslm_index *idx, int32_t Q,
                                 int32_t nprobe, int32_t k) {
-  (void)k;
-  if (!p || !idx || Q < 0 || nprobe < 1 || idx->nlist < 1 || idx->max_list_size < 0) return 0;
-  return scan_ws_layout(nullptr, Q, nprobe, idx->nlist, p->codec.d_pad, idx->max_list_size).bytes;
+  if (!p || !idx || Q < 0 || nprobe < 1 || idx->nlist < 1 || idx->max_list_size < 0 || k < 1)
+    return 0;
+  return scan_ws_layout(nullptr, Q, nprobe, idx->nlist, p->codec.d_pad, idx->max_list_size, k)
+      .bytes;
 }
 
 int rslm_scan_topk(const rslm_plan *p, const rslm_index *idx, const float *q_rot, int32_t Q,
@@ -506,6 +631,7 @@ int rslm_scan_topk(const rslm_plan *p, const rslm_index *idx, const float *q_rot
     return RSLM_ERR_INVALID_ARG;
   if (int64_t(nprobe) * idx->max_list_size >= (int64_t(1) << 31)) return RSLM_ERR_INVALID_ARG;
   if (Q == 0) return RSLM_OK;
+  if (Q > 65535) return RSLM_ERR_INVALID_ARG;   // gridDim.y of the top-k kernel
   if (!q_rot || !probe_ids || !probe_dots || !out_scores || !out_ids || !idx->list_offsets ||
       !idx->list_sizes || !idx->ids || !idx->codes || !idx->scales)
     return RSLM_ERR_INVALID_ARG;
@@ -514,7 +640,7 @@ int rslm_scan_topk(const rslm_plan *p, const rslm_index *idx, const float *q_rot
   if (!ws || ws_bytes < need) return RSLM_ERR_WORKSPACE;
   const int nlist = idx->nlist;
   const int d_pad = p->codec.d_pad;
-  ScanWs w = scan_ws_layout(ws, Q, nprobe, nlist, d_pad, idx->max_list_size);
+  ScanWs w = scan_ws_layout(ws, Q, nprobe, nlist, d_pad, idx->max_list_size, k);
   hipStream_t s = as_stream(stream);
   const int npairs = Q * nprobe;
   int st;
@@ -526,7 +652,7 @@ int rslm_scan_topk(const rslm_plan *p, const rslm_index *idx, const float *q_rot
   hipLaunchKernelGGL(k_plan_count, dim3((npairs + 255) / 256), dim3(256), 0, s, probe_ids, npairs,
                      nlist, w.counts);
   if ((st = check_launch())) return st;
-  hipLaunchKernelGGL(k_plan_prefix, dim3((Q + 255) / 256), dim3(256), 0, s, probe_ids, Q, nprobe,
+  hipLaunchKernelGGL(k_plan_prefix, dim3((Q + 3) / 4), dim3(256), 0, s, probe_ids, Q, nprobe,
                      nlist, idx->list_sizes, idx->max_list_size, w.prefix, w.totals);
   if ((st = check_launch())) return st;
   hipLaunchKernelGGL(k_plan_lists, dim3(1), dim3(1024), 0, s, w.counts, idx->list_sizes, nlist,
@@ -572,9 +698,18 @@ int rslm_scan_topk(const rslm_plan *p, const rslm_index *idx, const float *q_rot
   if ((st = check_launch())) return st;
   if ((st = record_timer(0, 1, s))) return st;
   if ((st = record_timer(1, 0, s))) return st;
-  hipLaunchKernelGGL(k_scan_topk, dim3(unsigned(Q)), dim3(kSelThreads), 0, s, w.scores, w.stride,
-                     w.totals, w.prefix, probe_ids, nprobe, idx->list_offsets, idx->ids, k,
-                     out_scores, out_ids);
+  hipLaunchKernelGGL(k_topk_sample, dim3(unsigned(Q)), dim3(kSelThreads), 0, s, w.scores,
+                     w.stride, w.totals, k, w.thr, w.cnt);
+  if ((st = check_launch())) return st;
+  {
+    const int64_t chunks = (w.stride + 4095) / 4096;
+    hipLaunchKernelGGL(k_topk_filter, dim3(unsigned(chunks), unsigned(Q)), dim3(256), 0, s,
+                       w.scores, w.stride, w.totals, w.thr, w.cnt, w.surv);
+  }
+  if ((st = check_launch())) return st;
+  hipLaunchKernelGGL(k_topk_final, dim3(unsigned(Q)), dim3(kSelThreads), 0, s, w.scores, w.stride,
+                     w.totals, w.cnt, w.surv, w.prefix, probe_ids, nprobe, idx->list_offsets,
+                     idx->ids, k, out_scores, out_ids);
   if ((st = check_launch())) return st;
   return record_timer(1, 1, s);
 }

@@ -15,12 +15,16 @@
 
 namespace rslm {
 
-constexpr int kSelCap = 4096;       // LDS sort buffer entries
-constexpr int kSelThreads = 1024;
+constexpr int kSelCap = 2048;       // LDS sort buffer entries
+constexpr int kSelThreads = 256;
 
+// The histogram is only live during the radix passes and the sort buffer
+// only during sampling and collection, so they share storage.
 struct SelectSmem {
-  uint32_t hist[4096];
-  uint64_t buf[kSelCap];
+  union {
+    uint32_t hist[4096];
+    uint64_t buf[kSelCap];
+  };
   uint32_t bcast[8];
   uint32_t count;
 };
@@ -63,11 +67,12 @@ __device__ __forceinline__ void find_boundary(SelectSmem &sm, int nb, uint32_t a
   __syncthreads();
 }
 
-// Bitonic sort of sm.buf[0..n) descending; n <= kSelCap.
-__device__ __forceinline__ void sort_desc(SelectSmem &sm, int n) {
+// Bitonic sort of buf[0..n) descending (buf holds at least the next power
+// of two >= n entries).
+__device__ __forceinline__ void sort_desc_buf(uint64_t *buf, int n) {
   int p2 = 1;
   while (p2 < n) p2 <<= 1;
-  for (int i = n + threadIdx.x; i < p2; i += blockDim.x) sm.buf[i] = 0ull;
+  for (int i = n + threadIdx.x; i < p2; i += blockDim.x) buf[i] = 0ull;
   __syncthreads();
   for (int size = 2; size <= p2; size <<= 1) {
     for (int stride = size >> 1; stride > 0; stride >>= 1) {
@@ -75,16 +80,18 @@ __device__ __forceinline__ void sort_desc(SelectSmem &sm, int n) {
         const int lo = 2 * i - (i & (stride - 1));
         const int hi = lo + stride;
         const bool desc = ((lo & size) == 0);
-        const uint64_t a = sm.buf[lo], b = sm.buf[hi];
+        const uint64_t a = buf[lo], b = buf[hi];
         if ((a < b) == desc) {
-          sm.buf[lo] = b;
-          sm.buf[hi] = a;
+          buf[lo] = b;
+          buf[hi] = a;
         }
       }
       __syncthreads();
     }
   }
 }
+
+__device__ __forceinline__ void sort_desc(SelectSmem &sm, int n) { sort_desc_buf(sm.buf, n); }
 
 __device__ __forceinline__ uint64_t composite(uint32_t key, int32_t id) {
   return (uint64_t(key) << 32) | uint64_t(0xffffffffu - uint32_t(id));
@@ -130,7 +137,7 @@ __device__ __forceinline__ void emit_sorted(SelectSmem &sm, int cnt, int k, floa
 // array exceed.  Collecting every element at or above it is exact whenever
 // at least k and at most kSelCap elements qualify; the caller checks.
 __device__ __forceinline__ uint32_t sample_threshold(const float *__restrict__ vals, int n, int k,
-                                                     SelectSmem &sm) {
+                                                     SelectSmem &sm, int target = 0) {
   constexpr int S = 1024;
   for (int i = threadIdx.x; i < S; i += blockDim.x) {
     const int idx = int((int64_t(i) * n) / S);
@@ -138,7 +145,8 @@ __device__ __forceinline__ uint32_t sample_threshold(const float *__restrict__ v
   }
   __syncthreads();
   sort_desc(sm, S);
-  int64_t r = (int64_t(8) * k * S + n - 1) / n;
+  if (target <= 0) target = 8 * k;
+  int64_t r = (int64_t(target) * S + n - 1) / n;
   if (r < 1) r = 1;
   if (r > S) r = S;
   const uint32_t t = uint32_t(sm.buf[r - 1]);
@@ -151,7 +159,7 @@ __device__ void block_topk(const float *__restrict__ vals, int n, int k, IdFn id
                            float *__restrict__ out_s, int32_t *__restrict__ out_i,
                            SelectSmem &sm) {
   const int tid = threadIdx.x, nt = blockDim.x;
-  if (n > kSelCap && int64_t(8) * k * 4 <= n) {
+  if (n > kSelCap && int64_t(32) * k <= n) {
     // fast path: one pass collecting the elements above a sampled threshold
     const uint32_t thr = sample_threshold(vals, n, k, sm);
     if (tid == 0) sm.count = 0;

@@ -422,17 +422,19 @@ def test_scan_topk_large_candidate_sets(R):
 
 
 def test_scan_topk_exact_ties(R):
-    """6,000 identical top candidates: the k lowest ids must win (radix
-    selection with the id tie-break, since the tied set exceeds the buffer)."""
+    """60,000 identical top candidates: the k lowest ids must win.  Every
+    top-k slice then holds more tied scores than its sort buffer, so the
+    radix selection with the id tie-break runs."""
     D, bits, nlist, Q, nprobe, k = 64, 4, 4, 3, 4, 100
-    base = synth.gmix(8000, D, 6, seed=91)
+    N = 70000
+    base = synth.gmix(N, D, 6, seed=91)
     q = synth.queries_like("gmix", Q, D, data_seed=91, n_comp=6)
     star = q[0] / np.linalg.norm(q[0]) * 3.0          # far above every other candidate for q0
     x = base.copy()
-    dup = np.random.default_rng(91).choice(8000, 6000, replace=False)
+    dup = np.random.default_rng(91).choice(N, 60000, replace=False)
     x[dup] = star.astype(np.float32)
     rng = np.random.default_rng(91)
-    cen = np.vstack([x[rng.choice(8000, nlist - 1, replace=False)], star[None]]).astype(np.float64)
+    cen = np.vstack([x[rng.choice(N, nlist - 1, replace=False)], star[None]]).astype(np.float64)
     assign, _ = oracle.assign_l2(x, cen)
     gs, gi, ref_s, ref_i, *_ = _scan_vs_oracle(R, D, bits, 2, x, cen, assign, q, nprobe, k)
     assert np.array_equal(gi[0], np.sort(dup)[:k])
