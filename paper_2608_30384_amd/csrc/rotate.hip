@@ -389,6 +389,8 @@ int rslm_fwht(const rslm_plan *p, const float *x, float *y, int64_t n, int inver
   if (!p || (!x && n) || (!y && n) || n < 0 || (inverse != 0 && inverse != 1))
     return RSLM_ERR_INVALID_ARG;
   if (n == 0) return RSLM_OK;
+  if ((n + 3) / 4 > 0x7fffffff) return RSLM_ERR_INVALID_ARG;
+  if (launch_rotate_reg(p, x, y, n, inverse, as_stream(stream))) return check_launch();
   const int D = p->rot.D;
   const int dstride = lds_floats(D);
   int waves = 4;
@@ -410,6 +412,10 @@ int rslm_encode(const rslm_plan *p, const float *x, int64_t n_rows, const int64_
   if (!x || !codes || !scales) return RSLM_ERR_INVALID_ARG;
   if (centroids && (!rec_list || !centroids_rot || nlist < 1)) return RSLM_ERR_INVALID_ARG;
   if (!src_row && n_records > n_rows) return RSLM_ERR_INVALID_ARG;
+  if ((n_records + 3) / 4 > 0x7fffffff) return RSLM_ERR_INVALID_ARG;
+  if (launch_encode_reg(p, x, n_rows, src_row, rec_list, n_records, centroids, centroids_rot,
+                        nlist, codes, scales, resid_rot, as_stream(stream)))
+    return check_launch();
   const int D = p->rot.D;
   const int dstride = lds_floats(D);
   int waves = 4;

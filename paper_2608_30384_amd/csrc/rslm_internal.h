@@ -96,6 +96,15 @@ bool device_ok();                    // current device is gfx950
 
 inline hipStream_t as_stream(void *s) { return reinterpret_cast<hipStream_t>(s); }
 
+// Register-resident rotation / 1-D encoder for D = 128 NB (rotate_reg.hip);
+// false when the plan is not handled there.
+bool launch_rotate_reg(const rslm_plan *p, const float *x, float *y, int64_t n, int inverse,
+                       hipStream_t s);
+bool launch_encode_reg(const rslm_plan *p, const float *x, int64_t n_rows, const int64_t *src_row,
+                       const int32_t *rec_list, int64_t n_records, const float *cen,
+                       const float *cen_rot, int nlist, uint8_t *codes, uint32_t *scales,
+                       float *resid, hipStream_t s);
+
 // ---- device helpers ------------------------------------------------------
 
 __device__ __forceinline__ float wave_sum(float v) {
