@@ -3,11 +3,12 @@
 // (paper, Section "End-to-End Comparison", Setup: Euclidean partitions,
 // routing by the dot product with the centres).
 //
-// Both modes are a dense [n x D] x [D x nlist] contraction in float32.  A
-// 64x64 output tile per 256-thread workgroup, 4x4 outputs per thread, K
-// staged through LDS in slices of 16.  Assignment keeps a running
-// (distance, id) minimum per row across all column tiles and never writes the
-// product; probing writes the dots and selects the top-nprobe per row.
+// Both modes are a dense [n x D] x [D x nlist] contraction in float32.
+// Probing runs it on the matrix cores (v_mfma_f32_16x16x4_f32, 32 x 32 output
+// tiles), writes the dots and selects the top-nprobe per row.  Assignment
+// uses a 64 x 64 tile with 4 x 4 outputs per thread and keeps a running
+// (distance, id) minimum per row across all column tiles, never writing the
+// product.
 #include "rslm_internal.h"
 #include "select_dev.h"
 
@@ -142,25 +143,54 @@ __global__ void __launch_bounds__(256) k_assign(const float *__restrict__ x, int
   }
 }
 
-__global__ void __launch_bounds__(256) k_dots(const float *__restrict__ x, int64_t n, int D,
-                                              const float *__restrict__ cen, int nlist,
-                                              float *__restrict__ dots) {
-  __shared__ float As[kTK][kTM + 4];
-  __shared__ float Bs[kTK][kTM + 4];
-  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
-  const int64_t r0 = int64_t(blockIdx.y) * kTM;
-  const int c0 = blockIdx.x * kTN;
-  float acc[4][4];
-  tile_product(x, n, cen, nlist, D, r0, c0, As, Bs, acc);
+// Probe dots on the matrix cores (v_mfma_f32_16x16x4_f32, full float32):
+// a 32 x 32 output tile per 256-thread workgroup, each wavefront one 16 x 16
+// MFMA tile, K staged through LDS in slabs of 32.
+typedef float floatx4_t __attribute__((ext_vector_type(4)));
+constexpr int kMT = 32, kMK = 32;
+
+__device__ __forceinline__ void stage32(const float *__restrict__ m, int64_t rows, int D,
+                                        int64_t r0, int k0, float (*lds)[kMK + 1]) {
+  const int t = threadIdx.x;        // 256 threads x 4 elements = 32 rows x 32 k
+  const int r = t >> 3;
+  const int kk = (t & 7) * 4;
+  const int64_t gr = r0 + r;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int gk = k0 + kk + e;
+    lds[r][kk + e] = (gr < rows && gk < D) ? m[gr * D + gk] : 0.f;
+  }
+}
+
+__global__ void __launch_bounds__(256) k_dots_mfma(const float *__restrict__ x, int64_t n, int D,
+                                                   const float *__restrict__ cen, int nlist,
+                                                   float *__restrict__ dots) {
+  __shared__ float As[kMT][kMK + 1];
+  __shared__ float Bs[kMT][kMK + 1];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t r0 = int64_t(blockIdx.y) * kMT;
+  const int c0 = blockIdx.x * kMT;
+  const int wr = (wave >> 1) * 16, wc = (wave & 1) * 16;   // this wave's 16 x 16 block
+  const int ml = lane & 15, kl = lane >> 4;
+  floatx4_t acc = {0.f, 0.f, 0.f, 0.f};
+  for (int k0 = 0; k0 < D; k0 += kMK) {
+    stage32(x, n, D, r0, k0, As);
+    stage32(cen, nlist, D, c0, k0, Bs);
+    __syncthreads();
+#pragma unroll
+    for (int ks = 0; ks < kMK; ks += 4) {
+      const float a = As[wr + ml][ks + kl];     // A[m][k]: lane -> (m = lane % 16, k = lane / 16)
+      const float b = Bs[wc + ml][ks + kl];     // B[k][n]: lane -> (k = lane / 16, n = lane % 16)
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
+    }
+    __syncthreads();
+  }
+  // lane holds C[4 (lane / 16) + i][lane % 16]
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const int64_t r = r0 + ty * 4 + i;
-    if (r >= n) continue;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int c = c0 + tx * 4 + j;
-      if (c < nlist) dots[r * nlist + c] = acc[i][j];
-    }
+    const int64_t r = r0 + wr + 4 * kl + i;
+    const int c = c0 + wc + ml;
+    if (r < n && c < nlist) dots[r * nlist + c] = acc[i];
   }
 }
 
@@ -223,10 +253,10 @@ int ivf_assign_probe(const float *x, int64_t n, int32_t dim, const float *centro
   }
   const size_t norms = (size_t(nlist) * sizeof(float) + 255) / 256 * 256;
   float *dots = reinterpret_cast<float *>(static_cast<char *>(ws) + norms);
-  const int64_t gy = (n + kTM - 1) / kTM;
-  if (gy > 65535) return RSLM_ERR_INVALID_ARG;   // gridDim.y limit: n <= 4,194,240
-  hipLaunchKernelGGL(k_dots, dim3((nlist + kTN - 1) / kTN, unsigned(gy)), dim3(256), 0, s, x, n,
-                     dim, centroids, nlist, dots);
+  const int64_t gy32 = (n + kMT - 1) / kMT;
+  if (gy32 > 65535) return RSLM_ERR_INVALID_ARG;
+  hipLaunchKernelGGL(k_dots_mfma, dim3((nlist + kMT - 1) / kMT, unsigned(gy32)), dim3(256), 0, s,
+                     x, n, dim, centroids, nlist, dots);
   int st = check_launch();
   if (st) return st;
   if (n > 0x7fffffff) return RSLM_ERR_INVALID_ARG;

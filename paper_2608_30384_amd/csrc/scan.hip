@@ -413,20 +413,24 @@ __global__ void __launch_bounds__(kScanThreads) k_scan(ScanArgs a) {
     }
     const int64_t rec_base = a.list_offsets[L];
     const int t_end = (cand1 + 15) / 16;
-    // Software pipeline: the codes of the wave's next tile are in flight
-    // while the current tile is decoded and multiplied.
-    uint32_t bufA[kWordsPerLane], bufB[kWordsPerLane];
+    // Software pipeline, depth 2: the codes of the wave's next two tiles are
+    // in flight while the current tile is decoded and multiplied.
+    uint32_t bufA[kWordsPerLane], bufB[kWordsPerLane], bufC[kWordsPerLane];
     int t = cand0 / 16 + wave;
     if (t < t_end) load_tile<kWordsPerLane>(bufA, a, rec_base, t, lane);
+    if (t + nwaves < t_end) load_tile<kWordsPerLane>(bufB, a, rec_base, t + nwaves, lane);
     while (t < t_end) {
-      const int t1 = t + nwaves;
-      if (t1 < t_end) load_tile<kWordsPerLane>(bufB, a, rec_base, t1, lane);
+      if (t + 2 * nwaves < t_end) load_tile<kWordsPerLane>(bufC, a, rec_base, t + 2 * nwaves, lane);
       score_tile<BITS, NC>(bufA, av, dtab, lane4, a, rec_base, t, cand1, m, ok, qc, qi, obase);
-      if (t1 >= t_end) break;
-      const int t2 = t1 + nwaves;
-      if (t2 < t_end) load_tile<kWordsPerLane>(bufA, a, rec_base, t2, lane);
-      score_tile<BITS, NC>(bufB, av, dtab, lane4, a, rec_base, t1, cand1, m, ok, qc, qi, obase);
-      t = t2;
+      t += nwaves;
+      if (t >= t_end) break;
+      if (t + 2 * nwaves < t_end) load_tile<kWordsPerLane>(bufA, a, rec_base, t + 2 * nwaves, lane);
+      score_tile<BITS, NC>(bufB, av, dtab, lane4, a, rec_base, t, cand1, m, ok, qc, qi, obase);
+      t += nwaves;
+      if (t >= t_end) break;
+      if (t + 2 * nwaves < t_end) load_tile<kWordsPerLane>(bufB, a, rec_base, t + 2 * nwaves, lane);
+      score_tile<BITS, NC>(bufC, av, dtab, lane4, a, rec_base, t, cand1, m, ok, qc, qi, obase);
+      t += nwaves;
     }
   }
 }
