@@ -210,6 +210,20 @@ def main():
     resid_e = torch.empty_like(xe)
     log(f"setup {time.time() - t_setup:.1f} s")
 
+    # context: what a plain read-only streaming kernel (a torch reduction over
+    # 4 GiB of the collection) achieves on this device
+    flat = x.view(-1)[: min(x.numel(), 1 << 30)]
+    for _ in range(2):
+        flat.sum()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(5):
+        flat.sum()
+    e1.record()
+    torch.cuda.synchronize()
+    stream_read_GBps = 5 * flat.numel() * 4 / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del flat
+
     batches = [q_all[i:i + args.batch].contiguous() for i in range(0, args.nq, args.batch)]
     sizes = index.list_sizes.long()
     rec_bytes = D * args.bits // 8 + 4
@@ -319,6 +333,8 @@ def main():
             "kernel": f"k_scan<{args.bits},{min(32, max(4, -(-plan.d_pad // 32)))}>",
             "algorithmic_bytes_per_launch": streamed_avg * rec_bytes,
             "kernel_ms": t_scan,
+            "stream_read_GBps_measured": stream_read_GBps,
+            "frac_of_measured_stream": achieved / stream_read_GBps,
         },
         "scan": {
             "pairs_per_step": pairs_avg,

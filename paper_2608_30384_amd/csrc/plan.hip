@@ -196,7 +196,25 @@ int rslm_plan_create(const rslm_plan_desc *d, rslm_plan **out) {
   p->dtab_entries = entries;
   p->dtab_words = words;
 
+  // source index of every output of the strided transpose, x'[k M + b] = x[b B + P(k)]
+  // for the first M B outputs, identity on the tail
+  int16_t *tsrc = new (std::nothrow) int16_t[D];
+  if (!tsrc) {
+    rslm_plan_destroy(p);
+    return RSLM_ERR_HIP;
+  }
+  {
+    const int M = r.n_full, MB = r.n_full * r.B;
+    for (int o = 0; o < D; ++o) tsrc[o] = int16_t(o < MB ? (o % M) * r.B + pi[o / M] : o);
+  }
   hipError_t e;
+  if ((e = hipMalloc(&p->d_tsrc, sizeof(int16_t) * D)) != hipSuccess ||
+      (e = hipMemcpy(p->d_tsrc, tsrc, sizeof(int16_t) * D, hipMemcpyHostToDevice)) != hipSuccess) {
+    delete[] tsrc;
+    rslm_plan_destroy(p);
+    return set_hip_error(e);
+  }
+  delete[] tsrc;
   if ((e = hipMalloc(&p->d_s1, sizeof(s1f))) != hipSuccess ||
       (e = hipMalloc(&p->d_pi, sizeof(pi))) != hipSuccess ||
       (e = hipMalloc(&p->d_dtab, sizeof(uint32_t) * entries * words)) != hipSuccess) {
@@ -212,6 +230,7 @@ int rslm_plan_create(const rslm_plan_desc *d, rslm_plan **out) {
   }
   r.s1 = p->d_s1;
   r.pi = p->d_pi;
+  r.tsrc = p->d_tsrc;
   for (int w = 0; w < 8; ++w) {
     uint32_t m = 0;
     for (int b = 0; b < 32; ++b)
@@ -227,6 +246,7 @@ int rslm_plan_destroy(rslm_plan *p) {
   if (p->d_s1) (void)hipFree(p->d_s1);
   if (p->d_pi) (void)hipFree(p->d_pi);
   if (p->d_dtab) (void)hipFree(p->d_dtab);
+  if (p->d_tsrc) (void)hipFree(p->d_tsrc);
   delete p;
   return RSLM_OK;
 }

@@ -43,27 +43,35 @@ __device__ __forceinline__ void fwht128_reg(float (&x)[J], int lane) {
   }
 }
 
-__device__ __forceinline__ int tsrc(int o, int M, const int16_t *pi) {
-  const int k = o / M;
-  const int b = o - k * M;
-  return b * 128 + int(pi[k]);
+// Per-lane sign words: element j of the lane takes sign word w[j mod 4]
+// (the sign index pattern repeats every 256 = 4 x 64 elements).
+struct SignWords {
+  uint32_t w[4];
+};
+__device__ __forceinline__ SignWords sign_words(uint32_t bits) {
+  SignWords s;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) s.w[t] = ((bits >> t) & 1u) << 31;
+  return s;
+}
+__device__ __forceinline__ float flipw(float v, const SignWords &s, int j) {
+  return __uint_as_float(__float_as_uint(v) ^ s.w[j & 3]);
 }
 
 // Forward rotation of x (already multiplied by S1) through buf (LDS, >= D +
 // D/32 floats) for the transpose.
 template <int J>
 __device__ __forceinline__ void rotate_fwd_reg(float (&x)[J], const RotParams &rp,
-                                               const int16_t *pi, uint32_t s2bits, float *buf,
+                                               const int16_t *ts, const SignWords &s2, float *buf,
                                                int lane) {
   if (rp.passes == 0) return;
   fwht128_reg<J>(x, lane);
   if (rp.passes == 1) return;
-  const int M = rp.n_full;
 #pragma unroll
   for (int j = 0; j < J; ++j) buf[px_r(lane + 64 * j)] = x[j];
   wave_sync_r();
 #pragma unroll
-  for (int j = 0; j < J; ++j) x[j] = flip(buf[px_r(tsrc(lane + 64 * j, M, pi))], s2bits, j);
+  for (int j = 0; j < J; ++j) x[j] = flipw(buf[px_r(ts[lane + 64 * j])], s2, j);
   wave_sync_r();
   fwht128_reg<J>(x, lane);
 }
@@ -71,14 +79,13 @@ __device__ __forceinline__ void rotate_fwd_reg(float (&x)[J], const RotParams &r
 // Inverse rotation R^T (without the final S1, applied by the caller).
 template <int J>
 __device__ __forceinline__ void rotate_inv_reg(float (&x)[J], const RotParams &rp,
-                                               const int16_t *pi, uint32_t s2bits, float *buf,
+                                               const int16_t *ts, const SignWords &s2, float *buf,
                                                int lane) {
   if (rp.passes == 0) return;
   fwht128_reg<J>(x, lane);
   if (rp.passes == 1) return;
-  const int M = rp.n_full;
 #pragma unroll
-  for (int j = 0; j < J; ++j) buf[px_r(tsrc(lane + 64 * j, M, pi))] = flip(x[j], s2bits, j);
+  for (int j = 0; j < J; ++j) buf[px_r(ts[lane + 64 * j])] = flipw(x[j], s2, j);
   wave_sync_r();
 #pragma unroll
   for (int j = 0; j < J; ++j) x[j] = buf[px_r(lane + 64 * j)];
@@ -86,8 +93,10 @@ __device__ __forceinline__ void rotate_inv_reg(float (&x)[J], const RotParams &r
   fwht128_reg<J>(x, lane);
 }
 
-__device__ __forceinline__ void load_perm_r(const RotParams &rp, int16_t *pi) {
-  for (int k = threadIdx.x; k < 128; k += blockDim.x) pi[k] = rp.pi[k];
+// Workgroup prologue: LDS copy of the transpose source table (D entries).
+__device__ __forceinline__ void load_tsrc_r(const RotParams &rp, int16_t *ts) {
+  if (rp.passes == 2)
+    for (int k = threadIdx.x; k < rp.D; k += blockDim.x) ts[k] = rp.tsrc[k];
   __syncthreads();
 }
 
@@ -96,27 +105,27 @@ __global__ void __launch_bounds__(256) k_rotate_reg(const float *__restrict__ x,
                                                     int64_t n, RotParams rp, int inverse,
                                                     int dstride) {
   extern __shared__ float lds[];
-  __shared__ int16_t pi[128];
-  load_perm_r(rp, pi);
+  __shared__ int16_t ts[64 * J];
+  load_tsrc_r(rp, ts);
   const int lane = threadIdx.x & 63;
   const int wid = threadIdx.x >> 6;
   const int64_t row = int64_t(blockIdx.x) * (blockDim.x >> 6) + wid;
   if (row >= n) return;   // no workgroup barriers below
   float *buf = lds + wid * dstride;
   const uint2 sm = lane_sign_masks(rp, lane);
-  const bool signs = rp.passes > 0;
+  const SignWords s1 = sign_words(rp.passes > 0 ? sm.x : 0u), s2 = sign_words(sm.y);
   const float *xr = x + row * (64 * J);
   float v[J];
 #pragma unroll
   for (int j = 0; j < J; ++j) v[j] = xr[lane + 64 * j];
   if (!inverse) {
 #pragma unroll
-    for (int j = 0; j < J; ++j) v[j] = flip(v[j], signs ? sm.x : 0u, j);
-    rotate_fwd_reg<J>(v, rp, pi, sm.y, buf, lane);
+    for (int j = 0; j < J; ++j) v[j] = flipw(v[j], s1, j);
+    rotate_fwd_reg<J>(v, rp, ts, s2, buf, lane);
   } else {
-    rotate_inv_reg<J>(v, rp, pi, sm.y, buf, lane);
+    rotate_inv_reg<J>(v, rp, ts, s2, buf, lane);
 #pragma unroll
-    for (int j = 0; j < J; ++j) v[j] = flip(v[j], signs ? sm.x : 0u, j);
+    for (int j = 0; j < J; ++j) v[j] = flipw(v[j], s1, j);
   }
   float *yr = y + row * (64 * J);
 #pragma unroll
@@ -144,12 +153,12 @@ __global__ void __launch_bounds__(256) k_encode_reg(
   constexpr int D = 64 * J;
   extern __shared__ float lds[];
   __shared__ float cbs[16];
-  __shared__ int16_t pi[128];
+  __shared__ int16_t ts[D];
   const int lane = threadIdx.x & 63;
   const int wid = threadIdx.x >> 6;
   const int nw = blockDim.x >> 6;
   if (threadIdx.x < 16) cbs[threadIdx.x] = cp.cb[threadIdx.x];
-  load_perm_r(rp, pi);
+  load_tsrc_r(rp, ts);
   const int64_t rec = int64_t(blockIdx.x) * nw + wid;
   int64_t row = -1;
   int L = -1;
@@ -164,6 +173,7 @@ __global__ void __launch_bounds__(256) k_encode_reg(
   if (row < 0) return;   // no workgroup barriers below
   float *buf = lds + wid * dstride;
   const uint2 sm = lane_sign_masks(rp, lane);
+  const SignWords s1 = sign_words(rp.passes > 0 ? sm.x : 0u), s2 = sign_words(sm.y);
 
   // residual r = x - c, its sums, and S1
   const float *xr = x + row * D;
@@ -183,9 +193,9 @@ __global__ void __launch_bounds__(256) k_encode_reg(
     xx += xv * xv;
     rr += r * r;
     cc += cv * cv;
-    z[j] = flip(r, rp.passes > 0 ? sm.x : 0u, j);
+    z[j] = flipw(r, s1, j);
   }
-  rotate_fwd_reg<J>(z, rp, pi, sm.y, buf, lane);
+  rotate_fwd_reg<J>(z, rp, ts, s2, buf, lane);
 
   // EVT scale and 1-D Lloyd-Max codes
   float m = 0.f;

@@ -26,6 +26,7 @@ struct RotParams {
   float inv_sqrt_b;
   const float *s1;     // device, 256 signs (+1/-1) as float
   const int16_t *pi;   // device, intra-block permutation of size B
+  const int16_t *tsrc; // device, D entries: source of output o of the strided transpose
   uint32_t s1mask[8];  // bit i set <=> S1[i] = -1
 };
 
@@ -83,6 +84,7 @@ struct rslm_plan {
   // device allocations owned by the plan
   float *d_s1 = nullptr;
   int16_t *d_pi = nullptr;
+  int16_t *d_tsrc = nullptr;
   uint32_t *d_dtab = nullptr;   // compact decode table (see scan.hip)
   int dtab_entries = 0;
   int dtab_words = 0;           // 32-bit words per entry
