@@ -30,10 +30,12 @@ namespace rslm {
 
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kChunkCands = 1024;   // candidates per work item
 constexpr int kGroupQ = 8;          // queries per work item (16 MFMA rows / 2)
 constexpr int kScanThreads = 256;
+static_assert(kChunkCands / 16 <= 4 * 16, "a wave scores at most 16 tiles of an item");
 
 static size_t align256(size_t b) { return (b + 255) / 256 * 256; }
 
@@ -42,6 +44,7 @@ struct ScanWs {
   float *qinv;
   int32_t *counts, *cursor, *pair_off, *item_off;
   int32_t *pairs, *prefix, *totals;
+  int4 *items;            // two int4 per work item (see k_plan_items)
   float *scores;
   uint32_t *thr, *cnt;    // per-query top-k threshold and survivor count
   uint64_t *surv;         // per-query survivors, kSurvCap each
@@ -69,6 +72,14 @@ static ScanWs scan_ws_layout(void *base, int Q, int nprobe, int nlist, int d_pad
   w.pairs = reinterpret_cast<int32_t *>(take(size_t(Q) * nprobe * 4));
   w.prefix = reinterpret_cast<int32_t *>(take(size_t(Q) * nprobe * 4));
   w.totals = reinterpret_cast<int32_t *>(take(size_t(Q) * 4));
+  {
+    // work items <= (groups of <= 8 queries) x (chunks of the longest list);
+    // groups <= npairs / 8 + (number of probed lists)
+    const int64_t npairs = int64_t(Q) * nprobe;
+    const int64_t groups = npairs / kGroupQ + std::min<int64_t>(nlist, npairs);
+    const int64_t chunks = std::max<int64_t>(1, (int64_t(max_list) + kChunkCands - 1) / kChunkCands);
+    w.items = reinterpret_cast<int4 *>(take(size_t(groups * chunks) * 2 * sizeof(int4)));
+  }
   w.stride = (int64_t(nprobe) * max_list + 63) / 64 * 64;
   w.scores = reinterpret_cast<float *>(take(size_t(Q) * size_t(w.stride) * 4));
   (void)k;
@@ -209,6 +220,35 @@ __global__ void k_plan_fill(const int32_t *__restrict__ probe_ids, int npairs, i
   pairs[pair_off[L] + pos] = i;
 }
 
+// One thread per list: the descriptors of the list's work items, in the
+// order of item_off.  Item = (group of <= 8 consecutive probing pairs,
+// chunk of <= kChunkCands candidates):
+//   d0 = {list, first candidate, candidate count, first pair (in pairs[])}
+//   d1 = {queries in the group, first record (low, high word), 0}
+__global__ void k_plan_items(const int32_t *__restrict__ counts, const int32_t *__restrict__ sizes,
+                             const int64_t *__restrict__ list_offsets, int nlist, int max_list,
+                             const int32_t *__restrict__ pair_off,
+                             const int32_t *__restrict__ item_off, int4 *__restrict__ items) {
+  const int L = blockIdx.x * blockDim.x + threadIdx.x;
+  if (L >= nlist) return;
+  const int c = counts[L];
+  const int sz = max(0, min(sizes[L], max_list));
+  if (c <= 0 || sz <= 0) return;
+  const int nch = (sz + kChunkCands - 1) / kChunkCands;
+  const int ngr = (c + kGroupQ - 1) / kGroupQ;
+  int it = item_off[L];
+  for (int g = 0; g < ngr; ++g) {
+    for (int ch = 0; ch < nch; ++ch, ++it) {
+      const int cand0 = ch * kChunkCands;
+      const int64_t rec0 = list_offsets[L] + cand0;
+      items[2 * int64_t(it)] = make_int4(L, cand0, min(sz - cand0, kChunkCands),
+                                         pair_off[L] + g * kGroupQ);
+      items[2 * int64_t(it) + 1] = make_int4(min(kGroupQ, c - g * kGroupQ), int(uint32_t(rec0)),
+                                             int(uint32_t(uint64_t(rec0) >> 32)), 0);
+    }
+  }
+}
+
 // ------------------------------------------------------------- scan kernel
 struct ScanArgs {
   const int64_t *list_offsets;
@@ -219,7 +259,8 @@ struct ScanArgs {
   const _Float16 *qh, *ql;
   const float *qinv;
   const float *probe_dots;
-  const int32_t *counts, *pair_off, *item_off, *pairs, *prefix;
+  const int32_t *item_off, *pairs, *prefix;
+  const int4 *items;
   float *scores;
   int64_t stride;
   int nlist, nprobe, d_pad, n_chunks, tile_bytes, lane_units, max_list;
@@ -286,18 +327,37 @@ __device__ __forceinline__ half8 decode8(const uint32_t *tab, uint32_t bits, uin
   return r.h;
 }
 
+// Buffer resources (gfx9 format: 48-bit base, stride 0, byte range, data
+// format word).  A raw buffer access past the range returns zeros (loads) or
+// is dropped (stores) without touching memory, so prefetches of tiles beyond
+// a work item need no branch.  Unconditional loads let the compiler count
+// outstanding loads exactly, which keeps the prefetched tiles in flight.
+constexpr int kRsrcWord3 = 0x00020000;
+// s_waitcnt immediate (gfx9 encoding) waiting for vmcnt = 0 only
+// (expcnt = 7 and lgkmcnt = 15 are "do not wait").
+constexpr int kWaitVmcnt0 = 0x0F70;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, int(bytes),
+                                           kRsrcWord3);
+}
+
+// Codes of local tile lt of a work item: this lane's 16-byte units.  The
+// resource is rebuilt per tile in scalar registers (base advanced by lt
+// tiles, range one tile, or zero past the item), so the per-lane offsets are
+// loop invariant and the tile loop does no vector address arithmetic.
 template <int W>
-__device__ __forceinline__ void load_tile(uint32_t (&sw)[W], const ScanArgs &a, int64_t rec_base,
-                                          int t, int lane) {
-  const int64_t rec0 = rec_base + int64_t(t) * 16;
-  const uint8_t *tp = a.codes + (rec0 >> 4) * a.tile_bytes + lane * 16;
+__device__ __forceinline__ void load_tile(uint32_t (&w)[W], const uint8_t *tiles, int lt,
+                                          int n_tiles, uint32_t tile_bytes, uint32_t voff) {
+  const __amdgpu_buffer_rsrc_t r =
+      make_rsrc(tiles + int64_t(lt) * tile_bytes, lt < n_tiles ? tile_bytes : 0u);
 #pragma unroll
   for (int u = 0; u < W / 4; ++u) {
-    const uint4 v = *reinterpret_cast<const uint4 *>(tp + u * 1024);
-    sw[4 * u + 0] = v.x;
-    sw[4 * u + 1] = v.y;
-    sw[4 * u + 2] = v.z;
-    sw[4 * u + 3] = v.w;
+    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, voff + u * 1024u, 0, 0);
+    w[4 * u + 0] = v.x;
+    w[4 * u + 1] = v.y;
+    w[4 * u + 2] = v.z;
+    w[4 * u + 3] = v.w;
   }
 }
 
@@ -305,32 +365,32 @@ __device__ __forceinline__ void load_tile(uint32_t (&sw)[W], const ScanArgs &a, 
 // lane (kq, m) ends with rows 4 kq + {0,1,2,3} of candidate column m, i.e.
 // query slots 2 kq (hi, lo) and 2 kq + 1 (hi, lo).
 template <int BITS, int NC, int W>
-__device__ __forceinline__ void score_tile(const uint32_t (&sw)[W], const half8 (&av)[NC],
-                                           const uint32_t *dtab, uint32_t lane4,
-                                           const ScanArgs &a, int64_t rec_base, int t, int cand1,
-                                           int m, const bool (&ok)[2], const float (&qc)[2],
-                                           const float (&qi)[2], const int64_t (&obase)[2]) {
+__device__ __forceinline__ void score_tile(const uint32_t (&tw)[W], uint32_t sc,
+                                           const half8 (&av)[NC], const uint32_t *dtab,
+                                           uint32_t lane4, int lt, int n_cand, int m,
+                                           const bool (&ok)[2],
+                                           const float (&qc)[2], const float (&qi)[2],
+                                           float *const (&out)[2]) {
   // Decoding runs two chunks ahead of the matrix multiply so that the LDS
   // latency of chunk c + 2 overlaps the MFMAs of chunks c and c + 1; even and
   // odd chunks accumulate separately to halve the dependent MFMA chain.
   floatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
   half8 b[3];
-  b[0] = decode8<BITS>(dtab, chunk_bits<BITS>(sw, 0), lane4);
-  if (NC > 1) b[1] = decode8<BITS>(dtab, chunk_bits<BITS>(sw, NC > 1 ? 1 : 0), lane4);
+  b[0] = decode8<BITS>(dtab, chunk_bits<BITS>(tw, 0), lane4);
+  if (NC > 1) b[1] = decode8<BITS>(dtab, chunk_bits<BITS>(tw, NC > 1 ? 1 : 0), lane4);
 #pragma unroll
   for (int c = 0; c < NC; ++c) {
-    if (c + 2 < NC) b[(c + 2) % 3] = decode8<BITS>(dtab, chunk_bits<BITS>(sw, c + 2 < NC ? c + 2 : 0), lane4);
+    if (c + 2 < NC) b[(c + 2) % 3] = decode8<BITS>(dtab, chunk_bits<BITS>(tw, c + 2 < NC ? c + 2 : 0), lane4);
     if (c & 1) acc1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(av[c], b[c % 3], acc1, 0, 0, 0);
     else acc0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(av[c], b[c % 3], acc0, 0, 0, 0);
   }
   const floatx4 acc = acc0 + acc1;
-  const int cand = t * 16 + m;
-  if (cand < cand1) {
-    const uint32_t sc = a.scales[rec_base + int64_t(t) * 16 + m];
+  const int cand = lt * 16 + m;   // item-local candidate index
+  if (cand < n_cand) {
     const float sh = dec_ue7m9(sc & 0xffffu);
     const float gh = dec_ue4m12(sc >> 16);
-    if (ok[0]) a.scores[obase[0] + cand] = gh * (qc[0] + sh * ((acc[0] + acc[1]) * qi[0]));
-    if (ok[1]) a.scores[obase[1] + cand] = gh * (qc[1] + sh * ((acc[2] + acc[3]) * qi[1]));
+    if (ok[0]) out[0][cand] = gh * (qc[0] + sh * ((acc[0] + acc[1]) * qi[0]));
+    if (ok[1]) out[1][cand] = gh * (qc[1] + sh * ((acc[2] + acc[3]) * qi[1]));
   }
 }
 
@@ -341,7 +401,7 @@ __global__ void __launch_bounds__(kScanThreads) k_scan(ScanArgs a) {
   constexpr int kWordsPerLane = ((NC * BITS + 15) / 16) * 4;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: scalar loop control
   const int nwaves = kScanThreads / 64;
   const uint32_t lane4 = uint32_t(lane) * 4u;
 
@@ -354,28 +414,21 @@ __global__ void __launch_bounds__(kScanThreads) k_scan(ScanArgs a) {
   }
   __syncthreads();
 
-  const int n_items = a.item_off[a.nlist];
+  const int n_items = __builtin_amdgcn_readfirstlane(a.item_off[a.nlist]);
   const int m = lane & 15;           // A row / B column of this lane
   const int kq = lane >> 4;          // k-quarter: coordinates 8 kq .. 8 kq + 7 of a chunk
   for (int item = blockIdx.x; item < n_items; item += gridDim.x) {
-    // list of this item: last L with item_off[L] <= item
-    int lo = 0, hi = a.nlist;
-    while (hi - lo > 1) {
-      const int mid = (lo + hi) >> 1;
-      if (a.item_off[mid] <= item) lo = mid;
-      else hi = mid;
-    }
-    const int L = lo;
-    const int local = item - a.item_off[L];
-    const int size = max(0, min(a.list_sizes[L], a.max_list));
-    const int nch = (size + kChunkCands - 1) / kChunkCands;
-    const int gi = local / nch;
-    const int ci = local - gi * nch;
-    const int npair = a.counts[L];
-    const int G = min(kGroupQ, npair - gi * kGroupQ);
-    const int cand0 = ci * kChunkCands;
-    const int cand1 = min(size, cand0 + kChunkCands);
-    const int pbase = a.pair_off[L] + gi * kGroupQ;
+    // The descriptor is the same for the whole wavefront: readfirstlane keeps
+    // every item-level quantity (and so the buffer resources and the tile
+    // loop) in scalar registers.
+    const int4 d0 = a.items[2 * int64_t(item)];
+    const int4 d1 = a.items[2 * int64_t(item) + 1];
+    const int cand0 = __builtin_amdgcn_readfirstlane(d0.y);
+    const int n_cand = __builtin_amdgcn_readfirstlane(d0.z);
+    const int pbase = __builtin_amdgcn_readfirstlane(d0.w);
+    const int G = __builtin_amdgcn_readfirstlane(d1.x);
+    const int64_t rec0 = int64_t((uint64_t(uint32_t(__builtin_amdgcn_readfirstlane(d1.z))) << 32) |
+                                 uint32_t(__builtin_amdgcn_readfirstlane(d1.y)));
 
     // A operands: row m = 2 * slot + part (part 0 = hi, 1 = lo)
     half8 av[NC];
@@ -411,27 +464,48 @@ __global__ void __launch_bounds__(kScanThreads) k_scan(ScanArgs a) {
         obase[i] = int64_t(q) * a.stride + a.prefix[pr];
       }
     }
-    const int64_t rec_base = a.list_offsets[L];
-    const int t_end = (cand1 + 15) / 16;
-    // Software pipeline, depth 2: the codes of the wave's next two tiles are
-    // in flight while the current tile is decoded and multiplied.
-    uint32_t bufA[kWordsPerLane], bufB[kWordsPerLane], bufC[kWordsPerLane];
-    int t = cand0 / 16 + wave;
-    if (t < t_end) load_tile<kWordsPerLane>(bufA, a, rec_base, t, lane);
-    if (t + nwaves < t_end) load_tile<kWordsPerLane>(bufB, a, rec_base, t + nwaves, lane);
-    while (t < t_end) {
-      if (t + 2 * nwaves < t_end) load_tile<kWordsPerLane>(bufC, a, rec_base, t + 2 * nwaves, lane);
-      score_tile<BITS, NC>(bufA, av, dtab, lane4, a, rec_base, t, cand1, m, ok, qc, qi, obase);
-      t += nwaves;
-      if (t >= t_end) break;
-      if (t + 2 * nwaves < t_end) load_tile<kWordsPerLane>(bufA, a, rec_base, t + 2 * nwaves, lane);
-      score_tile<BITS, NC>(bufB, av, dtab, lane4, a, rec_base, t, cand1, m, ok, qc, qi, obase);
-      t += nwaves;
-      if (t >= t_end) break;
-      if (t + 2 * nwaves < t_end) load_tile<kWordsPerLane>(bufB, a, rec_base, t + 2 * nwaves, lane);
-      score_tile<BITS, NC>(bufC, av, dtab, lane4, a, rec_base, t, cand1, m, ok, qc, qi, obase);
-      t += nwaves;
+    const int n_tiles = (n_cand + 15) / 16;
+    float *out[2] = {a.scores + obase[0] + cand0, a.scores + obase[1] + cand0};
+    // lists start on a tile boundary and cand0 is a multiple of 16
+    const uint8_t *tiles = a.codes + (rec0 >> 4) * a.tile_bytes;
+    const uint32_t tb = uint32_t(a.tile_bytes);
+    // Scale words of every tile this wave scores (tile lt = wave + 4 j,
+    // j < 16), loaded before any code tile: lane (kq, m) holds candidate m of
+    // tiles j = kq, kq + 4, kq + 8, kq + 12.  Issued first, they never make
+    // the tile loop wait for code tiles still in flight.
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(a.scales + rec0, uint32_t(n_cand) * 4u);
+    uint32_t sreg[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      sreg[r] = __builtin_amdgcn_raw_buffer_load_b32(
+          rs, uint32_t((wave + nwaves * (kq + 4 * r)) * 16 + m) * 4u, 0, 0);
+    auto scale_of = [&](int j) {   // j is uniform across the wave
+      const int r = j >> 2;
+      const uint32_t v = r == 0 ? sreg[0] : r == 1 ? sreg[1] : r == 2 ? sreg[2] : sreg[3];
+      return uint32_t(__shfl(int(v), 16 * (j & 3) + m, 64));
+    };
+    // Software pipeline, depth 1: the codes of the wave's next tile are in
+    // flight while the current tile is decoded and multiplied.  Tiles past
+    // the item read as zeros from the buffer range check and are not scored.
+    uint32_t bufA[kWordsPerLane], bufB[kWordsPerLane];
+    int lt = wave, j = 0;
+    const uint32_t voff = uint32_t(lane) * 16u;
+    load_tile(bufA, tiles, lt, n_tiles, tb, voff);
+    while (lt < n_tiles) {
+      load_tile(bufB, tiles, lt + nwaves, n_tiles, tb, voff);
+      score_tile<BITS, NC>(bufA, scale_of(j), av, dtab, lane4, lt, n_cand, m, ok, qc, qi, out);
+      lt += nwaves;
+      ++j;
+      if (lt >= n_tiles) break;
+      load_tile(bufA, tiles, lt + nwaves, n_tiles, tb, voff);
+      score_tile<BITS, NC>(bufB, scale_of(j), av, dtab, lane4, lt, n_cand, m, ok, qc, qi, out);
+      lt += nwaves;
+      ++j;
     }
+    // Retire the last (out-of-range, zero-traffic) prefetch before the next
+    // item, so the loop above always starts with a known set of loads in
+    // flight and the compiler keeps its waits partial.
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
   }
 }
 
@@ -665,6 +739,10 @@ int rslm_scan_topk(const rslm_plan *p, const rslm_index *idx, const float *q_rot
   hipLaunchKernelGGL(k_plan_fill, dim3((npairs + 255) / 256), dim3(256), 0, s, probe_ids, npairs,
                      nlist, w.pair_off, w.cursor, w.pairs);
   if ((st = check_launch())) return st;
+  hipLaunchKernelGGL(k_plan_items, dim3((nlist + 255) / 256), dim3(256), 0, s, w.counts,
+                     idx->list_sizes, idx->list_offsets, nlist, idx->max_list_size, w.pair_off,
+                     w.item_off, w.items);
+  if ((st = check_launch())) return st;
 
   ScanArgs a;
   a.list_offsets = idx->list_offsets;
@@ -676,9 +754,8 @@ int rslm_scan_topk(const rslm_plan *p, const rslm_index *idx, const float *q_rot
   a.ql = w.ql;
   a.qinv = w.qinv;
   a.probe_dots = probe_dots;
-  a.counts = w.counts;
-  a.pair_off = w.pair_off;
   a.item_off = w.item_off;
+  a.items = w.items;
   a.pairs = w.pairs;
   a.prefix = w.prefix;
   a.scores = w.scores;
