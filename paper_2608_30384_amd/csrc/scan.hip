@@ -20,6 +20,15 @@
 // is arranged so that each lane's share of a tile is contiguous in 16-byte
 // units and a wavefront's load is 1 KiB contiguous.
 //
+// Scheduling.  A work item is (list, group of <= 8 queries, chunk of the
+// list); lists are cut into equal chunks of at most 1,024 candidates and the
+// items are ordered by decreasing size.  A persistent grid (two 256-thread
+// workgroups per CU) takes items from an atomic counter, so the launch ends
+// on the smallest items.  Within an item each wavefront scores every fourth
+// tile with the next tile's codes in flight; all loads are range-checked
+// buffer loads, so no load is conditional and the compiler's wait counts
+// stay exact.
+//
 // Scores of every candidate are written to a per-query region of the
 // workspace; a second kernel selects each query's top-k exactly (radix
 // select, then a bitonic sort of the survivors) and maps positions to ids.
@@ -45,6 +54,7 @@ struct ScanWs {
   int32_t *counts, *cursor, *pair_off, *item_off;
   int32_t *pairs, *prefix, *totals;
   int4 *items;            // two int4 per work item (see k_plan_items)
+  int32_t *work;          // next work item of the scan (dynamic schedule)
   float *scores;
   uint32_t *thr, *cnt;    // per-query top-k threshold and survivor count
   uint64_t *surv;         // per-query survivors, kSurvCap each
@@ -72,6 +82,7 @@ static ScanWs scan_ws_layout(void *base, int Q, int nprobe, int nlist, int d_pad
   w.pairs = reinterpret_cast<int32_t *>(take(size_t(Q) * nprobe * 4));
   w.prefix = reinterpret_cast<int32_t *>(take(size_t(Q) * nprobe * 4));
   w.totals = reinterpret_cast<int32_t *>(take(size_t(Q) * 4));
+  w.work = reinterpret_cast<int32_t *>(take(4));
   {
     // work items <= (groups of <= 8 queries) x (chunks of the longest list);
     // groups <= npairs / 8 + (number of probed lists)
@@ -159,53 +170,81 @@ __global__ void k_plan_prefix(const int32_t *__restrict__ probe_ids, int Q, int 
   if (lane == 0) totals[q] = carry;
 }
 
-// Single workgroup: exclusive scans over lists of the pair counts and of the
-// work-item counts (groups of <= 8 queries x chunks of candidates).
+// Candidates per work item of a list of sz > 0 candidates: the list is split
+// into the fewest chunks of at most kChunkCands, of equal size rounded up to
+// whole tiles, so the items of a list have (almost) equal work.
+__device__ __forceinline__ int item_cands(int sz) {
+  const int nch = (sz + kChunkCands - 1) / kChunkCands;
+  return ((sz + nch - 1) / nch + 15) & ~15;
+}
+constexpr int kSizeClasses = kChunkCands / 16;   // item size class = cands / 16 - 1
+
+// Single workgroup: exclusive scan over lists of the pair counts, and the
+// position of each list's work items (groups of <= 8 queries x chunks) in an
+// order by decreasing item size, so that the scan hands out its largest
+// items first and finishes on the smallest (counting sort over size classes;
+// the order within a class is immaterial: every item writes its own scores).
+// Also resets the scan's work counter.
 __global__ void __launch_bounds__(1024) k_plan_lists(const int32_t *__restrict__ counts,
                                                      const int32_t *__restrict__ sizes, int nlist,
                                                      int max_list,
                                                      int32_t *__restrict__ pair_off,
                                                      int32_t *__restrict__ item_off,
-                                                     int32_t *__restrict__ cursor) {
-  __shared__ int32_t s_pairs[1024], s_items[1024];
-  __shared__ int32_t carry[2];
+                                                     int32_t *__restrict__ cursor,
+                                                     int32_t *__restrict__ work) {
+  __shared__ int32_t s_pairs[1024];
+  __shared__ int32_t s_hist[kSizeClasses], s_start[kSizeClasses];
+  __shared__ int32_t carry;
   const int t = threadIdx.x;
-  if (t == 0) carry[0] = carry[1] = 0;
+  if (t == 0) carry = 0;
+  if (t < kSizeClasses) s_hist[t] = 0;
   __syncthreads();
+  auto list_items = [&](int L, int &cls) {
+    const int cp = counts[L];
+    const int sz = max(0, min(sizes[L], max_list));
+    if (cp <= 0 || sz <= 0) return 0;
+    const int ic = item_cands(sz);
+    cls = ic / 16 - 1;
+    return ((cp + kGroupQ - 1) / kGroupQ) * ((sz + ic - 1) / ic);
+  };
   for (int base = 0; base < nlist; base += 1024) {
     const int L = base + t;
-    int cp = 0, ci = 0;
+    int cp = 0;
     if (L < nlist) {
       cp = counts[L];
-      const int sz = max(0, min(sizes[L], max_list));
-      ci = (cp > 0 && sz > 0) ? ((cp + kGroupQ - 1) / kGroupQ) * ((sz + kChunkCands - 1) / kChunkCands) : 0;
       cursor[L] = 0;
+      int cls = 0;
+      const int ni = list_items(L, cls);
+      if (ni > 0) atomicAdd(&s_hist[cls], ni);
     }
     s_pairs[t] = cp;
-    s_items[t] = ci;
     __syncthreads();
     for (int off = 1; off < 1024; off <<= 1) {  // Hillis-Steele inclusive scan
       const int a = (t >= off) ? s_pairs[t - off] : 0;
-      const int b = (t >= off) ? s_items[t - off] : 0;
       __syncthreads();
       s_pairs[t] += a;
-      s_items[t] += b;
       __syncthreads();
     }
-    if (L < nlist) {
-      pair_off[L] = carry[0] + s_pairs[t] - cp;
-      item_off[L] = carry[1] + s_items[t] - ci;
-    }
+    if (L < nlist) pair_off[L] = carry + s_pairs[t] - cp;
     __syncthreads();
-    if (t == 1023) {
-      carry[0] += s_pairs[1023];
-      carry[1] += s_items[1023];
-    }
+    if (t == 1023) carry += s_pairs[1023];
     __syncthreads();
   }
   if (t == 0) {
-    pair_off[nlist] = carry[0];
-    item_off[nlist] = carry[1];
+    int run = 0;
+    for (int c = kSizeClasses - 1; c >= 0; --c) {
+      s_start[c] = run;
+      run += s_hist[c];
+    }
+    pair_off[nlist] = carry;
+    item_off[nlist] = run;
+    *work = 0;
+  }
+  __syncthreads();
+  for (int L = t; L < nlist; L += 1024) {
+    int cls = 0;
+    const int ni = list_items(L, cls);
+    item_off[L] = ni > 0 ? atomicAdd(&s_start[cls], ni) : 0;
   }
 }
 
@@ -220,9 +259,9 @@ __global__ void k_plan_fill(const int32_t *__restrict__ probe_ids, int npairs, i
   pairs[pair_off[L] + pos] = i;
 }
 
-// One thread per list: the descriptors of the list's work items, in the
-// order of item_off.  Item = (group of <= 8 consecutive probing pairs,
-// chunk of <= kChunkCands candidates):
+// One thread per list: the descriptors of the list's work items, from
+// item_off[L] on.  Item = (group of <= 8 consecutive probing pairs, chunk of
+// item_cands(size) candidates):
 //   d0 = {list, first candidate, candidate count, first pair (in pairs[])}
 //   d1 = {queries in the group, first record (low, high word), 0}
 __global__ void k_plan_items(const int32_t *__restrict__ counts, const int32_t *__restrict__ sizes,
@@ -234,15 +273,15 @@ __global__ void k_plan_items(const int32_t *__restrict__ counts, const int32_t *
   const int c = counts[L];
   const int sz = max(0, min(sizes[L], max_list));
   if (c <= 0 || sz <= 0) return;
-  const int nch = (sz + kChunkCands - 1) / kChunkCands;
+  const int ic = item_cands(sz);
+  const int nch = (sz + ic - 1) / ic;
   const int ngr = (c + kGroupQ - 1) / kGroupQ;
   int it = item_off[L];
   for (int g = 0; g < ngr; ++g) {
     for (int ch = 0; ch < nch; ++ch, ++it) {
-      const int cand0 = ch * kChunkCands;
+      const int cand0 = ch * ic;
       const int64_t rec0 = list_offsets[L] + cand0;
-      items[2 * int64_t(it)] = make_int4(L, cand0, min(sz - cand0, kChunkCands),
-                                         pair_off[L] + g * kGroupQ);
+      items[2 * int64_t(it)] = make_int4(L, cand0, min(sz - cand0, ic), pair_off[L] + g * kGroupQ);
       items[2 * int64_t(it) + 1] = make_int4(min(kGroupQ, c - g * kGroupQ), int(uint32_t(rec0)),
                                              int(uint32_t(uint64_t(rec0) >> 32)), 0);
     }
@@ -261,6 +300,7 @@ struct ScanArgs {
   const float *probe_dots;
   const int32_t *item_off, *pairs, *prefix;
   const int4 *items;
+  int32_t *work;
   float *scores;
   int64_t stride;
   int nlist, nprobe, d_pad, n_chunks, tile_bytes, lane_units, max_list;
@@ -417,7 +457,20 @@ __global__ void __launch_bounds__(kScanThreads) k_scan(ScanArgs a) {
   const int n_items = __builtin_amdgcn_readfirstlane(a.item_off[a.nlist]);
   const int m = lane & 15;           // A row / B column of this lane
   const int kq = lane >> 4;          // k-quarter: coordinates 8 kq .. 8 kq + 7 of a chunk
-  for (int item = blockIdx.x; item < n_items; item += gridDim.x) {
+  // Dynamic schedule: workgroups take items (largest first) from a counter.
+  // The ticket for the next item is drawn when an item starts and published
+  // in LDS after its tiles are scored (by then the atomic has returned), in
+  // one of two slots: a slot is rewritten only two barriers after it was read.
+  __shared__ int s_ticket[2];
+  if (tid == 0) s_ticket[0] = atomicAdd(a.work, 1);
+  __syncthreads();
+  int k_it = 0;
+  for (int item = __builtin_amdgcn_readfirstlane(s_ticket[0]); item < n_items;
+       ++k_it, item = __builtin_amdgcn_readfirstlane(s_ticket[k_it & 1])) {
+    int next_ticket = 0;
+    // atomicInc (not add): left alone by the compiler's wave-aggregation rewrite,
+    // which would wait for the returned value right here
+    if (tid == 0) next_ticket = int(atomicInc(reinterpret_cast<unsigned *>(a.work), 0x7fffffffu));
     // The descriptor is the same for the whole wavefront: readfirstlane keeps
     // every item-level quantity (and so the buffer resources and the tile
     // loop) in scalar registers.
@@ -506,6 +559,8 @@ __global__ void __launch_bounds__(kScanThreads) k_scan(ScanArgs a) {
     // item, so the loop above always starts with a known set of loads in
     // flight and the compiler keeps its waits partial.
     __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    if (tid == 0) s_ticket[(k_it + 1) & 1] = next_ticket;
+    __syncthreads();
   }
 }
 
@@ -734,7 +789,7 @@ int rslm_scan_topk(const rslm_plan *p, const rslm_index *idx, const float *q_rot
                      nlist, idx->list_sizes, idx->max_list_size, w.prefix, w.totals);
   if ((st = check_launch())) return st;
   hipLaunchKernelGGL(k_plan_lists, dim3(1), dim3(1024), 0, s, w.counts, idx->list_sizes, nlist,
-                     idx->max_list_size, w.pair_off, w.item_off, w.cursor);
+                     idx->max_list_size, w.pair_off, w.item_off, w.cursor, w.work);
   if ((st = check_launch())) return st;
   hipLaunchKernelGGL(k_plan_fill, dim3((npairs + 255) / 256), dim3(256), 0, s, probe_ids, npairs,
                      nlist, w.pair_off, w.cursor, w.pairs);
@@ -756,6 +811,7 @@ int rslm_scan_topk(const rslm_plan *p, const rslm_index *idx, const float *q_rot
   a.probe_dots = probe_dots;
   a.item_off = w.item_off;
   a.items = w.items;
+  a.work = w.work;
   a.pairs = w.pairs;
   a.prefix = w.prefix;
   a.scores = w.scores;
