@@ -58,11 +58,17 @@ __device__ __forceinline__ float flipw(float v, const SignWords &s, int j) {
   return __uint_as_float(__float_as_uint(v) ^ s.w[j & 3]);
 }
 
+// LDS float at a byte offset (the transpose table holds padded byte offsets)
+__device__ __forceinline__ float &lds_at(float *buf, uint32_t byte_off) {
+  return *reinterpret_cast<float *>(reinterpret_cast<char *>(buf) + byte_off);
+}
+
 // Forward rotation of x (already multiplied by S1) through buf (LDS, >= D +
-// D/32 floats) for the transpose.
+// D/32 floats) for the transpose; ts[o] = byte offset in buf of the source of
+// output o.
 template <int J>
 __device__ __forceinline__ void rotate_fwd_reg(float (&x)[J], const RotParams &rp,
-                                               const int16_t *ts, const SignWords &s2, float *buf,
+                                               const uint16_t *ts, const SignWords &s2, float *buf,
                                                int lane) {
   if (rp.passes == 0) return;
   fwht128_reg<J>(x, lane);
@@ -71,7 +77,7 @@ __device__ __forceinline__ void rotate_fwd_reg(float (&x)[J], const RotParams &r
   for (int j = 0; j < J; ++j) buf[px_r(lane + 64 * j)] = x[j];
   wave_sync_r();
 #pragma unroll
-  for (int j = 0; j < J; ++j) x[j] = flipw(buf[px_r(ts[lane + 64 * j])], s2, j);
+  for (int j = 0; j < J; ++j) x[j] = flipw(lds_at(buf, ts[lane + 64 * j]), s2, j);
   wave_sync_r();
   fwht128_reg<J>(x, lane);
 }
@@ -79,13 +85,13 @@ __device__ __forceinline__ void rotate_fwd_reg(float (&x)[J], const RotParams &r
 // Inverse rotation R^T (without the final S1, applied by the caller).
 template <int J>
 __device__ __forceinline__ void rotate_inv_reg(float (&x)[J], const RotParams &rp,
-                                               const int16_t *ts, const SignWords &s2, float *buf,
+                                               const uint16_t *ts, const SignWords &s2, float *buf,
                                                int lane) {
   if (rp.passes == 0) return;
   fwht128_reg<J>(x, lane);
   if (rp.passes == 1) return;
 #pragma unroll
-  for (int j = 0; j < J; ++j) buf[px_r(ts[lane + 64 * j])] = flipw(x[j], s2, j);
+  for (int j = 0; j < J; ++j) lds_at(buf, ts[lane + 64 * j]) = flipw(x[j], s2, j);
   wave_sync_r();
 #pragma unroll
   for (int j = 0; j < J; ++j) x[j] = buf[px_r(lane + 64 * j)];
@@ -93,10 +99,12 @@ __device__ __forceinline__ void rotate_inv_reg(float (&x)[J], const RotParams &r
   fwht128_reg<J>(x, lane);
 }
 
-// Workgroup prologue: LDS copy of the transpose source table (D entries).
-__device__ __forceinline__ void load_tsrc_r(const RotParams &rp, int16_t *ts) {
+// Workgroup prologue: LDS copy of the transpose source table (D entries), as
+// byte offsets into the padded per-wave buffer.
+__device__ __forceinline__ void load_tsrc_r(const RotParams &rp, uint16_t *ts) {
   if (rp.passes == 2)
-    for (int k = threadIdx.x; k < rp.D; k += blockDim.x) ts[k] = rp.tsrc[k];
+    for (int k = threadIdx.x; k < rp.D; k += blockDim.x)
+      ts[k] = uint16_t(4 * px_r(rp.tsrc[k]));
   __syncthreads();
 }
 
@@ -105,7 +113,7 @@ __global__ void __launch_bounds__(256) k_rotate_reg(const float *__restrict__ x,
                                                     int64_t n, RotParams rp, int inverse,
                                                     int dstride) {
   extern __shared__ float lds[];
-  __shared__ int16_t ts[64 * J];
+  __shared__ uint16_t ts[64 * J];
   load_tsrc_r(rp, ts);
   const int lane = threadIdx.x & 63;
   const int wid = threadIdx.x >> 6;
@@ -143,7 +151,7 @@ __device__ __forceinline__ int64_t tile_addr_r(int64_t rec, int G, int t, const 
 }
 
 // Encoder for 1-D codebooks (3 and 4 bits), registers only after the loads.
-template <int J>
+template <int J, int BITS>
 __global__ void __launch_bounds__(256) k_encode_reg(
     const float *__restrict__ x, int64_t n_rows, const int64_t *__restrict__ src_row,
     const int32_t *__restrict__ rec_list, int64_t n_records, const float *__restrict__ cen,
@@ -151,22 +159,35 @@ __global__ void __launch_bounds__(256) k_encode_reg(
     uint32_t *__restrict__ scales, float *__restrict__ resid, RotParams rp, CodecParams cp,
     int dstride) {
   constexpr int D = 64 * J;
+  constexpr int K = 1 << BITS;
   extern __shared__ float lds[];
-  __shared__ float cbs[16];
-  __shared__ int16_t ts[D];
+  __shared__ float cbs[16], thr[16];
+  __shared__ uint16_t ts[D];
   const int lane = threadIdx.x & 63;
-  const int wid = threadIdx.x >> 6;
+  // record, source row and list are the same for the whole wavefront; kept
+  // in scalar registers so every address below is scalar base + lane offset
+  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int nw = blockDim.x >> 6;
-  if (threadIdx.x < 16) cbs[threadIdx.x] = cp.cb[threadIdx.x];
+  if (threadIdx.x < 16) {
+    cbs[threadIdx.x] = cp.cb[threadIdx.x];
+    // sorted decision thresholds, padded with +inf for the binary search
+    thr[threadIdx.x] = (int(threadIdx.x) + 1 < cp.K) ? cp.thr[threadIdx.x] : __builtin_inff();
+  }
   load_tsrc_r(rp, ts);
   const int64_t rec = int64_t(blockIdx.x) * nw + wid;
   int64_t row = -1;
   int L = -1;
   if (rec < n_records) {
-    row = src_row ? src_row[rec] : rec;
+    if (src_row) {
+      const int64_t sr = src_row[rec];
+      row = int64_t((uint64_t(uint32_t(__builtin_amdgcn_readfirstlane(int(uint64_t(sr) >> 32)))) << 32) |
+                    uint32_t(__builtin_amdgcn_readfirstlane(int(uint32_t(sr)))));
+    } else {
+      row = rec;
+    }
     if (row >= n_rows) row = -1;
     if (cen && row >= 0) {
-      L = rec_list[rec];
+      L = __builtin_amdgcn_readfirstlane(rec_list[rec]);
       if (L < 0 || L >= nlist) row = -1;
     }
   }
@@ -203,19 +224,28 @@ __global__ void __launch_bounds__(256) k_encode_reg(
   for (int j = 0; j < J; ++j) m = fmaxf(m, fabsf(z[j]));
   m = wave_max(m);
   const float inv_s0 = (m > 0.f) ? cp.emax / m : 0.f;
-  uint32_t code[J];
+  // Nearest centroid of the sorted 1-D codebook = number of thresholds below
+  // u, by an unrolled binary search over the sorted thresholds; c4 is 4 x the
+  // code (the byte offset of its centroid and thresholds in LDS).
+  uint32_t c4[J];
+#pragma unroll
+  for (int j = 0; j < J; ++j) c4[j] = 0u;
+#pragma unroll
+  for (int half = K >> 1; half >= 1; half >>= 1) {
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      const float u = z[j] * inv_s0;
+      c4[j] += (u > lds_at(thr, c4[j] + 4u * (half - 1))) ? 4u * half : 0u;
+    }
+  }
+  float cv[J];
   float cn2 = 0.f, rcd = 0.f;
 #pragma unroll
   for (int j = 0; j < J; ++j) {
-    const float u = z[j] * inv_s0;
-    uint32_t c = 0;
-#pragma unroll
-    for (int k = 0; k < 15; ++k) c += (k + 1 < cp.K && u > cp.thr[k]) ? 1u : 0u;
-    c = (m > 0.f) ? c : 0u;
-    code[j] = c;
-    const float cv = (m > 0.f) ? cbs[c] : 0.f;
-    cn2 += cv * cv;
-    rcd += rc[j] * cv;
+    c4[j] = (m > 0.f) ? c4[j] : 0u;
+    cv[j] = (m > 0.f) ? lds_at(cbs, c4[j]) : 0.f;
+    cn2 += cv[j] * cv[j];
+    rcd += rc[j] * cv[j];
   }
   xx = wave_sum(xx);
   rr = wave_sum(rr);
@@ -234,16 +264,15 @@ __global__ void __launch_bounds__(256) k_encode_reg(
   if (lane == 0) scales[rec] = su | (gu << 16);
 
   // pack: group G = 8 j + lane / 8 holds the codes of lanes 8 (lane / 8) .. + 7
-  const int w = cp.w;
 #pragma unroll
   for (int j = 0; j < J; ++j) {
-    uint32_t val = code[j] << (w * (lane & 7));
+    uint32_t val = (c4[j] >> 2) << (BITS * (lane & 7));
     val |= __shfl_xor(val, 1, 64);
     val |= __shfl_xor(val, 2, 64);
     val |= __shfl_xor(val, 4, 64);
     if ((lane & 7) == 0) {
       const int G = 8 * j + (lane >> 3);
-      if (cp.bits == 4) {
+      if (BITS == 4) {
         *reinterpret_cast<uint32_t *>(codes + tile_addr_r(rec, G, 0, cp)) = val;
       } else {
         for (int t = 0; t < 3; ++t) codes[tile_addr_r(rec, G, t, cp)] = uint8_t(val >> (8 * t));
@@ -252,17 +281,14 @@ __global__ void __launch_bounds__(256) k_encode_reg(
   }
   // padding groups of the tile layout (d_pad > D) carry code 0
   for (int G = (D >> 3) + lane; G < (cp.d_pad >> 3); G += 64) {
-    if (cp.bits == 4) *reinterpret_cast<uint32_t *>(codes + tile_addr_r(rec, G, 0, cp)) = 0u;
+    if (BITS == 4) *reinterpret_cast<uint32_t *>(codes + tile_addr_r(rec, G, 0, cp)) = 0u;
     else for (int t = 0; t < 3; ++t) codes[tile_addr_r(rec, G, t, cp)] = 0;
   }
   if (resid) {
     const float gh = dec_ue4m12(gu);
     float *out = resid + row * D;   // indexed by source row
 #pragma unroll
-    for (int j = 0; j < J; ++j) {
-      const float cv = (m > 0.f) ? cbs[code[j]] : 0.f;
-      out[lane + 64 * j] = z[j] + rc[j] - gh * (rc[j] + sh * cv);
-    }
+    for (int j = 0; j < J; ++j) out[lane + 64 * j] = z[j] + rc[j] - gh * (rc[j] + sh * cv[j]);
   }
 }
 
@@ -310,12 +336,18 @@ bool launch_encode_reg(const rslm_plan *p, const float *x, int64_t n_rows, const
   const int waves = 4;
   const size_t shm = size_t(waves) * dstride * sizeof(float);
   const unsigned grid = unsigned((n_records + waves - 1) / waves);
-#define CALL(J)                                                                              \
-  hipLaunchKernelGGL((k_encode_reg<J>), dim3(grid), dim3(64 * waves), shm, s, x, n_rows, src_row, \
-                     rec_list, n_records, cen, cen_rot, nlist, codes, scales, resid, p->rot,      \
-                     p->codec, dstride)
+#define CALL_B(J, B)                                                                           \
+  hipLaunchKernelGGL((k_encode_reg<J, B>), dim3(grid), dim3(64 * waves), shm, s, x, n_rows,       \
+                     src_row, rec_list, n_records, cen, cen_rot, nlist, codes, scales, resid,       \
+                     p->rot, p->codec, dstride)
+#define CALL(J)          \
+  if (p->codec.bits == 4) \
+    CALL_B(J, 4);         \
+  else                    \
+    CALL_B(J, 3)
   RSLM_REG_SWITCH(p->rot.D / 128, CALL)
 #undef CALL
+#undef CALL_B
   return true;
 }
 
