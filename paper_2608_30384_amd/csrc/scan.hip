@@ -56,8 +56,6 @@ struct ScanWs {
   int4 *items;            // two int4 per work item (see k_plan_items)
   int32_t *work;          // next work item of the scan (dynamic schedule)
   float *scores;
-  uint32_t *thr, *cnt;    // per-query top-k threshold and survivor count
-  uint64_t *surv;         // per-query survivors, kSurvCap each
   int64_t stride;
   size_t bytes;
 };
@@ -94,9 +92,6 @@ static ScanWs scan_ws_layout(void *base, int Q, int nprobe, int nlist, int d_pad
   w.stride = (int64_t(nprobe) * max_list + 63) / 64 * 64;
   w.scores = reinterpret_cast<float *>(take(size_t(Q) * size_t(w.stride) * 4));
   (void)k;
-  w.thr = reinterpret_cast<uint32_t *>(take(size_t(Q) * 4));
-  w.cnt = reinterpret_cast<uint32_t *>(take(size_t(Q) * 4));
-  w.surv = reinterpret_cast<uint64_t *>(take(size_t(Q) * 4096 * 8));
   w.bytes = off;
   return w;
 }
@@ -584,109 +579,211 @@ struct ScanId {
 };
 
 // ------------------------------------------------------------- top-k
-// Stage 1 (one workgroup per query): a threshold from a strided sample of the
-// query's scores that about 8 k of them reach (at most half the survivor
-// buffer); resets the survivor count.
-constexpr int kSurvCap = 4096;
+// One 1,024-thread workgroup per query streams the query's score region once.
+// Candidates are kept in LDS as (key << 32 | position) for every score whose
+// key is at or above a running threshold T.  T is the lower edge of a radix
+// bin that holds the k-th largest key among the candidates kept so far, so T
+// never exceeds the k-th largest key of the whole region: every element of
+// the exact top-k (ties at its k-th key included) is kept.  When more than
+// kStreamSoft candidates are held, T is raised by radix selection over them
+// and the buffer is compacted.  At the end the survivors (usually a few
+// hundred) get their ids and are sorted by (score desc, id asc).  If the
+// buffer ever overflows (runs of equal keys wider than it), the exact block
+// selection runs over the whole region instead.
+constexpr int kStreamThreads = 1024;
+constexpr int kStreamCap = 4096;
+constexpr int kStreamSoft = 2048;
 
-__global__ void __launch_bounds__(kSelThreads) k_topk_sample(const float *__restrict__ scores,
-                                                             int64_t stride,
-                                                             const int32_t *__restrict__ totals,
-                                                             int k, uint32_t *__restrict__ thr,
-                                                             uint32_t *__restrict__ cnt) {
-  __shared__ SelectSmem sm;
-  const int q = blockIdx.x;
-  const int n = totals[q];
-  uint32_t t = 0u;   // keep everything when the region is small
-  if (n > kSurvCap) t = sample_threshold(scores + int64_t(q) * stride, n, k, sm,
-                                         min(8 * k, kSurvCap / 2));
-  if (threadIdx.x == 0) {
-    thr[q] = t;
-    cnt[q] = 0u;
-  }
-}
+struct StreamSmem {
+  uint64_t buf[2][kStreamCap];
+  uint32_t hist[4096];
+  uint32_t bcast[4];
+  uint32_t count[2];
+  uint32_t overflow;
+  int32_t spre[kMaxNprobe], sprobe[kMaxNprobe];
+};
 
-// Stage 2 (streaming, all queries at once): every score at or above its
-// query's threshold is appended, as (key << 32 | position), to the query's
-// survivor list.  A workgroup covers 4,096 positions of one query with
-// 16-byte loads, stages its survivors in LDS and reserves their slots with a
-// single device atomic (per-survivor atomics on one counter serialise).
-__global__ void __launch_bounds__(256) k_topk_filter(const float *__restrict__ scores,
-                                                     int64_t stride,
-                                                     const int32_t *__restrict__ totals,
-                                                     const uint32_t *__restrict__ thr,
-                                                     uint32_t *__restrict__ cnt,
-                                                     uint64_t *__restrict__ surv) {
-  __shared__ uint64_t stage[4096];
-  __shared__ uint32_t lcount, gbase;
-  const int q = blockIdx.y;
-  const int n = totals[q];
-  const int base = blockIdx.x * 4096;
-  if (base >= n) return;   // uniform per workgroup
-  const uint32_t t = thr[q];
-  const float *row = scores + int64_t(q) * stride;   // stride is a multiple of 64
-  if (threadIdx.x == 0) lcount = 0;
-  float4 v[4];
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int i = base + (u * 256 + int(threadIdx.x)) * 4;
-    v[u] = (i < n) ? *reinterpret_cast<const float4 *>(row + i) : make_float4(0.f, 0.f, 0.f, 0.f);
-  }
+// The highest bin bb of hist[0..nb) with above + sum(hist[bb..nb)) >= k, and
+// the count strictly above it, into bcast[0..1].  Every thread must call it.
+__device__ __forceinline__ void stream_boundary(StreamSmem &sm, int nb, uint32_t above,
+                                                uint32_t k) {
   __syncthreads();
+  if (threadIdx.x < 64) {
+    const int lane = threadIdx.x;
+    const int per = nb / 64;
+    const int hi = nb - lane * per;   // lane 0 owns the highest bins
+    uint32_t sum = 0;
+    for (int b = hi - per; b < hi; ++b) sum += sm.hist[b];
+    uint32_t incl = sum;
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int i = base + (u * 256 + int(threadIdx.x)) * 4;
-    const float e[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const uint32_t key = order_key(e[c]);
-      if (i + c < n && key >= t) {
-        const uint32_t pos = atomicAdd(&lcount, 1u);
-        stage[pos] = (uint64_t(key) << 32) | uint32_t(i + c);
+    for (int off = 1; off < 64; off <<= 1) {
+      const uint32_t t = __shfl_up(incl, off, 64);
+      if (lane >= off) incl += t;
+    }
+    const uint32_t excl = incl - sum;
+    const uint64_t mask = __ballot(above + excl < k && above + incl >= k);
+    const int owner = mask ? __ffsll((unsigned long long)mask) - 1 : 63;
+    if (lane == owner) {
+      uint32_t acc = above + excl;
+      int bb = hi - per;
+      for (int b = hi - 1; b >= hi - per; --b) {
+        if (acc + sm.hist[b] >= k) {
+          bb = b;
+          break;
+        }
+        acc += sm.hist[b];
       }
+      sm.bcast[0] = uint32_t(bb);
+      sm.bcast[1] = acc;
     }
   }
   __syncthreads();
-  const uint32_t m = lcount;
-  if (threadIdx.x == 0) gbase = m ? atomicAdd(&cnt[q], m) : 0u;
-  __syncthreads();
-  const uint32_t g0 = gbase;
-  for (uint32_t j = threadIdx.x; j < m; j += blockDim.x)
-    if (g0 + j < uint32_t(kSurvCap)) surv[int64_t(q) * kSurvCap + g0 + j] = stage[j];
 }
 
-// Stage 3 (one workgroup per query): ids of the survivors (binary search of
-// the query's probe prefix in LDS), exact sort by (score desc, id asc), the k
-// best out.  When the sample misjudged (fewer than k or more than the buffer
-// survived) the exact block selection runs over the whole region instead.
-__global__ void __launch_bounds__(kSelThreads) k_topk_final(
+// Raises the threshold over the cnt >= k candidates of buffer `cur`: radix
+// passes (12, 12, 8 bits) narrow the bin holding the k-th largest key until
+// at most `target` candidates are at or above its lower edge; returns that
+// edge (never above the k-th largest key).
+__device__ uint32_t stream_threshold(StreamSmem &sm, int cur, int cnt, int k, int target) {
+  const int tid = threadIdx.x, nt = blockDim.x;
+  uint32_t prefix = 0, above = 0, edge = 0;
+  int pbits = 0;
+  const int digits[3] = {12, 12, 8};
+  for (int di = 0; di < 3; ++di) {
+    const int d = digits[di], nb = 1 << d, shift = 32 - pbits - d;
+    for (int b = tid; b < nb; b += nt) sm.hist[b] = 0;
+    __syncthreads();
+    for (int i = tid; i < cnt; i += nt) {
+      const uint32_t key = uint32_t(sm.buf[cur][i] >> 32);
+      if (pbits == 0 || (key >> (32 - pbits)) == prefix)
+        atomicAdd(&sm.hist[(key >> shift) & (nb - 1)], 1u);
+    }
+    stream_boundary(sm, nb, above, uint32_t(k));
+    const uint32_t bb = sm.bcast[0];
+    const uint32_t in_bin = sm.hist[bb];
+    above = sm.bcast[1];
+    prefix = (prefix << d) | bb;
+    pbits += d;
+    edge = prefix << (32 - pbits);
+    __syncthreads();
+    if (above + in_bin <= uint32_t(target)) break;
+  }
+  return edge;
+}
+
+// Moves the candidates of buffer `cur` with key >= T to the other buffer;
+// returns their number.
+__device__ int stream_compact(StreamSmem &sm, int cur, int cnt, uint32_t T) {
+  const int tid = threadIdx.x, nt = blockDim.x;
+  if (tid == 0) sm.count[cur ^ 1] = 0;
+  __syncthreads();
+  for (int i = tid; i < cnt; i += nt) {
+    const uint64_t e = sm.buf[cur][i];
+    if (uint32_t(e >> 32) >= T) sm.buf[cur ^ 1][atomicAdd(&sm.count[cur ^ 1], 1u)] = e;
+  }
+  __syncthreads();
+  return int(sm.count[cur ^ 1]);
+}
+
+__global__ void __launch_bounds__(kStreamThreads) k_topk_stream(
     const float *__restrict__ scores, int64_t stride, const int32_t *__restrict__ totals,
-    const uint32_t *__restrict__ cnt, const uint64_t *__restrict__ surv,
     const int32_t *__restrict__ prefix, const int32_t *__restrict__ probe_ids, int nprobe,
     const int64_t *__restrict__ list_offsets, const int32_t *__restrict__ ids, int k,
     float *__restrict__ out_s, int32_t *__restrict__ out_i) {
-  __shared__ uint64_t buf[kSurvCap];
-  __shared__ int32_t spre[kMaxNprobe], sprobe[kMaxNprobe];
+  __shared__ StreamSmem sm;
+  const int tid = threadIdx.x, nt = blockDim.x;
   const int q = blockIdx.x;
-  const int n = totals[q];
-  const uint32_t c = cnt[q];
-  for (int p = threadIdx.x; p < nprobe; p += blockDim.x) {
-    spre[p] = prefix[int64_t(q) * nprobe + p];
-    sprobe[p] = probe_ids[int64_t(q) * nprobe + p];
+  const int n = __builtin_amdgcn_readfirstlane(totals[q]);
+  const float *row = scores + int64_t(q) * stride;   // stride: a multiple of 64
+  for (int p = tid; p < nprobe; p += nt) {
+    sm.spre[p] = prefix[int64_t(q) * nprobe + p];
+    sm.sprobe[p] = probe_ids[int64_t(q) * nprobe + p];
   }
+  if (tid == 0) sm.overflow = 0;
+  // the first kStreamCap scores are all candidates
+  const int n0 = min(n, kStreamCap);
+  for (int i = tid; i < n0; i += nt) sm.buf[0][i] = (uint64_t(order_key(row[i])) << 32) | uint32_t(i);
   __syncthreads();
-  const ScanId f{spre, sprobe, list_offsets, ids, nprobe};
-  if ((c >= uint32_t(k) || c == uint32_t(n)) && c <= uint32_t(kSurvCap)) {
-    for (int j = threadIdx.x; j < int(c); j += blockDim.x) {
-      const uint64_t e = surv[int64_t(q) * kSurvCap + j];
-      buf[j] = composite(uint32_t(e >> 32), f(int(e & 0xffffffffu)));
+  int cur = 0, cnt = n0;
+  uint32_t T = 0;
+  if (n > n0) {
+    T = stream_threshold(sm, cur, cnt, k, kStreamSoft / 2);
+    cnt = stream_compact(sm, cur, cnt, T);
+    cur ^= 1;
+    // the rest, 16 scores per thread per round (four 16-byte loads); the
+    // next round's loads are issued before the current round is filtered
+    constexpr int kRound = kStreamThreads * 16;
+    // range-checked loads (unconditional, zeros past the region): the range
+    // is n rounded up to whole 16-byte groups, inside the region's stride
+    const __amdgpu_buffer_rsrc_t rr = make_rsrc(row, uint32_t((n + 3) & ~3) * 4u);
+    auto load_round = [&](float4 (&v)[4], int base) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const u32x4 w = __builtin_amdgcn_raw_buffer_load_b128(rr, uint32_t(base + (u * nt + tid) * 4) * 4u, 0, 0);
+        v[u] = make_float4(__uint_as_float(w.x), __uint_as_float(w.y), __uint_as_float(w.z),
+                           __uint_as_float(w.w));
+      }
+    };
+    // filter one round held in v; false when the buffer overflowed
+    auto filter_round = [&](const float4 (&v)[4], int base) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int i = base + (u * nt + tid) * 4;
+        const float e[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const uint32_t key = order_key(e[c]);
+          if (i + c < n && key >= T) {
+            const uint32_t pos = atomicAdd(&sm.count[cur], 1u);
+            if (pos < uint32_t(kStreamCap)) sm.buf[cur][pos] = (uint64_t(key) << 32) | uint32_t(i + c);
+            else sm.overflow = 1;
+          }
+        }
+      }
+      __syncthreads();
+      if (sm.overflow) return false;
+      cnt = int(sm.count[cur]);
+      if (cnt > kStreamSoft) {
+        T = stream_threshold(sm, cur, cnt, k, kStreamSoft / 2);
+        cnt = stream_compact(sm, cur, cnt, T);
+        cur ^= 1;
+      }
+      return true;
+    };
+    float4 va[4], vb[4];
+    load_round(va, n0);
+    for (int base = n0; base < n;) {
+      load_round(vb, base + kRound);
+      if (!filter_round(va, base)) break;
+      base += kRound;
+      if (base >= n) break;
+      load_round(va, base + kRound);
+      if (!filter_round(vb, base)) break;
+      base += kRound;
+    }
+    // retire the last (zero-traffic) prefetch
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+  }
+  const ScanId f{sm.spre, sm.sprobe, list_offsets, ids, nprobe};
+  // final narrowing, then ids and the exact order of the survivors
+  const int target = max(256, 2 * k);
+  if (!sm.overflow && cnt > target && cnt >= k) {
+    T = stream_threshold(sm, cur, cnt, k, target);
+    cnt = stream_compact(sm, cur, cnt, T);
+    cur ^= 1;
+  }
+  if (!sm.overflow && cnt <= kStreamCap) {
+    uint64_t *out = sm.buf[cur ^ 1];
+    for (int i = tid; i < cnt; i += nt) {
+      const uint64_t e = sm.buf[cur][i];
+      out[i] = composite(uint32_t(e >> 32), f(int(e & 0xffffffffu)));
     }
     __syncthreads();
-    sort_desc_buf(buf, int(c));
-    for (int j = threadIdx.x; j < k; j += blockDim.x) {
-      if (j < int(c)) {
-        out_s[int64_t(q) * k + j] = key_to_float(uint32_t(buf[j] >> 32));
-        out_i[int64_t(q) * k + j] = int32_t(0xffffffffu - uint32_t(buf[j] & 0xffffffffu));
+    sort_desc_buf(out, cnt);
+    for (int j = tid; j < k; j += nt) {
+      if (j < cnt) {
+        out_s[int64_t(q) * k + j] = key_to_float(uint32_t(out[j] >> 32));
+        out_i[int64_t(q) * k + j] = int32_t(0xffffffffu - uint32_t(out[j] & 0xffffffffu));
       } else {
         out_s[int64_t(q) * k + j] = -__builtin_inff();
         out_i[int64_t(q) * k + j] = -1;
@@ -694,9 +791,11 @@ __global__ void __launch_bounds__(kSelThreads) k_topk_final(
     }
     return;
   }
-  SelectSmem &sm = *reinterpret_cast<SelectSmem *>(buf);   // 32 KiB >= sizeof(SelectSmem)
-  block_topk(scores + int64_t(q) * stride, n, k, f, out_s + int64_t(q) * k, out_i + int64_t(q) * k,
-             sm);
+  // exact selection over the whole region (SelectSmem fits in one buffer)
+  __syncthreads();
+  static_assert(sizeof(SelectSmem) <= sizeof(uint64_t) * kStreamCap, "select scratch");
+  SelectSmem &ss = *reinterpret_cast<SelectSmem *>(sm.buf[0]);
+  block_topk(row, n, k, f, out_s + int64_t(q) * k, out_i + int64_t(q) * k, ss);
 }
 
 // Profiling hook: events recorded around the scan kernel (0) and the top-k
@@ -835,18 +934,9 @@ int rslm_scan_topk(const rslm_plan *p, const rslm_index *idx, const float *q_rot
   if ((st = check_launch())) return st;
   if ((st = record_timer(0, 1, s))) return st;
   if ((st = record_timer(1, 0, s))) return st;
-  hipLaunchKernelGGL(k_topk_sample, dim3(unsigned(Q)), dim3(kSelThreads), 0, s, w.scores,
-                     w.stride, w.totals, k, w.thr, w.cnt);
-  if ((st = check_launch())) return st;
-  {
-    const int64_t chunks = (w.stride + 4095) / 4096;
-    hipLaunchKernelGGL(k_topk_filter, dim3(unsigned(chunks), unsigned(Q)), dim3(256), 0, s,
-                       w.scores, w.stride, w.totals, w.thr, w.cnt, w.surv);
-  }
-  if ((st = check_launch())) return st;
-  hipLaunchKernelGGL(k_topk_final, dim3(unsigned(Q)), dim3(kSelThreads), 0, s, w.scores, w.stride,
-                     w.totals, w.cnt, w.surv, w.prefix, probe_ids, nprobe, idx->list_offsets,
-                     idx->ids, k, out_scores, out_ids);
+  hipLaunchKernelGGL(k_topk_stream, dim3(unsigned(Q)), dim3(kStreamThreads), 0, s, w.scores,
+                     w.stride, w.totals, w.prefix, probe_ids, nprobe, idx->list_offsets, idx->ids,
+                     k, out_scores, out_ids);
   if ((st = check_launch())) return st;
   return record_timer(1, 1, s);
 }
