@@ -198,6 +198,126 @@ struct IdentityId {
   __device__ int32_t operator()(int i) const { return i; }
 };
 
+// Probe dots without LDS (D a multiple of 16): each wavefront owns a 32 x 32
+// output tile as 2 x 2 v_mfma_f32_16x16x4f32 tiles and reads its operands
+// straight from L2 with 16-byte loads.  The reduction index is permuted the
+// same way for both operands: within a slab of 16, lane (m, h) (m = lane %
+// 16, h = lane / 16) supplies k = 4 h + t to MFMA step t, so one float4 per
+// row covers four steps.  The next slab's operands are loaded while the
+// current one is multiplied.
+constexpr int kDW = 4;   // wavefronts per workgroup (consecutive column tiles)
+
+__global__ void __launch_bounds__(64 * kDW) k_dots_direct(const float *__restrict__ x, int n,
+                                                          int D, const float *__restrict__ cen,
+                                                          int nlist, float *__restrict__ dots) {
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r0 = blockIdx.y * 32;
+  const int c0 = (blockIdx.x * kDW + wave) * 32;
+  if (c0 >= nlist) return;   // whole wavefront; no workgroup barriers
+  const int m = lane & 15, h = lane >> 4;
+  // clamped rows / columns: their products are computed and never written
+  const float *a0 = x + int64_t(min(r0 + m, n - 1)) * D + 4 * h;
+  const float *a1 = x + int64_t(min(r0 + 16 + m, n - 1)) * D + 4 * h;
+  const float *b0 = cen + int64_t(min(c0 + m, nlist - 1)) * D + 4 * h;
+  const float *b1 = cen + int64_t(min(c0 + 16 + m, nlist - 1)) * D + 4 * h;
+  floatx4_t acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  float4 A0 = *reinterpret_cast<const float4 *>(a0), A1 = *reinterpret_cast<const float4 *>(a1);
+  float4 B0 = *reinterpret_cast<const float4 *>(b0), B1 = *reinterpret_cast<const float4 *>(b1);
+  for (int k0 = 0; k0 < D; k0 += 16) {
+    const int kn = (k0 + 16 < D) ? k0 + 16 : k0;   // last slab: reload (no read past the row)
+    const float4 nA0 = *reinterpret_cast<const float4 *>(a0 + kn);
+    const float4 nA1 = *reinterpret_cast<const float4 *>(a1 + kn);
+    const float4 nB0 = *reinterpret_cast<const float4 *>(b0 + kn);
+    const float4 nB1 = *reinterpret_cast<const float4 *>(b1 + kn);
+    const float av[2][4] = {{A0.x, A0.y, A0.z, A0.w}, {A1.x, A1.y, A1.z, A1.w}};
+    const float bv[2][4] = {{B0.x, B0.y, B0.z, B0.w}, {B1.x, B1.y, B1.z, B1.w}};
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i][t], bv[j][t], acc[i][j], 0, 0, 0);
+    A0 = nA0;
+    A1 = nA1;
+    B0 = nB0;
+    B1 = nB1;
+  }
+  // lane holds C[4 (lane / 16) + e][lane % 16] of each 16 x 16 tile
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int r = r0 + 16 * i + 4 * h + e;
+        const int c = c0 + 16 * j + m;
+        if (r < n && c < nlist) dots[int64_t(r) * nlist + c] = acc[i][j][e];
+      }
+}
+
+// Top-nprobe of one row of dots (nlist <= 16,384): 1,024 threads hold the
+// row's order keys in registers; four 8-bit radix passes narrow the bin of
+// the nprobe-th largest key until the keys at or above its lower edge fit the
+// sort buffer; those are sorted on (key desc, list asc) and the first nprobe
+// written.  Wider runs of equal keys fall back to the block selection.
+constexpr int kPSelThreads = 1024;
+constexpr int kPSelPer = 16;
+
+__global__ void __launch_bounds__(kPSelThreads) k_probe_select_reg(const float *__restrict__ dots,
+                                                                   int nlist, int nprobe,
+                                                                   int32_t *__restrict__ out_ids,
+                                                                   float *__restrict__ out_s) {
+  __shared__ SelectSmem sm;   // hist during the radix passes, buf afterwards
+  const int tid = threadIdx.x, nt = blockDim.x;
+  const int64_t row = blockIdx.x;
+  const float *d = dots + row * nlist;
+  uint32_t key[kPSelPer];
+#pragma unroll
+  for (int v = 0; v < kPSelPer; ++v) {
+    const int i = v * nt + tid;
+    key[v] = (i < nlist) ? order_key(d[i]) : 0u;   // every real key is > 0
+  }
+  uint32_t prefix = 0, above = 0, edge = 0;
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    for (int b = tid; b < 256; b += nt) sm.hist[b] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int v = 0; v < kPSelPer; ++v) {
+      const int i = v * nt + tid;
+      if (i < nlist && (shift == 24 || (key[v] >> (shift + 8)) == prefix))
+        atomicAdd(&sm.hist[(key[v] >> shift) & 255u], 1u);
+    }
+    find_boundary(sm, 256, above, uint32_t(nprobe));
+    const uint32_t bb = sm.bcast[0];
+    const uint32_t in_bin = sm.hist[bb];
+    above = sm.bcast[1];
+    prefix = (prefix << 8) | bb;
+    edge = prefix << shift;
+    __syncthreads();
+    if (above + in_bin <= uint32_t(kSelCap)) break;
+    if (shift == 0) {   // more than kSelCap equal keys at the boundary
+      block_topk(d, nlist, nprobe, IdentityId(), out_s + row * nprobe, out_ids + row * nprobe, sm);
+      return;
+    }
+  }
+  if (tid == 0) sm.count = 0;
+  __syncthreads();
+#pragma unroll
+  for (int v = 0; v < kPSelPer; ++v) {
+    const int i = v * nt + tid;
+    if (i < nlist && key[v] >= edge) sm.buf[atomicAdd(&sm.count, 1u)] = composite(key[v], i);
+  }
+  __syncthreads();
+  emit_sorted(sm, int(sm.count), nprobe, out_s + row * nprobe, out_ids + row * nprobe);
+}
+
+
 __global__ void __launch_bounds__(kSelThreads) k_probe_select(const float *__restrict__ dots,
                                                               int nlist, int nprobe,
                                                               int32_t *__restrict__ out_ids,
@@ -255,13 +375,25 @@ int ivf_assign_probe(const float *x, int64_t n, int32_t dim, const float *centro
   float *dots = reinterpret_cast<float *>(static_cast<char *>(ws) + norms);
   const int64_t gy32 = (n + kMT - 1) / kMT;
   if (gy32 > 65535) return RSLM_ERR_INVALID_ARG;
-  hipLaunchKernelGGL(k_dots_mfma, dim3((nlist + kMT - 1) / kMT, unsigned(gy32)), dim3(256), 0, s,
-                     x, n, dim, centroids, nlist, dots);
-  int st = check_launch();
-  if (st) return st;
+  int st;
+  const bool aligned16 = (reinterpret_cast<uintptr_t>(x) % 16 == 0) &&
+                         (reinterpret_cast<uintptr_t>(centroids) % 16 == 0);
+  if (dim % 16 == 0 && aligned16) {   // rows are whole, aligned float4 runs
+    const unsigned gx = unsigned((nlist + 32 * kDW - 1) / (32 * kDW));
+    hipLaunchKernelGGL(k_dots_direct, dim3(gx, unsigned(gy32)), dim3(64 * kDW), 0, s, x, int(n), dim,
+                       centroids, nlist, dots);
+  } else {
+    hipLaunchKernelGGL(k_dots_mfma, dim3((nlist + kMT - 1) / kMT, unsigned(gy32)), dim3(256), 0, s,
+                       x, n, dim, centroids, nlist, dots);
+  }
+  if ((st = check_launch())) return st;
   if (n > 0x7fffffff) return RSLM_ERR_INVALID_ARG;
-  hipLaunchKernelGGL(k_probe_select, dim3(unsigned(n)), dim3(kSelThreads), 0, s, dots, nlist,
-                     nprobe, out_ids, out_scores);
+  if (nlist <= kPSelThreads * kPSelPer)
+    hipLaunchKernelGGL(k_probe_select_reg, dim3(unsigned(n)), dim3(kPSelThreads), 0, s, dots, nlist,
+                       nprobe, out_ids, out_scores);
+  else
+    hipLaunchKernelGGL(k_probe_select, dim3(unsigned(n)), dim3(kSelThreads), 0, s, dots, nlist,
+                       nprobe, out_ids, out_scores);
   return check_launch();
 }
 

@@ -195,7 +195,11 @@ def test_assign_parity(R, D, nlist, n):
 
 
 @pytest.mark.parametrize("D,nlist,nprobe,Q", [(96, 300, 32, 50), (768, 4096, 64, 20), (128, 16, 4, 100),
-                                              (64, 5000, 1, 7), (32, 100, 100, 3)])
+                                              (64, 5000, 1, 7), (32, 100, 100, 3),
+                                              # D not a multiple of 16; nlist above the
+                                              # register-resident selection (16,384)
+                                              (100, 700, 50, 9), (33, 40, 7, 5),
+                                              (128, 20000, 128, 3)])
 def test_probe_parity(R, D, nlist, nprobe, Q):
     rng = np.random.default_rng(nlist)
     cen = rng.standard_normal((nlist, D)).astype(np.float32)
@@ -213,6 +217,26 @@ def test_probe_parity(R, D, nlist, nprobe, Q):
         # ordered by (dot desc, id asc) in the returned dots
         for a, b in zip(range(nprobe - 1), range(1, nprobe)):
             assert dots[i, a] > dots[i, b] or (dots[i, a] == dots[i, b] and ids[i, a] < ids[i, b])
+
+
+@pytest.mark.parametrize("n_equal", [3000, 40])
+def test_probe_ties(R, n_equal):
+    """Equal dots are ordered by list id: n_equal identical centres (more than
+    the selection buffer when 3000) among distinct ones."""
+    D, nlist, nprobe, Q = 64, 4000, 64, 4
+    rng = np.random.default_rng(n_equal)
+    cen = rng.standard_normal((nlist, D)).astype(np.float32) * 0.01
+    dup = rng.choice(nlist, n_equal, replace=False)
+    cen[dup] = 1.0
+    q = np.ones((Q, D), np.float32)
+    ids, dots = R.ivf_assign_probe(_t(q), _t(cen), nprobe, R.IVF_PROBE_IP)
+    ids = ids.cpu().numpy()
+    want = np.sort(dup)[:nprobe] if n_equal >= nprobe else None
+    for i in range(Q):
+        if want is not None:
+            assert np.array_equal(ids[i], want)
+        else:
+            assert np.array_equal(ids[i, :n_equal], np.sort(dup))
 
 
 # ------------------------------------------------------------------ scan
