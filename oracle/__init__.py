@@ -27,7 +27,7 @@ from .codec import (
     decode_rotated, reconstruct,
 )
 from .search import (
-    assign_l2, probe_ip, kmeans, scan_scores_lut, scan_scores_dense, topk,
+    assign_l2, assign_l2_expanded, probe_ip, kmeans, scan_scores_lut, scan_scores_dense, topk,
     ivf_search, sq8_fit, sq8_encode, sq8_decode, rescore_sq8, brute_force_mips,
 )
 

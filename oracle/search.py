@@ -46,6 +46,25 @@ def assign_l2(x, centroids, chunk=2048):
     return ids, best
 
 
+def assign_l2_expanded(x, centroids, chunk=4096):
+    """The same argmin as ``assign_l2`` through the identity
+    ||x - c||^2 = ||x||^2 - 2 <x, c> + ||c||^2 (float64, library matmul), for
+    large centre sets where the direct difference tensor does not fit.
+    Rounding can move a distance by a few ulps of ||x||^2, so a row whose two
+    best centres are that close may pick the other one."""
+    x = np.asarray(x, dtype=np.float64)
+    c = np.asarray(centroids, dtype=np.float64)
+    cn = (c * c).sum(1)
+    ids = np.empty(len(x), dtype=np.int64)
+    best = np.empty(len(x))
+    for lo in range(0, len(x), chunk):
+        xb = x[lo:lo + chunk]
+        d = (xb * xb).sum(1)[:, None] - 2.0 * (xb @ c.T) + cn[None, :]
+        ids[lo:lo + chunk] = d.argmin(1)
+        best[lo:lo + chunk] = d.min(1)
+    return ids, best
+
+
 def probe_ip(q, centroids, nprobe):
     """The nprobe centres with the largest <q, c> per query (ties: lower id)."""
     q = np.asarray(q, dtype=np.float64)

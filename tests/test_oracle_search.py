@@ -58,6 +58,24 @@ def test_assign_lowest_on_tie():
     assert ids.tolist() == [0, 0]
 
 
+def test_assign_expanded_matches_direct():
+    """The expanded-distance route picks the direct route's centre, and its
+    minimum is the squared distance to that centre (brute force)."""
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal((300, 24)) * 3.0 + 1.0
+    c = rng.standard_normal((40, 24)) * 3.0
+    ids, d = oracle.assign_l2(x, c)
+    ide, de = oracle.assign_l2_expanded(x, c, chunk=64)
+    assert np.array_equal(ids, ide)
+    brute = np.array([((x[i] - c[ide[i]]) ** 2).sum() for i in range(len(x))])
+    assert np.allclose(de, brute, rtol=1e-12, atol=1e-9)
+    assert np.allclose(d, de, rtol=1e-12, atol=1e-9)
+    # exact ties still go to the lower centre id
+    c2 = np.array([[1.0, 0.0], [-1.0, 0.0], [1.0, 0.0]])
+    ide2, _ = oracle.assign_l2_expanded(np.array([[0.0, 1.0], [2.0, 0.0]]), c2)
+    assert ide2.tolist() == [0, 0]
+
+
 def test_topk_ties_and_padding():
     s, i = oracle.topk([1.0, 3.0, 3.0, 2.0], [9, 7, 4, 1], 3)
     assert i.tolist() == [4, 7, 1]
