@@ -56,7 +56,100 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calib", action="store_true",
                     help="only run a 1 GiB device copy (counter calibration) and exit")
+    ap.add_argument("--stats-summary", nargs=2, metavar=("KERNEL_STATS_CSV", "BENCH_JSON"),
+                    help="print a markdown summary of a rocprofv3 --stats run and exit")
+    ap.add_argument("--traffic-summary", nargs=5,
+                    metavar=("FETCH_CSV", "WRITE_CSV", "CALIB_FETCH_CSV", "CALIB_WRITE_CSV",
+                             "BENCH_JSON"),
+                    help="print the scan kernel's HBM traffic per launch from rocprofv3 "
+                         "FETCH_SIZE / WRITE_SIZE runs and a copy calibration, and exit")
     return ap.parse_args()
+
+
+# ------------------------------------------------------------------ profile summaries
+PROFILE_CMDS = {
+    "stats": ("cd /tmp && export TMPDIR=/tmp && rocprofv3 --kernel-trace --stats "
+              "--output-format csv -d /tmp/p_stats -o run -- python3 $REPO/bench.py "
+              "--no-cpu-baseline"),
+    "fetch": ("cd /tmp && rocprofv3 --pmc FETCH_SIZE --output-format csv -d /tmp/p_fetch -o run "
+              "-- python3 $REPO/bench.py --steps 5 --warmup 1 --no-cpu-baseline"),
+    "write": ("cd /tmp && rocprofv3 --pmc WRITE_SIZE --output-format csv -d /tmp/p_write -o run "
+              "-- python3 $REPO/bench.py --steps 5 --warmup 1 --no-cpu-baseline"),
+    "calib_fetch": ("cd /tmp && rocprofv3 --pmc FETCH_SIZE --output-format csv -d /tmp/p_cf -o run "
+                    "-- python3 $REPO/bench.py --copy-calib"),
+    "calib_write": ("cd /tmp && rocprofv3 --pmc WRITE_SIZE --output-format csv -d /tmp/p_cw -o run "
+                    "-- python3 $REPO/bench.py --copy-calib"),
+}
+
+STEP_KERNELS = ("k_scan<", "k_topk_stream", "k_dots", "k_probe_select", "k_rescore_sq8",
+                "k_encode", "k_rotate", "k_prep_queries", "k_plan")
+
+
+def stats_summary(stats_csv, bench_json):
+    import csv
+    rows = list(csv.DictReader(open(stats_csv)))
+    b = json.load(open(bench_json))
+    r = b["roofline"]
+    out = ["# rocprofv3 kernel statistics: RSLM IVF scan, text-embedding workload "
+           "(10M x 768, 4-bit)", "",
+           "Command (run from /tmp on one MI355X; `$REPO` is the repository root):", "",
+           "```", PROFILE_CMDS["stats"], "```", "",
+           f"Kernel sources hash: `{csrc_hash()}`.  The bench run under the profiler reported: "
+           f"value {b['value']:.3e} scored candidates/s, {b['ms_per_step']:.3f} ms/step, scan "
+           f"kernel {r['kernel_ms'] * 1e3:.1f} us by HIP events ({r['achieved']:.0f} GB/s "
+           f"algorithmic, {100 * r['frac']:.1f}% of 8 TB/s).", "",
+           "The run covers index construction (assignment and encoding of 10M vectors, SQ8 "
+           f"fit/encode) and {b['warmup']} warm-up + {b['steps']} timed steps; the per-step "
+           "kernels of the hot path are listed first (their averages include the one large "
+           "build-time call of the encoder).", "",
+           "| Kernel | Calls | Average (us) | Min (us) | Total (ms) | % |",
+           "|---|---|---|---|---|---|"]
+    step = [x for x in rows if any(k in x["Name"] for k in STEP_KERNELS)]
+    other = [x for x in rows if x not in step]
+    for x in step + other[:8]:
+        name = x["Name"].replace("|", "\\|")
+        name = name if len(name) <= 90 else name[:87] + "..."
+        out.append(f"| `{name}` | {x['Calls']} | {float(x['AverageNs']) / 1e3:.1f} | "
+                   f"{float(x['MinNs']) / 1e3:.1f} | {float(x['TotalDurationNs']) / 1e6:.2f} | "
+                   f"{float(x['Percentage']):.2f} |")
+    return "\n".join(out) + "\n"
+
+
+def _pmc_per_dispatch(csv_path, name_part, counter):
+    import csv
+    vals = [float(r["Counter_Value"]) for r in csv.DictReader(open(csv_path))
+            if name_part in r["Kernel_Name"] and r["Counter_Name"] == counter]
+    return vals
+
+
+def traffic_summary(fetch_csv, write_csv, cf_csv, cw_csv, bench_json):
+    b = json.load(open(bench_json))
+    fetch = _pmc_per_dispatch(fetch_csv, "k_scan<", "FETCH_SIZE")
+    write = _pmc_per_dispatch(write_csv, "k_scan<", "WRITE_SIZE")
+    # calibration: the largest copy dispatch of the 1 GiB device copy
+    cf = max(_pmc_per_dispatch(cf_csv, "", "FETCH_SIZE"))
+    cw = max(_pmc_per_dispatch(cw_csv, "", "WRITE_SIZE"))
+    calib = 1 << 30
+    ff, wf = calib / (cf * 1024), calib / (cw * 1024)
+    # the scan's launches of the timed steps (the last ones of the run)
+    n = b["steps"]
+    fk, wk = sum(fetch[-n:]) / n, sum(write[-n:]) / n
+    rd, wr = fk * 1024 * ff, wk * 1024 * wf
+    return {
+        "kernel": b["roofline"]["kernel"],
+        "workload": ("10,000,000 x 768 anisotropic Gaussian, nlist 4096, 4-bit RSLM global, "
+                     "batch 256, nprobe 64"),
+        "csrc_sha": csrc_hash(),
+        "fetch_KiB_per_launch": fk,
+        "write_KiB_per_launch": wk,
+        "copy_calibration": {"bytes": calib, "fetch_KiB": cf, "write_KiB": cw,
+                             "fetch_factor": ff, "write_factor": wf},
+        "hbm_bytes_per_launch": rd + wr,
+        "hbm_read_bytes_per_launch": rd,
+        "hbm_write_bytes_per_launch": wr,
+        "algorithmic_read_bytes_per_launch_same_run": b["roofline"]["algorithmic_bytes_per_launch"],
+        "commands": [PROFILE_CMDS[k] for k in ("fetch", "write", "calib_fetch", "calib_write")],
+    }
 
 
 def csrc_hash():
@@ -158,6 +251,12 @@ def cpu_baseline(R, plan, index, qrot, pid, pdot, k, budget_s):
 # ------------------------------------------------------------------ main
 def main():
     args = parse()
+    if args.stats_summary:
+        sys.stdout.write(stats_summary(*args.stats_summary))
+        return
+    if args.traffic_summary:
+        print(json.dumps(traffic_summary(*args.traffic_summary), indent=1))
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build measures one GPU only; run with --gpus 1"}))
         sys.exit(2)

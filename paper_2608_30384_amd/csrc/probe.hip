@@ -198,112 +198,175 @@ struct IdentityId {
   __device__ int32_t operator()(int i) const { return i; }
 };
 
-// Probe dots without LDS (D a multiple of 16): each wavefront owns a 32 x 32
-// output tile as 2 x 2 v_mfma_f32_16x16x4f32 tiles and reads its operands
-// straight from L2 with 16-byte loads.  The reduction index is permuted the
-// same way for both operands: within a slab of 16, lane (m, h) (m = lane %
-// 16, h = lane / 16) supplies k = 4 h + t to MFMA step t, so one float4 per
-// row covers four steps.  The next slab's operands are loaded while the
-// current one is multiplied.
-constexpr int kDW = 4;   // wavefronts per workgroup (consecutive column tiles)
+// Probe dots without operand staging (D a multiple of 16): a 32 x 32 output
+// tile is computed by two wavefronts, each over one half of the slabs of 16
+// reduction indices, as 2 x 2 v_mfma_f32_16x16x4f32 tiles with operands read
+// straight from L2 in 16-byte runs.  The reduction index is permuted the same
+// way for both operands: within a slab, lane (m, h) (m = lane % 16, h = lane /
+// 16) supplies k = 4 h + t to MFMA step t, so one float4 per row covers four
+// steps; the next slab is loaded while the current one is multiplied.  The
+// second half's accumulators are added through LDS (one addition of two
+// partial sums: the result does not depend on the order of the waves).
+constexpr int kDTiles = 2;   // output tiles per workgroup (consecutive columns)
 
-__global__ void __launch_bounds__(64 * kDW) k_dots_direct(const float *__restrict__ x, int n,
-                                                          int D, const float *__restrict__ cen,
-                                                          int nlist, float *__restrict__ dots) {
+__global__ void __launch_bounds__(128 * kDTiles) k_dots_direct(const float *__restrict__ x, int n,
+                                                               int D, const float *__restrict__ cen,
+                                                               int nlist, float *__restrict__ dots) {
+  __shared__ floatx4_t part[kDTiles][4][64];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int tile = wave >> 1, half = wave & 1;
   const int r0 = blockIdx.y * 32;
-  const int c0 = (blockIdx.x * kDW + wave) * 32;
-  if (c0 >= nlist) return;   // whole wavefront; no workgroup barriers
+  const int c0 = (blockIdx.x * kDTiles + tile) * 32;
   const int m = lane & 15, h = lane >> 4;
   // clamped rows / columns: their products are computed and never written
   const float *a0 = x + int64_t(min(r0 + m, n - 1)) * D + 4 * h;
   const float *a1 = x + int64_t(min(r0 + 16 + m, n - 1)) * D + 4 * h;
   const float *b0 = cen + int64_t(min(c0 + m, nlist - 1)) * D + 4 * h;
   const float *b1 = cen + int64_t(min(c0 + 16 + m, nlist - 1)) * D + 4 * h;
+  const int nslab = D / 16;
+  const int s_lo = half ? nslab / 2 : 0, s_hi = half ? nslab : nslab / 2;
   floatx4_t acc[2][2];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
-  float4 A0 = *reinterpret_cast<const float4 *>(a0), A1 = *reinterpret_cast<const float4 *>(a1);
-  float4 B0 = *reinterpret_cast<const float4 *>(b0), B1 = *reinterpret_cast<const float4 *>(b1);
-  for (int k0 = 0; k0 < D; k0 += 16) {
-    const int kn = (k0 + 16 < D) ? k0 + 16 : k0;   // last slab: reload (no read past the row)
-    const float4 nA0 = *reinterpret_cast<const float4 *>(a0 + kn);
-    const float4 nA1 = *reinterpret_cast<const float4 *>(a1 + kn);
-    const float4 nB0 = *reinterpret_cast<const float4 *>(b0 + kn);
-    const float4 nB1 = *reinterpret_cast<const float4 *>(b1 + kn);
-    const float av[2][4] = {{A0.x, A0.y, A0.z, A0.w}, {A1.x, A1.y, A1.z, A1.w}};
-    const float bv[2][4] = {{B0.x, B0.y, B0.z, B0.w}, {B1.x, B1.y, B1.z, B1.w}};
+  if (s_lo < s_hi) {
+    int k0 = 16 * s_lo;
+    float4 A0 = *reinterpret_cast<const float4 *>(a0 + k0), A1 = *reinterpret_cast<const float4 *>(a1 + k0);
+    float4 B0 = *reinterpret_cast<const float4 *>(b0 + k0), B1 = *reinterpret_cast<const float4 *>(b1 + k0);
+    for (int sl = s_lo; sl < s_hi; ++sl, k0 += 16) {
+      const int kn = (sl + 1 < s_hi) ? k0 + 16 : k0;   // last slab: reload (no read past the row)
+      const float4 nA0 = *reinterpret_cast<const float4 *>(a0 + kn);
+      const float4 nA1 = *reinterpret_cast<const float4 *>(a1 + kn);
+      const float4 nB0 = *reinterpret_cast<const float4 *>(b0 + kn);
+      const float4 nB1 = *reinterpret_cast<const float4 *>(b1 + kn);
+      const float av[2][4] = {{A0.x, A0.y, A0.z, A0.w}, {A1.x, A1.y, A1.z, A1.w}};
+      const float bv[2][4] = {{B0.x, B0.y, B0.z, B0.w}, {B1.x, B1.y, B1.z, B1.w}};
 #pragma unroll
-    for (int t = 0; t < 4; ++t)
+      for (int t = 0; t < 4; ++t)
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i][t], bv[j][t], acc[i][j], 0, 0, 0);
-    A0 = nA0;
-    A1 = nA1;
-    B0 = nB0;
-    B1 = nB1;
+          for (int j = 0; j < 2; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i][t], bv[j][t], acc[i][j], 0, 0, 0);
+      A0 = nA0;
+      A1 = nA1;
+      B0 = nB0;
+      B1 = nB1;
+    }
   }
+  if (half) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) part[tile][2 * i + j][lane] = acc[i][j];
+  }
+  __syncthreads();
+  if (half || c0 >= nlist) return;
   // lane holds C[4 (lane / 16) + e][lane % 16] of each 16 x 16 tile
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < 2; ++j) {
+      const floatx4_t sum = acc[i][j] + part[tile][2 * i + j][lane];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int r = r0 + 16 * i + 4 * h + e;
         const int c = c0 + 16 * j + m;
-        if (r < n && c < nlist) dots[int64_t(r) * nlist + c] = acc[i][j][e];
+        if (r < n && c < nlist) dots[int64_t(r) * nlist + c] = sum[e];
       }
+    }
 }
 
 // Top-nprobe of one row of dots (nlist <= 16,384): 1,024 threads hold the
-// row's order keys in registers; four 8-bit radix passes narrow the bin of
-// the nprobe-th largest key until the keys at or above its lower edge fit the
-// sort buffer; those are sorted on (key desc, list asc) and the first nprobe
-// written.  Wider runs of equal keys fall back to the block selection.
+// row in registers.  The dots are binned linearly over [min, max] of the row
+// (1,024 bins; the bin index is a non-decreasing function of the dot, so "bin
+// >= b" is an up-set of the order), the bin holding the nprobe-th largest dot
+// is found, and every dot in it or above is sorted on (dot desc, list asc).
+// Value bins spread the row evenly, unlike the leading bits of the float
+// keys, which most dots share (LDS atomics on a few bins serialise).  If the
+// boundary bin is crowded (equal or clustered dots), 8-bit radix passes over
+// the keys take over, and beyond that the block selection.
 constexpr int kPSelThreads = 1024;
 constexpr int kPSelPer = 16;
+constexpr int kPSelBins = 1024;
 
 __global__ void __launch_bounds__(kPSelThreads) k_probe_select_reg(const float *__restrict__ dots,
                                                                    int nlist, int nprobe,
                                                                    int32_t *__restrict__ out_ids,
                                                                    float *__restrict__ out_s) {
-  __shared__ SelectSmem sm;   // hist during the radix passes, buf afterwards
+  __shared__ SelectSmem sm;   // hist during the counting passes, buf afterwards
+  __shared__ float red[2][kPSelThreads / 64];
   const int tid = threadIdx.x, nt = blockDim.x;
   const int64_t row = blockIdx.x;
   const float *d = dots + row * nlist;
+  float val[kPSelPer];
   uint32_t key[kPSelPer];
+  float lo = __builtin_inff(), hi = -__builtin_inff();
 #pragma unroll
   for (int v = 0; v < kPSelPer; ++v) {
     const int i = v * nt + tid;
-    key[v] = (i < nlist) ? order_key(d[i]) : 0u;   // every real key is > 0
+    val[v] = (i < nlist) ? d[i] : 0.f;
+    key[v] = (i < nlist) ? order_key(val[v]) : 0u;   // every real key is > 0
+    if (i < nlist) {
+      lo = fminf(lo, val[v]);
+      hi = fmaxf(hi, val[v]);
+    }
   }
-  uint32_t prefix = 0, above = 0, edge = 0;
-  for (int shift = 24; shift >= 0; shift -= 8) {
-    for (int b = tid; b < 256; b += nt) sm.hist[b] = 0;
+  lo = -wave_max(-lo);
+  hi = wave_max(hi);
+  if ((tid & 63) == 0) {
+    red[0][tid >> 6] = lo;
+    red[1][tid >> 6] = hi;
+  }
+  __syncthreads();
+  lo = red[0][0];
+  hi = red[1][0];
+  for (int w = 1; w < nt / 64; ++w) {
+    lo = fminf(lo, red[0][w]);
+    hi = fmaxf(hi, red[1][w]);
+  }
+  const float scale = (hi > lo) ? float(kPSelBins) / (hi - lo) : 0.f;
+  auto bin_of = [&](float x) { return min(kPSelBins - 1, int((x - lo) * scale)); };
+  bool collect_by_bin = false;
+  int bbin = 0;
+  uint32_t edge = 0;
+  if (scale > 0.f && scale < 3.0e38f) {
+    for (int b = tid; b < kPSelBins; b += nt) sm.hist[b] = 0;
     __syncthreads();
 #pragma unroll
-    for (int v = 0; v < kPSelPer; ++v) {
-      const int i = v * nt + tid;
-      if (i < nlist && (shift == 24 || (key[v] >> (shift + 8)) == prefix))
-        atomicAdd(&sm.hist[(key[v] >> shift) & 255u], 1u);
-    }
-    find_boundary(sm, 256, above, uint32_t(nprobe));
-    const uint32_t bb = sm.bcast[0];
-    const uint32_t in_bin = sm.hist[bb];
-    above = sm.bcast[1];
-    prefix = (prefix << 8) | bb;
-    edge = prefix << shift;
+    for (int v = 0; v < kPSelPer; ++v)
+      if (v * nt + tid < nlist) atomicAdd(&sm.hist[bin_of(val[v])], 1u);
+    find_boundary(sm, kPSelBins, 0u, uint32_t(nprobe));
+    bbin = int(sm.bcast[0]);
+    collect_by_bin = sm.bcast[1] + sm.hist[bbin] <= uint32_t(kSelCap);
     __syncthreads();
-    if (above + in_bin <= uint32_t(kSelCap)) break;
-    if (shift == 0) {   // more than kSelCap equal keys at the boundary
-      block_topk(d, nlist, nprobe, IdentityId(), out_s + row * nprobe, out_ids + row * nprobe, sm);
-      return;
+  }
+  if (!collect_by_bin) {
+    uint32_t prefix = 0, above = 0;
+    for (int shift = 24; shift >= 0; shift -= 8) {
+      for (int b = tid; b < 256; b += nt) sm.hist[b] = 0;
+      __syncthreads();
+#pragma unroll
+      for (int v = 0; v < kPSelPer; ++v) {
+        const int i = v * nt + tid;
+        if (i < nlist && (shift == 24 || (key[v] >> (shift + 8)) == prefix))
+          atomicAdd(&sm.hist[(key[v] >> shift) & 255u], 1u);
+      }
+      find_boundary(sm, 256, above, uint32_t(nprobe));
+      const uint32_t bb = sm.bcast[0];
+      const uint32_t in_bin = sm.hist[bb];
+      above = sm.bcast[1];
+      prefix = (prefix << 8) | bb;
+      edge = prefix << shift;
+      __syncthreads();
+      if (above + in_bin <= uint32_t(kSelCap)) break;
+      if (shift == 0) {   // more than kSelCap equal keys at the boundary
+        block_topk(d, nlist, nprobe, IdentityId(), out_s + row * nprobe, out_ids + row * nprobe,
+                   sm);
+        return;
+      }
     }
   }
   if (tid == 0) sm.count = 0;
@@ -311,13 +374,14 @@ __global__ void __launch_bounds__(kPSelThreads) k_probe_select_reg(const float *
 #pragma unroll
   for (int v = 0; v < kPSelPer; ++v) {
     const int i = v * nt + tid;
-    if (i < nlist && key[v] >= edge) sm.buf[atomicAdd(&sm.count, 1u)] = composite(key[v], i);
+    const bool take = collect_by_bin ? bin_of(val[v]) >= bbin : key[v] >= edge;
+    if (i < nlist && take) sm.buf[atomicAdd(&sm.count, 1u)] = composite(key[v], i);
   }
   __syncthreads();
   emit_sorted(sm, int(sm.count), nprobe, out_s + row * nprobe, out_ids + row * nprobe);
 }
 
-
+// Top-nprobe for rows longer than the register-resident kernel holds.
 __global__ void __launch_bounds__(kSelThreads) k_probe_select(const float *__restrict__ dots,
                                                               int nlist, int nprobe,
                                                               int32_t *__restrict__ out_ids,
@@ -379,9 +443,9 @@ int ivf_assign_probe(const float *x, int64_t n, int32_t dim, const float *centro
   const bool aligned16 = (reinterpret_cast<uintptr_t>(x) % 16 == 0) &&
                          (reinterpret_cast<uintptr_t>(centroids) % 16 == 0);
   if (dim % 16 == 0 && aligned16) {   // rows are whole, aligned float4 runs
-    const unsigned gx = unsigned((nlist + 32 * kDW - 1) / (32 * kDW));
-    hipLaunchKernelGGL(k_dots_direct, dim3(gx, unsigned(gy32)), dim3(64 * kDW), 0, s, x, int(n), dim,
-                       centroids, nlist, dots);
+    const unsigned gx = unsigned((nlist + 32 * kDTiles - 1) / (32 * kDTiles));
+    hipLaunchKernelGGL(k_dots_direct, dim3(gx, unsigned(gy32)), dim3(128 * kDTiles), 0, s, x, int(n),
+                       dim, centroids, nlist, dots);
   } else {
     hipLaunchKernelGGL(k_dots_mfma, dim3((nlist + kMT - 1) / kMT, unsigned(gy32)), dim3(256), 0, s,
                        x, n, dim, centroids, nlist, dots);
