@@ -140,118 +140,253 @@ __global__ void __launch_bounds__(256) k_rotate_reg(const float *__restrict__ x,
   for (int j = 0; j < J; ++j) yr[lane + 64 * j] = v[j];
 }
 
-// Byte address of group G (coordinates [8G, 8G + 8)) of record rec in the
-// scan tile layout (see the general encoder for the layout).
-__device__ __forceinline__ int64_t tile_addr_r(int64_t rec, int G, int t, const CodecParams &cp) {
-  const int64_t tile = rec >> 4;
-  const int n = int(rec & 15);
-  const int c = G >> 2, r = G & 3;
-  const int off = c * cp.bits + t;
-  return tile * cp.tile_bytes + int64_t((off >> 4) * 64 + r * 16 + n) * 16 + (off & 15);
+// ---------------------------------------------------------------------------
+// Encoder for 1-D codebooks (3 and 4 bits) at D = 128 NB, four vectors per
+// wavefront.  Row rho = lane / 16 of the wavefront holds one vector; lane r =
+// lane % 16 of the row holds, of every 128-block b, the 8 consecutive
+// coordinates 128 b + 8 r + i (i < 8).  In a block, coordinate bits 0..2 are
+// the register index i and bits 3..6 are r, so three butterfly stages are in
+// registers and four exchange lanes inside the row through DPP (quad_perm for
+// lane xor 1 and 2, half-mirror + quad_perm for xor 4, row_ror:8 for xor 8);
+// row reductions are four DPP steps.  The strided transpose between the two
+// passes goes through a per-vector LDS buffer.  Codes of a lane's 8
+// coordinates form one packed word, stored straight into the tile layout.
+
+constexpr int kDppQuadXor1 = 0xB1;   // quad_perm [1, 0, 3, 2]
+constexpr int kDppQuadXor2 = 0x4E;   // quad_perm [2, 3, 0, 1]
+constexpr int kDppQuadRev = 0x1B;    // quad_perm [3, 2, 1, 0]
+constexpr int kDppHalfMirror = 0x141;
+constexpr int kDppRowRor4 = 0x124;
+constexpr int kDppRowRor8 = 0x128;
+
+template <int CTRL>
+__device__ __forceinline__ float dppf(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xf, 0xf, true));
+}
+// value of lane r ^ 4 of the row: half-mirror (r ^ 7) then quad reverse (^ 3)
+__device__ __forceinline__ float dpp_xor4(float v) {
+  return dppf<kDppQuadRev>(dppf<kDppHalfMirror>(v));
+}
+__device__ __forceinline__ float row_sum16(float v) {
+  v += dppf<kDppQuadXor1>(v);
+  v += dppf<kDppQuadXor2>(v);
+  v += dppf<kDppRowRor4>(v);   // quads now uniform: + the next quad
+  v += dppf<kDppRowRor8>(v);   // + the two others
+  return v;
+}
+__device__ __forceinline__ float row_max16(float v) {
+  v = fmaxf(v, dppf<kDppQuadXor1>(v));
+  v = fmaxf(v, dppf<kDppQuadXor2>(v));
+  v = fmaxf(v, dppf<kDppRowRor4>(v));
+  v = fmaxf(v, dppf<kDppRowRor8>(v));
+  return v;
 }
 
-// Encoder for 1-D codebooks (3 and 4 bits), registers only after the loads.
-template <int J, int BITS>
-__global__ void __launch_bounds__(256) k_encode_reg(
+// Unnormalised FWHT of every 128-block of the row's vector; sg[k] = -1 where
+// bit k of r is set (that lane computes partner - own).
+template <int E>
+__device__ __forceinline__ void fwht_rows(float (&z)[E], const float (&sg)[4]) {
+#pragma unroll
+  for (int b = 0; b < E / 8; ++b) {
+#pragma unroll
+    for (int s = 1; s < 8; s <<= 1) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        if (i & s) continue;
+        const float a = z[8 * b + i], c = z[8 * b + i + s];
+        z[8 * b + i] = a + c;
+        z[8 * b + i + s] = a - c;
+      }
+    }
+  }
+  // lane stages, one block at a time: the scheduling barrier keeps the
+  // compiler from batching every exchange of a stage (48 live temporaries)
+#pragma unroll
+  for (int b = 0; b < E / 8; ++b) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) z[8 * b + i] = fmaf(sg[0], z[8 * b + i], dppf<kDppQuadXor1>(z[8 * b + i]));
+#pragma unroll
+    for (int i = 0; i < 8; ++i) z[8 * b + i] = fmaf(sg[1], z[8 * b + i], dppf<kDppQuadXor2>(z[8 * b + i]));
+#pragma unroll
+    for (int i = 0; i < 8; ++i) z[8 * b + i] = fmaf(sg[2], z[8 * b + i], dpp_xor4(z[8 * b + i]));
+#pragma unroll
+    for (int i = 0; i < 8; ++i) z[8 * b + i] = fmaf(sg[3], z[8 * b + i], dppf<kDppRowRor8>(z[8 * b + i]));
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+// sign bit (bit 31) of coordinate 128 b + 8 r + i from the lane's 16-bit
+// mask: bit 8 (b mod 2) + i (the sign tables repeat every 256 coordinates)
+__device__ __forceinline__ uint32_t sgnbit(uint32_t m, int b, int i) {
+  return ((m >> (8 * (b & 1) + i)) & 1u) << 31;
+}
+
+template <int NB, int BITS>
+__global__ void __launch_bounds__(256) k_encode_rows(
     const float *__restrict__ x, int64_t n_rows, const int64_t *__restrict__ src_row,
     const int32_t *__restrict__ rec_list, int64_t n_records, const float *__restrict__ cen,
     const float *__restrict__ cen_rot, int nlist, uint8_t *__restrict__ codes,
-    uint32_t *__restrict__ scales, float *__restrict__ resid, RotParams rp, CodecParams cp,
-    int dstride) {
-  constexpr int D = 64 * J;
+    uint32_t *__restrict__ scales, float *__restrict__ resid, RotParams rp, CodecParams cp) {
+  constexpr int D = 128 * NB;
+  constexpr int E = 8 * NB;
   constexpr int K = 1 << BITS;
-  extern __shared__ float lds[];
+  constexpr int kVecStride = D + 4;   // floats per vector buffer (offset of 4 banks per row)
+  __shared__ float buf[16 * kVecStride];
   __shared__ float cbs[16], thr[16];
+  __shared__ uint32_t rmask[16];
   __shared__ uint16_t ts[D];
   const int lane = threadIdx.x & 63;
-  // record, source row and list are the same for the whole wavefront; kept
-  // in scalar registers so every address below is scalar base + lane offset
-  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int nw = blockDim.x >> 6;
+  const int wid = threadIdx.x >> 6;
+  const int rho = lane >> 4, r = lane & 15;
   if (threadIdx.x < 16) {
     cbs[threadIdx.x] = cp.cb[threadIdx.x];
     // sorted decision thresholds, padded with +inf for the binary search
-    thr[threadIdx.x] = (int(threadIdx.x) + 1 < cp.K) ? cp.thr[threadIdx.x] : __builtin_inff();
+    thr[threadIdx.x] = (int(threadIdx.x) + 1 < K) ? cp.thr[threadIdx.x] : __builtin_inff();
+    // S1 (low half) and S2 (high half) sign bits of coordinates 128 p + 8 t + i
+    uint32_t m = 0;
+    for (int pi = 0; pi < 16; ++pi) {
+      const int c = 128 * (pi >> 3) + 8 * int(threadIdx.x) + (pi & 7);
+      m |= sign_bit(rp.s1mask, c) << pi;
+      m |= sign_bit(rp.s1mask, c + 127) << (16 + pi);
+    }
+    rmask[threadIdx.x] = m;
   }
-  load_tsrc_r(rp, ts);
-  const int64_t rec = int64_t(blockIdx.x) * nw + wid;
+  if (rp.passes == 2)
+    for (int k = threadIdx.x; k < D; k += blockDim.x) ts[k] = uint16_t(4 * rp.tsrc[k]);
+  __syncthreads();
+  const int64_t rec = (int64_t(blockIdx.x) * (blockDim.x >> 6) + wid) * 4 + rho;
   int64_t row = -1;
   int L = -1;
   if (rec < n_records) {
-    if (src_row) {
-      const int64_t sr = src_row[rec];
-      row = int64_t((uint64_t(uint32_t(__builtin_amdgcn_readfirstlane(int(uint64_t(sr) >> 32)))) << 32) |
-                    uint32_t(__builtin_amdgcn_readfirstlane(int(uint32_t(sr)))));
-    } else {
-      row = rec;
-    }
+    row = src_row ? src_row[rec] : rec;
     if (row >= n_rows) row = -1;
     if (cen && row >= 0) {
-      L = __builtin_amdgcn_readfirstlane(rec_list[rec]);
+      L = rec_list[rec];
       if (L < 0 || L >= nlist) row = -1;
     }
   }
-  if (row < 0) return;   // no workgroup barriers below
-  float *buf = lds + wid * dstride;
-  const uint2 sm = lane_sign_masks(rp, lane);
-  const SignWords s1 = sign_words(rp.passes > 0 ? sm.x : 0u), s2 = sign_words(sm.y);
+  // A row without a vector leaves; rows never exchange data, and no
+  // workgroup barrier follows.
+  if (row < 0) return;
+  const uint32_t m1 = rmask[r] & 0xffffu, m2 = rmask[r] >> 16;
+  const float sg[4] = {(r & 1) ? -1.f : 1.f, (r & 2) ? -1.f : 1.f, (r & 4) ? -1.f : 1.f,
+                       (r & 8) ? -1.f : 1.f};
 
   // residual r = x - c, its sums, and S1
-  const float *xr = x + row * D;
-  const float *cr = (L >= 0) ? cen + int64_t(L) * D : xr;   // branch-free: weight 0 without c
+  const float *xr = x + row * D + 8 * r;
+  const float *cr = (L >= 0) ? cen + int64_t(L) * D + 8 * r : xr;   // weight 0 without c
   const float cw = (L >= 0) ? 1.f : 0.f;
-  const bool has_rc = L >= 0 && cen_rot;
-  const float *rcr = has_rc ? cen_rot + int64_t(L) * D : xr;
-  const float rcw = has_rc ? 1.f : 0.f;
-  float z[J], rc[J];
+  float z[E];
   float xx = 0.f, rr = 0.f, cc = 0.f;
 #pragma unroll
-  for (int j = 0; j < J; ++j) {
-    const float xv = xr[lane + 64 * j];
-    const float cv = cr[lane + 64 * j] * cw;
-    rc[j] = rcr[lane + 64 * j] * rcw;
-    const float r = xv - cv;
-    xx += xv * xv;
-    rr += r * r;
-    cc += cv * cv;
-    z[j] = flipw(r, s1, j);
+  for (int b = 0; b < NB; ++b) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const float4 xv = *reinterpret_cast<const float4 *>(xr + 128 * b + 4 * h);
+      const float4 cv4 = *reinterpret_cast<const float4 *>(cr + 128 * b + 4 * h);
+      const float xa[4] = {xv.x, xv.y, xv.z, xv.w};
+      const float ca[4] = {cv4.x * cw, cv4.y * cw, cv4.z * cw, cv4.w * cw};
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int i = 4 * h + t;
+        const float d = xa[t] - ca[t];
+        xx = fmaf(xa[t], xa[t], xx);
+        rr = fmaf(d, d, rr);
+        cc = fmaf(ca[t], ca[t], cc);
+        const uint32_t sb = (rp.passes > 0) ? sgnbit(m1, b, i) : 0u;
+        z[8 * b + i] = __uint_as_float(__float_as_uint(d) ^ sb);
+      }
+    }
+    if (b % 2 == 1) __builtin_amdgcn_sched_barrier(0);   // at most 2 blocks of loads in flight
   }
-  rotate_fwd_reg<J>(z, rp, ts, s2, buf, lane);
-
-  // EVT scale and 1-D Lloyd-Max codes
-  float m = 0.f;
+  // reduce right away: a late use lets the compiler sink the accumulation
+  // chains and keep every input alive until then
+  xx = row_sum16(xx);
+  rr = row_sum16(rr);
+  cc = row_sum16(cc);
+  // rotation: FWHT, [permute + strided transpose, S2, FWHT]; 1/sqrt(128) per pass
+  float scale = 1.f;
+  if (rp.passes > 0) {
+    fwht_rows<E>(z, sg);
+    scale = rp.inv_sqrt_b;
+    if (rp.passes == 2) {
+      float *vb = buf + (4 * wid + rho) * kVecStride;
 #pragma unroll
-  for (int j = 0; j < J; ++j) m = fmaxf(m, fabsf(z[j]));
-  m = wave_max(m);
-  const float inv_s0 = (m > 0.f) ? cp.emax / m : 0.f;
-  // Nearest centroid of the sorted 1-D codebook = number of thresholds below
-  // u, by an unrolled binary search over the sorted thresholds; c4 is 4 x the
-  // code (the byte offset of its centroid and thresholds in LDS).
-  uint32_t c4[J];
+      for (int b = 0; b < NB; ++b)
 #pragma unroll
-  for (int j = 0; j < J; ++j) c4[j] = 0u;
+        for (int h = 0; h < 2; ++h)
+          *reinterpret_cast<float4 *>(vb + 128 * b + 8 * r + 4 * h) =
+              make_float4(z[8 * b + 4 * h], z[8 * b + 4 * h + 1], z[8 * b + 4 * h + 2],
+                          z[8 * b + 4 * h + 3]);
+      wave_sync_r();
 #pragma unroll
-  for (int half = K >> 1; half >= 1; half >>= 1) {
+      for (int b = 0; b < NB; ++b) {
+        const uint4 t8 = *reinterpret_cast<const uint4 *>(ts + 128 * b + 8 * r);
+        const uint32_t tw[4] = {t8.x, t8.y, t8.z, t8.w};
 #pragma unroll
-    for (int j = 0; j < J; ++j) {
-      const float u = z[j] * inv_s0;
-      c4[j] += (u > lds_at(thr, c4[j] + 4u * (half - 1))) ? 4u * half : 0u;
+        for (int i = 0; i < 8; ++i) {
+          const uint32_t off = (tw[i >> 1] >> (16 * (i & 1))) & 0xffffu;
+          z[8 * b + i] = __uint_as_float(__float_as_uint(lds_at(vb, off)) ^ sgnbit(m2, b, i));
+        }
+      }
+      wave_sync_r();
+      fwht_rows<E>(z, sg);
+      scale = rp.inv_sqrt_b * rp.inv_sqrt_b;
     }
   }
-  float cv[J];
-  float cn2 = 0.f, rcd = 0.f;
+  float m = 0.f;
 #pragma unroll
-  for (int j = 0; j < J; ++j) {
-    c4[j] = (m > 0.f) ? c4[j] : 0u;
-    cv[j] = (m > 0.f) ? lds_at(cbs, c4[j]) : 0.f;
-    cn2 += cv[j] * cv[j];
-    rcd += rc[j] * cv[j];
+  for (int e = 0; e < E; ++e) {
+    z[e] *= scale;
+    m = fmaxf(m, fabsf(z[e]));
   }
-  xx = wave_sum(xx);
-  rr = wave_sum(rr);
-  cc = wave_sum(cc);
-  cn2 = wave_sum(cn2);
-  rcd = wave_sum(rcd);
+  m = row_max16(m);
+  const float inv_s0 = (m > 0.f) ? cp.emax / m : 0.f;
+
+  // nearest centroid of the sorted 1-D codebook = number of thresholds below
+  // u, by an unrolled binary search (c4 = 4 x code, the LDS byte offset).
+  // Only the packed words are kept; centroid values are looked up again
+  // where needed (registers, not recomputation, bound this kernel).
+  uint32_t word[NB];
+  float cn2 = 0.f;
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    uint32_t c4[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int half = K >> 1; half >= 1; half >>= 1)
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        c4[i] += (z[8 * b + i] * inv_s0 > lds_at(thr, c4[i] + 4u * (half - 1))) ? 4u * half : 0u;
+    word[b] = 0u;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const uint32_t c = (m > 0.f) ? (c4[i] >> 2) : 0u;
+      word[b] |= c << (BITS * i);
+      const float v = lds_at(cbs, 4u * c);
+      cn2 = fmaf(v, v, cn2);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  cn2 = row_sum16(cn2);
+  auto centroid = [&](int b, int i) {   // code 0 of a zero residual decodes to 0
+    const float v = lds_at(cbs, 4u * ((word[b] >> (BITS * i)) & uint32_t(K - 1)));
+    return (m > 0.f) ? v : 0.f;
+  };
+  // <R c, c^> with the rotated centre (read again for the residual output)
+  const bool has_rc = L >= 0 && cen_rot;
+  const float *rcr = has_rc ? cen_rot + int64_t(L) * D + 8 * r : xr;
+  const float rcw = has_rc ? 1.f : 0.f;
+  float rcd = 0.f;
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const float4 v = *reinterpret_cast<const float4 *>(rcr + 128 * b + 4 * h);
+      const float va[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int t = 0; t < 4; ++t) rcd = fmaf(va[t] * rcw, centroid(b, 4 * h + t), rcd);
+    }
+  rcd = row_sum16(rcd);
   const float s = (m > 0.f && cn2 > 0.f) ? sqrtf(rr / cn2) : 0.f;
   const uint32_t su = enc_ue7m9(s);
   const float sh = dec_ue7m9(su);
@@ -261,34 +396,44 @@ __global__ void __launch_bounds__(256) k_encode_reg(
     const float gv = (den2 > 0.f) ? sqrtf(xx / den2) : 0.f;
     gu = enc_ue4m12(gv);
   }
-  if (lane == 0) scales[rec] = su | (gu << 16);
+  if (r == 0) scales[rec] = su | (gu << 16);
 
-  // pack: group G = 8 j + lane / 8 holds the codes of lanes 8 (lane / 8) .. + 7
+  // packed words into the scan tile layout: group G = 16 b + r of record n
+  // goes to lane stream 16 (r & 3) + n at byte c BITS, c = G / 4 = 4 b + r / 4
+  uint8_t *tile = codes + (rec >> 4) * int64_t(cp.tile_bytes);
+  const int n = int(rec & 15);
 #pragma unroll
-  for (int j = 0; j < J; ++j) {
-    uint32_t val = (c4[j] >> 2) << (BITS * (lane & 7));
-    val |= __shfl_xor(val, 1, 64);
-    val |= __shfl_xor(val, 2, 64);
-    val |= __shfl_xor(val, 4, 64);
-    if ((lane & 7) == 0) {
-      const int G = 8 * j + (lane >> 3);
-      if (BITS == 4) {
-        *reinterpret_cast<uint32_t *>(codes + tile_addr_r(rec, G, 0, cp)) = val;
-      } else {
-        for (int t = 0; t < 3; ++t) codes[tile_addr_r(rec, G, t, cp)] = uint8_t(val >> (8 * t));
+  for (int b = 0; b < NB; ++b) {
+    const int c = 4 * b + (r >> 2);
+    if (BITS == 4) {
+      const int off = 4 * c;   // 4 bytes inside one 16-byte unit
+      *reinterpret_cast<uint32_t *>(tile + ((off >> 4) * 64 + 16 * (r & 3) + n) * 16 + (off & 15)) =
+          word[b];
+    } else {
+#pragma unroll
+      for (int t = 0; t < 3; ++t) {
+        const int off = 3 * c + t;
+        tile[((off >> 4) * 64 + 16 * (r & 3) + n) * 16 + (off & 15)] = uint8_t(word[b] >> (8 * t));
       }
     }
   }
-  // padding groups of the tile layout (d_pad > D) carry code 0
-  for (int G = (D >> 3) + lane; G < (cp.d_pad >> 3); G += 64) {
-    if (BITS == 4) *reinterpret_cast<uint32_t *>(codes + tile_addr_r(rec, G, 0, cp)) = 0u;
-    else for (int t = 0; t < 3; ++t) codes[tile_addr_r(rec, G, t, cp)] = 0;
-  }
   if (resid) {
     const float gh = dec_ue4m12(gu);
-    float *out = resid + row * D;   // indexed by source row
+    float *out = resid + row * D + 8 * r;   // indexed by source row
 #pragma unroll
-    for (int j = 0; j < J; ++j) out[lane + 64 * j] = z[j] + rc[j] - gh * (rc[j] + sh * cv[j]);
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const float4 v = *reinterpret_cast<const float4 *>(rcr + 128 * b + 4 * h);
+        const float va[4] = {v.x * rcw, v.y * rcw, v.z * rcw, v.w * rcw};
+        float o[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const int e = 8 * b + 4 * h + t;
+          o[t] = z[e] + va[t] - gh * (va[t] + sh * centroid(b, 4 * h + t));
+        }
+        *reinterpret_cast<float4 *>(out + 128 * b + 4 * h) = make_float4(o[0], o[1], o[2], o[3]);
+      }
   }
 }
 
@@ -331,20 +476,23 @@ bool launch_encode_reg(const rslm_plan *p, const float *x, int64_t n_rows, const
                        const int32_t *rec_list, int64_t n_records, const float *cen,
                        const float *cen_rot, int nlist, uint8_t *codes, uint32_t *scales,
                        float *resid, hipStream_t s) {
-  if (!reg_path_ok(p->rot) || p->codec.g != 1) return false;
-  const int dstride = reg_dstride(p->rot.D);
-  const int waves = 4;
-  const size_t shm = size_t(waves) * dstride * sizeof(float);
-  const unsigned grid = unsigned((n_records + waves - 1) / waves);
-#define CALL_B(J, B)                                                                           \
-  hipLaunchKernelGGL((k_encode_reg<J, B>), dim3(grid), dim3(64 * waves), shm, s, x, n_rows,       \
-                     src_row, rec_list, n_records, cen, cen_rot, nlist, codes, scales, resid,       \
-                     p->rot, p->codec, dstride)
-#define CALL(J)          \
-  if (p->codec.bits == 4) \
-    CALL_B(J, 4);         \
-  else                    \
-    CALL_B(J, 3)
+  if (!reg_path_ok(p->rot) || p->codec.g != 1 || p->codec.d_pad != p->rot.D) return false;
+  // 16-byte vector loads and stores of every row
+  if ((reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(cen) |
+       reinterpret_cast<uintptr_t>(cen_rot) | reinterpret_cast<uintptr_t>(resid)) % 16)
+    return false;
+  const int64_t groups = (n_records + 15) / 16;   // 16 vectors per 256-thread workgroup
+  if (groups > 0x7fffffff) return false;
+  const unsigned grid = unsigned(groups);
+#define CALL_B(NB, B)                                                                         \
+  hipLaunchKernelGGL((k_encode_rows<NB, B>), dim3(grid), dim3(256), 0, s, x, n_rows, src_row,  \
+                     rec_list, n_records, cen, cen_rot, nlist, codes, scales, resid, p->rot,    \
+                     p->codec)
+#define CALL(J)                  \
+  if (p->codec.bits == 4)        \
+    CALL_B((J) / 2, 4);          \
+  else                           \
+    CALL_B((J) / 2, 3)
   RSLM_REG_SWITCH(p->rot.D / 128, CALL)
 #undef CALL
 #undef CALL_B
