@@ -94,7 +94,7 @@ def stats_summary(stats_csv, bench_json):
            "(10M x 768, 4-bit)", "",
            "Command (run from /tmp on one MI355X; `$REPO` is the repository root):", "",
            "```", PROFILE_CMDS["stats"], "```", "",
-           f"Kernel sources hash: `{csrc_hash()}`.  The bench run under the profiler reported: "
+           f"Kernel sources hash: `{csrc_hash()}` (scan kernel sources `{scan_src_hash()}`).  The bench run under the profiler reported: "
            f"value {b['value']:.3e} scored candidates/s, {b['ms_per_step']:.3f} ms/step, scan "
            f"kernel {r['kernel_ms'] * 1e3:.1f} us by HIP events ({r['achieved']:.0f} GB/s "
            f"algorithmic, {100 * r['frac']:.1f}% of 8 TB/s).", "",
@@ -139,7 +139,7 @@ def traffic_summary(fetch_csv, write_csv, cf_csv, cw_csv, bench_json):
         "kernel": b["roofline"]["kernel"],
         "workload": ("10,000,000 x 768 anisotropic Gaussian, nlist 4096, 4-bit RSLM global, "
                      "batch 256, nprobe 64"),
-        "csrc_sha": csrc_hash(),
+        "scan_src_sha": scan_src_hash(),
         "fetch_KiB_per_launch": fk,
         "write_KiB_per_launch": wk,
         "copy_calibration": {"bytes": calib, "fetch_KiB": cf, "write_KiB": cw,
@@ -161,6 +161,19 @@ def csrc_hash():
     return h.hexdigest()[:16]
 
 
+SCAN_SOURCES = ("paper_2608_30384_amd/csrc/scan.hip", "paper_2608_30384_amd/csrc/select_dev.h",
+                "paper_2608_30384_amd/csrc/rslm_internal.h", "include/rslm.h")
+
+
+def scan_src_hash():
+    """Hash of the files the scan kernel is compiled from."""
+    h = hashlib.sha256()
+    for f in SCAN_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(f.encode() + fh.read())
+    return h.hexdigest()[:16]
+
+
 def traffic_from_profiles(streamed_records_per_launch):
     """HBM bytes per scan launch from committed rocprofv3 counters, if they
     were taken on the current kernel sources; else None."""
@@ -169,7 +182,7 @@ def traffic_from_profiles(streamed_records_per_launch):
         return None
     with open(p) as f:
         t = json.load(f)
-    if t.get("csrc_sha") != csrc_hash():
+    if t.get("scan_src_sha") != scan_src_hash():
         return None
     return t.get("hbm_bytes_per_launch")
 
@@ -451,6 +464,7 @@ def main():
             "GBps": enc_bytes / (enc_ms * 1e-3) / 1e9,
         },
         "kernel_sources": csrc_hash(),
+        "scan_sources": scan_src_hash(),
     }
     if not args.no_cpu_baseline:
         log("CPU oracle baseline")
