@@ -24,11 +24,11 @@ from .rotation import (
 from .codec import (
     codec_shape, e_max, enc_ue7m9, dec_ue7m9, enc_ue4m12, dec_ue4m12,
     encode, pack_canonical, unpack_canonical, canonical_code_bytes,
-    decode_rotated, reconstruct,
+    decode_rotated, reconstruct, first_stage_rotated, encode_rescore, reconstruct_rescore,
 )
 from .search import (
     assign_l2, assign_l2_expanded, probe_ip, kmeans, scan_scores_lut, scan_scores_dense, topk,
-    ivf_search, sq8_fit, sq8_encode, sq8_decode, rescore_sq8, brute_force_mips,
+    ivf_search, sq8_fit, sq8_encode, sq8_decode, rescore_sq8, rescore_rslm, brute_force_mips,
 )
 
 __all__ = [n for n in dir() if not n.startswith("_")]

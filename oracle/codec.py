@@ -198,3 +198,39 @@ def reconstruct(codes, s_code, g_code, C, R, centroids=None):
     base = 0.0 if centroids is None else np.asarray(centroids, dtype=np.float64)
     gh = np.array([dec_ue4m12(u) for u in g_code])
     return gh[:, None] * (base + rr @ R)
+
+
+def first_stage_rotated(codes, s_code, g_code, C, R, centroids=None):
+    """R a for the first-stage approximation a = x~1 = g^ (c + R^T s^ c^):
+    R a = g^ (R c + s^ c^) (R is orthogonal), the base of the rescoring codec."""
+    rr = decode_rotated(codes, s_code, C, R.shape[0])
+    base = 0.0 if centroids is None else np.asarray(centroids, dtype=np.float64) @ R.T
+    gh = np.array([dec_ue4m12(u) for u in g_code])
+    return gh[:, None] * (base + rr)
+
+
+def encode_rescore(x, R, enc1, C1, C2, bits2, centroids=None, scale_mode="global"):
+    """Rescoring codec of Section "Relative Quantization": the second residual
+    r2 = x - a, with a = x~1 the first-stage approximation, RSLM-encoded
+    relative to a.
+
+    Reading: the codec's rotation is a fixed table, so the first stage's R
+    serves both stages and the second residual is quantised in the rotated
+    space without a further rotation: the rows R x are encoded against the
+    bases R a with R = I, which gives s2 = ||r2|| / ||C2[codes2]|| and, in
+    the global mode, g2 = ||x|| / ||a + R^T s2^ c2^|| (the decoded s2^).
+    Returns the dict of ``encode`` for the second stage.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    ra = first_stage_rotated(enc1["codes"], enc1["s_code"], enc1["g_code"], C1, R, centroids)
+    eye = np.eye(x.shape[1])
+    return encode(x @ R.T, eye, C2, bits2, centroids=ra, scale_mode=scale_mode)
+
+
+def reconstruct_rescore(enc1, enc2, C1, C2, R, centroids=None):
+    """x~2 = g2^ (a + R^T s2^ c2^) in the original space, a = x~1."""
+    a = reconstruct(enc1["codes"], enc1["s_code"], enc1["g_code"], C1, R, centroids)
+    rr = decode_rotated(enc2["codes"], enc2["s_code"], C2, R.shape[0])
+    gh = np.array([dec_ue4m12(u) for u in enc2["g_code"]])
+    return gh[:, None] * (a + rr @ R)
+

@@ -32,6 +32,8 @@ Readings where the paper is not explicit:
 
 import numpy as np
 
+from .codec import dec_ue4m12, dec_ue7m9
+
 
 def assign_l2(x, centroids, chunk=2048):
     """argmin_p ||x - c_p||^2 per row (lowest p on ties); also the minimum."""
@@ -186,6 +188,31 @@ def rescore_sq8(q_rot, cand_scores, cand_ids, codes2, lo, hi, k_out):
             continue
         r2 = sq8_decode(codes2[ids], lo, hi)
         s2 = np.asarray(cand_scores[i][ok], dtype=np.float64) + r2 @ q_rot[i]
+        out_s[i], out_i[i] = topk(s2, ids, k_out)
+    return out_s, out_i
+
+
+def rescore_rslm(q_rot, cand_scores, cand_ids, codes2, s2_code, g2_code, C2, k_out):
+    """RSLM rescoring codec (global relative scaling, Section "Relative
+    Quantization"): score2 = g2^ (score1 + s2^ sum_j LUT[j, code2_j]) with
+    LUT[j, k] = <q_rot[j g:(j+1) g], C2_k> and score1 = <q, a> the
+    shortlist's first-stage score; then the top-k_out.
+
+    codes2 (N, n_sub), s2_code / g2_code (N,) are indexed by vector id;
+    cand_* are (Q, k_in) with ids < 0 for empty slots.
+    """
+    Q, _ = cand_ids.shape
+    sh = np.array([dec_ue7m9(u) for u in s2_code])
+    gh = np.array([dec_ue4m12(u) for u in g2_code])
+    out_s = np.full((Q, k_out), -np.inf)
+    out_i = np.full((Q, k_out), -1, dtype=np.int64)
+    for i in range(Q):
+        ok = cand_ids[i] >= 0
+        ids = cand_ids[i][ok]
+        if len(ids) == 0:
+            continue
+        s1 = np.asarray(cand_scores[i][ok], dtype=np.float64)
+        s2 = scan_scores_lut(q_rot[i], s1, codes2[ids], sh[ids], gh[ids], C2)
         out_s[i], out_i[i] = topk(s2, ids, k_out)
     return out_s, out_i
 
