@@ -133,6 +133,34 @@ int rslm_encode(const rslm_plan *plan, const float *x, int64_t n_rows,
                 const float *centroids_rot, int32_t nlist, uint8_t *codes,
                 uint32_t *scales, float *resid_rot, void *stream);
 
+/* ------------------------------------------------------------------------
+ * rslm_encode_two_stage -- rslm_encode plus, in the same pass, the rescoring
+ * codec of Section "Relative Quantization" applied to the first stage's
+ * error (two-stage relative coding, the RelApprox(Global)-Rslm rescoring
+ * records of table tab:recall_eval_relative).  With the first-stage
+ * approximation a = g^ (c + R^T s^ C[code]) of record r (row `row`):
+ *   r2    = R x - R a                  (rotated space; no further rotation:
+ *                                        the rotation is a fixed table)
+ *   u2    = r2 * E_max(D) / max|r2|
+ *   code2 = nearest centroid of plan2's codebook per g2-sub-vector
+ *   s2^   = UE7M9(||r2|| / ||C2[code2]||)
+ *   g2^   = UE4M12(||x|| / ||R a + s2^ C2[code2]||) if plan2 is global,
+ *           else 1.0 (code 0x7000)
+ * A zero r2 gives codes2 = 0 and s2^ = 0.
+ *   plan2   : same dim as plan, passes == 0.
+ *   codes2  : n_rows x canon_bytes(plan2) uint8, canonical layout (see
+ *             rslm_pack_codes), row `row` written for record r.
+ *   scales2 : n_rows uint32, lo16 = s2^ (UE7M9), hi16 = g2^ (UE4M12).
+ * Every other argument and output is as in rslm_encode (no rotated residual
+ * is produced).  Rows not referenced by a record are left untouched.
+ * ------------------------------------------------------------------------ */
+int rslm_encode_two_stage(const rslm_plan *plan, const rslm_plan *plan2, const float *x,
+                          int64_t n_rows, const int64_t *src_row, const int32_t *rec_list,
+                          int64_t n_records, const float *centroids,
+                          const float *centroids_rot, int32_t nlist, uint8_t *codes,
+                          uint32_t *scales, uint8_t *codes2, uint32_t *scales2,
+                          void *stream);
+
 /* Canonical <-> scan layout of packed codes (Section "Codecs Description":
  * codes are a packed bit stream, code j of a record at bits [w j, w j + w),
  * w = log2 K, little-endian).  canon: n x canon_bytes; tiles: ceil(n/16) *
@@ -215,20 +243,30 @@ int rslm_sq8_encode(const float *v, int64_t n, int32_t dim, const float *lo,
 /* ------------------------------------------------------------------------
  * rslm_rescore -- second stage of two-stage retrieval (Sections "Background
  * and Related Work" and "Relative Quantization"): for each shortlisted
- * candidate, score2 = score1 + <q_rot, r~2> where r~2 decodes the
- * candidate's rescoring record; then the k_out best by (score2 desc, id asc).
- *   codec kind RSLM_RESCORE_SQ8: codes is n_vectors x dim uint8 indexed by
- *   id, lo / hi the SQ8 ranges.  cand_ids < 0 are empty slots.
+ * candidate, with score1 = <q, a> its first-stage score,
+ *   RSLM_RESCORE_SQ8 : score2 = score1 + <q_rot, r~2>, r~2 the SQ8 decode
+ *                      (local relative scaling);
+ *   RSLM_RESCORE_RSLM: score2 = g2^ (score1 + s2^ sum_j <q_rot[j g2:(j+1) g2],
+ *                      C2[code2_j]>) (g2^ = 1.0 for a local plan);
+ * then the k_out best by (score2 desc, id asc).
+ *   SQ8 : codes is n_vectors x dim uint8 indexed by id, lo / hi the ranges.
+ *   RSLM: codes is n_vectors x canon_bytes(plan) (rslm_encode_two_stage's
+ *         codes2), scales n_vectors uint32, plan the rescoring codec
+ *         (passes == 0, dim == dim).
+ *   cand_ids < 0 are empty slots; ids >= n_vectors are skipped as well.
  *   cand_scores / cand_ids: Q x k_in; out_*: Q x k_out; k_out <= k_in <= 1024.
  * ------------------------------------------------------------------------ */
 #define RSLM_RESCORE_SQ8 0
+#define RSLM_RESCORE_RSLM 1
 typedef struct rslm_rescore_codec {
   int32_t kind;
   int32_t dim;
   int64_t n_vectors;
   const uint8_t *codes;
-  const float *lo;
-  const float *hi;
+  const float *lo;            /* SQ8 only */
+  const float *hi;            /* SQ8 only */
+  const uint32_t *scales;     /* RSLM only: lo16 s2^ | hi16 g2^ */
+  const rslm_plan *plan;      /* RSLM only */
 } rslm_rescore_codec;
 
 int rslm_rescore(const rslm_rescore_codec *codec, const float *q_rot,

@@ -16,11 +16,12 @@ STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported", 3: "HIP error",
 IVF_ASSIGN_L2 = 0
 IVF_PROBE_IP = 1
 RSLM_RESCORE_SQ8 = 0
+RSLM_RESCORE_RSLM = 1
 
 EXPORTS = [
     "rslm_status_string", "rslm_last_hip_error", "rslm_version",
     "rslm_plan_create", "rslm_plan_destroy", "rslm_plan_get_info",
-    "rslm_fwht", "rslm_encode", "rslm_pack_codes", "rslm_unpack_codes",
+    "rslm_fwht", "rslm_encode", "rslm_encode_two_stage", "rslm_pack_codes", "rslm_unpack_codes",
     "ivf_assign_probe_workspace", "ivf_assign_probe",
     "rslm_scan_topk_workspace", "rslm_scan_topk",
     "rslm_sq8_fit", "rslm_sq8_encode", "rslm_rescore", "rslm_set_timer",
@@ -49,7 +50,8 @@ class Index(C.Structure):
 
 class RescoreCodec(C.Structure):
     _fields_ = [("kind", C.c_int32), ("dim", C.c_int32), ("n_vectors", C.c_int64),
-                ("codes", C.c_void_p), ("lo", C.c_void_p), ("hi", C.c_void_p)]
+                ("codes", C.c_void_p), ("lo", C.c_void_p), ("hi", C.c_void_p),
+                ("scales", C.c_void_p), ("plan", C.c_void_p)]
 
 
 _lib = None
@@ -70,6 +72,8 @@ def _declare(lib):
         "rslm_plan_get_info": (C.c_int, [P, C.POINTER(PlanInfo)]),
         "rslm_fwht": (C.c_int, [P, P, P, I64, C.c_int, P]),
         "rslm_encode": (C.c_int, [P, P, I64, P, P, I64, P, P, I32, P, P, P, P]),
+        "rslm_encode_two_stage": (C.c_int, [P, P, P, I64, P, P, I64, P, P, I32, P, P, P, P,
+                                            P]),
         "rslm_pack_codes": (C.c_int, [P, P, I64, P, P]),
         "rslm_unpack_codes": (C.c_int, [P, P, I64, P, P]),
         "ivf_assign_probe_workspace": (SZ, [I64, I32, I32, I32, C.c_int]),

@@ -136,6 +136,35 @@ def rslm_encode(plan, x, codes, scales, n_records=None, src_row=None, rec_list=N
         _ptr(resid_rot), _stream(stream)))
 
 
+def rslm_encode_two_stage(plan, plan2, x, codes, scales, codes2, scales2, n_records=None,
+                          src_row=None, rec_list=None, centroids=None, centroids_rot=None,
+                          stream=None):
+    """``rslm_encode`` plus the rescoring codec ``plan2`` on the second
+    residual; codes2 (n_rows x plan2.canon_bytes uint8) and scales2 (n_rows
+    int32) are indexed by row of x."""
+    _need(x, torch.float32, "x")
+    _need(codes, torch.uint8, "codes")
+    _need(scales, torch.int32, "scales")
+    _need(codes2, torch.uint8, "codes2")
+    _need(scales2, torch.int32, "scales2")
+    _need(src_row, torch.int64, "src_row")
+    _need(rec_list, torch.int32, "rec_list")
+    _need(centroids, torch.float32, "centroids")
+    _need(centroids_rot, torch.float32, "centroids_rot")
+    n_rows = x.shape[0]
+    if n_records is None:
+        n_records = src_row.shape[0] if src_row is not None else n_rows
+    if codes.numel() < plan.code_bytes(n_records) or scales.numel() < n_records:
+        raise ValueError("codes / scales too small")
+    if codes2.numel() < n_rows * plan2.canon_bytes or scales2.numel() < n_rows:
+        raise ValueError("codes2 / scales2 too small")
+    nlist = centroids.shape[0] if centroids is not None else 0
+    L.check("rslm_encode_two_stage", L.lib().rslm_encode_two_stage(
+        plan.handle, plan2.handle, _ptr(x), n_rows, _ptr(src_row), _ptr(rec_list), n_records,
+        _ptr(centroids), _ptr(centroids_rot), nlist, _ptr(codes), _ptr(scales), _ptr(codes2),
+        _ptr(scales2), _stream(stream)))
+
+
 def rslm_pack_codes(plan, canon, n, stream=None):
     _need(canon, torch.uint8, "canon")
     tiles = torch.empty(plan.code_bytes(n), dtype=torch.uint8, device=canon.device)
@@ -255,7 +284,33 @@ def rslm_rescore(codes2, lo, hi, q_rot, cand_scores, cand_ids, k_out, out_scores
     if out_ids is None:
         out_ids = torch.empty((Q, k_out), dtype=torch.int32, device=q_rot.device)
     codec = L.RescoreCodec(L.RSLM_RESCORE_SQ8, dim, codes2.numel() // dim, codes2.data_ptr(),
-                           lo.data_ptr(), hi.data_ptr())
+                           lo.data_ptr(), hi.data_ptr(), None, None)
+    L.check("rslm_rescore", L.lib().rslm_rescore(C.byref(codec), _ptr(q_rot), Q,
+                                                 _ptr(cand_scores), _ptr(cand_ids), k_in, k_out,
+                                                 _ptr(out_scores), _ptr(out_ids),
+                                                 _stream(stream)))
+    return out_scores, out_ids
+
+
+def rslm_rescore_rslm(plan2, codes2, scales2, q_rot, cand_scores, cand_ids, k_out,
+                      out_scores=None, out_ids=None, stream=None):
+    """``rslm_rescore`` with the RSLM rescoring codec (``rslm_encode_two_stage``
+    records, indexed by vector id)."""
+    _need(codes2, torch.uint8, "codes2")
+    _need(scales2, torch.int32, "scales2")
+    _need(q_rot, torch.float32, "q_rot")
+    _need(cand_scores, torch.float32, "cand_scores")
+    _need(cand_ids, torch.int32, "cand_ids")
+    Q, k_in = cand_ids.shape
+    if out_scores is None:
+        out_scores = torch.empty((Q, k_out), dtype=torch.float32, device=q_rot.device)
+    if out_ids is None:
+        out_ids = torch.empty((Q, k_out), dtype=torch.int32, device=q_rot.device)
+    n_vec = scales2.numel()
+    if codes2.numel() < n_vec * plan2.canon_bytes:
+        raise ValueError("codes2 smaller than scales2's vectors")
+    codec = L.RescoreCodec(L.RSLM_RESCORE_RSLM, plan2.dim, n_vec, codes2.data_ptr(), None, None,
+                           scales2.data_ptr(), plan2.handle.value)
     L.check("rslm_rescore", L.lib().rslm_rescore(C.byref(codec), _ptr(q_rot), Q,
                                                  _ptr(cand_scores), _ptr(cand_ids), k_in, k_out,
                                                  _ptr(out_scores), _ptr(out_ids),

@@ -151,6 +151,11 @@ int rslm_plan_create(const rslm_plan_desc *d, rslm_plan **out) {
   p->emax = emax_of(D);
   c.emax = float(p->emax);
   for (int i = 0; i < 64; ++i) c.cb[i] = (i < K * g) ? d->codebook[i] : 0.0f;
+  for (int k = 0; k < 16; ++k) {   // half squared norms of the centroids
+    float h = 0.0f;
+    for (int t = 0; t < g && k < K; ++t) h += d->codebook[k * g + t] * d->codebook[k * g + t];
+    c.cbh[k] = (k < K) ? 0.5f * h : 3.0e38f;
+  }
   for (int k = 0; k < 16; ++k)
     c.thr[k] = (g == 1 && k + 1 < K) ? 0.5f * (d->codebook[k] + d->codebook[k + 1]) : 0.0f;
 

@@ -70,6 +70,46 @@ __global__ void k_sq8_encode(const float *__restrict__ v, int64_t n, int dim,
 
 constexpr int kRescoreThreads = 256;
 
+// Sorts the n (key, id) entries of buf descending (LDS bitonic sort over the
+// next power of two) and writes the first k_out of query q, padding with
+// (-inf, -1).  Every thread of the workgroup calls it.
+__device__ void sort_emit(uint64_t *buf, int n, int q, int k_out, float *__restrict__ out_s,
+                          int32_t *__restrict__ out_i) {
+  const int tid = threadIdx.x;
+  int p2 = 1;
+  while (p2 < n) p2 <<= 1;
+  for (int i = n + tid; i < p2; i += blockDim.x) buf[i] = 0ull;
+  __syncthreads();
+  for (int size = 2; size <= p2; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int i = tid; i < p2 / 2; i += blockDim.x) {
+        const int a0 = 2 * i - (i & (stride - 1));
+        const int a1 = a0 + stride;
+        const bool desc = ((a0 & size) == 0);
+        const uint64_t x = buf[a0], y = buf[a1];
+        if ((x < y) == desc) {
+          buf[a0] = y;
+          buf[a1] = x;
+        }
+      }
+      __syncthreads();
+    }
+  }
+  for (int j = tid; j < k_out; j += blockDim.x) {
+    if (j < n) {
+      out_s[int64_t(q) * k_out + j] = key_to_float(uint32_t(buf[j] >> 32));
+      out_i[int64_t(q) * k_out + j] = int32_t(0xffffffffu - uint32_t(buf[j] & 0xffffffffu));
+    } else {
+      out_s[int64_t(q) * k_out + j] = -__builtin_inff();
+      out_i[int64_t(q) * k_out + j] = -1;
+    }
+  }
+}
+
+__device__ __forceinline__ uint64_t score_key(float s, int32_t id) {
+  return (uint64_t(order_key(s)) << 32) | uint64_t(0xffffffffu - uint32_t(id));
+}
+
 __global__ void __launch_bounds__(kRescoreThreads) k_rescore_sq8(
     const uint8_t *__restrict__ codes, int64_t n_vec, int dim, const float *__restrict__ lo,
     const float *__restrict__ hi, const float *__restrict__ q_rot,
@@ -126,39 +166,82 @@ __global__ void __launch_bounds__(kRescoreThreads) k_rescore_sq8(
     if (valid && gl == 0) {
       const float s2 = cand_s[int64_t(q) * k_in + j] + (qlo + dot);
       const uint32_t pos = atomicAdd(&count, 1u);
-      buf[pos] = (uint64_t(order_key(s2)) << 32) | uint64_t(0xffffffffu - uint32_t(id));
+      buf[pos] = score_key(s2, id);
     }
   }
   __syncthreads();
-  const int n = int(count);
-  int p2 = 1;
-  while (p2 < n) p2 <<= 1;
-  for (int i = n + tid; i < p2; i += kRescoreThreads) buf[i] = 0ull;
+  sort_emit(buf, int(count), q, k_out, out_s, out_i);
+}
+
+// RSLM rescoring records (canonical layout, w-bit codes of g-sub-vectors):
+// score2 = g2^ (score1 + s2^ sum_j <q_rot[j g:(j+1) g], C2[code_j]>).  A
+// workgroup per query holds the zero-padded rotated query and the codebook
+// in LDS; 16 lanes per candidate, lane j of a group decoding the 8-code
+// groups j, j + 16, ... (w bytes each: one dword for 4-bit codes).
+template <int W, int G>
+__global__ void __launch_bounds__(kRescoreThreads) k_rescore_rslm(
+    const uint8_t *__restrict__ codes, const uint32_t *__restrict__ scales, int64_t n_vec,
+    int dim, int n_sub, int canon_bytes, CodecParams cp, const float *__restrict__ q_rot, const float *__restrict__ cand_s,
+    const int32_t *__restrict__ cand_i, int k_in, int k_out, float *__restrict__ out_s,
+    int32_t *__restrict__ out_i) {
+  extern __shared__ float qs[];   // n_groups * 8 * G floats, zero beyond dim
+  __shared__ uint64_t buf[kMaxK];
+  __shared__ float cbs[16 * G];
+  __shared__ uint32_t count;
+  const int q = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n_groups = (n_sub + 7) / 8;
+  const float *qr = q_rot + int64_t(q) * dim;
+  for (int d = tid; d < n_groups * 8 * G; d += kRescoreThreads) qs[d] = (d < dim) ? qr[d] : 0.f;
+  if (tid < 16 * G && tid < (1 << W) * G) cbs[tid] = cp.cb[tid];
+  if (tid == 0) count = 0;
   __syncthreads();
-  for (int size = 2; size <= p2; size <<= 1) {
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      for (int i = tid; i < p2 / 2; i += kRescoreThreads) {
-        const int a0 = 2 * i - (i & (stride - 1));
-        const int a1 = a0 + stride;
-        const bool desc = ((a0 & size) == 0);
-        const uint64_t x = buf[a0], y = buf[a1];
-        if ((x < y) == desc) {
-          buf[a0] = y;
-          buf[a1] = x;
+  const int grp = lane >> 4, gl = lane & 15;
+  const int ngroups = (kRescoreThreads / 64) * 4;
+  const bool dword_ok = (W == 4) && (canon_bytes % 4 == 0) &&
+                        (reinterpret_cast<uintptr_t>(codes) % 4 == 0);
+  for (int j0 = wave * 4; j0 < k_in; j0 += ngroups) {
+    const int j = j0 + grp;
+    int32_t id = -1;
+    if (j < k_in) id = cand_i[int64_t(q) * k_in + j];
+    const bool valid = id >= 0 && id < n_vec;
+    float dot = 0.f;
+    if (valid) {
+      const uint8_t *cr = codes + int64_t(id) * canon_bytes;
+      for (int G8 = gl; G8 < n_groups; G8 += 16) {
+        // the w bytes of 8 codes (bytes past the record read as 0)
+        uint32_t bits;
+        if (dword_ok) {
+          bits = reinterpret_cast<const uint32_t *>(cr)[G8];
+        } else {
+          bits = 0u;
+#pragma unroll
+          for (int t = 0; t < W; ++t) {
+            const int byte = W * G8 + t;
+            if (byte < canon_bytes) bits |= uint32_t(cr[byte]) << (8 * t);
+          }
+        }
+        const float *qv = qs + G8 * 8 * G;
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+          const uint32_t code = (bits >> (W * c)) & ((1u << W) - 1u);
+#pragma unroll
+          for (int t = 0; t < G; ++t) dot = fmaf(qv[c * G + t], cbs[code * G + t], dot);
         }
       }
-      __syncthreads();
+    }
+#pragma unroll
+    for (int off = 8; off >= 1; off >>= 1) dot += __shfl_xor(dot, off, 64);
+    if (valid && gl == 0) {
+      const uint32_t sc = scales[id];
+      const float s2 = dec_ue4m12(sc >> 16) *
+                       (cand_s[int64_t(q) * k_in + j] + dec_ue7m9(sc & 0xffffu) * dot);
+      const uint32_t pos = atomicAdd(&count, 1u);
+      buf[pos] = score_key(s2, id);
     }
   }
-  for (int j = tid; j < k_out; j += kRescoreThreads) {
-    if (j < n) {
-      out_s[int64_t(q) * k_out + j] = key_to_float(uint32_t(buf[j] >> 32));
-      out_i[int64_t(q) * k_out + j] = int32_t(0xffffffffu - uint32_t(buf[j] & 0xffffffffu));
-    } else {
-      out_s[int64_t(q) * k_out + j] = -__builtin_inff();
-      out_i[int64_t(q) * k_out + j] = -1;
-    }
-  }
+  __syncthreads();
+  sort_emit(buf, int(count), q, k_out, out_s, out_i);
 }
 
 }  // namespace rslm
@@ -206,16 +289,37 @@ int rslm_rescore(const rslm_rescore_codec *c, const float *q_rot, int32_t Q,
                  float *out_scores, int32_t *out_ids, void *stream) {
   if (!c || Q < 0 || k_in < 1 || k_in > kMaxK || k_out < 1 || k_out > k_in)
     return RSLM_ERR_INVALID_ARG;
-  if (c->kind != RSLM_RESCORE_SQ8) return RSLM_ERR_UNSUPPORTED;
+  if (c->kind != RSLM_RESCORE_SQ8 && c->kind != RSLM_RESCORE_RSLM) return RSLM_ERR_UNSUPPORTED;
   if (c->dim < 1 || c->dim > kMaxDim || c->n_vectors < 0) return RSLM_ERR_INVALID_ARG;
-  if (Q == 0) return RSLM_OK;
-  if (!c->codes || !c->lo || !c->hi || !q_rot || !cand_scores || !cand_ids || !out_scores ||
-      !out_ids)
+  if (c->kind == RSLM_RESCORE_RSLM &&
+      (!c->plan || c->plan->rot.D != c->dim || c->plan->rot.passes != 0))
     return RSLM_ERR_INVALID_ARG;
-  hipLaunchKernelGGL(k_rescore_sq8, dim3(unsigned(Q)), dim3(kRescoreThreads),
-                     size_t(c->dim) * sizeof(float), as_stream(stream), c->codes, c->n_vectors,
-                     c->dim, c->lo, c->hi, q_rot, cand_scores, cand_ids, k_in, k_out, out_scores,
-                     out_ids);
+  if (Q == 0) return RSLM_OK;
+  if (!c->codes || !q_rot || !cand_scores || !cand_ids || !out_scores || !out_ids)
+    return RSLM_ERR_INVALID_ARG;
+  hipStream_t s = as_stream(stream);
+  if (c->kind == RSLM_RESCORE_SQ8) {
+    if (!c->lo || !c->hi) return RSLM_ERR_INVALID_ARG;
+    hipLaunchKernelGGL(k_rescore_sq8, dim3(unsigned(Q)), dim3(kRescoreThreads),
+                       size_t(c->dim) * sizeof(float), s, c->codes, c->n_vectors, c->dim, c->lo,
+                       c->hi, q_rot, cand_scores, cand_ids, k_in, k_out, out_scores, out_ids);
+    return check_launch();
+  }
+  if (!c->scales) return RSLM_ERR_INVALID_ARG;
+  const CodecParams &cp = c->plan->codec;
+  const int n_groups = (cp.n_sub + 7) / 8;
+  const size_t shm = size_t(n_groups) * 8 * cp.g * sizeof(float);
+#define RSLM_RESCORE_CALL(W, G)                                                               \
+  hipLaunchKernelGGL((k_rescore_rslm<W, G>), dim3(unsigned(Q)), dim3(kRescoreThreads), shm, s, \
+                     c->codes, c->scales, c->n_vectors, c->dim, cp.n_sub, cp.canon_bytes, cp,  \
+                     q_rot, cand_scores, cand_ids, k_in, k_out, out_scores, out_ids)
+  switch (cp.bits) {
+    case 1: RSLM_RESCORE_CALL(4, 4); break;
+    case 2: RSLM_RESCORE_CALL(4, 2); break;
+    case 3: RSLM_RESCORE_CALL(3, 1); break;
+    default: RSLM_RESCORE_CALL(4, 1); break;
+  }
+#undef RSLM_RESCORE_CALL
   return check_launch();
 }
 

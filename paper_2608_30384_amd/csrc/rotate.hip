@@ -205,14 +205,18 @@ __global__ void __launch_bounds__(256) k_encode(
     const int32_t *__restrict__ rec_list, int64_t n_records, const float *__restrict__ cen,
     const float *__restrict__ cen_rot, int nlist, uint8_t *__restrict__ codes,
     uint32_t *__restrict__ scales, float *__restrict__ resid, RotParams rp, CodecParams cp,
-    int dstride) {
+    int dstride, uint8_t *__restrict__ codes2, uint32_t *__restrict__ scales2,
+    CodecParams cp2) {
   extern __shared__ float lds[];
-  __shared__ float cbs[64];
+  __shared__ float cbs[64], cbs2[64];
   __shared__ int16_t pi[128];
   const int lane = threadIdx.x & 63;
   const int wid = threadIdx.x >> 6;
   const int nw = blockDim.x >> 6;
-  if (threadIdx.x < 64) cbs[threadIdx.x] = cp.cb[threadIdx.x];
+  if (threadIdx.x < 64) {
+    cbs[threadIdx.x] = cp.cb[threadIdx.x];
+    cbs2[threadIdx.x] = cp2.cb[threadIdx.x];
+  }
   load_perm(rp, pi);
   const int64_t rec = int64_t(blockIdx.x) * nw + wid;
   int64_t row = -1;
@@ -229,6 +233,8 @@ __global__ void __launch_bounds__(256) k_encode(
   float *v = lds + wid * 2 * dstride;
   float *w = v + dstride;
   uint8_t *cl = reinterpret_cast<uint8_t *>(lds + nw * 2 * dstride) + wid * (dstride / 1);
+  // second-stage codes follow the first-stage ones (allocated only with codes2)
+  uint8_t *cl2 = reinterpret_cast<uint8_t *>(lds + nw * 2 * dstride) + (nw + wid) * dstride;
   const int D = rp.D;
   float xx = 0.f, rr = 0.f, cc = 0.f;
   const uint2 sm = lane_sign_masks(rp, lane);
@@ -311,13 +317,102 @@ __global__ void __launch_bounds__(256) k_encode(
   const uint32_t su = enc_ue7m9(s);
   const float sh = dec_ue7m9(su);
   uint32_t gu = 0x7000u;
+  const float den2 = cc + 2.f * sh * rcd + sh * sh * cn2;   // ||c + R^T s^ c^||^2
   if (cp.global) {
-    const float den2 = cc + 2.f * sh * rcd + sh * sh * cn2;
     const float gv = (den2 > 0.f) ? sqrtf(xx / den2) : 0.f;
     gu = enc_ue4m12(gv);
   }
   if (lane == 0) scales[rec] = su | (gu << 16);
   __builtin_amdgcn_wave_barrier();  // codes in cl are written by other lanes
+
+  if (codes2) {
+    // Second stage: r2 = R x - R a with R a = g^ (R c + s^ c^), quantised in
+    // the rotated space with the second codebook (no further rotation).
+    const float gh = dec_ue4m12(gu);
+    float *r2 = (z == v) ? w : v;   // the buffer the rotation left free
+    float m2 = 0.f, rr2 = 0.f;
+#pragma unroll 4
+    for (int i = lane; i < D; i += kWave) {
+      const float cv = (m > 0.f) ? cbs[cl[i / g] * g + (i % g)] : 0.f;
+      const float rcv = rc[i] * rcw;
+      const float d = z[px(i)] + rcv - gh * (rcv + sh * cv);
+      r2[px(i)] = d;
+      m2 = fmaxf(m2, fabsf(d));
+      rr2 += d * d;
+    }
+    wave_sync();
+    m2 = wave_max(m2);
+    rr2 = wave_sum(rr2);
+    const float inv2 = (m2 > 0.f) ? cp2.emax / m2 : 0.f;
+    const int g2 = cp2.g;
+    float cn22 = 0.f, rad = 0.f;   // ||c2^||^2 and <R a, c2^> / g^
+#pragma unroll 2
+    for (int j = lane; j < cp2.n_sub; j += kWave) {
+      int code = 0;
+      if (m2 > 0.f) {
+        if (g2 == 1) {
+          const float u = r2[px(j)] * inv2;
+#pragma unroll
+          for (int k = 0; k < 15; ++k) code += (k + 1 < cp2.K && u > cp2.thr[k]) ? 1 : 0;
+        } else {
+          float u[4];
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            const int i = j * g2 + t;
+            u[t] = (t < g2 && i < D) ? r2[px(i)] * inv2 : 0.f;
+          }
+          float best = 3.4e38f;
+          for (int k = 0; k < 16; ++k) {
+            float d = 0.f;
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+              if (t < g2) {
+                const float e = u[t] - cbs2[k * g2 + t];
+                d += e * e;
+              }
+            }
+            if (d < best) {
+              best = d;
+              code = k;
+            }
+          }
+        }
+        for (int t = 0; t < g2; ++t) {
+          const int i = j * g2 + t;
+          if (i >= D) break;
+          const float c2 = cbs2[code * g2 + t];
+          const float c1 = (m > 0.f) ? cbs[cl[i / g] * g + (i % g)] : 0.f;
+          cn22 += c2 * c2;
+          rad += (rc[i] * rcw + sh * c1) * c2;
+        }
+      }
+      cl2[j] = uint8_t(code);
+    }
+    cn22 = wave_sum(cn22);
+    rad = wave_sum(rad) * gh;
+    const float s2 = (m2 > 0.f && cn22 > 0.f) ? sqrtf(rr2 / cn22) : 0.f;
+    const uint32_t su2 = enc_ue7m9(s2);
+    const float sh2 = dec_ue7m9(su2);
+    uint32_t gu2 = 0x7000u;
+    if (cp2.global) {
+      const float dd = gh * gh * den2 + 2.f * sh2 * rad + sh2 * sh2 * cn22;
+      gu2 = enc_ue4m12((dd > 0.f) ? sqrtf(xx / dd) : 0.f);
+    }
+    if (lane == 0) scales2[row] = su2 | (gu2 << 16);
+    __builtin_amdgcn_wave_barrier();   // cl2 is written by other lanes
+    // canonical bit stream: code j at bits [w j, w j + w)
+    uint8_t *dst = codes2 + row * int64_t(cp2.canon_bytes);
+    const int w2 = cp2.w;
+    for (int t = lane; t < cp2.canon_bytes; t += kWave) {
+      uint32_t val = 0;
+      for (int b = 0; b < 8; ++b) {
+        const int p = 8 * t + b;
+        const int j = p / w2;
+        if (j < cp2.n_sub) val |= ((uint32_t(cl2[j]) >> (p - j * w2)) & 1u) << b;
+      }
+      dst[t] = uint8_t(val);
+    }
+  }
 
   // pack: group G covers coordinates [8G, 8G + 8) = sub-vectors [8G/g, 8G/g + 8/g)
   const int n_groups = cp.d_pad >> 3;
@@ -403,31 +498,69 @@ int rslm_fwht(const rslm_plan *p, const float *x, float *y, int64_t n, int inver
   return check_launch();
 }
 
-int rslm_encode(const rslm_plan *p, const float *x, int64_t n_rows, const int64_t *src_row,
-                const int32_t *rec_list, int64_t n_records, const float *centroids,
-                const float *centroids_rot, int32_t nlist, uint8_t *codes, uint32_t *scales,
-                float *resid_rot, void *stream) {
+static int encode_impl(const rslm_plan *p, const rslm_plan *p2, const float *x, int64_t n_rows,
+                       const int64_t *src_row, const int32_t *rec_list, int64_t n_records,
+                       const float *centroids, const float *centroids_rot, int32_t nlist,
+                       uint8_t *codes, uint32_t *scales, float *resid_rot, uint8_t *codes2,
+                       uint32_t *scales2, hipStream_t s) {
+  if (launch_encode_reg(p, p2, x, n_rows, src_row, rec_list, n_records, centroids,
+                        centroids_rot, nlist, codes, scales, resid_rot, codes2, scales2, s))
+    return check_launch();
+  const int D = p->rot.D;
+  const int dstride = lds_floats(D);
+  // two float buffers plus one byte per sub-vector (<= dstride bytes) per
+  // wave, and another for the second stage
+  const size_t per_wave = 2 * size_t(dstride) * 4 + size_t(dstride) * (p2 ? 2 : 1);
+  int waves = 4;
+  while (waves > 1 && size_t(waves) * per_wave > 65536) waves >>= 1;
+  const size_t shm = size_t(waves) * per_wave;
+  const int64_t grid = (n_records + waves - 1) / waves;
+  if (grid > 0x7fffffff) return RSLM_ERR_INVALID_ARG;
+  hipLaunchKernelGGL(k_encode, dim3(unsigned(grid)), dim3(64 * waves), shm, s, x, n_rows, src_row,
+                     rec_list, n_records, centroids, centroids_rot, nlist, codes, scales,
+                     resid_rot, p->rot, p->codec, dstride, codes2, scales2,
+                     p2 ? p2->codec : p->codec);
+  return check_launch();
+}
+
+static int encode_args_ok(const rslm_plan *p, const float *x, int64_t n_rows,
+                          const int64_t *src_row, const int32_t *rec_list, int64_t n_records,
+                          const float *centroids, const float *centroids_rot, int32_t nlist,
+                          uint8_t *codes, uint32_t *scales) {
   if (!p || n_records < 0 || n_rows < 0) return RSLM_ERR_INVALID_ARG;
   if (n_records == 0) return RSLM_OK;
   if (!x || !codes || !scales) return RSLM_ERR_INVALID_ARG;
   if (centroids && (!rec_list || !centroids_rot || nlist < 1)) return RSLM_ERR_INVALID_ARG;
   if (!src_row && n_records > n_rows) return RSLM_ERR_INVALID_ARG;
   if ((n_records + 3) / 4 > 0x7fffffff) return RSLM_ERR_INVALID_ARG;
-  if (launch_encode_reg(p, x, n_rows, src_row, rec_list, n_records, centroids, centroids_rot,
-                        nlist, codes, scales, resid_rot, as_stream(stream)))
-    return check_launch();
-  const int D = p->rot.D;
-  const int dstride = lds_floats(D);
-  int waves = 4;
-  // two float buffers plus one byte per sub-vector (<= dstride bytes) per wave
-  while (waves > 1 && size_t(waves) * (2 * dstride * 4 + dstride) > 65536) waves >>= 1;
-  const size_t shm = size_t(waves) * (2 * dstride * 4 + dstride);
-  const int64_t grid = (n_records + waves - 1) / waves;
-  if (grid > 0x7fffffff) return RSLM_ERR_INVALID_ARG;
-  hipLaunchKernelGGL(k_encode, dim3(unsigned(grid)), dim3(64 * waves), shm, as_stream(stream), x,
-                     n_rows, src_row, rec_list, n_records, centroids, centroids_rot, nlist, codes,
-                     scales, resid_rot, p->rot, p->codec, dstride);
-  return check_launch();
+  return RSLM_OK;
+}
+
+int rslm_encode(const rslm_plan *p, const float *x, int64_t n_rows, const int64_t *src_row,
+                const int32_t *rec_list, int64_t n_records, const float *centroids,
+                const float *centroids_rot, int32_t nlist, uint8_t *codes, uint32_t *scales,
+                float *resid_rot, void *stream) {
+  const int st = encode_args_ok(p, x, n_rows, src_row, rec_list, n_records, centroids,
+                                centroids_rot, nlist, codes, scales);
+  if (st || n_records == 0) return st;
+  return encode_impl(p, nullptr, x, n_rows, src_row, rec_list, n_records, centroids,
+                     centroids_rot, nlist, codes, scales, resid_rot, nullptr, nullptr,
+                     as_stream(stream));
+}
+
+int rslm_encode_two_stage(const rslm_plan *p, const rslm_plan *p2, const float *x,
+                          int64_t n_rows, const int64_t *src_row, const int32_t *rec_list,
+                          int64_t n_records, const float *centroids, const float *centroids_rot,
+                          int32_t nlist, uint8_t *codes, uint32_t *scales, uint8_t *codes2,
+                          uint32_t *scales2, void *stream) {
+  const int st = encode_args_ok(p, x, n_rows, src_row, rec_list, n_records, centroids,
+                                centroids_rot, nlist, codes, scales);
+  if (st) return st;
+  if (!p2 || p2->rot.D != p->rot.D || p2->rot.passes != 0) return RSLM_ERR_INVALID_ARG;
+  if (n_records == 0) return RSLM_OK;
+  if (!codes2 || !scales2) return RSLM_ERR_INVALID_ARG;
+  return encode_impl(p, p2, x, n_rows, src_row, rec_list, n_records, centroids, centroids_rot,
+                     nlist, codes, scales, nullptr, codes2, scales2, as_stream(stream));
 }
 
 static int64_t pack_grid(int64_t total) {

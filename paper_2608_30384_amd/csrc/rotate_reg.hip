@@ -221,23 +221,33 @@ __device__ __forceinline__ uint32_t sgnbit(uint32_t m, int b, int i) {
   return ((m >> (8 * (b & 1) + i)) & 1u) << 31;
 }
 
-template <int NB, int BITS>
+// TWO = true adds the second (rescoring) stage with a 2-D K = 16 codebook
+// (the 2-bit codec): the pairs (8 r + 2 k, 8 r + 2 k + 1) of a block are
+// sub-vectors 64 b + 4 r + k, so a lane's four codes of a block are 16
+// consecutive bits of the canonical record at byte 32 b + 2 r.
+template <int NB, int BITS, bool TWO>
 __global__ void __launch_bounds__(256) k_encode_rows(
     const float *__restrict__ x, int64_t n_rows, const int64_t *__restrict__ src_row,
     const int32_t *__restrict__ rec_list, int64_t n_records, const float *__restrict__ cen,
     const float *__restrict__ cen_rot, int nlist, uint8_t *__restrict__ codes,
-    uint32_t *__restrict__ scales, float *__restrict__ resid, RotParams rp, CodecParams cp) {
+    uint32_t *__restrict__ scales, float *__restrict__ resid, RotParams rp, CodecParams cp,
+    uint8_t *__restrict__ codes2, uint32_t *__restrict__ scales2, CodecParams cp2) {
   constexpr int D = 128 * NB;
   constexpr int E = 8 * NB;
   constexpr int K = 1 << BITS;
   constexpr int kVecStride = D + 4;   // floats per vector buffer (offset of 4 banks per row)
   __shared__ float buf[16 * kVecStride];
   __shared__ float cbs[16], thr[16];
+  __shared__ float cb2[16], cb2y[16];   // second codebook, first and second coordinates
   __shared__ uint32_t rmask[16];
   __shared__ uint16_t ts[D];
   const int lane = threadIdx.x & 63;
   const int wid = threadIdx.x >> 6;
   const int rho = lane >> 4, r = lane & 15;
+  if (TWO && threadIdx.x < 16) {
+    cb2[threadIdx.x] = cp2.cb[2 * threadIdx.x];
+    cb2y[threadIdx.x] = cp2.cb[2 * threadIdx.x + 1];
+  }
   if (threadIdx.x < 16) {
     cbs[threadIdx.x] = cp.cb[threadIdx.x];
     // sorted decision thresholds, padded with +inf for the binary search
@@ -391,8 +401,8 @@ __global__ void __launch_bounds__(256) k_encode_rows(
   const uint32_t su = enc_ue7m9(s);
   const float sh = dec_ue7m9(su);
   uint32_t gu = 0x7000u;
+  const float den2 = cc + 2.f * sh * rcd + sh * sh * cn2;   // ||c + R^T s^ c^||^2
   if (cp.global) {
-    const float den2 = cc + 2.f * sh * rcd + sh * sh * cn2;
     const float gv = (den2 > 0.f) ? sqrtf(xx / den2) : 0.f;
     gu = enc_ue4m12(gv);
   }
@@ -417,7 +427,101 @@ __global__ void __launch_bounds__(256) k_encode_rows(
       }
     }
   }
-  if (resid) {
+  if (TWO) {
+    // second residual r2 = R x - R a, R a = g^ (R c + s^ c^), kept in z.
+    // The rotated centre is read again where it is needed rather than kept
+    // (opaque zero offsets stop the compiler from holding earlier loads).
+    const float gh = dec_ue4m12(gu);
+    float m2 = 0.f, rr2 = 0.f;
+    int off1 = 0;
+    asm volatile("" : "+v"(off1));
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const float4 v = *reinterpret_cast<const float4 *>(rcr + off1 + 128 * b + 4 * h);
+        const float va[4] = {v.x * rcw, v.y * rcw, v.z * rcw, v.w * rcw};
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const int e = 8 * b + 4 * h + t;
+          const float d = z[e] + va[t] - gh * (va[t] + sh * centroid(b, 4 * h + t));
+          z[e] = d;
+          m2 = fmaxf(m2, fabsf(d));
+          rr2 = fmaf(d, d, rr2);
+        }
+      }
+    m2 = row_max16(m2);
+    rr2 = row_sum16(rr2);
+    const float inv2 = (m2 > 0.f) ? cp2.emax / m2 : 0.f;
+    // Nearest 2-D centroid: argmin_k |c_k|^2 / 2 - <u, c_k> (lower k on
+    // ties); the codebook terms are uniform (kernel arguments, scalar
+    // registers).  With the codes of a block: ||c2^||^2, <c^, c2^> and
+    // <R c, c2^>.  A zero r2 (m2 = 0) gets codes 0 and s2^ = 0, which
+    // removes these sums from g2^, so they need no guard.
+    uint32_t w2[NB];
+    float cn22 = 0.f, c12 = 0.f, rc2 = 0.f;
+    int off2 = 0;
+    asm volatile("" : "+v"(off2));
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const float4 ra = *reinterpret_cast<const float4 *>(rcr + off2 + 128 * b);
+      const float4 rb = *reinterpret_cast<const float4 *>(rcr + off2 + 128 * b + 4);
+      float nu0[4], nu1[4], best[4];
+      uint32_t code[4];
+#pragma unroll
+      for (int k2 = 0; k2 < 4; ++k2) {
+        nu0[k2] = -z[8 * b + 2 * k2] * inv2;
+        nu1[k2] = -z[8 * b + 2 * k2 + 1] * inv2;
+        best[k2] = 3.4e38f;
+        code[k2] = 0u;
+      }
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        const float c0 = cp2.cb[2 * k], c1 = cp2.cb[2 * k + 1], hk = cp2.cbh[k];
+#pragma unroll
+        for (int k2 = 0; k2 < 4; ++k2) {
+          const float d = fmaf(nu1[k2], c1, fmaf(nu0[k2], c0, hk));
+          code[k2] = (d < best[k2]) ? uint32_t(k) : code[k2];
+          best[k2] = fminf(best[k2], d);
+        }
+      }
+      const float rcv[8] = {ra.x * rcw, ra.y * rcw, ra.z * rcw, ra.w * rcw,
+                            rb.x * rcw, rb.y * rcw, rb.z * rcw, rb.w * rcw};
+      uint32_t wb = word[b];   // first-stage codes, looked up again
+      asm volatile("" : "+v"(wb));
+      w2[b] = 0u;
+#pragma unroll
+      for (int k2 = 0; k2 < 4; ++k2) {
+        const uint32_t cd = code[k2];
+        w2[b] |= cd << (4 * k2);
+        const float c0 = cb2[cd], c1 = cb2y[cd];
+        cn22 = fmaf(c0, c0, fmaf(c1, c1, cn22));
+        const float e0 = lds_at(cbs, 4u * ((wb >> (BITS * 2 * k2)) & uint32_t(K - 1)));
+        const float e1 = lds_at(cbs, 4u * ((wb >> (BITS * (2 * k2 + 1))) & uint32_t(K - 1)));
+        c12 = fmaf(e0, c0, fmaf(e1, c1, c12));
+        rc2 = fmaf(rcv[2 * k2], c0, fmaf(rcv[2 * k2 + 1], c1, rc2));
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (!(m2 > 0.f))
+#pragma unroll
+      for (int b = 0; b < NB; ++b) w2[b] = 0u;
+    cn22 = row_sum16(cn22);
+    const float rad = gh * row_sum16(fmaf(sh, c12, rc2));   // <R a, c2^>
+    const float s2 = (m2 > 0.f && cn22 > 0.f) ? sqrtf(rr2 / cn22) : 0.f;
+    const uint32_t su2 = enc_ue7m9(s2);
+    const float sh2 = dec_ue7m9(su2);
+    uint32_t gu2 = 0x7000u;
+    if (cp2.global) {
+      const float dd = gh * gh * den2 + 2.f * sh2 * rad + sh2 * sh2 * cn22;
+      gu2 = enc_ue4m12((dd > 0.f) ? sqrtf(xx / dd) : 0.f);
+    }
+    if (r == 0) scales2[row] = su2 | (gu2 << 16);
+    uint8_t *dst = codes2 + row * int64_t(cp2.canon_bytes) + 2 * r;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) *reinterpret_cast<uint16_t *>(dst + 32 * b) = uint16_t(w2[b]);
+  }
+  if (!TWO && resid) {   // (the two-stage launch passes no residual output)
     const float gh = dec_ue4m12(gu);
     float *out = resid + row * D + 8 * r;   // indexed by source row
 #pragma unroll
@@ -472,27 +576,38 @@ bool launch_rotate_reg(const rslm_plan *p, const float *x, float *y, int64_t n, 
   return true;
 }
 
-bool launch_encode_reg(const rslm_plan *p, const float *x, int64_t n_rows, const int64_t *src_row,
-                       const int32_t *rec_list, int64_t n_records, const float *cen,
-                       const float *cen_rot, int nlist, uint8_t *codes, uint32_t *scales,
-                       float *resid, hipStream_t s) {
+bool launch_encode_reg(const rslm_plan *p, const rslm_plan *p2, const float *x, int64_t n_rows,
+                       const int64_t *src_row, const int32_t *rec_list, int64_t n_records,
+                       const float *cen, const float *cen_rot, int nlist, uint8_t *codes,
+                       uint32_t *scales, float *resid, uint8_t *codes2, uint32_t *scales2,
+                       hipStream_t s) {
   if (!reg_path_ok(p->rot) || p->codec.g != 1 || p->codec.d_pad != p->rot.D) return false;
+  // the second stage here is the 2-D K = 16 codec only
+  const bool two = p2 != nullptr;
+  if (two && (p2->codec.g != 2 || p2->codec.K != 16 || p2->codec.n_sub * 2 != p->rot.D ||
+              p2->codec.canon_bytes * 4 != p->rot.D || resid))
+    return false;
   // 16-byte vector loads and stores of every row
   if ((reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(cen) |
        reinterpret_cast<uintptr_t>(cen_rot) | reinterpret_cast<uintptr_t>(resid)) % 16)
     return false;
+  if (two && (reinterpret_cast<uintptr_t>(codes2) % 2)) return false;
   const int64_t groups = (n_records + 15) / 16;   // 16 vectors per 256-thread workgroup
   if (groups > 0x7fffffff) return false;
   const unsigned grid = unsigned(groups);
-#define CALL_B(NB, B)                                                                         \
-  hipLaunchKernelGGL((k_encode_rows<NB, B>), dim3(grid), dim3(256), 0, s, x, n_rows, src_row,  \
-                     rec_list, n_records, cen, cen_rot, nlist, codes, scales, resid, p->rot,    \
-                     p->codec)
+  const CodecParams &cp2 = two ? p2->codec : p->codec;
+#define CALL_B(NB, B, T)                                                                        \
+  hipLaunchKernelGGL((k_encode_rows<NB, B, T>), dim3(grid), dim3(256), 0, s, x, n_rows, src_row, \
+                     rec_list, n_records, cen, cen_rot, nlist, codes, scales, resid, p->rot,      \
+                     p->codec, codes2, scales2, cp2)
 #define CALL(J)                  \
-  if (p->codec.bits == 4)        \
-    CALL_B((J) / 2, 4);          \
+  if (two)                       \
+    CALL_B((J) / 2, 4, true);    \
+  else if (p->codec.bits == 4)   \
+    CALL_B((J) / 2, 4, false);   \
   else                           \
-    CALL_B((J) / 2, 3)
+    CALL_B((J) / 2, 3, false)
+  if (two && p->codec.bits != 4) return false;
   RSLM_REG_SWITCH(p->rot.D / 128, CALL)
 #undef CALL
 #undef CALL_B

@@ -70,6 +70,7 @@ struct CodecParams {
   float emax;                 // E_max(D) as float
   float cb[64];               // codebook, K*g values
   float thr[16];              // 1-D decision thresholds (K-1 used)
+  float cbh[16];              // |C_k|^2 / 2 (unused k: a huge value)
 };
 
 }  // namespace rslm
@@ -102,10 +103,13 @@ inline hipStream_t as_stream(void *s) { return reinterpret_cast<hipStream_t>(s);
 // false when the plan is not handled there.
 bool launch_rotate_reg(const rslm_plan *p, const float *x, float *y, int64_t n, int inverse,
                        hipStream_t s);
-bool launch_encode_reg(const rslm_plan *p, const float *x, int64_t n_rows, const int64_t *src_row,
-                       const int32_t *rec_list, int64_t n_records, const float *cen,
-                       const float *cen_rot, int nlist, uint8_t *codes, uint32_t *scales,
-                       float *resid, hipStream_t s);
+// p2 / codes2 / scales2: the optional second (rescoring) stage of
+// rslm_encode_two_stage (p2 == nullptr: none).
+bool launch_encode_reg(const rslm_plan *p, const rslm_plan *p2, const float *x, int64_t n_rows,
+                       const int64_t *src_row, const int32_t *rec_list, int64_t n_records,
+                       const float *cen, const float *cen_rot, int nlist, uint8_t *codes,
+                       uint32_t *scales, float *resid, uint8_t *codes2, uint32_t *scales2,
+                       hipStream_t s);
 
 // ---- device helpers ------------------------------------------------------
 
