@@ -187,6 +187,35 @@ def traffic_from_profiles(streamed_records_per_launch):
     return t.get("hbm_bytes_per_launch")
 
 
+def calibrate_read(torch, lib, x, reps=5):
+    """Best read bandwidth (GB/s) of the calibration kernel over the first
+    4 GiB of x, across grid sizes and with / without non-temporal loads."""
+    import ctypes
+    flat = x.view(-1)[: min(x.numel(), 1 << 30)]
+    nbytes = flat.numel() * 4
+    out = torch.empty(1 << 16, dtype=torch.int32, device=x.device)
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    best = (0.0, None)
+    for nt in (0, 1):
+        for grid in (2048, 8192, 32768, 65536):
+            call = lambda: lib.rslm_calibrate_read(ctypes.c_void_p(flat.data_ptr()), nbytes,
+                                                   ctypes.c_void_p(out.data_ptr()), grid, nt,
+                                                   stream)
+            for _ in range(2):
+                call()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                st = call()
+                assert st == 0, st
+            e1.record()
+            torch.cuda.synchronize()
+            bw = reps * nbytes / (e0.elapsed_time(e1) * 1e-3) / 1e9
+            if bw > best[0]:
+                best = (bw, {"grid": grid, "nontemporal": bool(nt)})
+    return best
+
+
 # ------------------------------------------------------------------ CPU baseline
 _CPU = {}
 
@@ -322,19 +351,9 @@ def main():
     resid_e = torch.empty_like(xe)
     log(f"setup {time.time() - t_setup:.1f} s")
 
-    # context: what a plain read-only streaming kernel (a torch reduction over
-    # 4 GiB of the collection) achieves on this device
-    flat = x.view(-1)[: min(x.numel(), 1 << 30)]
-    for _ in range(2):
-        flat.sum()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(5):
-        flat.sum()
-    e1.record()
-    torch.cuda.synchronize()
-    stream_read_GBps = 5 * flat.numel() * 4 / (e0.elapsed_time(e1) * 1e-3) / 1e9
-    del flat
+    # context: the read bandwidth a plain streaming kernel sustains on this
+    # device (rslm_calibrate_read over 4 GiB of the collection, best grid)
+    stream_read_GBps, stream_read_cfg = calibrate_read(torch, LL.lib(), x)
 
     batches = [q_all[i:i + args.batch].contiguous() for i in range(0, args.nq, args.batch)]
     sizes = index.list_sizes.long()
@@ -355,6 +374,10 @@ def main():
     ev = lambda: torch.cuda.Event(enable_timing=True)
 
     def step(b, timers):
+        """One pass of every row over one batch: rotate, probe, scan + top-k,
+        rescore, and the encode of new vectors (row a7).  (Running the encode
+        concurrently on a second stream was slower: it takes the CUs the
+        probe and top-k need.)"""
         qb = batches[b % len(batches)]
         e = timers
         e[0].record()
@@ -446,6 +469,7 @@ def main():
             "algorithmic_bytes_per_launch": streamed_avg * rec_bytes,
             "kernel_ms": t_scan,
             "stream_read_GBps_measured": stream_read_GBps,
+            "stream_read_kernel": stream_read_cfg,
             "frac_of_measured_stream": achieved / stream_read_GBps,
         },
         "scan": {
@@ -465,6 +489,31 @@ def main():
         },
         "kernel_sources": csrc_hash(),
         "scan_sources": scan_src_hash(),
+    }
+    # two-stage encode (4-bit scan codes + 2-bit RSLM rescoring codes, the
+    # capacity configuration's records) of the same chunk, outside the step
+    plan2 = R.Plan(D, 2, passes=0, scale_mode="global")
+    codes2_e = torch.empty((args.encode_chunk, plan2.canon_bytes), dtype=torch.uint8, device=dev)
+    scales2_e = torch.empty(args.encode_chunk, dtype=torch.int32, device=dev)
+
+    def enc2():
+        R.rslm_encode_two_stage(plan, plan2, xe, codes_e, scales_e, codes2_e, scales2_e,
+                                rec_list=ae, centroids=cen, centroids_rot=crot)
+    for _ in range(2):
+        enc2()
+    e0, e1 = ev(), ev()
+    e0.record()
+    for _ in range(10):
+        enc2()
+    e1.record()
+    torch.cuda.synchronize()
+    t2 = e0.elapsed_time(e1) / 10
+    b2 = args.encode_chunk * (4 * D + rec_bytes + plan2.canon_bytes + 4)
+    out["encode_two_stage"] = {
+        "vectors": args.encode_chunk, "ms": t2,
+        "vectors_per_s": args.encode_chunk / (t2 * 1e-3),
+        "GBps": b2 / (t2 * 1e-3) / 1e9,
+        "record_bytes": [rec_bytes, plan2.canon_bytes + 4],
     }
     if not args.no_cpu_baseline:
         log("CPU oracle baseline")

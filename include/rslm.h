@@ -286,6 +286,17 @@ int rslm_rescore(const rslm_rescore_codec *codec, const float *q_rot,
 #define RSLM_TIMER_TOPK 1
 int rslm_set_timer(int which, void *ev_begin, void *ev_end);
 
+/* ------------------------------------------------------------------------
+ * Measurement utility (not part of the method): a plain streaming read of
+ * `bytes` bytes of device memory at buf (16-byte aligned, bytes a multiple of
+ * 16) by `grid` workgroups of 256 threads, each writing the XOR of the words
+ * it read to out[blockIdx] (out: grid uint32); nontemporal != 0 uses
+ * non-temporal loads.  Timing it gives the read bandwidth the device
+ * sustains, the reference for the scan's bandwidth.
+ * ------------------------------------------------------------------------ */
+int rslm_calibrate_read(const void *buf, int64_t bytes, uint32_t *out, int32_t grid,
+                        int nontemporal, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -24,7 +24,7 @@ EXPORTS = [
     "rslm_fwht", "rslm_encode", "rslm_encode_two_stage", "rslm_pack_codes", "rslm_unpack_codes",
     "ivf_assign_probe_workspace", "ivf_assign_probe",
     "rslm_scan_topk_workspace", "rslm_scan_topk",
-    "rslm_sq8_fit", "rslm_sq8_encode", "rslm_rescore", "rslm_set_timer",
+    "rslm_sq8_fit", "rslm_sq8_encode", "rslm_rescore", "rslm_set_timer", "rslm_calibrate_read",
 ]
 
 
@@ -85,6 +85,7 @@ def _declare(lib):
         "rslm_sq8_encode": (C.c_int, [P, I64, I32, P, P, P, I64, P, P]),
         "rslm_rescore": (C.c_int, [C.POINTER(RescoreCodec), P, I32, P, P, I32, I32, P, P, P]),
         "rslm_set_timer": (C.c_int, [C.c_int, P, P]),
+        "rslm_calibrate_read": (C.c_int, [P, I64, P, I32, C.c_int, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
