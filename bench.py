@@ -54,6 +54,10 @@ def parse():
     ap.add_argument("--encode-chunk", type=int, default=65536)
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--workload", choices=("text768", "capacity", "sweep"), default="text768",
+                    help="text768 (default): the metric's configuration; capacity: 100M x 768 "
+                         "at nlist 16,384 with 2-bit RSLM rescoring records; sweep: 10M x 1,024 "
+                         "unit-norm at 1, 2, 3 and 4 bits with recall@10")
     ap.add_argument("--copy-calib", action="store_true",
                     help="only run a 1 GiB device copy (counter calibration) and exit")
     ap.add_argument("--stats-summary", nargs=2, metavar=("KERNEL_STATS_CSV", "BENCH_JSON"),
@@ -302,6 +306,10 @@ def main():
     if args.gpus != 1:
         print(json.dumps({"error": "this build measures one GPU only; run with --gpus 1"}))
         sys.exit(2)
+    if args.workload == "capacity":
+        return run_capacity(args)
+    if args.workload == "sweep":
+        return run_sweep(args)
     import torch
 
     import synth
@@ -522,6 +530,284 @@ def main():
         torch.cuda.synchronize()
         out["cpu_baseline"] = cpu_baseline(R, plan, index, qrot, pid, pdot, args.k,
                                            args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+# ------------------------------------------------------------------ other workloads
+def _timed_batches(torch, batches, fn, warmup):
+    """Runs fn over every batch (after `warmup` untimed ones); returns the
+    wall time of the timed pass (host clock between synchronisations)."""
+    for i in range(warmup):
+        fn(batches[i % len(batches)])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for qb in batches:
+        fn(qb)
+    torch.cuda.synchronize()
+    return time.perf_counter() - t0
+
+
+def _streamed(torch, R, cen, batches, nprobe, sizes, nlist):
+    """Scored pairs and streamed records (lists read once per group of <= 8
+    queries) of each batch, computed outside the timed region."""
+    out = []
+    for qb in batches:
+        pid, _ = R.ivf_assign_probe(qb, cen, nprobe, R.IVF_PROBE_IP)
+        pl = pid.long().reshape(-1)
+        m = torch.bincount(pl, minlength=nlist)
+        out.append((int(sizes[pl].sum().item()), int((((m + 7) // 8) * sizes).sum().item())))
+    return out
+
+
+def run_capacity(args):
+    """Capacity configuration: 100,000,000 x 768 anisotropic vectors (raw
+    float32 never resident: generated, assigned and encoded in blocks of
+    2^22 rows), nlist 16,384, 4-bit RSLM scan records + 2-bit RSLM rescoring
+    records (two-stage encode, global scales) resident in HBM; 100,000 queries
+    in batches of 1,024, nprobe 128, top-100 from the scan rescored to top-10.
+    Reports the scan path's throughput over every batch and the bulk
+    two-stage encode rate on a device-resident block."""
+    import torch
+
+    import synth
+    import paper_2608_30384_amd as R
+    from paper_2608_30384_amd import _lib as LL
+    from paper_2608_30384_amd import ivf
+
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+    N, D, nlist, nprobe, B = 100_000_000, 768, 16384, 128, 1024
+    nq, k, k_out = 100_000, 100, 10
+    BLK = synth.TORCH_BLOCK
+    nblk = (N + BLK - 1) // BLK
+    t_setup = time.time()
+    plan = R.Plan(D, 4, passes=-1, scale_mode="global")
+    plan2 = R.Plan(D, 2, passes=0, scale_mode="global")
+    xb = torch.empty((BLK, D), dtype=torch.float32, device=dev)
+
+    def block(b):
+        synth.aniso_torch_block(b, D, seed=100, out=xb)
+        rows = min(BLK, N - b * BLK)
+        return xb[:rows]
+
+    log(f"k-means: {nlist} lists on the first {256 * nlist} rows, {args.kmeans_iters} iterations")
+    sample = block(0)[: 256 * nlist].contiguous()
+    cen = ivf.kmeans(sample, nlist, iters=args.kmeans_iters, seed=0)
+    del sample
+    torch.cuda.synchronize()
+    log(f"k-means done at {time.time() - t_setup:.0f} s; assigning {N} rows")
+    assign = torch.empty(N, dtype=torch.int32, device=dev)
+    for b in range(nblk):
+        xs = block(b)
+        R.ivf_assign_probe(xs, cen, 1, R.IVF_ASSIGN_L2, out_ids=assign[b * BLK:b * BLK + len(xs)])
+        if b % 6 == 5:
+            torch.cuda.synchronize()
+            log(f"  assigned {min(N, (b + 1) * BLK)} rows at {time.time() - t_setup:.0f} s")
+    torch.cuda.synchronize()
+    log(f"assignment done at {time.time() - t_setup:.0f} s")
+    crot = R.rslm_fwht(plan, cen)
+    offsets, sizes, src_row, rec_list, ids, total = ivf.layout(assign, nlist)
+    del assign
+    codes = torch.zeros(plan.code_bytes(total), dtype=torch.uint8, device=dev)
+    scales = torch.zeros(total, dtype=torch.int32, device=dev)
+    codes2 = torch.zeros((N, plan2.canon_bytes), dtype=torch.uint8, device=dev)
+    scales2 = torch.zeros(N, dtype=torch.int32, device=dev)
+    for b in range(nblk):
+        xs = block(b)
+        lo = b * BLK
+        src_local = src_row - lo    # records of other blocks fall outside [0, rows): skipped
+        R.rslm_encode_two_stage(plan, plan2, xs, codes, scales, codes2[lo:lo + len(xs)],
+                                scales2[lo:lo + len(xs)], n_records=total, src_row=src_local,
+                                rec_list=rec_list, centroids=cen, centroids_rot=crot)
+        del src_local
+    torch.cuda.synchronize()
+    del src_row
+    index = R.Index(offsets, sizes, ids, codes, scales)
+    resident = (codes.numel() + scales.numel() * 4 + codes2.numel() + scales2.numel() * 4 +
+                ids.numel() * 4)
+    log(f"index built at {time.time() - t_setup:.0f} s: {total} records, max list "
+        f"{index.max_list_size}, {resident / 1e9:.1f} GB resident")
+
+    # bulk two-stage encode rate on one device-resident block (records = rows)
+    xs = block(0)
+    a0, _ = R.ivf_assign_probe(xs, cen, 1, R.IVF_ASSIGN_L2)
+    c_e = torch.empty(plan.code_bytes(len(xs)), dtype=torch.uint8, device=dev)
+    s_e = torch.empty(len(xs), dtype=torch.int32, device=dev)
+    c2_e = torch.empty((len(xs), plan2.canon_bytes), dtype=torch.uint8, device=dev)
+    s2_e = torch.empty(len(xs), dtype=torch.int32, device=dev)
+    enc = lambda: R.rslm_encode_two_stage(plan, plan2, xs, c_e, s_e, c2_e, s2_e, rec_list=a0,
+                                          centroids=cen, centroids_rot=crot)
+    enc()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(3):
+        enc()
+    e1.record()
+    torch.cuda.synchronize()
+    t_enc = e0.elapsed_time(e1) / 3
+    del c_e, s_e, c2_e, s2_e, xb, xs
+    torch.cuda.empty_cache()
+
+    q_all = torch.from_numpy(synth.queries_like("aniso", nq, D, data_seed=100,
+                                                query_seed=200)).to(dev)
+    batches = [q_all[i:i + B].contiguous() for i in range(0, nq, B)]
+    work = _streamed(torch, R, cen, batches, nprobe, sizes.long(), nlist)
+    ws = torch.empty(R.rslm_scan_topk_workspace(plan, index, B, nprobe, k), dtype=torch.uint8,
+                     device=dev)
+    log(f"setup {time.time() - t_setup:.0f} s; scan workspace {ws.numel() / 1e9:.1f} GB")
+
+    def query(qb):
+        qrot = R.rslm_fwht(plan, qb)
+        pid, pdot = R.ivf_assign_probe(qb, cen, nprobe, R.IVF_PROBE_IP)
+        s1, i1 = R.rslm_scan_topk(plan, index, qrot, pid, pdot, k, ws=ws)
+        R.rslm_rescore_rslm(plan2, codes2, scales2, qrot, s1, i1, k_out)
+
+    wall = _timed_batches(torch, batches, query, args.warmup)
+    # the scan kernel alone (HIP events around its launch), on every batch
+    lib = LL.lib()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in batches]
+    for a, b_ in evs:
+        a.record()
+        b_.record()
+    torch.cuda.synchronize()
+    for (a, b_), qb in zip(evs, batches):
+        lib.rslm_set_timer(0, a._as_parameter_, b_._as_parameter_)
+        query(qb)
+    torch.cuda.synchronize()
+    lib.rslm_set_timer(0, None, None)
+    t_scan = sum(a.elapsed_time(b_) for a, b_ in evs) * 1e-3
+    pairs = sum(w[0] for w in work)
+    streamed = sum(w[1] for w in work)
+    rec_bytes = D * 4 // 8 + 4
+    achieved = streamed * rec_bytes / t_scan / 1e9
+    out = {
+        "metric": METRIC,
+        "value": pairs / wall,
+        "unit": "scored candidates/s",
+        "n_gpus": 1, "steps": len(batches), "warmup": args.warmup,
+        "ms_per_step": wall * 1e3 / len(batches),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": ("capacity: N=100,000,000 x d=768 anisotropic Gaussian, "
+                                "nlist=16384, 4-bit RSLM global + 2-bit RSLM global rescoring "
+                                "records resident, 100,000 queries in batches of 1,024, "
+                                "nprobe=128, top-100 -> top-10"),
+                   "N": N, "dim": D, "nlist": nlist, "nprobe": nprobe, "batch": B,
+                   "k": k, "k_out": k_out, "bits": 4, "rescore_bits": 2},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                     "kernel": "k_scan<4,24>", "kernel_ms_per_batch": t_scan * 1e3 / len(batches),
+                     "algorithmic_bytes_per_batch": streamed * rec_bytes / len(batches)},
+        "scan": {"pairs_per_batch": pairs / len(batches),
+                 "streamed_records_per_batch": streamed / len(batches),
+                 "candidates_per_s_scan_kernel": pairs / t_scan},
+        "resident_index_GB": resident / 1e9,
+        "max_list_size": index.max_list_size,
+        "encode_two_stage": {"vectors": BLK, "ms": t_enc, "vectors_per_s": BLK / (t_enc * 1e-3),
+                             "GBps": BLK * (4 * D + rec_bytes + plan2.canon_bytes + 4) /
+                             (t_enc * 1e-3) / 1e9},
+        "build_s": time.time() - t_setup,
+        "kernel_sources": csrc_hash(),
+    }
+    print(json.dumps(out), flush=True)
+
+
+def run_sweep(args):
+    """Bit-width sweep: 10,000,000 x 1,024 anisotropic unit-norm vectors,
+    nlist 4,096, RSLM codes at 1, 2, 3 and 4 bits (global scales) of the same
+    data; 10,000 queries in batches of 256, nprobe 64, top-10.  Per bit
+    width: scored candidates/s over every batch, the scan kernel's
+    algorithmic GB/s, and recall@10 against exact float32 MIPS over the raw
+    vectors (torch matmul on the device; the reference of a quality figure,
+    not of a kernel)."""
+    import torch
+
+    import synth
+    import paper_2608_30384_amd as R
+    from paper_2608_30384_amd import _lib as LL
+    from paper_2608_30384_amd import ivf
+
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+    N, D, nlist, nprobe, B, nq, k = 10_000_000, 1024, 4096, 64, 256, 10_000, 10
+    t_setup = time.time()
+    x = synth.aniso_torch(N, D, alpha=1.0, seed=100, normalize=True, device=dev)
+    cen = ivf.kmeans(x, nlist, iters=args.kmeans_iters, seed=0, sample=256 * nlist)
+    assign, _ = R.ivf_assign_probe(x, cen, 1, R.IVF_ASSIGN_L2)
+    q_all = torch.from_numpy(synth.queries_like("aniso", nq, D, data_seed=100, query_seed=200,
+                                                normalize=True)).to(dev)
+    batches = [q_all[i:i + B].contiguous() for i in range(0, nq, B)]
+    # exact top-10 by float32 inner product over the raw vectors
+    exact = []
+    for qb in batches:
+        s = torch.matmul(qb, x.T)
+        exact.append(torch.topk(s, k, dim=1).indices.int())
+        del s
+    torch.cuda.synchronize()
+    log(f"data, partitions and exact top-{k} in {time.time() - t_setup:.0f} s")
+    lib = LL.lib()
+    res = {}
+    for bits in (1, 2, 3, 4):
+        plan = R.Plan(D, bits, passes=-1, scale_mode="global")
+        index, crot, _ = ivf.build_index(plan, x, cen, assign=assign)
+        sizes = index.list_sizes.long()
+        work = _streamed(torch, R, cen, batches, nprobe, sizes, nlist)
+        ws = torch.empty(R.rslm_scan_topk_workspace(plan, index, B, nprobe, k),
+                         dtype=torch.uint8, device=dev)
+        found = []
+
+        def query(qb, keep=False):
+            qrot = R.rslm_fwht(plan, qb)
+            pid, pdot = R.ivf_assign_probe(qb, cen, nprobe, R.IVF_PROBE_IP)
+            s1, i1 = R.rslm_scan_topk(plan, index, qrot, pid, pdot, k, ws=ws)
+            if keep:
+                found.append(i1)
+        wall = _timed_batches(torch, batches, query, args.warmup)
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in batches]
+        for a, b_ in evs:
+            a.record()
+            b_.record()
+        torch.cuda.synchronize()
+        for (a, b_), qb in zip(evs, batches):
+            lib.rslm_set_timer(0, a._as_parameter_, b_._as_parameter_)
+            query(qb, keep=True)
+        torch.cuda.synchronize()
+        lib.rslm_set_timer(0, None, None)
+        t_scan = sum(a.elapsed_time(b_) for a, b_ in evs) * 1e-3
+        hits = 0
+        for f, e in zip(found, exact):
+            hits += int((f[:, :, None] == e[:, None, :]).any(2).sum().item())
+        pairs = sum(w[0] for w in work)
+        streamed = sum(w[1] for w in work)
+        rec_bytes = D * bits // 8 + 4
+        res[str(bits)] = {
+            "scored_candidates_per_s": pairs / wall,
+            "scan_kernel_candidates_per_s": pairs / t_scan,
+            "scan_kernel_GBps": streamed * rec_bytes / t_scan / 1e9,
+            "scan_kernel_frac_of_8TBps": streamed * rec_bytes / t_scan / 1e9 / HBM_PEAK_GBPS,
+            "record_bytes": rec_bytes,
+            "recall_at_10": hits / (nq * k),
+            "ms_per_batch": wall * 1e3 / len(batches),
+        }
+        log(f"{bits}-bit: {res[str(bits)]}")
+        del index, ws, found
+        torch.cuda.empty_cache()
+    out = {
+        "metric": "scored candidates/s, GB/s and recall@10 per bit width, d=1024 IVF scan, 1 GPU",
+        "value": res["4"]["scored_candidates_per_s"], "unit": "scored candidates/s",
+        "n_gpus": 1, "steps": len(batches), "warmup": args.warmup,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": ("bit-width sweep: N=10,000,000 x d=1024 anisotropic Gaussian, "
+                                "unit norm, nlist=4096, RSLM 1/2/3/4-bit global, 10,000 queries "
+                                "in batches of 256, nprobe=64, top-10"),
+                   "N": N, "dim": D, "nlist": nlist, "nprobe": nprobe, "batch": B, "k": k},
+        "per_bits": res,
+        "setup_s": time.time() - t_setup,
+        "kernel_sources": csrc_hash(),
+    }
     print(json.dumps(out), flush=True)
 
 

@@ -10,11 +10,12 @@ bytes without sharing any computation.
 
 from .tables import sign_table, permutation_table, codebook, codebook_shape
 from .data import (
-    gmix_means, gmix, aniso_params, aniso, aniso_torch, queries_like, random_rows,
+    gmix_means, gmix, aniso_params, aniso, aniso_torch, aniso_torch_block, TORCH_BLOCK,
+    queries_like, random_rows,
 )
 
 __all__ = [
     "sign_table", "permutation_table", "codebook", "codebook_shape",
-    "gmix_means", "gmix", "aniso_params", "aniso", "aniso_torch", "queries_like",
-    "random_rows",
+    "gmix_means", "gmix", "aniso_params", "aniso", "aniso_torch", "aniso_torch_block",
+    "TORCH_BLOCK", "queries_like", "random_rows",
 ]

@@ -110,6 +110,32 @@ def aniso_torch(n, d, alpha=1.0, seed=100, mean_seed=None, normalize=False,
     return out
 
 
+TORCH_BLOCK = 1 << 22
+
+
+def aniso_torch_block(b, d, alpha=1.0, seed=100, mean_seed=None, normalize=False,
+                      device="cuda", out=None, block=TORCH_BLOCK):
+    """Rows [b * block, (b + 1) * block) of a collection too large to hold
+    at once (same distribution as ``aniso``), generated on ``device`` with a
+    torch generator seeded by (seed, b), so any block regenerates on its own.
+    """
+    import torch
+
+    mean_seed = seed if mean_seed is None else mean_seed
+    sd, mu = aniso_params(d, alpha, mean_seed)
+    sd_t = torch.tensor(sd, dtype=torch.float32, device=device)
+    mu_t = torch.tensor(mu, dtype=torch.float32, device=device)
+    if out is None:
+        out = torch.empty((block, d), dtype=torch.float32, device=device)
+    gen = torch.Generator(device=device)
+    gen.manual_seed(int(seed) * 1_000_003 + int(b))
+    out.normal_(generator=gen)
+    out.mul_(sd_t).add_(mu_t)
+    if normalize:
+        out.div_(out.norm(dim=1, keepdim=True))
+    return out
+
+
 def queries_like(kind, n, d, data_seed=100, query_seed=200, **kw):
     """Queries drawn from the same distribution as a collection (same means)."""
     if kind == "gmix":
