@@ -9,7 +9,8 @@ rescoring; 10,000 queries from the same distribution in batches of 256,
 nprobe = 64, top-100 from the scan, rescored to top-10.
 
 A step is one pass of the whole path over one batch: query rotation,
-probing, scan + top-k, rescoring, and the encoding of 65,536 new vectors.
+probing, scan + top-k, rescoring, and the encoding of 65,536 new vectors
+into scan records and SQ8 rescoring codes (the collection's fitted ranges).
 ``value`` is the number of scored (query, candidate) pairs per second of
 whole-step time, inputs resident in HBM.  The JSON line also carries the
 roofline of the scan kernel, per-stage times, encode throughput and the CPU
@@ -356,7 +357,7 @@ def main():
     ae, _ = R.ivf_assign_probe(xe, cen, 1, R.IVF_ASSIGN_L2)
     codes_e = torch.empty(plan.code_bytes(args.encode_chunk), dtype=torch.uint8, device=dev)
     scales_e = torch.empty(args.encode_chunk, dtype=torch.int32, device=dev)
-    resid_e = torch.empty_like(xe)
+    sq8_e = torch.empty((args.encode_chunk, D), dtype=torch.uint8, device=dev)
     log(f"setup {time.time() - t_setup:.1f} s")
 
     # context: the read bandwidth a plain streaming kernel sustains on this
@@ -383,7 +384,8 @@ def main():
 
     def step(b, timers):
         """One pass of every row over one batch: rotate, probe, scan + top-k,
-        rescore, and the encode of new vectors (row a7).  (Running the encode
+        rescore, and the encode of new vectors into scan records and SQ8
+        rescoring codes (row a7).  (Running the encode
         concurrently on a second stream was slower: it takes the CUs the
         probe and top-k need.)"""
         qb = batches[b % len(batches)]
@@ -397,8 +399,8 @@ def main():
         e[3].record()
         R.rslm_rescore(codes2, lo, hi, qrot, s1, i1, args.k_out)
         e[4].record()
-        R.rslm_encode(plan, xe, codes_e, scales_e, rec_list=ae, centroids=cen, centroids_rot=crot,
-                      resid_rot=resid_e)
+        R.rslm_encode_sq8(plan, xe, codes_e, scales_e, lo, hi, sq8_e, rec_list=ae, centroids=cen,
+                          centroids_rot=crot)
         e[5].record()
         return qrot, pid, pdot
 
@@ -440,7 +442,7 @@ def main():
     achieved = streamed_avg * rec_bytes / (t_scan * 1e-3) / 1e9
     traffic = traffic_from_profiles(streamed_avg)
     enc_ms = stage["encode"] / args.steps
-    enc_bytes = args.encode_chunk * (4 * D + rec_bytes + 4 * D)
+    enc_bytes = args.encode_chunk * (4 * D + rec_bytes + D)
 
     out = {
         "metric": METRIC,

@@ -161,6 +161,24 @@ int rslm_encode_two_stage(const rslm_plan *plan, const rslm_plan *plan2, const f
                           uint32_t *scales, uint8_t *codes2, uint32_t *scales2,
                           void *stream);
 
+/* ------------------------------------------------------------------------
+ * rslm_encode_sq8 -- rslm_encode with the rotated second residual
+ * r2 = R x - g^ (R c + s^ C[code]) written directly as SQ8 codes with given
+ * ranges (the RelApprox-SQ8 rescoring records; Sections "Background and
+ * Related Work" and "Relative Quantization"): for d < D,
+ *   codes2[row][d] = clamp(rne((r2_d - sq8_lo[d]) / step_d), 0, 255),
+ *   step_d = (sq8_hi[d] - sq8_lo[d]) / 255 (a zero step gives 0),
+ * exactly what rslm_sq8_encode computes from the float residual.  Used to
+ * encode vectors added to a collection whose ranges were fitted already.
+ *   sq8_lo, sq8_hi : D float32 (device); codes2 : n_rows x D uint8, row
+ *   `row` written for record r.  Everything else as in rslm_encode.
+ * ------------------------------------------------------------------------ */
+int rslm_encode_sq8(const rslm_plan *plan, const float *x, int64_t n_rows,
+                    const int64_t *src_row, const int32_t *rec_list, int64_t n_records,
+                    const float *centroids, const float *centroids_rot, int32_t nlist,
+                    uint8_t *codes, uint32_t *scales, const float *sq8_lo,
+                    const float *sq8_hi, uint8_t *codes2, void *stream);
+
 /* Canonical <-> scan layout of packed codes (Section "Codecs Description":
  * codes are a packed bit stream, code j of a record at bits [w j, w j + w),
  * w = log2 K, little-endian).  canon: n x canon_bytes; tiles: ceil(n/16) *
@@ -232,7 +250,10 @@ int rslm_scan_topk(const rslm_plan *plan, const rslm_index *index,
  *   rslm_sq8_fit   : lo[d] / hi[d] = min / max over the n rows of v (n x dim);
  *                    accumulate != 0 folds into the existing lo / hi.
  *   rslm_sq8_encode: codes[dest_row[i] or i] = clamp(rne((v - lo) / step),
- *                    0, 255), step = (hi - lo) / 255 (a zero step gives 0).
+ *                    0, 255), step = (hi - lo) / 255 (a zero step gives 0),
+ *                    evaluated as (v - lo) * (255 / (hi - lo)) with a 1-ulp
+ *                    reciprocal (results differ from exact division only for
+ *                    values within ~1e-5 of a rounding midpoint).
  * ------------------------------------------------------------------------ */
 int rslm_sq8_fit(const float *v, int64_t n, int32_t dim, float *lo, float *hi,
                  int accumulate, void *stream);

@@ -21,7 +21,7 @@ RSLM_RESCORE_RSLM = 1
 EXPORTS = [
     "rslm_status_string", "rslm_last_hip_error", "rslm_version",
     "rslm_plan_create", "rslm_plan_destroy", "rslm_plan_get_info",
-    "rslm_fwht", "rslm_encode", "rslm_encode_two_stage", "rslm_pack_codes", "rslm_unpack_codes",
+    "rslm_fwht", "rslm_encode", "rslm_encode_two_stage", "rslm_encode_sq8", "rslm_pack_codes", "rslm_unpack_codes",
     "ivf_assign_probe_workspace", "ivf_assign_probe",
     "rslm_scan_topk_workspace", "rslm_scan_topk",
     "rslm_sq8_fit", "rslm_sq8_encode", "rslm_rescore", "rslm_set_timer", "rslm_calibrate_read",
@@ -74,6 +74,7 @@ def _declare(lib):
         "rslm_encode": (C.c_int, [P, P, I64, P, P, I64, P, P, I32, P, P, P, P]),
         "rslm_encode_two_stage": (C.c_int, [P, P, P, I64, P, P, I64, P, P, I32, P, P, P, P,
                                             P]),
+        "rslm_encode_sq8": (C.c_int, [P, P, I64, P, P, I64, P, P, I32, P, P, P, P, P, P]),
         "rslm_pack_codes": (C.c_int, [P, P, I64, P, P]),
         "rslm_unpack_codes": (C.c_int, [P, P, I64, P, P]),
         "ivf_assign_probe_workspace": (SZ, [I64, I32, I32, I32, C.c_int]),

@@ -165,6 +165,34 @@ def rslm_encode_two_stage(plan, plan2, x, codes, scales, codes2, scales2, n_reco
         _ptr(scales2), _stream(stream)))
 
 
+def rslm_encode_sq8(plan, x, codes, scales, lo, hi, codes2, n_records=None, src_row=None,
+                    rec_list=None, centroids=None, centroids_rot=None, stream=None):
+    """``rslm_encode`` with the second residual written as SQ8 codes (ranges
+    lo / hi); codes2 (n_rows x dim uint8) is indexed by row of x."""
+    _need(x, torch.float32, "x")
+    _need(codes, torch.uint8, "codes")
+    _need(scales, torch.int32, "scales")
+    _need(lo, torch.float32, "lo")
+    _need(hi, torch.float32, "hi")
+    _need(codes2, torch.uint8, "codes2")
+    _need(src_row, torch.int64, "src_row")
+    _need(rec_list, torch.int32, "rec_list")
+    _need(centroids, torch.float32, "centroids")
+    _need(centroids_rot, torch.float32, "centroids_rot")
+    n_rows = x.shape[0]
+    if n_records is None:
+        n_records = src_row.shape[0] if src_row is not None else n_rows
+    if codes.numel() < plan.code_bytes(n_records) or scales.numel() < n_records:
+        raise ValueError("codes / scales too small")
+    if codes2.numel() < n_rows * plan.dim or lo.numel() < plan.dim or hi.numel() < plan.dim:
+        raise ValueError("codes2 / lo / hi too small")
+    nlist = centroids.shape[0] if centroids is not None else 0
+    L.check("rslm_encode_sq8", L.lib().rslm_encode_sq8(
+        plan.handle, _ptr(x), n_rows, _ptr(src_row), _ptr(rec_list), n_records,
+        _ptr(centroids), _ptr(centroids_rot), nlist, _ptr(codes), _ptr(scales), _ptr(lo),
+        _ptr(hi), _ptr(codes2), _stream(stream)))
+
+
 def rslm_pack_codes(plan, canon, n, stream=None):
     _need(canon, torch.uint8, "canon")
     tiles = torch.empty(plan.code_bytes(n), dtype=torch.uint8, device=canon.device)

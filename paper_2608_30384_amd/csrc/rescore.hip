@@ -61,10 +61,7 @@ __global__ void k_sq8_encode(const float *__restrict__ v, int64_t n, int dim,
     const int d = int(t - r * dim);
     const int64_t o = dest ? int64_t(dest[r]) : r;
     if (o < 0 || o >= n_dest) continue;
-    const float step = (hi[d] - lo[d]) / 255.f;
-    float c = 0.f;
-    if (step > 0.f) c = fminf(fmaxf(rintf((v[t] - lo[d]) / step), 0.f), 255.f);
-    codes[o * dim + d] = uint8_t(c);
+    codes[o * dim + d] = uint8_t(sq8_code(v[t], lo[d], hi[d]));
   }
 }
 

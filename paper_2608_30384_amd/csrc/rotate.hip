@@ -206,7 +206,7 @@ __global__ void __launch_bounds__(256) k_encode(
     const float *__restrict__ cen_rot, int nlist, uint8_t *__restrict__ codes,
     uint32_t *__restrict__ scales, float *__restrict__ resid, RotParams rp, CodecParams cp,
     int dstride, uint8_t *__restrict__ codes2, uint32_t *__restrict__ scales2,
-    CodecParams cp2) {
+    CodecParams cp2, const float *__restrict__ sq8_lo, const float *__restrict__ sq8_hi) {
   extern __shared__ float lds[];
   __shared__ float cbs[64], cbs2[64];
   __shared__ int16_t pi[128];
@@ -325,7 +325,7 @@ __global__ void __launch_bounds__(256) k_encode(
   if (lane == 0) scales[rec] = su | (gu << 16);
   __builtin_amdgcn_wave_barrier();  // codes in cl are written by other lanes
 
-  if (codes2) {
+  if (codes2 && !sq8_lo) {
     // Second stage: r2 = R x - R a with R a = g^ (R c + s^ c^), quantised in
     // the rotated space with the second codebook (no further rotation).
     const float gh = dec_ue4m12(gu);
@@ -426,15 +426,18 @@ __global__ void __launch_bounds__(256) k_encode(
     }
     store_group(codes, rec, G, val, cp);
   }
-  if (resid) {
+  if (resid || sq8_lo) {
+    // the rotated second residual, as floats and / or as SQ8 codes (the
+    // rslm_sq8_encode arithmetic), both indexed by source row
     const float gh = dec_ue4m12(gu);
-    float *out = resid + row * D;   // indexed by source row
   #pragma unroll 4
     for (int i = lane; i < D; i += kWave) {
       const int code = cl[i / g];
       const float cv = (m > 0.f) ? cbs[code * g + (i % g)] : 0.f;
       const float rcv = rc[i] * rcw;
-      out[i] = z[px(i)] + rcv - gh * (rcv + sh * cv);
+      const float o = z[px(i)] + rcv - gh * (rcv + sh * cv);
+      if (resid) resid[row * D + i] = o;
+      if (sq8_lo) codes2[row * D + i] = uint8_t(sq8_code(o, sq8_lo[i], sq8_hi[i]));
     }
   }
 }
@@ -502,14 +505,16 @@ static int encode_impl(const rslm_plan *p, const rslm_plan *p2, const float *x, 
                        const int64_t *src_row, const int32_t *rec_list, int64_t n_records,
                        const float *centroids, const float *centroids_rot, int32_t nlist,
                        uint8_t *codes, uint32_t *scales, float *resid_rot, uint8_t *codes2,
-                       uint32_t *scales2, hipStream_t s) {
+                       uint32_t *scales2, const float *sq8_lo, const float *sq8_hi,
+                       hipStream_t s) {
   if (launch_encode_reg(p, p2, x, n_rows, src_row, rec_list, n_records, centroids,
-                        centroids_rot, nlist, codes, scales, resid_rot, codes2, scales2, s))
+                        centroids_rot, nlist, codes, scales, resid_rot, codes2, scales2, sq8_lo,
+                        sq8_hi, s))
     return check_launch();
   const int D = p->rot.D;
   const int dstride = lds_floats(D);
   // two float buffers plus one byte per sub-vector (<= dstride bytes) per
-  // wave, and another for the second stage
+  // wave, and another for an RSLM second stage
   const size_t per_wave = 2 * size_t(dstride) * 4 + size_t(dstride) * (p2 ? 2 : 1);
   int waves = 4;
   while (waves > 1 && size_t(waves) * per_wave > 65536) waves >>= 1;
@@ -519,7 +524,7 @@ static int encode_impl(const rslm_plan *p, const rslm_plan *p2, const float *x, 
   hipLaunchKernelGGL(k_encode, dim3(unsigned(grid)), dim3(64 * waves), shm, s, x, n_rows, src_row,
                      rec_list, n_records, centroids, centroids_rot, nlist, codes, scales,
                      resid_rot, p->rot, p->codec, dstride, codes2, scales2,
-                     p2 ? p2->codec : p->codec);
+                     p2 ? p2->codec : p->codec, sq8_lo, sq8_hi);
   return check_launch();
 }
 
@@ -544,8 +549,8 @@ int rslm_encode(const rslm_plan *p, const float *x, int64_t n_rows, const int64_
                                 centroids_rot, nlist, codes, scales);
   if (st || n_records == 0) return st;
   return encode_impl(p, nullptr, x, n_rows, src_row, rec_list, n_records, centroids,
-                     centroids_rot, nlist, codes, scales, resid_rot, nullptr, nullptr,
-                     as_stream(stream));
+                     centroids_rot, nlist, codes, scales, resid_rot, nullptr, nullptr, nullptr,
+                     nullptr, as_stream(stream));
 }
 
 int rslm_encode_two_stage(const rslm_plan *p, const rslm_plan *p2, const float *x,
@@ -560,7 +565,21 @@ int rslm_encode_two_stage(const rslm_plan *p, const rslm_plan *p2, const float *
   if (n_records == 0) return RSLM_OK;
   if (!codes2 || !scales2) return RSLM_ERR_INVALID_ARG;
   return encode_impl(p, p2, x, n_rows, src_row, rec_list, n_records, centroids, centroids_rot,
-                     nlist, codes, scales, nullptr, codes2, scales2, as_stream(stream));
+                     nlist, codes, scales, nullptr, codes2, scales2, nullptr, nullptr,
+                     as_stream(stream));
+}
+
+int rslm_encode_sq8(const rslm_plan *p, const float *x, int64_t n_rows, const int64_t *src_row,
+                    const int32_t *rec_list, int64_t n_records, const float *centroids,
+                    const float *centroids_rot, int32_t nlist, uint8_t *codes, uint32_t *scales,
+                    const float *sq8_lo, const float *sq8_hi, uint8_t *codes2, void *stream) {
+  const int st = encode_args_ok(p, x, n_rows, src_row, rec_list, n_records, centroids,
+                                centroids_rot, nlist, codes, scales);
+  if (st || n_records == 0) return st;
+  if (!sq8_lo || !sq8_hi || !codes2) return RSLM_ERR_INVALID_ARG;
+  return encode_impl(p, nullptr, x, n_rows, src_row, rec_list, n_records, centroids,
+                     centroids_rot, nlist, codes, scales, nullptr, codes2, nullptr, sq8_lo,
+                     sq8_hi, as_stream(stream));
 }
 
 static int64_t pack_grid(int64_t total) {

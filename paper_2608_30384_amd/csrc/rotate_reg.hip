@@ -221,17 +221,22 @@ __device__ __forceinline__ uint32_t sgnbit(uint32_t m, int b, int i) {
   return ((m >> (8 * (b & 1) + i)) & 1u) << 31;
 }
 
-// TWO = true adds the second (rescoring) stage with a 2-D K = 16 codebook
-// (the 2-bit codec): the pairs (8 r + 2 k, 8 r + 2 k + 1) of a block are
-// sub-vectors 64 b + 4 r + k, so a lane's four codes of a block are 16
-// consecutive bits of the canonical record at byte 32 b + 2 r.
-template <int NB, int BITS, bool TWO>
+// S2 selects the output of the second residual R x - g^ (R c + s^ c^):
+//   0: float32 rows (resid, when given);
+//   1: the second (rescoring) RSLM stage with a 2-D K = 16 codebook (the
+//      2-bit codec): the pairs (8 r + 2 k, 8 r + 2 k + 1) of a block are
+//      sub-vectors 64 b + 4 r + k, so a lane's four codes of a block are 16
+//      consecutive bits of the canonical record at byte 32 b + 2 r;
+//   2: SQ8 codes with the ranges sq8_lo / sq8_hi, 8 bytes per lane and block.
+template <int NB, int BITS, int S2>
 __global__ void __launch_bounds__(256) k_encode_rows(
     const float *__restrict__ x, int64_t n_rows, const int64_t *__restrict__ src_row,
     const int32_t *__restrict__ rec_list, int64_t n_records, const float *__restrict__ cen,
     const float *__restrict__ cen_rot, int nlist, uint8_t *__restrict__ codes,
     uint32_t *__restrict__ scales, float *__restrict__ resid, RotParams rp, CodecParams cp,
-    uint8_t *__restrict__ codes2, uint32_t *__restrict__ scales2, CodecParams cp2) {
+    uint8_t *__restrict__ codes2, uint32_t *__restrict__ scales2, CodecParams cp2,
+    const float *__restrict__ sq8_lo, const float *__restrict__ sq8_hi) {
+  constexpr bool TWO = S2 == 1;
   constexpr int D = 128 * NB;
   constexpr int E = 8 * NB;
   constexpr int K = 1 << BITS;
@@ -521,7 +526,34 @@ __global__ void __launch_bounds__(256) k_encode_rows(
 #pragma unroll
     for (int b = 0; b < NB; ++b) *reinterpret_cast<uint16_t *>(dst + 32 * b) = uint16_t(w2[b]);
   }
-  if (!TWO && resid) {   // (the two-stage launch passes no residual output)
+  if (S2 == 2) {
+    // SQ8 codes of the second residual (the rslm_sq8_encode arithmetic)
+    const float gh = dec_ue4m12(gu);
+    uint8_t *dst = codes2 + row * D + 8 * r;   // indexed by source row
+    const float *lo_r = sq8_lo + 8 * r, *hi_r = sq8_hi + 8 * r;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      uint32_t word2[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const float4 v = *reinterpret_cast<const float4 *>(rcr + 128 * b + 4 * h);
+        const float4 l4 = *reinterpret_cast<const float4 *>(lo_r + 128 * b + 4 * h);
+        const float4 h4 = *reinterpret_cast<const float4 *>(hi_r + 128 * b + 4 * h);
+        const float va[4] = {v.x * rcw, v.y * rcw, v.z * rcw, v.w * rcw};
+        const float la[4] = {l4.x, l4.y, l4.z, l4.w}, ha[4] = {h4.x, h4.y, h4.z, h4.w};
+        uint32_t wv = 0u;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const int e = 8 * b + 4 * h + t;
+          const float o = z[e] + va[t] - gh * (va[t] + sh * centroid(b, 4 * h + t));
+          wv |= sq8_code(o, la[t], ha[t]) << (8 * t);
+        }
+        word2[h] = wv;
+      }
+      *reinterpret_cast<uint2 *>(dst + 128 * b) = make_uint2(word2[0], word2[1]);
+    }
+  }
+  if (S2 == 0 && resid) {
     const float gh = dec_ue4m12(gu);
     float *out = resid + row * D + 8 * r;   // indexed by source row
 #pragma unroll
@@ -580,34 +612,38 @@ bool launch_encode_reg(const rslm_plan *p, const rslm_plan *p2, const float *x, 
                        const int64_t *src_row, const int32_t *rec_list, int64_t n_records,
                        const float *cen, const float *cen_rot, int nlist, uint8_t *codes,
                        uint32_t *scales, float *resid, uint8_t *codes2, uint32_t *scales2,
-                       hipStream_t s) {
+                       const float *sq8_lo, const float *sq8_hi, hipStream_t s) {
   if (!reg_path_ok(p->rot) || p->codec.g != 1 || p->codec.d_pad != p->rot.D) return false;
-  // the second stage here is the 2-D K = 16 codec only
-  const bool two = p2 != nullptr;
-  if (two && (p2->codec.g != 2 || p2->codec.K != 16 || p2->codec.n_sub * 2 != p->rot.D ||
-              p2->codec.canon_bytes * 4 != p->rot.D || resid))
+  const int s2 = p2 ? 1 : (sq8_lo ? 2 : 0);
+  // the RSLM second stage here is the 2-D K = 16 codec only
+  if (s2 == 1 && (p2->codec.g != 2 || p2->codec.K != 16 || p2->codec.n_sub * 2 != p->rot.D ||
+                  p2->codec.canon_bytes * 4 != p->rot.D || resid))
     return false;
+  if (s2 != 0 && p->codec.bits != 4) return false;
   // 16-byte vector loads and stores of every row
   if ((reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(cen) |
-       reinterpret_cast<uintptr_t>(cen_rot) | reinterpret_cast<uintptr_t>(resid)) % 16)
+       reinterpret_cast<uintptr_t>(cen_rot) | reinterpret_cast<uintptr_t>(resid) |
+       reinterpret_cast<uintptr_t>(sq8_lo) | reinterpret_cast<uintptr_t>(sq8_hi)) % 16)
     return false;
-  if (two && (reinterpret_cast<uintptr_t>(codes2) % 2)) return false;
+  if (s2 == 1 && (reinterpret_cast<uintptr_t>(codes2) % 2)) return false;
+  if (s2 == 2 && (reinterpret_cast<uintptr_t>(codes2) % 8 || resid)) return false;
   const int64_t groups = (n_records + 15) / 16;   // 16 vectors per 256-thread workgroup
   if (groups > 0x7fffffff) return false;
   const unsigned grid = unsigned(groups);
-  const CodecParams &cp2 = two ? p2->codec : p->codec;
+  const CodecParams &cp2 = p2 ? p2->codec : p->codec;
 #define CALL_B(NB, B, T)                                                                        \
   hipLaunchKernelGGL((k_encode_rows<NB, B, T>), dim3(grid), dim3(256), 0, s, x, n_rows, src_row, \
                      rec_list, n_records, cen, cen_rot, nlist, codes, scales, resid, p->rot,      \
-                     p->codec, codes2, scales2, cp2)
+                     p->codec, codes2, scales2, cp2, sq8_lo, sq8_hi)
 #define CALL(J)                  \
-  if (two)                       \
-    CALL_B((J) / 2, 4, true);    \
+  if (s2 == 1)                   \
+    CALL_B((J) / 2, 4, 1);       \
+  else if (s2 == 2)              \
+    CALL_B((J) / 2, 4, 2);       \
   else if (p->codec.bits == 4)   \
-    CALL_B((J) / 2, 4, false);   \
+    CALL_B((J) / 2, 4, 0);       \
   else                           \
-    CALL_B((J) / 2, 3, false)
-  if (two && p->codec.bits != 4) return false;
+    CALL_B((J) / 2, 3, 0)
   RSLM_REG_SWITCH(p->rot.D / 128, CALL)
 #undef CALL
 #undef CALL_B

@@ -103,13 +103,14 @@ inline hipStream_t as_stream(void *s) { return reinterpret_cast<hipStream_t>(s);
 // false when the plan is not handled there.
 bool launch_rotate_reg(const rslm_plan *p, const float *x, float *y, int64_t n, int inverse,
                        hipStream_t s);
-// p2 / codes2 / scales2: the optional second (rescoring) stage of
-// rslm_encode_two_stage (p2 == nullptr: none).
+// Optional second output: the RSLM rescoring stage of rslm_encode_two_stage
+// (p2, codes2, scales2), or the SQ8 codes of rslm_encode_sq8 (sq8_lo,
+// sq8_hi, codes2); neither: p2 == nullptr and sq8_lo == nullptr.
 bool launch_encode_reg(const rslm_plan *p, const rslm_plan *p2, const float *x, int64_t n_rows,
                        const int64_t *src_row, const int32_t *rec_list, int64_t n_records,
                        const float *cen, const float *cen_rot, int nlist, uint8_t *codes,
                        uint32_t *scales, float *resid, uint8_t *codes2, uint32_t *scales2,
-                       hipStream_t s);
+                       const float *sq8_lo, const float *sq8_hi, hipStream_t s);
 
 // ---- device helpers ------------------------------------------------------
 
@@ -159,6 +160,16 @@ __device__ __forceinline__ uint32_t enc_ue4m12(float s) {
 
 __device__ __forceinline__ float dec_ue4m12(uint32_t u) {
   return u ? __uint_as_float((u << 11) + (120u << 23)) : 0.0f;
+}
+
+// SQ8 code of v for the range [lo, hi]: clamp(rne((v - lo) / step), 0, 255)
+// with step = (hi - lo) / 255, evaluated as (v - lo) * (255 / (hi - lo)) with
+// the hardware reciprocal (1 ulp); an empty range gives 0.
+__device__ __forceinline__ uint32_t sq8_code(float v, float lo, float hi) {
+  const float w = hi - lo;
+  if (!(w > 0.0f)) return 0u;
+  const float inv = __builtin_amdgcn_rcpf(w) * 255.0f;
+  return uint32_t(fminf(fmaxf(rintf((v - lo) * inv), 0.0f), 255.0f));
 }
 
 // Float -> uint32 whose unsigned order equals the float order.

@@ -174,3 +174,49 @@ def test_rescore_rslm_parity(R, D, bits2, k_in, k_out):
     for i in range(Q):
         tol = H.score_tol(ref_s[i], np.linalg.norm(qr[i]), xn)
         H.check_topk(gs[i], gi[i], ref_s[i], ref_i[i], np.where(np.isfinite(tol), tol, 0))
+
+
+@pytest.mark.parametrize("D,passes,n", [(768, 2, 500), (256, 1, 300), (96, 2, 333)])
+def test_encode_sq8_parity(R, D, passes, n):
+    """rslm_encode_sq8: SQ8 codes of the rotated second residual written in the
+    encoding pass, against the oracle's residual R x - R a quantised with the
+    same float32 ranges; rows whose first stage agrees must match except at
+    rounding midpoints (+-1 there)."""
+    nlist = 5
+    x = synth.aniso(n, D, seed=D + 7)
+    cen = x[np.random.default_rng(D + 1).choice(n, nlist, replace=False)] * 0.9
+    assign, _ = oracle.assign_l2(x, cen)
+    Rm = H.rot(D, passes)
+    C = synth.codebook(4)
+    ref = oracle.encode(x, Rm, C, 4, centroids=cen[assign], scale_mode="global")
+    ra = oracle.first_stage_rotated(ref["codes"], ref["s_code"], ref["g_code"], C, Rm, cen[assign])
+    r2 = x.astype(np.float64) @ Rm.T - ra
+    lo, hi = oracle.sq8_fit(r2)
+    lo32, hi32 = lo.astype(np.float32), hi.astype(np.float32)
+    ref2 = oracle.sq8_encode(r2, lo32.astype(np.float64), hi32.astype(np.float64))
+    plan = R.Plan(D, 4, passes=passes, scale_mode="global")
+    xt, ct = _t(x), _t(cen.astype(np.float32))
+    crot = R.rslm_fwht(plan, ct)
+    codes = torch.zeros(plan.code_bytes(n), dtype=torch.uint8, device=DEV)
+    scales = torch.zeros(n, dtype=torch.int32, device=DEV)
+    codes2 = torch.full((n, D), 0xEE, dtype=torch.uint8, device=DEV)
+    R.rslm_encode_sq8(plan, xt, codes, scales, _t(lo32), _t(hi32), codes2,
+                      rec_list=_t(assign, torch.int32), centroids=ct, centroids_rot=crot)
+    g1 = oracle.unpack_canonical(R.rslm_unpack_codes(plan, codes, n).cpu().numpy(), 4, D)
+    sc = scales.cpu().numpy().astype(np.uint32)
+    same = ((g1 == ref["codes"]).all(1) & ((sc & 0xFFFF) == ref["s_code"]) &
+            ((sc >> 16) == ref["g_code"]))
+    assert same.mean() > 0.98
+    got = codes2.cpu().numpy()
+    step = (hi32.astype(np.float64) - lo32) / 255.0
+    frac = (r2 - lo32) / np.where(step > 0, step, 1.0)
+    near = np.abs(frac - np.floor(frac) - 0.5) < 1e-3
+    d = np.abs(got.astype(int) - ref2.astype(int))[same]
+    assert np.all(d <= 1)
+    assert np.all((d == 0) | near[same])
+    # the same codes as the two-call route (float residual, then SQ8)
+    resid = torch.zeros((n, D), dtype=torch.float32, device=DEV)
+    R.rslm_encode(plan, xt, codes, scales, rec_list=_t(assign, torch.int32), centroids=ct,
+                  centroids_rot=crot, resid_rot=resid)
+    two_call = R.rslm_sq8_encode(resid, _t(lo32), _t(hi32)).cpu().numpy()
+    assert np.array_equal(got, two_call)
