@@ -59,6 +59,8 @@ def parse():
                     help="text768 (default): the metric's configuration; capacity: 100M x 768 "
                          "at nlist 16,384 with 2-bit RSLM rescoring records; sweep: 10M x 1,024 "
                          "unit-norm at 1, 2, 3 and 4 bits with recall@10")
+    ap.add_argument("--counter-summary", nargs=2, metavar=("SQ_A_CSV", "SQ_B_CSV"),
+                    help="print a markdown summary of the two SQ counter runs and exit")
     ap.add_argument("--copy-calib", action="store_true",
                     help="only run a 1 GiB device copy (counter calibration) and exit")
     ap.add_argument("--stats-summary", nargs=2, metavar=("KERNEL_STATS_CSV", "BENCH_JSON"),
@@ -84,6 +86,14 @@ PROFILE_CMDS = {
                     "-- python3 $REPO/bench.py --copy-calib"),
     "calib_write": ("cd /tmp && rocprofv3 --pmc WRITE_SIZE --output-format csv -d /tmp/p_cw -o run "
                     "-- python3 $REPO/bench.py --copy-calib"),
+    "sq_a": ("cd /tmp && rocprofv3 --pmc SQ_WAVES SQ_WAVE_CYCLES SQ_BUSY_CYCLES SQ_WAIT_INST_ANY "
+             "SQ_ACTIVE_INST_VALU SQ_INSTS_VALU SQ_INSTS_LDS SQ_LDS_BANK_CONFLICT GRBM_GUI_ACTIVE "
+             "--output-format csv -d /tmp/p_a -o run -- python3 $REPO/bench.py --steps 5 "
+             "--warmup 1 --no-cpu-baseline"),
+    "sq_b": ("cd /tmp && rocprofv3 --pmc SQ_INSTS_MFMA SQ_VALU_MFMA_BUSY_CYCLES SQ_ACTIVE_INST_LDS "
+             "SQ_WAIT_INST_LDS SQ_INSTS_VMEM_RD SQ_THREAD_CYCLES_VALU SQ_ACTIVE_INST_ANY "
+             "SQ_LDS_ADDR_CONFLICT GRBM_GUI_ACTIVE --output-format csv -d /tmp/p_b -o run -- "
+             "python3 $REPO/bench.py --steps 5 --warmup 1 --no-cpu-baseline"),
 }
 
 STEP_KERNELS = ("k_scan<", "k_topk_stream", "k_dots", "k_probe_select", "k_rescore_sq8",
@@ -117,6 +127,63 @@ def stats_summary(stats_csv, bench_json):
         out.append(f"| `{name}` | {x['Calls']} | {float(x['AverageNs']) / 1e3:.1f} | "
                    f"{float(x['MinNs']) / 1e3:.1f} | {float(x['TotalDurationNs']) / 1e6:.2f} | "
                    f"{float(x['Percentage']):.2f} |")
+    return "\n".join(out) + "\n"
+
+
+def counter_summary(a_csv, b_csv, n_steps=5):
+    """Per-kernel SQ counters of the timed steps (the last n_steps dispatches
+    of each kernel), with derived utilisations.  Chip-wide cycles of a
+    dispatch = GRBM_GUI_ACTIVE / 8 (the counter sums the 8 XCDs); the SQ_*
+    cycle counters sum over the 1,024 SIMDs; a wave64 VALU instruction
+    occupies its SIMD for 4 cycles."""
+    import collections
+    import csv
+
+    def load(path):
+        d = collections.OrderedDict()
+        for r in csv.DictReader(open(path)):
+            key = (r["Dispatch_Id"], r["Kernel_Name"])
+            d.setdefault(key, collections.Counter())[r["Counter_Name"]] += float(r["Counter_Value"])
+        return d
+    da, db = load(a_csv), load(b_csv)
+    kern = [("k_scan<", "scan (a3+a4)"), ("k_topk_stream", "top-k (a5)"),
+            ("k_dots_direct", "probe dots (a2)"), ("k_probe_select_reg", "probe selection (a2)"),
+            ("k_rotate_reg", "query rotation (a1)"), ("k_rescore_sq8", "rescore (a6)"),
+            ("k_encode_rows", "encode (a7)")]
+
+    def avg(d, part):
+        ds = [v for (i, n), v in d.items() if part in n][-n_steps:]
+        if not ds:
+            return None
+        return {c: sum(x[c] for x in ds) / len(ds) for c in ds[0]}
+    out = ["# rocprofv3 SQ counters of the step's kernels: RSLM IVF scan, text-embedding workload "
+           "(10M x 768, 4-bit)", "",
+           "Commands (run from /tmp on one MI355X; `$REPO` is the repository root):", "",
+           "```", PROFILE_CMDS["sq_a"], PROFILE_CMDS["sq_b"], "```", "",
+           f"Kernel sources hash: `{csrc_hash()}`.  Averages over the 5 timed steps.  Chip cycles "
+           "= GRBM_GUI_ACTIVE / 8; VALU busy = 4 x SQ_ACTIVE_INST_VALU / 1,024 SIMDs / chip "
+           "cycles; VALU lane use = SQ_THREAD_CYCLES_VALU / (64 x SQ_ACTIVE_INST_VALU); MFMA busy = "
+           "SQ_VALU_MFMA_BUSY_CYCLES / 1,024 / chip cycles; LDS bank-conflict share = "
+           "SQ_LDS_BANK_CONFLICT / SQ_ACTIVE_INST_LDS; wait share = SQ_WAIT_INST_ANY / "
+           "SQ_WAVE_CYCLES.", "",
+           "| Kernel | chip cycles | waves | VALU instr / wave | VALU busy | VALU lane use | MFMA "
+           "busy | LDS instr / wave | LDS bank-conflict share | wait share |",
+           "|---|---|---|---|---|---|---|---|---|---|"]
+    for part, label in kern:
+        a, b = avg(da, part), avg(db, part)
+        if a is None or b is None:
+            continue
+        cyc = a["GRBM_GUI_ACTIVE"] / 8
+        waves = max(a["SQ_WAVES"], 1)
+        valu_busy = 4 * a["SQ_ACTIVE_INST_VALU"] / 1024 / cyc
+        lane_use = b["SQ_THREAD_CYCLES_VALU"] / max(64 * a["SQ_ACTIVE_INST_VALU"], 1)
+        mfma = b["SQ_VALU_MFMA_BUSY_CYCLES"] / 1024 / cyc
+        lds_conf = a["SQ_LDS_BANK_CONFLICT"] / max(b["SQ_ACTIVE_INST_LDS"], 1)
+        wait = a["SQ_WAIT_INST_ANY"] / max(a["SQ_WAVE_CYCLES"], 1)
+        out.append(f"| {label} `{part.rstrip('<')}` | {cyc:,.0f} | {waves:,.0f} | "
+                   f"{a['SQ_INSTS_VALU'] / waves:,.0f} | {100 * valu_busy:.0f}% | "
+                   f"{100 * lane_use:.0f}% | {100 * mfma:.0f}% | "
+                   f"{a['SQ_INSTS_LDS'] / waves:,.0f} | {100 * lds_conf:.1f}% | {100 * wait:.0f}% |")
     return "\n".join(out) + "\n"
 
 
@@ -300,6 +367,9 @@ def main():
     args = parse()
     if args.stats_summary:
         sys.stdout.write(stats_summary(*args.stats_summary))
+        return
+    if args.counter_summary:
+        sys.stdout.write(counter_summary(*args.counter_summary))
         return
     if args.traffic_summary:
         print(json.dumps(traffic_summary(*args.traffic_summary), indent=1))
