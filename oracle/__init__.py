@@ -25,6 +25,7 @@ from .codec import (
     codec_shape, e_max, enc_ue7m9, dec_ue7m9, enc_ue4m12, dec_ue4m12,
     encode, pack_canonical, unpack_canonical, canonical_code_bytes,
     decode_rotated, reconstruct, first_stage_rotated, encode_rescore, reconstruct_rescore,
+    lite_lead, record_bytes, pack_records, unpack_records,
 )
 from .search import (
     assign_l2, assign_l2_expanded, probe_ip, kmeans, scan_scores_lut, scan_scores_dense, topk,

@@ -103,8 +103,19 @@ def dec_ue4m12(u):
 UE4M12_ONE = 0x7000
 
 
-def encode(x, R, C, bits, centroids=None, scale_mode="global", chunk=512):
+def lite_lead(scale_mode):
+    """Rslm4Lite: number of leading coordinates coded with the K = 8 codebook,
+    whose freed top code bits carry the scales -- 16 for one UE7M9 scale,
+    32 when the global UE4M12 scale is embedded as well (Sections "Codecs
+    Description" and "Relative Quantization")."""
+    return 32 if scale_mode == "global" else 16
+
+
+def encode(x, R, C, bits, centroids=None, scale_mode="global", chunk=512, C_lead=None):
     """Encode rows of x relative to ``centroids`` (or 0) with rotation R.
+
+    ``C_lead`` (Rslm4Lite, 4 bits only): the K = 8 1-D codebook used for the
+    first ``lite_lead(scale_mode)`` coordinates instead of C.
 
     Returns a dict with ``codes`` (n, n_sub) int64, ``s_code`` / ``g_code``
     (n,) uint16 scale codes and the diagnostic values ``u`` (normalised
@@ -118,6 +129,11 @@ def encode(x, R, C, bits, centroids=None, scale_mode="global", chunk=512):
     n_sub = -(-D // g)
     D_pad = n_sub * g
     emax = e_max(D)
+    lead = 0
+    if C_lead is not None:
+        C_lead = np.asarray(C_lead, dtype=np.float64)
+        assert bits == 4 and C_lead.shape == (8, 1) and D >= 64
+        lead = lite_lead(scale_mode)
     cen = np.zeros_like(x) if centroids is None else np.asarray(centroids, dtype=np.float64)
     codes = np.zeros((n, n_sub), dtype=np.int64)
     u_all = np.zeros((n, D_pad))
@@ -136,8 +152,13 @@ def encode(x, R, C, bits, centroids=None, scale_mode="global", chunk=512):
         sub = u.reshape(hi - lo, n_sub, g)
         dist = ((sub[:, :, None, :] - C[None, None, :, :]) ** 2).sum(-1)
         cd = np.argmin(dist, axis=-1)                 # first minimum: lower k on ties
+        chat = C[cd].reshape(hi - lo, D_pad)
+        if lead:
+            dl = ((sub[:, :lead, None, :] - C_lead[None, None, :, :]) ** 2).sum(-1)
+            cd[:, :lead] = np.argmin(dl, axis=-1)
+            chat[:, :lead] = C_lead[cd[:, :lead], 0]
         cd[~nz] = 0
-        chat = C[cd].reshape(hi - lo, D_pad)[:, :D]
+        chat = chat[:, :D]
         rn = np.linalg.norm(r, axis=1)
         cn = np.linalg.norm(chat, axis=1)
         for i in range(hi - lo):
@@ -183,18 +204,82 @@ def unpack_canonical(packed, bits, n_sub):
     return (bitarr << np.arange(w)[None, None, :]).sum(-1)
 
 
-def decode_rotated(codes, s_code, C, D):
-    """s^ * C[codes] over the D valid coordinates (rotated space)."""
+def record_bytes(D, bits, scale_mode, lite=False):
+    """Bytes of one packed record (table tab:rslm_codecs): the codes followed
+    by a 2-byte scale suffix (two with the global scale); Rslm4Lite embeds
+    its scales, ceil(D / 2) bytes."""
+    if lite:
+        return -(-D // 2)
+    return canonical_code_bytes(D, bits) + (4 if scale_mode == "global" else 2)
+
+
+def pack_records(codes, s_code, g_code, bits, scale_mode, lite=False):
+    """Packed records (Section "Codecs Description": pack the codes and the
+    scale factor).  Reading: scales are little-endian uint16 suffixes, the
+    UE7M9 scale first, then the UE4M12 global scale.  Rslm4Lite: the leading
+    lite_lead coordinates hold 3-bit codes and bit 3 of coordinate j's nibble
+    holds bit j of the UE7M9 scale (j < 16) or bit j - 16 of the UE4M12 scale
+    (16 <= j < 32), least significant bit first."""
+    codes = np.asarray(codes, dtype=np.int64).copy()
+    n = codes.shape[0]
+    s_code = np.asarray(s_code, dtype=np.int64)
+    g_code = np.asarray(g_code, dtype=np.int64)
+    if lite:
+        assert bits == 4
+        lead = lite_lead(scale_mode)
+        assert codes[:, :lead].max(initial=0) < 8
+        for j in range(lead):
+            word = s_code if j < 16 else g_code
+            codes[:, j] |= ((word >> (j % 16)) & 1) << 3
+        return pack_canonical(codes, bits)
+    body = pack_canonical(codes, bits)
+    suf = [s_code] + ([g_code] if scale_mode == "global" else [])
+    tail = np.concatenate([np.stack([v & 0xFF, v >> 8], 1) for v in suf], 1).astype(np.uint8)
+    return np.concatenate([body, tail.reshape(n, -1)], 1)
+
+
+def unpack_records(rec, bits, D, scale_mode, lite=False):
+    """Inverse of pack_records: (codes, s_code, g_code); g_code is the code of
+    1.0 (0x7000) for local records."""
+    K, g = codec_shape(bits)
+    n_sub = -(-D // g)
+    rec = np.asarray(rec, dtype=np.uint8)
+    nb = canonical_code_bytes(D, bits)
+    codes = unpack_canonical(rec[:, :nb], bits, n_sub)
+    n = rec.shape[0]
+    g_code = np.full(n, UE4M12_ONE, dtype=np.uint16)
+    if lite:
+        lead = lite_lead(scale_mode)
+        top = (codes[:, :lead] >> 3) & 1
+        codes[:, :lead] &= 7
+        w = (top << np.arange(lead) % 16).astype(np.int64)
+        s_code = w[:, :16].sum(1).astype(np.uint16)
+        if lead == 32:
+            g_code = w[:, 16:32].sum(1).astype(np.uint16)
+        return codes, s_code, g_code
+    tail = rec[:, nb:].astype(np.int64)
+    s_code = (tail[:, 0] | (tail[:, 1] << 8)).astype(np.uint16)
+    if scale_mode == "global":
+        g_code = (tail[:, 2] | (tail[:, 3] << 8)).astype(np.uint16)
+    return codes, s_code, g_code
+
+
+def decode_rotated(codes, s_code, C, D, C_lead=None, lead=0):
+    """s^ * C[codes] over the D valid coordinates (rotated space); the first
+    ``lead`` coordinates decode through C_lead (Rslm4Lite)."""
     C = np.asarray(C, dtype=np.float64)
     n = codes.shape[0]
-    chat = C[codes].reshape(n, -1)[:, :D]
+    chat = C[codes].reshape(n, -1)
+    if lead:
+        chat[:, :lead] = np.asarray(C_lead, dtype=np.float64)[codes[:, :lead], 0]
+    chat = chat[:, :D]
     sh = np.array([dec_ue7m9(u) for u in s_code])
     return sh[:, None] * chat
 
 
-def reconstruct(codes, s_code, g_code, C, R, centroids=None):
+def reconstruct(codes, s_code, g_code, C, R, centroids=None, C_lead=None, lead=0):
     """x~ = g^ (c + R^T s^ c^) in the original space."""
-    rr = decode_rotated(codes, s_code, C, R.shape[0])
+    rr = decode_rotated(codes, s_code, C, R.shape[0], C_lead, lead)
     base = 0.0 if centroids is None else np.asarray(centroids, dtype=np.float64)
     gh = np.array([dec_ue4m12(u) for u in g_code])
     return gh[:, None] * (base + rr @ R)

@@ -96,11 +96,12 @@ def kmeans(x, nlist, iters=10, seed=0):
     return c
 
 
-def scan_scores_lut(q_rot, qc_dot, codes, s_hat, g_hat, C):
+def scan_scores_lut(q_rot, qc_dot, codes, s_hat, g_hat, C, C_lead=None, lead=0):
     """LUT route: g^ (<q, c> + s^ sum_j LUT[j, code_j]) for one query.
 
     q_rot: rotated query (length D, zero-padded here to n_sub * g);
     codes: (n, n_sub); s_hat / g_hat: decoded scales (n,); qc_dot: <q, c_p>.
+    The first ``lead`` sub-vectors look up C_lead (Rslm4Lite).
     """
     C = np.asarray(C, dtype=np.float64)
     K, g = C.shape
@@ -108,6 +109,10 @@ def scan_scores_lut(q_rot, qc_dot, codes, s_hat, g_hat, C):
     qp = np.zeros(n_sub * g)
     qp[:len(q_rot)] = q_rot
     lut = qp.reshape(n_sub, g) @ C.T                  # LUT[j, k]
+    if lead:
+        Cl = np.asarray(C_lead, dtype=np.float64)
+        lut[:lead] = 0.0
+        lut[:lead, :Cl.shape[0]] = qp[:lead, None] * Cl[None, :, 0]
     resid = lut[np.arange(n_sub)[None, :], codes].sum(1)
     return g_hat * (qc_dot + s_hat * resid)
 
