@@ -72,6 +72,15 @@ typedef struct rslm_plan_desc {
   const float *codebook;  /* host, K*g floats, centroid k at [k*g, k*g+g);
                              every value exactly representable in float16;
                              for g == 1 strictly ascending */
+  int32_t lite;           /* 1: Rslm4Lite (bits == 4, dim >= 64; Section
+                             "Codecs Description"): the first 16 coordinates
+                             (32 with the global scale) use the K = 8
+                             codebook_lead and bit 3 of their codes holds
+                             the scales, bit j of UE7M9 s^ in coordinate j
+                             (j < 16), bit j - 16 of UE4M12 g^ in coordinate
+                             j (16 <= j < 32); 0: standard codec */
+  const float *codebook_lead;  /* host, 8 ascending float16-exact floats
+                                  (lite only, else ignored) */
 } rslm_plan_desc;
 
 typedef struct rslm_plan_info {
@@ -84,6 +93,9 @@ typedef struct rslm_plan_info {
   int32_t tile_records;    /* records per scan tile (16) */
   int32_t tile_bytes;      /* bytes of one tile of packed codes */
   double emax;             /* E_max(D) = E[max_i |Z_i|], Z_i ~ N(0,1) i.i.d. */
+  int32_t lite;            /* 1 for Rslm4Lite */
+  int32_t record_bytes;    /* packed record (rslm_pack_records): canon_bytes
+                              + 2 (local) or + 4 (global); Lite: canon_bytes */
 } rslm_plan_info;
 
 /* Creates a plan on the current HIP device; copies the host tables.
@@ -189,6 +201,32 @@ int rslm_unpack_codes(const rslm_plan *plan, const uint8_t *tiles, int64_t n,
                       uint8_t *canon, void *stream);
 
 /* ------------------------------------------------------------------------
+ * Packed records (Section "Codecs Description", table tab:rslm_codecs: the
+ * codes followed by the scale factor): record r = canonical codes
+ * (canon_bytes) then UE7M9 s^ as a little-endian uint16, then for a global
+ * plan UE4M12 g^ likewise; a Lite plan's record is its canonical codes alone
+ * (scales embedded), ceil(D / 2) bytes.  record_bytes in rslm_plan_info.
+ *   rslm_pack_records: tiles (rslm_encode's layout) + scales (n uint32; may
+ *   be NULL for Lite) -> records, n x record_bytes.
+ * ------------------------------------------------------------------------ */
+int rslm_pack_records(const rslm_plan *plan, const uint8_t *tiles, const uint32_t *scales,
+                      int64_t n, uint8_t *records, void *stream);
+
+/* ------------------------------------------------------------------------
+ * rslm_score -- OneToMany scoring (Section "Performance Impact and Memory
+ * Savings": a rotated query against many encoded vectors, contiguous or
+ * gathered from a large pool): for query q < Q and entry j < n,
+ *   r = ids ? ids[j] : j
+ *   out[q * n + j] = g^_r s^_r sum_i <q_rot[q][i g:(i+1) g], C[code_{r,i}]>
+ * (g^ = 1 for a local plan), records as above, n_pool records in `records`;
+ * an id outside [0, n_pool) gives -inf.  q_rot: Q x D (rslm_fwht);
+ * ids: n int64 or NULL (then n <= n_pool); Q <= 65535.
+ * ------------------------------------------------------------------------ */
+int rslm_score(const rslm_plan *plan, const uint8_t *records, int64_t n_pool,
+               const int64_t *ids, int64_t n, const float *q_rot, int32_t Q, float *out,
+               void *stream);
+
+/* ------------------------------------------------------------------------
  * ivf_assign_probe -- IVF routing (Section "End-to-End Comparison", Setup):
  *   IVF_ASSIGN_L2: out_ids[i] = argmin_p ||x_i - c_p||^2 (lowest p on ties),
  *                  out_scores[i] = that squared distance (may be NULL);
@@ -233,6 +271,8 @@ typedef struct rslm_index {
  * padded with (-inf, -1).
  *   q_rot: Q x D rotated queries (rslm_fwht); probe_ids / probe_dots:
  *   Q x nprobe; out_scores / out_ids: Q x k.  1 <= k <= 1024, Q <= 65535.
+ *   D <= 1024; a Lite plan gives RSLM_ERR_UNSUPPORTED (score Lite records
+ *   with rslm_score).
  * ------------------------------------------------------------------------ */
 size_t rslm_scan_topk_workspace(const rslm_plan *plan, const rslm_index *index,
                                 int32_t Q, int32_t nprobe, int32_t k);

@@ -21,7 +21,8 @@ RSLM_RESCORE_RSLM = 1
 EXPORTS = [
     "rslm_status_string", "rslm_last_hip_error", "rslm_version",
     "rslm_plan_create", "rslm_plan_destroy", "rslm_plan_get_info",
-    "rslm_fwht", "rslm_encode", "rslm_encode_two_stage", "rslm_encode_sq8", "rslm_pack_codes", "rslm_unpack_codes",
+    "rslm_fwht", "rslm_encode", "rslm_encode_two_stage", "rslm_encode_sq8", "rslm_pack_codes",
+    "rslm_pack_records", "rslm_score", "rslm_unpack_codes",
     "ivf_assign_probe_workspace", "ivf_assign_probe",
     "rslm_scan_topk_workspace", "rslm_scan_topk",
     "rslm_sq8_fit", "rslm_sq8_encode", "rslm_rescore", "rslm_set_timer", "rslm_calibrate_read",
@@ -31,7 +32,8 @@ EXPORTS = [
 class PlanDesc(C.Structure):
     _fields_ = [("dim", C.c_int32), ("bits", C.c_int32), ("passes", C.c_int32),
                 ("scale_mode", C.c_int32), ("signs", C.POINTER(C.c_int8)),
-                ("perm", C.POINTER(C.c_int32)), ("codebook", C.POINTER(C.c_float))]
+                ("perm", C.POINTER(C.c_int32)), ("codebook", C.POINTER(C.c_float)),
+                ("lite", C.c_int32), ("codebook_lead", C.POINTER(C.c_float))]
 
 
 class PlanInfo(C.Structure):
@@ -39,7 +41,8 @@ class PlanInfo(C.Structure):
                 ("scale_mode", C.c_int32), ("K", C.c_int32), ("g", C.c_int32),
                 ("block", C.c_int32), ("n_full_blocks", C.c_int32), ("d_pad", C.c_int32),
                 ("canon_bytes", C.c_int32), ("tile_records", C.c_int32),
-                ("tile_bytes", C.c_int32), ("emax", C.c_double)]
+                ("tile_bytes", C.c_int32), ("emax", C.c_double), ("lite", C.c_int32),
+                ("record_bytes", C.c_int32)]
 
 
 class Index(C.Structure):
@@ -76,6 +79,8 @@ def _declare(lib):
                                             P]),
         "rslm_encode_sq8": (C.c_int, [P, P, I64, P, P, I64, P, P, I32, P, P, P, P, P, P]),
         "rslm_pack_codes": (C.c_int, [P, P, I64, P, P]),
+        "rslm_pack_records": (C.c_int, [P, P, P, I64, P, P]),
+        "rslm_score": (C.c_int, [P, P, I64, P, I64, P, I32, P, P]),
         "rslm_unpack_codes": (C.c_int, [P, P, I64, P, P]),
         "ivf_assign_probe_workspace": (SZ, [I64, I32, I32, I32, C.c_int]),
         "ivf_assign_probe": (C.c_int, [P, I64, I32, P, I32, I32, C.c_int, P, P, P, SZ, P]),

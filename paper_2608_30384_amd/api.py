@@ -56,7 +56,7 @@ class Plan:
     """An RSLM codec plan (``rslm_plan_create``) on the current device."""
 
     def __init__(self, dim, bits, passes=-1, scale_mode="global", signs=None, perm=None,
-                 codebook=None):
+                 codebook=None, lite=False):
         import synth  # the fixed tables are inputs shared as data
 
         signs = synth.sign_table() if signs is None else np.asarray(signs, dtype=np.int8)
@@ -65,11 +65,14 @@ class Plan:
         self._signs = np.ascontiguousarray(signs, dtype=np.int8)
         self._perm = np.ascontiguousarray(perm, dtype=np.int32)
         self._cb = np.ascontiguousarray(cb, dtype=np.float32).reshape(-1)
+        # Rslm4Lite: the K = 8 (3-bit) codebook for the leading coordinates
+        self._cbl = np.ascontiguousarray(synth.codebook(3), dtype=np.float32).reshape(-1)
         mode = {"local": 0, "global": 1}.get(scale_mode, scale_mode)
         desc = L.PlanDesc(dim, bits, passes, int(mode),
                           self._signs.ctypes.data_as(C.POINTER(C.c_int8)),
                           self._perm.ctypes.data_as(C.POINTER(C.c_int32)),
-                          self._cb.ctypes.data_as(C.POINTER(C.c_float)))
+                          self._cb.ctypes.data_as(C.POINTER(C.c_float)), int(bool(lite)),
+                          self._cbl.ctypes.data_as(C.POINTER(C.c_float)))
         h = C.c_void_p()
         L.check("rslm_plan_create", L.lib().rslm_plan_create(C.byref(desc), C.byref(h)))
         self.handle = h
@@ -81,6 +84,8 @@ class Plan:
         self.d_pad = info.d_pad
         self.tile_bytes = info.tile_bytes
         self.canon_bytes = info.canon_bytes
+        self.record_bytes = info.record_bytes
+        self.lite = bool(info.lite)
         self.emax = info.emax
         self.device = torch.device("cuda", torch.cuda.current_device())
 
@@ -199,6 +204,34 @@ def rslm_pack_codes(plan, canon, n, stream=None):
     L.check("rslm_pack_codes", L.lib().rslm_pack_codes(plan.handle, _ptr(canon), n,
                                                        _ptr(tiles), _stream(stream)))
     return tiles
+
+
+def rslm_pack_records(plan, tiles, scales, n, stream=None):
+    """Packed records (codes + scale suffix; Lite: codes alone), n x record_bytes."""
+    _need(tiles, torch.uint8, "tiles")
+    _need(scales, torch.int32, "scales")
+    records = torch.empty((n, plan.record_bytes), dtype=torch.uint8, device=tiles.device)
+    L.check("rslm_pack_records", L.lib().rslm_pack_records(plan.handle, _ptr(tiles), _ptr(scales),
+                                                           n, _ptr(records), _stream(stream)))
+    return records
+
+
+def rslm_score(plan, records, q_rot, ids=None, n=None, out=None, stream=None):
+    """OneToMany scores (Q x n) of packed records, contiguous (ids None) or
+    gathered by int64 ids."""
+    _need(records, torch.uint8, "records")
+    _need(q_rot, torch.float32, "q_rot")
+    _need(ids, torch.int64, "ids")
+    n_pool = records.numel() // plan.record_bytes
+    if n is None:
+        n = ids.numel() if ids is not None else n_pool
+    Q = q_rot.shape[0]
+    if out is None:
+        out = torch.empty((Q, n), dtype=torch.float32, device=q_rot.device)
+    _need(out, torch.float32, "out")
+    L.check("rslm_score", L.lib().rslm_score(plan.handle, _ptr(records), n_pool, _ptr(ids), n,
+                                             _ptr(q_rot), Q, _ptr(out), _stream(stream)))
+    return out
 
 
 def rslm_unpack_codes(plan, tiles, n, stream=None):

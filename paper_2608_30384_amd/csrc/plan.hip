@@ -103,6 +103,15 @@ int rslm_plan_create(const rslm_plan_desc *d, rslm_plan **out) {
   if (g == 1)
     for (int k = 0; k + 1 < K; ++k)
       if (!(d->codebook[k] < d->codebook[k + 1])) return RSLM_ERR_INVALID_ARG;
+  if (d->lite != 0 && d->lite != 1) return RSLM_ERR_INVALID_ARG;
+  if (d->lite) {
+    if (bits != 4 || D < 64 || !d->codebook_lead) return RSLM_ERR_INVALID_ARG;
+    for (int k = 0; k < 8; ++k) {
+      const float v = d->codebook_lead[k];
+      if (!std::isfinite(v) || !f16_exact(v)) return RSLM_ERR_INVALID_ARG;
+      if (k > 0 && !(d->codebook_lead[k - 1] < v)) return RSLM_ERR_INVALID_ARG;
+    }
+  }
   if (!device_ok()) return RSLM_ERR_NO_DEVICE;
 
   rslm_plan *p = new (std::nothrow) rslm_plan();
@@ -158,6 +167,12 @@ int rslm_plan_create(const rslm_plan_desc *d, rslm_plan **out) {
   }
   for (int k = 0; k < 16; ++k)
     c.thr[k] = (g == 1 && k + 1 < K) ? 0.5f * (d->codebook[k] + d->codebook[k + 1]) : 0.0f;
+  c.lead = d->lite ? (d->scale_mode ? 32 : 16) : 0;
+  c.record_bytes = c.canon_bytes + (d->lite ? 0 : (d->scale_mode ? 4 : 2));
+  for (int k = 0; k < 8; ++k) c.cb_lead[k] = d->lite ? d->codebook_lead[k] : 0.0f;
+  for (int k = 0; k < 16; ++k)
+    c.thr_lead[k] = (d->lite && k < 7) ? 0.5f * (d->codebook_lead[k] + d->codebook_lead[k + 1])
+                                       : __builtin_inff();
 
   // --- device tables: signs, intra-block permutation, compact decode table
   float s1f[256];
@@ -271,6 +286,8 @@ int rslm_plan_get_info(const rslm_plan *p, rslm_plan_info *info) {
   info->tile_records = kTileRecords;
   info->tile_bytes = p->codec.tile_bytes;
   info->emax = p->emax;
+  info->lite = p->codec.lead > 0;
+  info->record_bytes = p->codec.record_bytes;
   return RSLM_OK;
 }
 

@@ -241,6 +241,91 @@ __global__ void __launch_bounds__(kRescoreThreads) k_rescore_rslm(
   sort_emit(buf, int(count), q, k_out, out_s, out_i);
 }
 
+// OneToMany scoring of packed records: score = g^ s^ sum_j <q_rot[j g:(j+1) g],
+// C[code_j]> for record ids[j] (or j).  A workgroup covers `per_block`
+// consecutive entries of one query (grid.y); 16 lanes per record, lane j of a
+// group decoding the 8-code groups j, j + 16, ... from one 4-byte load (any
+// alignment; 3-bit records: three bytes).  LITE: the first cp.lead codes are
+// 3-bit codes on the K = 8 codebook whose bit 3 carries the scales, gathered
+// from the 16 lanes by an OR reduction.
+struct __attribute__((packed, aligned(1))) U32Unaligned {
+  uint32_t v;
+};
+
+template <int W, int G, bool LITE>
+__global__ void __launch_bounds__(kRescoreThreads) k_score(
+    const uint8_t *__restrict__ records, int64_t n_pool, const int64_t *__restrict__ ids,
+    int64_t n, int64_t per_block, const float *__restrict__ q_rot, int dim, CodecParams cp,
+    float *__restrict__ out) {
+  extern __shared__ float qs[];   // n_groups * 8 * G floats, zero beyond dim
+  __shared__ float cbs[16 * G], cbl[8];
+  const int q = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n_groups = (cp.n_sub + 7) / 8;
+  const float *qr = q_rot + int64_t(q) * dim;
+  for (int d = tid; d < n_groups * 8 * G; d += kRescoreThreads) qs[d] = (d < dim) ? qr[d] : 0.f;
+  if (tid < 16 * G && tid < (1 << W) * G) cbs[tid] = cp.cb[tid];
+  if (LITE && tid < 8) cbl[tid] = cp.cb_lead[tid];
+  __syncthreads();
+  const int grp = wave * 4 + (lane >> 4), gl = lane & 15;
+  const int64_t j0 = int64_t(blockIdx.x) * per_block;
+  const int64_t j1 = min(n, j0 + per_block);
+  for (int64_t j = j0 + grp; j < j1; j += (kRescoreThreads / 16)) {
+    const int64_t r = ids ? ids[j] : j;
+    const bool valid = r >= 0 && r < n_pool;
+    const uint8_t *rec = records + (valid ? r : 0) * int64_t(cp.record_bytes);
+    float dot = 0.f;
+    uint32_t sbits = 0u, gbits = 0u;
+    for (int G8 = gl; G8 < n_groups; G8 += 16) {
+      uint32_t bits = 0u;
+      if (W * G8 + 4 <= cp.record_bytes) {
+        bits = reinterpret_cast<const U32Unaligned *>(rec + W * G8)->v;
+      } else {
+#pragma unroll
+        for (int t = 0; t < W; ++t)
+          if (W * G8 + t < cp.canon_bytes) bits |= uint32_t(rec[W * G8 + t]) << (8 * t);
+      }
+      if (W * G8 + W > cp.canon_bytes)   // the record's last group: only its code bytes
+        bits &= (cp.canon_bytes - W * G8 >= 4) ? 0xffffffffu
+                                              : ((1u << (8 * (cp.canon_bytes - W * G8))) - 1u);
+      const float *qv = qs + G8 * 8 * G;
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        uint32_t code = (bits >> (W * c)) & ((1u << W) - 1u);
+        if (LITE && G8 * 8 + c < cp.lead) {
+          const int jj = G8 * 8 + c;
+          if (jj < 16) sbits |= (code >> 3) << jj;
+          else gbits |= (code >> 3) << (jj - 16);
+          dot = fmaf(qv[c], cbl[code & 7u], dot);
+          continue;
+        }
+#pragma unroll
+        for (int t = 0; t < G; ++t) dot = fmaf(qv[c * G + t], cbs[code * G + t], dot);
+      }
+    }
+#pragma unroll
+    for (int off = 8; off >= 1; off >>= 1) {
+      dot += __shfl_xor(dot, off, 64);
+      if (LITE) {
+        sbits |= __shfl_xor(sbits, off, 64);
+        gbits |= __shfl_xor(gbits, off, 64);
+      }
+    }
+    if (gl == 0) {
+      uint32_t su, gu;
+      if (LITE) {
+        su = sbits;
+        gu = cp.global ? gbits : 0x7000u;
+      } else {
+        const uint8_t *sf = rec + cp.canon_bytes;
+        su = uint32_t(sf[0]) | (uint32_t(sf[1]) << 8);
+        gu = cp.global ? (uint32_t(sf[2]) | (uint32_t(sf[3]) << 8)) : 0x7000u;
+      }
+      out[int64_t(q) * n + j] = valid ? dec_ue4m12(gu) * (dec_ue7m9(su) * dot) : -__builtin_inff();
+    }
+  }
+}
+
 }  // namespace rslm
 
 using namespace rslm;
@@ -291,6 +376,7 @@ int rslm_rescore(const rslm_rescore_codec *c, const float *q_rot, int32_t Q,
   if (c->kind == RSLM_RESCORE_RSLM &&
       (!c->plan || c->plan->rot.D != c->dim || c->plan->rot.passes != 0))
     return RSLM_ERR_INVALID_ARG;
+  if (c->kind == RSLM_RESCORE_RSLM && c->plan->codec.lead > 0) return RSLM_ERR_UNSUPPORTED;
   if (Q == 0) return RSLM_OK;
   if (!c->codes || !q_rot || !cand_scores || !cand_ids || !out_scores || !out_ids)
     return RSLM_ERR_INVALID_ARG;
@@ -317,6 +403,39 @@ int rslm_rescore(const rslm_rescore_codec *c, const float *q_rot, int32_t Q,
     default: RSLM_RESCORE_CALL(4, 1); break;
   }
 #undef RSLM_RESCORE_CALL
+  return check_launch();
+}
+
+int rslm_score(const rslm_plan *p, const uint8_t *records, int64_t n_pool, const int64_t *ids,
+               int64_t n, const float *q_rot, int32_t Q, float *out, void *stream) {
+  if (!p || n_pool < 0 || n < 0 || Q < 0) return RSLM_ERR_INVALID_ARG;
+  if (Q > 65535) return RSLM_ERR_INVALID_ARG;
+  if (!ids && n > n_pool) return RSLM_ERR_INVALID_ARG;
+  if (n == 0 || Q == 0) return RSLM_OK;
+  if (!records || !q_rot || !out) return RSLM_ERR_INVALID_ARG;
+  const CodecParams &cp = p->codec;
+  const int n_groups = (cp.n_sub + 7) / 8;
+  const size_t shm = size_t(n_groups) * 8 * cp.g * sizeof(float);
+  // workgroups of 256 records (16 per pass of the 16-lane groups)
+  const int64_t per_block = 256;
+  const int64_t blocks = (n + per_block - 1) / per_block;
+  if (blocks > 0x7fffffff) return RSLM_ERR_INVALID_ARG;
+  const dim3 grid(static_cast<unsigned>(blocks), static_cast<unsigned>(Q));
+  hipStream_t s = as_stream(stream);
+#define RSLM_SCORE_CALL(W, G, LT)                                                             \
+  hipLaunchKernelGGL((k_score<W, G, LT>), grid, dim3(kRescoreThreads), shm, s, records, n_pool, \
+                     ids, n, per_block, q_rot, cp.D, cp, out)
+  if (cp.lead > 0) {
+    RSLM_SCORE_CALL(4, 1, true);
+  } else {
+    switch (cp.bits) {
+      case 1: RSLM_SCORE_CALL(4, 4, false); break;
+      case 2: RSLM_SCORE_CALL(4, 2, false); break;
+      case 3: RSLM_SCORE_CALL(3, 1, false); break;
+      default: RSLM_SCORE_CALL(4, 1, false); break;
+    }
+  }
+#undef RSLM_SCORE_CALL
   return check_launch();
 }
 

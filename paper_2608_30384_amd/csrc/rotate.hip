@@ -208,7 +208,7 @@ __global__ void __launch_bounds__(256) k_encode(
     int dstride, uint8_t *__restrict__ codes2, uint32_t *__restrict__ scales2,
     CodecParams cp2, const float *__restrict__ sq8_lo, const float *__restrict__ sq8_hi) {
   extern __shared__ float lds[];
-  __shared__ float cbs[64], cbs2[64];
+  __shared__ float cbs[64], cbs2[64], cbl[8];
   __shared__ int16_t pi[128];
   const int lane = threadIdx.x & 63;
   const int wid = threadIdx.x >> 6;
@@ -217,6 +217,7 @@ __global__ void __launch_bounds__(256) k_encode(
     cbs[threadIdx.x] = cp.cb[threadIdx.x];
     cbs2[threadIdx.x] = cp2.cb[threadIdx.x];
   }
+  if (threadIdx.x < 8) cbl[threadIdx.x] = cp.cb_lead[threadIdx.x];
   load_perm(rp, pi);
   const int64_t rec = int64_t(blockIdx.x) * nw + wid;
   int64_t row = -1;
@@ -272,7 +273,11 @@ __global__ void __launch_bounds__(256) k_encode(
   for (int j = lane; j < cp.n_sub; j += kWave) {
     int code = 0;
     if (m > 0.f) {
-      if (g == 1) {
+      if (g == 1 && j < cp.lead) {   // Rslm4Lite leading coordinate: K = 8
+        const float u = z[px(j)] * inv_s0;
+#pragma unroll
+        for (int k = 0; k < 7; ++k) code += (u > cp.thr_lead[k]) ? 1 : 0;
+      } else if (g == 1) {
         const float u = z[px(j)] * inv_s0;
 #pragma unroll
         for (int k = 0; k < 15; ++k) code += (k + 1 < cp.K && u > cp.thr[k]) ? 1 : 0;
@@ -301,7 +306,7 @@ __global__ void __launch_bounds__(256) k_encode(
       }
       for (int t = 0; t < g; ++t) {
         const int i = j * g + t;
-        const float cv = (i < D) ? cbs[code * g + t] : 0.f;
+        const float cv = (i < D) ? ((i < cp.lead) ? cbl[code] : cbs[code * g + t]) : 0.f;
         cn2 += cv * cv;
         rcd += rc[i < D ? i : 0] * rcw * cv;
       }
@@ -324,6 +329,11 @@ __global__ void __launch_bounds__(256) k_encode(
   }
   if (lane == 0) scales[rec] = su | (gu << 16);
   __builtin_amdgcn_wave_barrier();  // codes in cl are written by other lanes
+  // first-stage centroid value of valid coordinate i (0 for a zero residual)
+  auto cval = [&](int i) {
+    if (!(m > 0.f)) return 0.f;
+    return (i < cp.lead) ? cbl[cl[i]] : cbs[cl[i / g] * g + (i % g)];
+  };
 
   if (codes2 && !sq8_lo) {
     // Second stage: r2 = R x - R a with R a = g^ (R c + s^ c^), quantised in
@@ -333,7 +343,7 @@ __global__ void __launch_bounds__(256) k_encode(
     float m2 = 0.f, rr2 = 0.f;
 #pragma unroll 4
     for (int i = lane; i < D; i += kWave) {
-      const float cv = (m > 0.f) ? cbs[cl[i / g] * g + (i % g)] : 0.f;
+      const float cv = cval(i);
       const float rcv = rc[i] * rcw;
       const float d = z[px(i)] + rcv - gh * (rcv + sh * cv);
       r2[px(i)] = d;
@@ -381,7 +391,7 @@ __global__ void __launch_bounds__(256) k_encode(
           const int i = j * g2 + t;
           if (i >= D) break;
           const float c2 = cbs2[code * g2 + t];
-          const float c1 = (m > 0.f) ? cbs[cl[i / g] * g + (i % g)] : 0.f;
+          const float c1 = cval(i);
           cn22 += c2 * c2;
           rad += (rc[i] * rcw + sh * c1) * c2;
         }
@@ -421,7 +431,8 @@ __global__ void __launch_bounds__(256) k_encode(
     uint32_t val = 0;
     for (int t = 0; t < per; ++t) {
       const int j = G * per + t;
-      const uint32_t code = (j < cp.n_sub) ? cl[j] : 0u;
+      uint32_t code = (j < cp.n_sub) ? cl[j] : 0u;
+      if (j < cp.lead) code |= (((j < 16 ? su : gu) >> (j & 15)) & 1u) << 3;   // Rslm4Lite
       val |= code << (cp.w * t);
     }
     store_group(codes, rec, G, val, cp);
@@ -432,8 +443,7 @@ __global__ void __launch_bounds__(256) k_encode(
     const float gh = dec_ue4m12(gu);
   #pragma unroll 4
     for (int i = lane; i < D; i += kWave) {
-      const int code = cl[i / g];
-      const float cv = (m > 0.f) ? cbs[code * g + (i % g)] : 0.f;
+      const float cv = cval(i);
       const float rcv = rc[i] * rcw;
       const float o = z[px(i)] + rcv - gh * (rcv + sh * cv);
       if (resid) resid[row * D + i] = o;
@@ -471,6 +481,34 @@ __global__ void k_unpack(const uint8_t *__restrict__ tiles, int64_t n, uint8_t *
     for (int b = 0; b < cp.bits; ++b) {
       const int cb = G * cp.bits + b;
       if (cb < cp.canon_bytes) canon[rec * cp.canon_bytes + cb] = tiles[tile_byte_addr(rec, G, b, cp)];
+    }
+  }
+}
+
+// Packed records (canonical codes + scale suffix, or Lite codes alone) from
+// the scan tile layout and the scales array.  Thread per (record, group of 8
+// coordinates); group 0 also writes the suffix.
+__global__ void k_pack_records(const uint8_t *__restrict__ tiles, const uint32_t *__restrict__ scales,
+                               int64_t n, uint8_t *__restrict__ records, CodecParams cp) {
+  const int n_groups = cp.d_pad >> 3;
+  const int64_t total = n * n_groups;
+  for (int64_t t = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; t < total;
+       t += int64_t(gridDim.x) * blockDim.x) {
+    const int64_t rec = t / n_groups;
+    const int G = int(t - rec * n_groups);
+    uint8_t *dst = records + rec * cp.record_bytes;
+    for (int b = 0; b < cp.bits; ++b) {
+      const int cb = G * cp.bits + b;
+      if (cb < cp.canon_bytes) dst[cb] = tiles[tile_byte_addr(rec, G, b, cp)];
+    }
+    if (G == 0 && cp.lead == 0) {
+      const uint32_t sc = scales[rec];
+      dst[cp.canon_bytes] = uint8_t(sc);
+      dst[cp.canon_bytes + 1] = uint8_t(sc >> 8);
+      if (cp.global) {
+        dst[cp.canon_bytes + 2] = uint8_t(sc >> 16);
+        dst[cp.canon_bytes + 3] = uint8_t(sc >> 24);
+      }
     }
   }
 }
@@ -595,6 +633,17 @@ int rslm_pack_codes(const rslm_plan *p, const uint8_t *canon, int64_t n, uint8_t
   const int64_t total = (n + 15) / 16 * 16 * (p->codec.d_pad / 8);
   hipLaunchKernelGGL(k_pack, dim3(unsigned(pack_grid(total))), dim3(256), 0, as_stream(stream),
                      canon, n, tiles, p->codec);
+  return check_launch();
+}
+
+int rslm_pack_records(const rslm_plan *p, const uint8_t *tiles, const uint32_t *scales, int64_t n,
+                      uint8_t *records, void *stream) {
+  if (!p || n < 0) return RSLM_ERR_INVALID_ARG;
+  if (n == 0) return RSLM_OK;
+  if (!tiles || !records || (!scales && p->codec.lead == 0)) return RSLM_ERR_INVALID_ARG;
+  const int64_t total = n * (p->codec.d_pad / 8);
+  hipLaunchKernelGGL(k_pack_records, dim3(unsigned(pack_grid(total))), dim3(256), 0,
+                     as_stream(stream), tiles, scales, n, records, p->codec);
   return check_launch();
 }
 

@@ -228,7 +228,11 @@ __device__ __forceinline__ uint32_t sgnbit(uint32_t m, int b, int i) {
 //      sub-vectors 64 b + 4 r + k, so a lane's four codes of a block are 16
 //      consecutive bits of the canonical record at byte 32 b + 2 r;
 //   2: SQ8 codes with the ranges sq8_lo / sq8_hi, 8 bytes per lane and block.
-template <int NB, int BITS, int S2>
+// LITE (Rslm4Lite): the lanes holding the first cp.lead coordinates (block 0,
+// r < cp.lead / 8) search the K = 8 thresholds (padded with +inf, so the same
+// four-step search yields codes 0..7) and decode with the K = 8 codebook;
+// their stored code words carry the scale bits in bit 3 of each nibble.
+template <int NB, int BITS, int S2, bool LITE = false>
 __global__ void __launch_bounds__(256) k_encode_rows(
     const float *__restrict__ x, int64_t n_rows, const int64_t *__restrict__ src_row,
     const int32_t *__restrict__ rec_list, int64_t n_records, const float *__restrict__ cen,
@@ -243,6 +247,7 @@ __global__ void __launch_bounds__(256) k_encode_rows(
   constexpr int kVecStride = D + 4;   // floats per vector buffer (offset of 4 banks per row)
   __shared__ float buf[16 * kVecStride];
   __shared__ float cbs[16], thr[16];
+  __shared__ float cb8[16], thr8[16];   // Rslm4Lite: K = 8 codebook of the leading lanes
   __shared__ float cb2[16], cb2y[16];   // second codebook, first and second coordinates
   __shared__ uint32_t rmask[16];
   __shared__ uint16_t ts[D];
@@ -252,6 +257,10 @@ __global__ void __launch_bounds__(256) k_encode_rows(
   if (TWO && threadIdx.x < 16) {
     cb2[threadIdx.x] = cp2.cb[2 * threadIdx.x];
     cb2y[threadIdx.x] = cp2.cb[2 * threadIdx.x + 1];
+  }
+  if (LITE && threadIdx.x < 16) {
+    cb8[threadIdx.x] = (threadIdx.x < 8) ? cp.cb_lead[threadIdx.x] : 0.f;
+    thr8[threadIdx.x] = cp.thr_lead[threadIdx.x];
   }
   if (threadIdx.x < 16) {
     cbs[threadIdx.x] = cp.cb[threadIdx.x];
@@ -364,27 +373,31 @@ __global__ void __launch_bounds__(256) k_encode_rows(
   // where needed (registers, not recomputation, bound this kernel).
   uint32_t word[NB];
   float cn2 = 0.f;
+  const bool lead_lane = LITE && r < cp.lead / 8;   // block 0 of these lanes is on cb8
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
+    float *tb = (LITE && b == 0 && lead_lane) ? thr8 : thr;
+    float *cbb = (LITE && b == 0 && lead_lane) ? cb8 : cbs;
     uint32_t c4[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
 #pragma unroll
     for (int half = K >> 1; half >= 1; half >>= 1)
 #pragma unroll
       for (int i = 0; i < 8; ++i)
-        c4[i] += (z[8 * b + i] * inv_s0 > lds_at(thr, c4[i] + 4u * (half - 1))) ? 4u * half : 0u;
+        c4[i] += (z[8 * b + i] * inv_s0 > lds_at(tb, c4[i] + 4u * (half - 1))) ? 4u * half : 0u;
     word[b] = 0u;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const uint32_t c = (m > 0.f) ? (c4[i] >> 2) : 0u;
       word[b] |= c << (BITS * i);
-      const float v = lds_at(cbs, 4u * c);
+      const float v = lds_at(cbb, 4u * c);
       cn2 = fmaf(v, v, cn2);
     }
     __builtin_amdgcn_sched_barrier(0);
   }
   cn2 = row_sum16(cn2);
   auto centroid = [&](int b, int i) {   // code 0 of a zero residual decodes to 0
-    const float v = lds_at(cbs, 4u * ((word[b] >> (BITS * i)) & uint32_t(K - 1)));
+    float *cbb = (LITE && b == 0 && lead_lane) ? cb8 : cbs;
+    const float v = lds_at(cbb, 4u * ((word[b] >> (BITS * i)) & uint32_t(K - 1)));
     return (m > 0.f) ? v : 0.f;
   };
   // <R c, c^> with the rotated centre (read again for the residual output)
@@ -417,13 +430,19 @@ __global__ void __launch_bounds__(256) k_encode_rows(
   // goes to lane stream 16 (r & 3) + n at byte c BITS, c = G / 4 = 4 b + r / 4
   uint8_t *tile = codes + (rec >> 4) * int64_t(cp.tile_bytes);
   const int n = int(rec & 15);
+  uint32_t emb = 0u;   // Rslm4Lite: scale byte of this lane spread into bit 3 of each nibble
+  if (LITE && lead_lane) {
+    const uint32_t byte = ((r < 2 ? su : gu) >> (8 * (r & 1))) & 0xffu;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) emb |= ((byte >> i) & 1u) << (4 * i + 3);
+  }
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
     const int c = 4 * b + (r >> 2);
     if (BITS == 4) {
       const int off = 4 * c;   // 4 bytes inside one 16-byte unit
       *reinterpret_cast<uint32_t *>(tile + ((off >> 4) * 64 + 16 * (r & 3) + n) * 16 + (off & 15)) =
-          word[b];
+          (b == 0) ? (word[b] | emb) : word[b];
     } else {
 #pragma unroll
       for (int t = 0; t < 3; ++t) {
@@ -620,6 +639,8 @@ bool launch_encode_reg(const rslm_plan *p, const rslm_plan *p2, const float *x, 
                   p2->codec.canon_bytes * 4 != p->rot.D || resid))
     return false;
   if (s2 != 0 && p->codec.bits != 4) return false;
+  const bool lite = p->codec.lead > 0;
+  if (lite && s2 != 0) return false;   // Lite with a second output: general path
   // 16-byte vector loads and stores of every row
   if ((reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(cen) |
        reinterpret_cast<uintptr_t>(cen_rot) | reinterpret_cast<uintptr_t>(resid) |
@@ -631,8 +652,9 @@ bool launch_encode_reg(const rslm_plan *p, const rslm_plan *p2, const float *x, 
   if (groups > 0x7fffffff) return false;
   const unsigned grid = unsigned(groups);
   const CodecParams &cp2 = p2 ? p2->codec : p->codec;
-#define CALL_B(NB, B, T)                                                                        \
-  hipLaunchKernelGGL((k_encode_rows<NB, B, T>), dim3(grid), dim3(256), 0, s, x, n_rows, src_row, \
+#define CALL_B(NB, B, ...)                                                                      \
+  hipLaunchKernelGGL((k_encode_rows<NB, B, __VA_ARGS__>), dim3(grid), dim3(256), 0, s, x, n_rows,  \
+                     src_row,                                                                    \
                      rec_list, n_records, cen, cen_rot, nlist, codes, scales, resid, p->rot,      \
                      p->codec, codes2, scales2, cp2, sq8_lo, sq8_hi)
 #define CALL(J)                  \
@@ -640,6 +662,8 @@ bool launch_encode_reg(const rslm_plan *p, const rslm_plan *p2, const float *x, 
     CALL_B((J) / 2, 4, 1);       \
   else if (s2 == 2)              \
     CALL_B((J) / 2, 4, 2);       \
+  else if (lite)                 \
+    CALL_B((J) / 2, 4, 0, true); \
   else if (p->codec.bits == 4)   \
     CALL_B((J) / 2, 4, 0);       \
   else                           \

@@ -71,6 +71,10 @@ struct CodecParams {
   float cb[64];               // codebook, K*g values
   float thr[16];              // 1-D decision thresholds (K-1 used)
   float cbh[16];              // |C_k|^2 / 2 (unused k: a huge value)
+  int lead;                   // Rslm4Lite: leading coordinates on cb_lead (16 or 32), else 0
+  int record_bytes;           // packed record: canon_bytes + scale suffix (Lite: none)
+  float cb_lead[8];           // Rslm4Lite: K = 8 codebook of the leading coordinates
+  float thr_lead[16];         // its 7 thresholds, padded with +inf
 };
 
 }  // namespace rslm

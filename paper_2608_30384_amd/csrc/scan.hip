@@ -868,6 +868,7 @@ int rslm_scan_topk(const rslm_plan *p, const rslm_index *idx, const float *q_rot
       !idx->list_sizes || !idx->ids || !idx->codes || !idx->scales)
     return RSLM_ERR_INVALID_ARG;
   if (p->codec.n_chunks > 32) return RSLM_ERR_UNSUPPORTED;   // D > 1024
+  if (p->codec.lead > 0) return RSLM_ERR_UNSUPPORTED;         // Rslm4Lite: rslm_score only
   const size_t need = rslm_scan_topk_workspace(p, idx, Q, nprobe, k);
   if (!ws || ws_bytes < need) return RSLM_ERR_WORKSPACE;
   const int nlist = idx->nlist;

@@ -1,0 +1,168 @@
+"""Parity of packed records, Rslm4Lite encoding and OneToMany scoring on the
+GPU with the float64 oracle.
+
+* Rslm4Lite encoding (register and general encoders): codes, embedded
+  scales and scale codes against ``oracle.encode(..., C_lead=...)`` with the
+  near-tie and rounding-boundary allowances of the other encoder tests.
+* ``rslm_pack_records``: byte-identical to ``oracle.pack_records`` of the
+  library's own codes and scales (a pure layout operation).
+* ``rslm_score``: records written by the oracle, scored for several queries,
+  contiguous and gathered by ids (including ids outside the pool), against
+  the oracle's LUT route with no partition centre; every bit width, local
+  and global scales, Lite, ragged record sizes.
+"""
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from tests import helpers as H
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+@pytest.fixture(scope="module")
+def R():
+    import paper_2608_30384_amd as R
+    return R
+
+
+def _t(a, dtype=None):
+    t = torch.from_numpy(np.ascontiguousarray(a))
+    if dtype is not None:
+        t = t.to(dtype)
+    return t.to(DEV)
+
+
+LITE_CASES = [(256, 1, "local", 333), (768, 2, "global", 300), (96, 2, "global", 200),
+              (200, 2, "local", 150), (128, 1, "global", 170)]
+
+
+@pytest.mark.parametrize("D,passes,mode,n", LITE_CASES)
+def test_lite_encode_parity(R, D, passes, mode, n):
+    nlist = 4
+    x = synth.aniso(n, D, seed=D + 3)
+    cen = x[np.random.default_rng(D).choice(n, nlist, replace=False)] * 0.9
+    assign, _ = oracle.assign_l2(x, cen)
+    Rm = H.rot(D, passes)
+    C16, C8 = synth.codebook(4), synth.codebook(3)
+    lead = oracle.lite_lead(mode)
+    ref = oracle.encode(x, Rm, C16, 4, centroids=cen[assign], scale_mode=mode, C_lead=C8)
+    plan = R.Plan(D, 4, passes=passes, scale_mode=mode, lite=True)
+    assert plan.lite and plan.record_bytes == oracle.record_bytes(D, 4, mode, lite=True)
+    xt, ct = _t(x), _t(cen.astype(np.float32))
+    crot = R.rslm_fwht(plan, ct)
+    codes = torch.zeros(plan.code_bytes(n), dtype=torch.uint8, device=DEV)
+    scales = torch.zeros(n, dtype=torch.int32, device=DEV)
+    R.rslm_encode(plan, xt, codes, scales, rec_list=_t(assign, torch.int32), centroids=ct,
+                  centroids_rot=crot)
+    sc = scales.cpu().numpy().astype(np.uint32)
+    su, gu = sc & 0xFFFF, sc >> 16
+    recs = R.rslm_pack_records(plan, codes, scales, n).cpu().numpy()
+    g, es, eg = oracle.unpack_records(recs, 4, D, mode, lite=True)
+    # the embedded scales are the scale codes
+    assert np.array_equal(es, su)
+    if mode == "global":
+        assert np.array_equal(eg, gu)
+    # codes: leading coordinates on the K = 8 thresholds, the rest on K = 16
+    u = ref["u"]
+    near = H.near_threshold(u, C16)
+    near[:, :lead] = H.near_threshold(u[:, :lead], C8)
+    mism = g != ref["codes"]
+    assert not np.any(mism & ~near), np.argwhere(mism & ~near)[:5]
+    assert mism.sum() <= max(2, 1e-4 * mism.size)
+    ok = ~mism.any(1)
+    s_near = H.near_rounding(ref["s"], oracle.dec_ue7m9, oracle.enc_ue7m9)
+    assert not np.any(ok & ~s_near & (su != ref["s_code"]))
+    if mode == "global":
+        g_near = H.near_rounding(ref["g"], oracle.dec_ue4m12, oracle.enc_ue4m12)
+        okg = ok & ~g_near & (su == ref["s_code"])
+        assert np.all(gu[okg] == ref["g_code"][okg])
+    # packed records equal the oracle's packing of the library's codes
+    assert np.array_equal(recs, oracle.pack_records(g, su, gu, 4, mode, lite=True))
+
+
+@pytest.mark.parametrize("D,bits,mode", [(256, 4, "local"), (100, 1, "global"), (98, 2, "local"),
+                                         (101, 3, "global")])
+def test_pack_records_layout(R, D, bits, mode):
+    n = 77
+    x = synth.aniso(n, D, seed=D)
+    plan = R.Plan(D, bits, passes=2, scale_mode=mode)
+    codes = torch.zeros(plan.code_bytes(n), dtype=torch.uint8, device=DEV)
+    scales = torch.zeros(n, dtype=torch.int32, device=DEV)
+    R.rslm_encode(plan, _t(x), codes, scales)
+    recs = R.rslm_pack_records(plan, codes, scales, n).cpu().numpy()
+    assert recs.shape == (n, oracle.record_bytes(D, bits, mode))
+    K, g = oracle.codec_shape(bits)
+    canon = R.rslm_unpack_codes(plan, codes, n).cpu().numpy()
+    c = oracle.unpack_canonical(canon, bits, -(-D // g))
+    sc = scales.cpu().numpy().astype(np.uint32)
+    assert np.array_equal(recs, oracle.pack_records(c, sc & 0xFFFF, sc >> 16, bits, mode))
+
+
+SCORE_CASES = [
+    # D, bits, mode, lite, n_pool, n (gathered), Q
+    (256, 4, "local", False, 3000, 1000, 3),
+    (256, 4, "local", True, 3000, 1000, 3),
+    (768, 4, "global", True, 1200, 700, 2),
+    (100, 1, "local", False, 2500, 900, 2),
+    (98, 2, "global", False, 2000, 513, 4),
+    (101, 3, "global", False, 2000, 777, 2),
+    (101, 4, "local", False, 1500, 300, 1),
+    (1536, 1, "global", False, 600, 333, 2),
+]
+
+
+@pytest.mark.parametrize("D,bits,mode,lite,n_pool,n,Q", SCORE_CASES)
+def test_score_parity(R, D, bits, mode, lite, n_pool, n, Q):
+    rng = np.random.default_rng(D + bits + lite)
+    x = synth.aniso(n_pool, D, seed=D + 1, normalize=(bits < 4))
+    Rm = H.rot(D, 2)
+    C = synth.codebook(bits)
+    C8 = synth.codebook(3) if lite else None
+    lead = oracle.lite_lead(mode) if lite else 0
+    enc = oracle.encode(x, Rm, C, bits, scale_mode=mode, C_lead=C8)
+    recs = oracle.pack_records(enc["codes"], enc["s_code"], enc["g_code"], bits, mode, lite)
+    plan = R.Plan(D, bits, passes=2, scale_mode=mode, lite=lite)
+    assert plan.record_bytes == recs.shape[1]
+    q = synth.queries_like("aniso", Q, D, data_seed=D + 1, query_seed=9)
+    qr = q.astype(np.float64) @ Rm.T
+    sh, gh = H.dec_scales(enc["s_code"].astype(np.uint32) | (enc["g_code"].astype(np.uint32) << 16))
+    ref = np.stack([oracle.scan_scores_lut(qr[i], 0.0, enc["codes"], sh, gh, C, C8, lead)
+                    for i in range(Q)])
+    xt = oracle.reconstruct(enc["codes"], enc["s_code"], enc["g_code"], C, Rm, None, C8, lead)
+    xn = np.linalg.norm(xt, axis=1)
+    recs_t = _t(recs)
+    qr_t = _t(qr.astype(np.float32))
+    # contiguous: every record of the pool
+    got = R.rslm_score(plan, recs_t, qr_t).cpu().numpy()
+    for i in range(Q):
+        tol = H.score_tol(ref[i], np.linalg.norm(q[i]), xn)
+        assert np.all(np.abs(got[i] - ref[i]) <= tol), np.abs(got[i] - ref[i]).max()
+    # gathered by ids, some outside the pool
+    ids = rng.integers(0, n_pool, n).astype(np.int64)
+    ids[:3] = [-1, n_pool, n_pool + 5]
+    got = R.rslm_score(plan, recs_t, qr_t, ids=_t(ids)).cpu().numpy()
+    assert np.all(np.isneginf(got[:, :3]))
+    for i in range(Q):
+        sel = ids[3:]
+        tol = H.score_tol(ref[i][sel], np.linalg.norm(q[i]), xn[sel])
+        assert np.all(np.abs(got[i, 3:] - ref[i][sel]) <= tol)
+
+
+def test_lite_plan_is_rejected_by_the_ivf_scan(R):
+    from paper_2608_30384_amd import _lib as L
+    plan = R.Plan(256, 4, passes=1, scale_mode="local", lite=True)
+    n = 32
+    codes = torch.zeros(plan.code_bytes(n), dtype=torch.uint8, device=DEV)
+    index = R.Index(_t(np.array([0], np.int64)), _t(np.array([n], np.int32)),
+                    _t(np.arange(n, dtype=np.int32)), codes,
+                    torch.zeros(n, dtype=torch.int32, device=DEV))
+    q = torch.zeros((1, 256), dtype=torch.float32, device=DEV)
+    with pytest.raises(L.RslmError):
+        R.rslm_scan_topk(plan, index, q, torch.zeros((1, 1), dtype=torch.int32, device=DEV),
+                         torch.zeros((1, 1), dtype=torch.float32, device=DEV), 5)
