@@ -55,10 +55,13 @@ def parse():
     ap.add_argument("--encode-chunk", type=int, default=65536)
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--workload", choices=("text768", "capacity", "sweep"), default="text768",
+    ap.add_argument("--workload", choices=("text768", "capacity", "sweep", "onetomany"),
+                    default="text768",
                     help="text768 (default): the metric's configuration; capacity: 100M x 768 "
                          "at nlist 16,384 with 2-bit RSLM rescoring records; sweep: 10M x 1,024 "
-                         "unit-norm at 1, 2, 3 and 4 bits with recall@10")
+                         "unit-norm at 1, 2, 3 and 4 bits with recall@10; onetomany: the paper's "
+                         "codec microbenchmarks (OneToMany scoring at D = 256, contiguous and "
+                         "gathered from a 128M-record pool, and compression at D = 2049)")
     ap.add_argument("--counter-summary", nargs=2, metavar=("SQ_A_CSV", "SQ_B_CSV"),
                     help="print a markdown summary of the two SQ counter runs and exit")
     ap.add_argument("--copy-calib", action="store_true",
@@ -381,6 +384,8 @@ def main():
         return run_capacity(args)
     if args.workload == "sweep":
         return run_sweep(args)
+    if args.workload == "onetomany":
+        return run_onetomany(args)
     import torch
 
     import synth
@@ -877,6 +882,122 @@ def run_sweep(args):
                                 "in batches of 256, nprobe=64, top-10"),
                    "N": N, "dim": D, "nlist": nlist, "nprobe": nprobe, "batch": B, "k": k},
         "per_bits": res,
+        "setup_s": time.time() - t_setup,
+        "kernel_sources": csrc_hash(),
+    }
+    print(json.dumps(out), flush=True)
+
+
+# The paper's CPU figures for the same shapes (M items/s; AMD Milan / Intel
+# Cascade Lake), quoted as context only.
+PAPER_ONETOMANY = {
+    "Rslm1": {"contiguous": (388.31, 233.57), "largepool": (175.06, 153.24)},
+    "Rslm2": {"contiguous": (225.47, 168.78), "largepool": (103.29, 80.15)},
+    "Rslm3": {"contiguous": (58.49, 41.60), "largepool": (38.13, 21.53)},
+    "Rslm4": {"contiguous": (151.61, 93.68), "largepool": (55.88, 43.33)},
+    "Rslm4Lite": {"contiguous": (137.43, 104.98), "largepool": (105.58, 61.46)},
+}
+PAPER_COMPRESS_2049 = 0.128   # M items/s, Rslm4 on AMD Milan
+
+
+def run_onetomany(args):
+    """The paper's codec microbenchmarks on one GPU.  OneToMany: one rotated
+    query scored against 16,777,216 packed records of D = 256 (codes + 2-byte
+    UE7M9 suffix; Rslm4Lite: ceil(D/2) bytes with the scale embedded), either
+    contiguous or gathered at uniformly random positions of a pool of
+    134,217,728 records ("LargePool 128M").  Records are real encodings of
+    isotropic Gaussian unit vectors, encoded block by block.  Compress: Rslm4
+    encoding (rotation, Lloyd-Max codes, norm correction, packed records) of
+    1,048,576 device-resident vectors of D = 2049 (block-wise cascaded FWHT
+    with an overlap block)."""
+    import torch
+
+    import synth
+    import paper_2608_30384_amd as R
+
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+    D, POOL, N = 256, 1 << 27, 1 << 24
+    BLK = synth.TORCH_BLOCK
+    reps = 10
+    t_setup = time.time()
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(11)
+    ids = torch.randint(0, POOL, (N,), generator=gen, device=dev, dtype=torch.int64)
+    q = torch.from_numpy(synth.aniso(1, D, alpha=0.0, seed=77, normalize=True)).to(dev)
+    xb = torch.empty((BLK, D), dtype=torch.float32, device=dev)
+    codecs = [("Rslm1", 1, False), ("Rslm2", 2, False), ("Rslm3", 3, False), ("Rslm4", 4, False),
+              ("Rslm4Lite", 4, True)]
+    res = {}
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps * 1e-3
+    for name, bits, lite in codecs:
+        plan = R.Plan(D, bits, passes=-1, scale_mode="local", lite=lite)
+        rb = plan.record_bytes
+        pool = torch.empty((POOL, rb), dtype=torch.uint8, device=dev)
+        tiles = torch.empty(plan.code_bytes(BLK), dtype=torch.uint8, device=dev)
+        sc = torch.empty(BLK, dtype=torch.int32, device=dev)
+        for b in range(POOL // BLK):
+            synth.aniso_torch_block(b, D, alpha=0.0, seed=100, normalize=True, out=xb)
+            R.rslm_encode(plan, xb, tiles, sc)
+            pool[b * BLK:(b + 1) * BLK] = R.rslm_pack_records(plan, tiles, sc, BLK)
+        del tiles, sc
+        qrot = R.rslm_fwht(plan, q)
+        out = torch.empty((1, N), dtype=torch.float32, device=dev)
+        t_c = timed(lambda: R.rslm_score(plan, pool, qrot, n=N, out=out))
+        t_g = timed(lambda: R.rslm_score(plan, pool, qrot, ids=ids, out=out))
+        # 128-byte lines a gathered record touches, on average
+        off = (ids[: 1 << 20] * rb) % 128
+        lines = float(((off + rb + 127) // 128).float().mean().item())
+        res[name] = {
+            "record_bytes": rb,
+            "contiguous": {"M_items_per_s": N / t_c / 1e6, "GBps": N * rb / t_c / 1e9,
+                           "paper_M_items_per_s_milan_cascadelake":
+                               PAPER_ONETOMANY[name]["contiguous"]},
+            "largepool": {"M_items_per_s": N / t_g / 1e6, "record_GBps": N * rb / t_g / 1e9,
+                          "lines_per_record": lines,
+                          "line_GBps": N * lines * 128 / t_g / 1e9,
+                          "paper_M_items_per_s_milan_cascadelake":
+                              PAPER_ONETOMANY[name]["largepool"]},
+        }
+        log(f"{name}: {res[name]}")
+        del pool, out
+        torch.cuda.empty_cache()
+    del xb
+    # compress at D = 2049
+    D2, n2 = 2049, 1 << 20
+    plan = R.Plan(D2, 4, passes=-1, scale_mode="local")
+    x2 = synth.aniso_torch(n2, D2, alpha=0.0, seed=5, normalize=True, device=dev)
+    tiles = torch.empty(plan.code_bytes(n2), dtype=torch.uint8, device=dev)
+    sc = torch.empty(n2, dtype=torch.int32, device=dev)
+
+    def compress():
+        R.rslm_encode(plan, x2, tiles, sc)
+        R.rslm_pack_records(plan, tiles, sc, n2)
+    t_e = timed(compress)
+    out = {
+        "metric": "OneToMany scored items/s (D = 256) and Rslm4 compress items/s (D = 2049), 1 GPU",
+        "value": res["Rslm4"]["contiguous"]["M_items_per_s"] * 1e6, "unit": "items/s",
+        "n_gpus": 1, "higher_is_better": True, "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": ("codec microbenchmarks: one query vs 16,777,216 packed D=256 "
+                                "records, contiguous and gathered from a 134,217,728-record pool; "
+                                "Rslm4 compress of 1,048,576 vectors at D=2049"),
+                   "dim": D, "pool": POOL, "n": N, "queries": 1},
+        "onetomany": res,
+        "compress_2049": {"codec": "Rslm4", "vectors": n2, "ms": t_e * 1e3,
+                          "M_items_per_s": n2 / t_e / 1e6,
+                          "paper_M_items_per_s_milan": PAPER_COMPRESS_2049,
+                          "GBps": n2 * (4 * D2 + plan.record_bytes) / t_e / 1e9},
         "setup_s": time.time() - t_setup,
         "kernel_sources": csrc_hash(),
     }

@@ -276,7 +276,7 @@ __global__ void __launch_bounds__(kRescoreThreads) k_score(
     const uint8_t *rec = records + (valid ? r : 0) * int64_t(cp.record_bytes);
     float dot = 0.f;
     uint32_t sbits = 0u, gbits = 0u;
-    for (int G8 = gl; G8 < n_groups; G8 += 16) {
+    for (int G8 = gl; valid && G8 < n_groups; G8 += 16) {
       uint32_t bits = 0u;
       if (W * G8 + 4 <= cp.record_bytes) {
         bits = reinterpret_cast<const U32Unaligned *>(rec + W * G8)->v;
@@ -312,16 +312,129 @@ __global__ void __launch_bounds__(kRescoreThreads) k_score(
       }
     }
     if (gl == 0) {
-      uint32_t su, gu;
+      uint32_t su = 0u, gu = 0u;
       if (LITE) {
         su = sbits;
         gu = cp.global ? gbits : 0x7000u;
-      } else {
+      } else if (valid) {
         const uint8_t *sf = rec + cp.canon_bytes;
         su = uint32_t(sf[0]) | (uint32_t(sf[1]) << 8);
         gu = cp.global ? (uint32_t(sf[2]) | (uint32_t(sf[3]) << 8)) : 0x7000u;
       }
       out[int64_t(q) * n + j] = valid ? dec_ue4m12(gu) * (dec_ue7m9(su) * dot) : -__builtin_inff();
+    }
+  }
+}
+
+// The same scoring with the query held in registers (D <= 1024): lane j of a
+// record's 16 lanes always decodes the groups j + 16 k (k < 8 / G), so it
+// loads its q values once; per code: a field extract, one LDS lookup of the
+// 16-entry codebook (16 banks, broadcast-friendly) and G multiply-adds.
+// Each 16-lane group scores two records per pass with all loads issued first.
+template <int W, int G, bool LITE, int KMAX>
+__global__ void __launch_bounds__(kRescoreThreads) k_score_reg(
+    const uint8_t *__restrict__ records, int64_t n_pool, const int64_t *__restrict__ ids,
+    int64_t n, int64_t per_block, const float *__restrict__ q_rot, int dim, CodecParams cp,
+    float *__restrict__ out) {
+  // KMAX: groups per lane (n_groups <= 16 KMAX)
+  constexpr uint32_t kMask = (1u << W) - 1u;
+  __shared__ float cbs[16 * G], cbl[16];
+  const int q = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n_groups = (cp.n_sub + 7) / 8;
+  if (tid < 16 * G) cbs[tid] = (tid < (1 << W) * G) ? cp.cb[tid] : 0.f;
+  if (LITE && tid < 16) cbl[tid] = cp.cb_lead[tid & 7];
+  const int gl = lane & 15;
+  const float *qr = q_rot + int64_t(q) * dim;
+  float qv[KMAX][8 * G];
+#pragma unroll
+  for (int k = 0; k < KMAX; ++k)
+#pragma unroll
+    for (int t = 0; t < 8 * G; ++t) {
+      const int d = (gl + 16 * k) * 8 * G + t;
+      qv[k][t] = (d < dim) ? qr[d] : 0.f;
+    }
+  __syncthreads();
+  const int grp = wave * 4 + (lane >> 4);
+  const int64_t j0 = int64_t(blockIdx.x) * per_block;
+  const int64_t j1 = min(n, j0 + per_block);
+  constexpr int kGroups = kRescoreThreads / 16;
+  for (int64_t jb = j0 + grp; jb < j1; jb += 2 * kGroups) {
+    const uint8_t *rec[2];
+    bool valid[2];
+    uint32_t bits[2][KMAX];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int64_t j = jb + u * kGroups;
+      int64_t r = -1;
+      if (j < j1) r = ids ? ids[j] : j;
+      valid[u] = r >= 0 && r < n_pool;
+      rec[u] = records + (valid[u] ? r : 0) * int64_t(cp.record_bytes);
+#pragma unroll
+      for (int k = 0; k < KMAX; ++k) {
+        const int G8 = gl + 16 * k;
+        uint32_t b = 0u;
+        if (valid[u] && G8 < n_groups) {
+          if (W * G8 + 4 <= cp.record_bytes) {
+            b = reinterpret_cast<const U32Unaligned *>(rec[u] + W * G8)->v;
+          } else {
+#pragma unroll
+            for (int t = 0; t < W; ++t)
+              if (W * G8 + t < cp.canon_bytes) b |= uint32_t(rec[u][W * G8 + t]) << (8 * t);
+          }
+          if (W * G8 + W > cp.canon_bytes && cp.canon_bytes - W * G8 < 4)
+            b &= (1u << (8 * (cp.canon_bytes - W * G8))) - 1u;
+        }
+        bits[u][k] = b;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int64_t j = jb + u * kGroups;
+      float dot = 0.f;
+      uint32_t sbits = 0u, gbits = 0u;
+#pragma unroll
+      for (int k = 0; k < KMAX; ++k) {
+        uint32_t b = bits[u][k];
+        if (LITE && k == 0 && gl < cp.lead / 8) {
+          // leading coordinates: 3-bit codes on the K = 8 codebook, bit 3 a scale bit
+          uint32_t top = 0u;
+#pragma unroll
+          for (int c = 0; c < 8; ++c) top |= ((b >> (4 * c + 3)) & 1u) << c;
+          if (gl < 2) sbits = top << (8 * gl);
+          else gbits = top << (8 * (gl - 2));
+#pragma unroll
+          for (int c = 0; c < 8; ++c) dot = fmaf(qv[k][c], cbl[(b >> (4 * c)) & 7u], dot);
+          continue;
+        }
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+          const uint32_t code = (b >> (W * c)) & kMask;
+#pragma unroll
+          for (int t = 0; t < G; ++t) dot = fmaf(qv[k][c * G + t], cbs[code * G + t], dot);
+        }
+      }
+#pragma unroll
+      for (int off = 8; off >= 1; off >>= 1) {
+        dot += __shfl_xor(dot, off, 64);
+        if (LITE) {
+          sbits |= __shfl_xor(sbits, off, 64);
+          gbits |= __shfl_xor(gbits, off, 64);
+        }
+      }
+      if (gl == 0 && j < j1) {
+        uint32_t su = 0u, gu = 0u;
+        if (LITE) {
+          su = sbits;
+          gu = cp.global ? gbits : 0x7000u;
+        } else if (valid[u]) {
+          const uint8_t *sf = rec[u] + cp.canon_bytes;
+          su = uint32_t(sf[0]) | (uint32_t(sf[1]) << 8);
+          gu = cp.global ? (uint32_t(sf[2]) | (uint32_t(sf[3]) << 8)) : 0x7000u;
+        }
+        out[int64_t(q) * n + j] =
+            valid[u] ? dec_ue4m12(gu) * (dec_ue7m9(su) * dot) : -__builtin_inff();
+      }
     }
   }
 }
@@ -422,9 +535,30 @@ int rslm_score(const rslm_plan *p, const uint8_t *records, int64_t n_pool, const
   if (blocks > 0x7fffffff) return RSLM_ERR_INVALID_ARG;
   const dim3 grid(static_cast<unsigned>(blocks), static_cast<unsigned>(Q));
   hipStream_t s = as_stream(stream);
-#define RSLM_SCORE_CALL(W, G, LT)                                                             \
-  hipLaunchKernelGGL((k_score<W, G, LT>), grid, dim3(kRescoreThreads), shm, s, records, n_pool, \
-                     ids, n, per_block, q_rot, cp.D, cp, out)
+  // query in registers when every lane's groups fit (at most 8 / g groups of
+  // 8 codes per lane): the instantiated group counts 1, 2, 4, 6, 8
+  const int need = (n_groups + 15) / 16;
+  int ngl = 0;
+  for (int v : {1, 2, 4, 6, 8})
+    if (v >= need) {
+      ngl = v;
+      break;
+    }
+  if (ngl * cp.g > 8) ngl = 0;
+#define RSLM_SCORE_REG(W, G, LT, NG)                                                                \
+  hipLaunchKernelGGL((k_score_reg<W, G, LT, NG>), grid, dim3(kRescoreThreads), 0, s, records,       \
+                     n_pool, ids, n, per_block, q_rot, cp.D, cp, out)
+#define RSLM_SCORE_CALL(W, G, LT)                                                                   \
+  switch (ngl * int(8 / G >= ngl)) {                                                               \
+    case 1: RSLM_SCORE_REG(W, G, LT, 1); break;                                                    \
+    case 2: if (8 / G >= 2) RSLM_SCORE_REG(W, G, LT, (8 / G >= 2 ? 2 : 1)); break;                 \
+    case 4: if (8 / G >= 4) RSLM_SCORE_REG(W, G, LT, (8 / G >= 4 ? 4 : 1)); break;                 \
+    case 6: if (8 / G >= 6) RSLM_SCORE_REG(W, G, LT, (8 / G >= 6 ? 6 : 1)); break;                 \
+    case 8: if (8 / G >= 8) RSLM_SCORE_REG(W, G, LT, (8 / G >= 8 ? 8 : 1)); break;                 \
+    default:                                                                                       \
+      hipLaunchKernelGGL((k_score<W, G, LT>), grid, dim3(kRescoreThreads), shm, s, records, n_pool, \
+                         ids, n, per_block, q_rot, cp.D, cp, out);                                 \
+  }
   if (cp.lead > 0) {
     RSLM_SCORE_CALL(4, 1, true);
   } else {
@@ -436,6 +570,7 @@ int rslm_score(const rslm_plan *p, const uint8_t *records, int64_t n_pool, const
     }
   }
 #undef RSLM_SCORE_CALL
+#undef RSLM_SCORE_REG
   return check_launch();
 }
 

@@ -114,6 +114,8 @@ SCORE_CASES = [
     (101, 3, "global", False, 2000, 777, 2),
     (101, 4, "local", False, 1500, 300, 1),
     (1536, 1, "global", False, 600, 333, 2),
+    (2049, 4, "local", False, 300, 200, 2),     # query beyond the register path: LDS path
+    (1100, 4, "global", True, 300, 150, 1),     # Lite on the LDS path
 ]
 
 
