@@ -191,6 +191,19 @@ int rslm_encode_sq8(const rslm_plan *plan, const float *x, int64_t n_rows,
                     uint8_t *codes, uint32_t *scales, const float *sq8_lo,
                     const float *sq8_hi, uint8_t *codes2, void *stream);
 
+/* ------------------------------------------------------------------------
+ * rslm_decode -- Decompress (Section "Performance Impact and Memory
+ * Savings": Compress / Decompress; Section "Relative Quantization"): the
+ * reconstruction of record r (tile layout codes and scales as rslm_encode
+ * wrote them)
+ *   x~_r = g^ (c + R^T s^ C[code])      (g^ = 1.0 for a local plan)
+ * with c = centroids[rec_list[r]] when centroids is given, else 0; R^T runs
+ * the blocks in reverse order.  out: n x D float32.
+ * ------------------------------------------------------------------------ */
+int rslm_decode(const rslm_plan *plan, const uint8_t *codes, const uint32_t *scales, int64_t n,
+                const int32_t *rec_list, const float *centroids, int32_t nlist, float *out,
+                void *stream);
+
 /* Canonical <-> scan layout of packed codes (Section "Codecs Description":
  * codes are a packed bit stream, code j of a record at bits [w j, w j + w),
  * w = log2 K, little-endian).  canon: n x canon_bytes; tiles: ceil(n/16) *

@@ -22,7 +22,7 @@ EXPORTS = [
     "rslm_status_string", "rslm_last_hip_error", "rslm_version",
     "rslm_plan_create", "rslm_plan_destroy", "rslm_plan_get_info",
     "rslm_fwht", "rslm_encode", "rslm_encode_two_stage", "rslm_encode_sq8", "rslm_pack_codes",
-    "rslm_pack_records", "rslm_score", "rslm_unpack_codes",
+    "rslm_pack_records", "rslm_score", "rslm_decode", "rslm_unpack_codes",
     "ivf_assign_probe_workspace", "ivf_assign_probe",
     "rslm_scan_topk_workspace", "rslm_scan_topk",
     "rslm_sq8_fit", "rslm_sq8_encode", "rslm_rescore", "rslm_set_timer", "rslm_calibrate_read",
@@ -81,6 +81,7 @@ def _declare(lib):
         "rslm_pack_codes": (C.c_int, [P, P, I64, P, P]),
         "rslm_pack_records": (C.c_int, [P, P, P, I64, P, P]),
         "rslm_score": (C.c_int, [P, P, I64, P, I64, P, I32, P, P]),
+        "rslm_decode": (C.c_int, [P, P, P, I64, P, P, I32, P, P]),
         "rslm_unpack_codes": (C.c_int, [P, P, I64, P, P]),
         "ivf_assign_probe_workspace": (SZ, [I64, I32, I32, I32, C.c_int]),
         "ivf_assign_probe": (C.c_int, [P, I64, I32, P, I32, I32, C.c_int, P, P, P, SZ, P]),

@@ -206,6 +206,22 @@ def rslm_pack_codes(plan, canon, n, stream=None):
     return tiles
 
 
+def rslm_decode(plan, codes, scales, n, rec_list=None, centroids=None, out=None, stream=None):
+    """Reconstructions x~ = g^ (c + R^T s^ C[code]) of n records (n x dim)."""
+    _need(codes, torch.uint8, "codes")
+    _need(scales, torch.int32, "scales")
+    _need(rec_list, torch.int32, "rec_list")
+    _need(centroids, torch.float32, "centroids")
+    if out is None:
+        out = torch.empty((n, plan.dim), dtype=torch.float32, device=codes.device)
+    _need(out, torch.float32, "out")
+    nlist = centroids.shape[0] if centroids is not None else 0
+    L.check("rslm_decode", L.lib().rslm_decode(plan.handle, _ptr(codes), _ptr(scales), n,
+                                               _ptr(rec_list), _ptr(centroids), nlist, _ptr(out),
+                                               _stream(stream)))
+    return out
+
+
 def rslm_pack_records(plan, tiles, scales, n, stream=None):
     """Packed records (codes + scale suffix; Lite: codes alone), n x record_bytes."""
     _need(tiles, torch.uint8, "tiles")

@@ -452,6 +452,62 @@ __global__ void __launch_bounds__(256) k_encode(
   }
 }
 
+// --------------------------------------------------------------- rslm_decode
+// Decompress: x~ = g^ (c + R^T s^ C[code]) per record, one wavefront per
+// record through LDS: the decoded rotated residual s^ C[code] is placed in
+// the vector buffer, rotated back (blocks in reverse, inverse transpose, S1
+// last) and scaled.
+__global__ void __launch_bounds__(256) k_decode(const uint8_t *__restrict__ codes,
+                                                const uint32_t *__restrict__ scales, int64_t n,
+                                                const int32_t *__restrict__ rec_list,
+                                                const float *__restrict__ cen, int nlist,
+                                                float *__restrict__ out, RotParams rp,
+                                                CodecParams cp, int dstride) {
+  extern __shared__ float lds[];
+  __shared__ float cbs[64], cbl[8];
+  __shared__ int16_t pi[128];
+  if (threadIdx.x < 64) cbs[threadIdx.x] = cp.cb[threadIdx.x];
+  if (threadIdx.x < 8) cbl[threadIdx.x] = cp.cb_lead[threadIdx.x];
+  load_perm(rp, pi);   // includes the barrier that publishes cbs / cbl
+  const int lane = threadIdx.x & 63;
+  const int wid = threadIdx.x >> 6;
+  const int64_t rec = int64_t(blockIdx.x) * (blockDim.x >> 6) + wid;
+  if (rec >= n) return;   // no workgroup barriers below
+  float *v = lds + wid * 2 * dstride;
+  float *w = v + dstride;
+  const int D = rp.D, g = cp.g;
+  const uint32_t sc = scales[rec];
+  const float sh = dec_ue7m9(sc & 0xffffu);
+  const float gh = cp.global ? dec_ue4m12(sc >> 16) : 1.f;
+  int L = -1;
+  if (cen) {
+    L = rec_list[rec];
+    if (L < 0 || L >= nlist) L = -1;
+  }
+  const int per = 8 / g;   // sub-vectors per group of 8 coordinates
+#pragma unroll 4
+  for (int i = lane; i < D; i += kWave) {
+    const int j = i / g;             // sub-vector
+    const int G = j / per;           // group of 8 coordinates
+    uint32_t bits = 0;
+    for (int b = 0; b < cp.bits; ++b) bits |= uint32_t(codes[tile_byte_addr(rec, G, b, cp)]) << (8 * b);
+    const uint32_t code = (bits >> (cp.w * (j - G * per))) & ((1u << cp.w) - 1u);
+    const float c = (j < cp.lead) ? cbl[code & 7u] : cbs[code * g + (i % g)];
+    v[px(i)] = sh * c;
+  }
+  wave_sync();
+  const uint2 sm = lane_sign_masks(rp, lane);
+  const uint32_t s1out = (rp.passes > 0) ? sm.x : 0u;
+  const float *res = rotate_inverse(v, w, rp, pi, sm.y, lane);
+  const float *cr = (L >= 0) ? cen + int64_t(L) * D : nullptr;
+  float *orow = out + rec * D;
+#pragma unroll 4
+  for (int i = lane, t = 0; i < D; i += kWave, ++t) {
+    const float base = cr ? cr[i] : 0.f;
+    orow[i] = gh * (base + flip(res[px(i)], s1out, t));
+  }
+}
+
 // --------------------------------------------------------- pack / unpack
 // Group G of a record is the `bits` canonical bytes [G bits, G bits + bits).
 __global__ void k_pack(const uint8_t *__restrict__ canon, int64_t n, uint8_t *__restrict__ tiles,
@@ -633,6 +689,25 @@ int rslm_pack_codes(const rslm_plan *p, const uint8_t *canon, int64_t n, uint8_t
   const int64_t total = (n + 15) / 16 * 16 * (p->codec.d_pad / 8);
   hipLaunchKernelGGL(k_pack, dim3(unsigned(pack_grid(total))), dim3(256), 0, as_stream(stream),
                      canon, n, tiles, p->codec);
+  return check_launch();
+}
+
+int rslm_decode(const rslm_plan *p, const uint8_t *codes, const uint32_t *scales, int64_t n,
+                const int32_t *rec_list, const float *centroids, int32_t nlist, float *out,
+                void *stream) {
+  if (!p || n < 0) return RSLM_ERR_INVALID_ARG;
+  if (n == 0) return RSLM_OK;
+  if (!codes || !scales || !out) return RSLM_ERR_INVALID_ARG;
+  if (centroids && (!rec_list || nlist < 1)) return RSLM_ERR_INVALID_ARG;
+  const int D = p->rot.D;
+  const int dstride = lds_floats(D);
+  int waves = 4;
+  while (waves > 1 && size_t(waves) * 2 * dstride * 4 > 65536) waves >>= 1;
+  const size_t shm = size_t(waves) * 2 * dstride * sizeof(float);
+  const int64_t grid = (n + waves - 1) / waves;
+  if (grid > 0x7fffffff) return RSLM_ERR_INVALID_ARG;
+  hipLaunchKernelGGL(k_decode, dim3(unsigned(grid)), dim3(64 * waves), shm, as_stream(stream),
+                     codes, scales, n, rec_list, centroids, nlist, out, p->rot, p->codec, dstride);
   return check_launch();
 }
 

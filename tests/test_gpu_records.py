@@ -168,3 +168,38 @@ def test_lite_plan_is_rejected_by_the_ivf_scan(R):
     with pytest.raises(L.RslmError):
         R.rslm_scan_topk(plan, index, q, torch.zeros((1, 1), dtype=torch.int32, device=DEV),
                          torch.zeros((1, 1), dtype=torch.float32, device=DEV), 5)
+
+
+DECODE_CASES = [(768, 4, 2, "global", False), (96, 4, 2, "local", False), (101, 3, 2, "global", False),
+                (100, 1, 2, "global", False), (98, 2, 1, "local", False), (256, 4, 1, "global", True),
+                (2049, 4, 2, "local", False), (64, 2, 0, "global", False)]
+
+
+@pytest.mark.parametrize("D,bits,passes,mode,lite", DECODE_CASES)
+def test_decode_parity(R, D, bits, passes, mode, lite):
+    """rslm_decode (Decompress) against the oracle's reconstruction of the same
+    codes and scales: x~ = g^ (c + R^T s^ C[code])."""
+    n, nlist = 150, 5
+    x = synth.aniso(n, D, seed=D + bits)
+    cen = x[np.random.default_rng(D).choice(n, nlist, replace=False)] * 0.9
+    assign, _ = oracle.assign_l2(x, cen)
+    Rm = H.rot(D, passes)
+    C = synth.codebook(bits)
+    C8 = synth.codebook(3) if lite else None
+    lead = oracle.lite_lead(mode) if lite else 0
+    enc = oracle.encode(x, Rm, C, bits, centroids=cen[assign], scale_mode=mode, C_lead=C8)
+    ref = oracle.reconstruct(enc["codes"], enc["s_code"], enc["g_code"], C, Rm, cen[assign], C8,
+                             lead)
+    plan = R.Plan(D, bits, passes=passes, scale_mode=mode, lite=lite)
+    codes = enc["codes"].copy()
+    if lite:   # the scan layout carries the embedded scale bits as well
+        for j in range(lead):
+            w = enc["s_code"] if j < 16 else enc["g_code"]
+            codes[:, j] |= ((w.astype(np.int64) >> (j % 16)) & 1) << 3
+    tiles = R.rslm_pack_codes(plan, _t(oracle.pack_canonical(codes, bits)), n)
+    sc = (enc["s_code"].astype(np.uint32) | (enc["g_code"].astype(np.uint32) << 16)).view(np.int32)
+    got = R.rslm_decode(plan, tiles, _t(sc), n, rec_list=_t(assign, torch.int32),
+                        centroids=_t(cen.astype(np.float32))).cpu().numpy()
+    scale = np.maximum(np.linalg.norm(ref, axis=1), np.linalg.norm(cen[assign], axis=1))
+    err = np.abs(got - ref).max(1)
+    assert np.all(err <= 5e-6 * scale), (err / scale).max()
