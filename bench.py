@@ -55,6 +55,8 @@ def parse():
     ap.add_argument("--encode-chunk", type=int, default=65536)
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--lite", action="store_true",
+                    help="text768 workload with Rslm4Lite records (scales in the codes)")
     ap.add_argument("--workload", choices=("text768", "capacity", "sweep", "onetomany"),
                     default="text768",
                     help="text768 (default): the metric's configuration; capacity: 100M x 768 "
@@ -417,7 +419,7 @@ def main():
     cen = ivf.kmeans(x, nlist, iters=args.kmeans_iters, seed=0, sample=256 * nlist)
     torch.cuda.synchronize()
     log(f"k-means done in {time.time() - t0:.1f} s")
-    plan = R.Plan(D, args.bits, passes=-1, scale_mode="global")
+    plan = R.Plan(D, args.bits, passes=-1, scale_mode="global", lite=args.lite)
     resid = torch.empty_like(x)
     t0 = time.time()
     index, crot, assign = ivf.build_index(plan, x, cen, resid_rot=resid)
@@ -441,7 +443,7 @@ def main():
 
     batches = [q_all[i:i + args.batch].contiguous() for i in range(0, args.nq, args.batch)]
     sizes = index.list_sizes.long()
-    rec_bytes = D * args.bits // 8 + 4
+    rec_bytes = D * args.bits // 8 + (0 if args.lite else 4)
     # per-batch work, computed outside the timed region from the probe result
     work = []
     for qb in batches:
@@ -535,7 +537,8 @@ def main():
         "config": {
             "workload": (f"text-embedding shaped IVF scan: N={N:,} x d={D} anisotropic Gaussian "
                          f"(power-law spectrum, exponent 1, mean offset, unnormalised), "
-                         f"nlist={nlist}, {args.bits}-bit RSLM global scale + SQ8 rescore, "
+                         f"nlist={nlist}, {args.bits}-bit RSLM{'4Lite' if args.lite else ''} "
+                         f"global scale + SQ8 rescore, "
                          f"batches of {args.batch} queries, nprobe={args.nprobe}, "
                          f"top-{args.k} -> top-{args.k_out}; each step also encodes "
                          f"{args.encode_chunk:,} vectors"),
@@ -600,7 +603,7 @@ def main():
         "GBps": b2 / (t2 * 1e-3) / 1e9,
         "record_bytes": [rec_bytes, plan2.canon_bytes + 4],
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not args.lite:
         log("CPU oracle baseline")
         qb = batches[0]
         qrot, pid, pdot = step(0, [ev() for _ in range(6)])

@@ -272,7 +272,8 @@ typedef struct rslm_index {
   const int32_t *list_sizes;    /* nlist */
   const int32_t *ids;           /* per record */
   const uint8_t *codes;         /* scan tile layout */
-  const uint32_t *scales;       /* per record: lo16 s^ | hi16 g^ */
+  const uint32_t *scales;       /* per record: lo16 s^ | hi16 g^ (unused, may be
+                                   NULL, for Rslm4Lite plans) */
 } rslm_index;
 
 /* ------------------------------------------------------------------------
@@ -284,8 +285,8 @@ typedef struct rslm_index {
  * padded with (-inf, -1).
  *   q_rot: Q x D rotated queries (rslm_fwht); probe_ids / probe_dots:
  *   Q x nprobe; out_scores / out_ids: Q x k.  1 <= k <= 1024, Q <= 65535.
- *   D <= 1024; a Lite plan gives RSLM_ERR_UNSUPPORTED (score Lite records
- *   with rslm_score).
+ *   D <= 1024.  With a Lite plan the scales are read from the codes (the
+ *   index's scales array is not used and may be NULL).
  * ------------------------------------------------------------------------ */
 size_t rslm_scan_topk_workspace(const rslm_plan *plan, const rslm_index *index,
                                 int32_t Q, int32_t nprobe, int32_t k);

@@ -285,10 +285,10 @@ def reconstruct(codes, s_code, g_code, C, R, centroids=None, C_lead=None, lead=0
     return gh[:, None] * (base + rr @ R)
 
 
-def first_stage_rotated(codes, s_code, g_code, C, R, centroids=None):
+def first_stage_rotated(codes, s_code, g_code, C, R, centroids=None, C_lead=None, lead=0):
     """R a for the first-stage approximation a = x~1 = g^ (c + R^T s^ c^):
     R a = g^ (R c + s^ c^) (R is orthogonal), the base of the rescoring codec."""
-    rr = decode_rotated(codes, s_code, C, R.shape[0])
+    rr = decode_rotated(codes, s_code, C, R.shape[0], C_lead, lead)
     base = 0.0 if centroids is None else np.asarray(centroids, dtype=np.float64) @ R.T
     gh = np.array([dec_ue4m12(u) for u in g_code])
     return gh[:, None] * (base + rr)

@@ -134,10 +134,11 @@ def topk(scores, ids, k):
     return out_s, out_i
 
 
-def ivf_search(q, q_rot, centroids, lists, C, nprobe, k):
+def ivf_search(q, q_rot, centroids, lists, C, nprobe, k, C_lead=None, lead=0):
     """Route, scan (LUT route) and select for a batch of queries.
 
     ``lists[p]`` = dict(ids, codes (n_p, n_sub), s_hat (n_p,), g_hat (n_p,)).
+    Rslm4Lite: the first ``lead`` codes look up C_lead.
     Returns (scores (Q, k), ids (Q, k), probe ids (Q, nprobe)).
     """
     pid, pdot, _ = probe_ip(q, centroids, nprobe)
@@ -151,7 +152,7 @@ def ivf_search(q, q_rot, centroids, lists, C, nprobe, k):
             if len(L["ids"]) == 0:
                 continue
             all_s.append(scan_scores_lut(q_rot[i], pdot[i, j], L["codes"],
-                                         L["s_hat"], L["g_hat"], C))
+                                         L["s_hat"], L["g_hat"], C, C_lead, lead))
             all_i.append(L["ids"])
         if all_s:
             out_s[i], out_i[i] = topk(np.concatenate(all_s), np.concatenate(all_i), k)

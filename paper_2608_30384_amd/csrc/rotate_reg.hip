@@ -640,7 +640,7 @@ bool launch_encode_reg(const rslm_plan *p, const rslm_plan *p2, const float *x, 
     return false;
   if (s2 != 0 && p->codec.bits != 4) return false;
   const bool lite = p->codec.lead > 0;
-  if (lite && s2 != 0) return false;   // Lite with a second output: general path
+  if (lite && s2 == 1) return false;   // Lite with an RSLM second stage: general path
   // 16-byte vector loads and stores of every row
   if ((reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(cen) |
        reinterpret_cast<uintptr_t>(cen_rot) | reinterpret_cast<uintptr_t>(resid) |
@@ -660,6 +660,8 @@ bool launch_encode_reg(const rslm_plan *p, const rslm_plan *p2, const float *x, 
 #define CALL(J)                  \
   if (s2 == 1)                   \
     CALL_B((J) / 2, 4, 1);       \
+  else if (s2 == 2 && lite)      \
+    CALL_B((J) / 2, 4, 2, true); \
   else if (s2 == 2)              \
     CALL_B((J) / 2, 4, 2);       \
   else if (lite)                 \

@@ -299,6 +299,9 @@ struct ScanArgs {
   float *scores;
   int64_t stride;
   int nlist, nprobe, d_pad, n_chunks, tile_bytes, lane_units, max_list;
+  int lead;               // Rslm4Lite: leading coordinates on the K = 8 codebook (16 or 32)
+  int global;             // Rslm4Lite: the global scale is embedded too
+  float cb_lead[8];       // Rslm4Lite: the K = 8 codebook
 };
 
 template <int BITS> struct DecodeTab {
@@ -399,19 +402,53 @@ __device__ __forceinline__ void load_tile(uint32_t (&w)[W], const uint8_t *tiles
 // Decode one tile (16 candidates) and multiply it with the item's queries;
 // lane (kq, m) ends with rows 4 kq + {0,1,2,3} of candidate column m, i.e.
 // query slots 2 kq (hi, lo) and 2 kq + 1 (hi, lo).
-template <int BITS, int NC, int W>
+// Rslm4Lite, chunk 0 of a lead lane: the nibbles' low three bits index the
+// K = 8 codebook (a 256-entry table by byte symbol, not replicated: only this
+// chunk of these lanes reads it), bit 3 is a scale bit.
+__device__ __forceinline__ half8 decode8_lite(const uint32_t *ltab, uint32_t bits) {
+  union {
+    uint32_t u[4];
+    half8 h;
+  } r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) r.u[i] = ltab[(bits >> (8 * i)) & 0xffu];
+  return r.h;
+}
+
+// The top bit of each nibble of a 32-bit word, packed: bit i = bit 4 i + 3.
+__device__ __forceinline__ uint32_t nibble_tops(uint32_t w) {
+  uint32_t t = 0u;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) t |= ((w >> (4 * i + 3)) & 1u) << i;
+  return t;
+}
+
+template <int BITS, int NC, int W, bool LITE = false>
 __device__ __forceinline__ void score_tile(const uint32_t (&tw)[W], uint32_t sc,
                                            const half8 (&av)[NC], const uint32_t *dtab,
                                            uint32_t lane4, int lt, int n_cand, int m,
                                            const bool (&ok)[2],
                                            const float (&qc)[2], const float (&qi)[2],
-                                           float *const (&out)[2]) {
+                                           float *const (&out)[2],
+                                           const uint32_t *ltab = nullptr, bool lead_lane = false,
+                                           int global = 0) {
   // Decoding runs two chunks ahead of the matrix multiply so that the LDS
   // latency of chunk c + 2 overlaps the MFMAs of chunks c and c + 1; even and
   // odd chunks accumulate separately to halve the dependent MFMA chain.
   floatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
   half8 b[3];
-  b[0] = decode8<BITS>(dtab, chunk_bits<BITS>(tw, 0), lane4);
+  if (LITE) {
+    // scales from the code stream: lane (kq, m) holds 8 scale bits of
+    // candidate m in chunk 0 (kq 0, 1: s^; kq 2, 3: g^)
+    const uint32_t t = nibble_tops(chunk_bits<BITS>(tw, 0));
+    const uint32_t t0 = __shfl(int(t), m, 64), t1 = __shfl(int(t), 16 + m, 64);
+    const uint32_t t2 = __shfl(int(t), 32 + m, 64), t3 = __shfl(int(t), 48 + m, 64);
+    sc = (t0 | (t1 << 8)) | ((global ? (t2 | (t3 << 8)) : 0x7000u) << 16);
+    b[0] = lead_lane ? decode8_lite(ltab, chunk_bits<BITS>(tw, 0))
+                     : decode8<BITS>(dtab, chunk_bits<BITS>(tw, 0), lane4);
+  } else {
+    b[0] = decode8<BITS>(dtab, chunk_bits<BITS>(tw, 0), lane4);
+  }
   if (NC > 1) b[1] = decode8<BITS>(dtab, chunk_bits<BITS>(tw, NC > 1 ? 1 : 0), lane4);
 #pragma unroll
   for (int c = 0; c < NC; ++c) {
@@ -429,10 +466,20 @@ __device__ __forceinline__ void score_tile(const uint32_t (&tw)[W], uint32_t sc,
   }
 }
 
-template <int BITS, int NC>
+template <int BITS, int NC, bool LITE = false>
 __global__ void __launch_bounds__(kScanThreads) k_scan(ScanArgs a) {
   using T = DecodeTab<BITS>;
   __shared__ uint32_t dtab[T::kEntries * 64 * T::kWords];
+  __shared__ uint32_t ltab[LITE ? 256 : 1];
+  if (LITE) {   // Rslm4Lite chunk-0 table: byte -> half2(C8[lo & 7], C8[hi & 7])
+    const int e = threadIdx.x;   // kScanThreads == 256 entries
+    const _Float16 lo = static_cast<_Float16>(a.cb_lead[e & 7]);
+    const _Float16 hi = static_cast<_Float16>(a.cb_lead[(e >> 4) & 7]);
+    uint16_t lb, hb;
+    __builtin_memcpy(&lb, &lo, 2);
+    __builtin_memcpy(&hb, &hi, 2);
+    ltab[e] = uint32_t(lb) | (uint32_t(hb) << 16);
+  }
   constexpr int kWordsPerLane = ((NC * BITS + 15) / 16) * 4;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -521,12 +568,16 @@ __global__ void __launch_bounds__(kScanThreads) k_scan(ScanArgs a) {
     // j < 16), loaded before any code tile: lane (kq, m) holds candidate m of
     // tiles j = kq, kq + 4, kq + 8, kq + 12.  Issued first, they never make
     // the tile loop wait for code tiles still in flight.
-    const __amdgpu_buffer_rsrc_t rs = make_rsrc(a.scales + rec0, uint32_t(n_cand) * 4u);
+    // (Rslm4Lite: the scales are in the code stream; no scales array read.)
+    const __amdgpu_buffer_rsrc_t rs =
+        make_rsrc(LITE ? static_cast<const void *>(a.codes) : static_cast<const void *>(a.scales + rec0),
+                  LITE ? 0u : uint32_t(n_cand) * 4u);
     uint32_t sreg[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r)
-      sreg[r] = __builtin_amdgcn_raw_buffer_load_b32(
-          rs, uint32_t((wave + nwaves * (kq + 4 * r)) * 16 + m) * 4u, 0, 0);
+      sreg[r] = LITE ? 0u : __builtin_amdgcn_raw_buffer_load_b32(
+                                rs, uint32_t((wave + nwaves * (kq + 4 * r)) * 16 + m) * 4u, 0, 0);
+    const bool lead_lane = LITE && kq < a.lead / 8;
     auto scale_of = [&](int j) {   // j is uniform across the wave
       const int r = j >> 2;
       const uint32_t v = r == 0 ? sreg[0] : r == 1 ? sreg[1] : r == 2 ? sreg[2] : sreg[3];
@@ -541,12 +592,16 @@ __global__ void __launch_bounds__(kScanThreads) k_scan(ScanArgs a) {
     load_tile(bufA, tiles, lt, n_tiles, tb, voff);
     while (lt < n_tiles) {
       load_tile(bufB, tiles, lt + nwaves, n_tiles, tb, voff);
-      score_tile<BITS, NC>(bufA, scale_of(j), av, dtab, lane4, lt, n_cand, m, ok, qc, qi, out);
+      score_tile<BITS, NC, kWordsPerLane, LITE>(bufA, LITE ? 0u : scale_of(j), av, dtab, lane4, lt,
+                                                n_cand, m, ok, qc, qi, out, ltab, lead_lane,
+                                                a.global);
       lt += nwaves;
       ++j;
       if (lt >= n_tiles) break;
       load_tile(bufA, tiles, lt + nwaves, n_tiles, tb, voff);
-      score_tile<BITS, NC>(bufB, scale_of(j), av, dtab, lane4, lt, n_cand, m, ok, qc, qi, out);
+      score_tile<BITS, NC, kWordsPerLane, LITE>(bufB, LITE ? 0u : scale_of(j), av, dtab, lane4, lt,
+                                                n_cand, m, ok, qc, qi, out, ltab, lead_lane,
+                                                a.global);
       lt += nwaves;
       ++j;
     }
@@ -823,20 +878,23 @@ static int cu_count() {
   return cached[dev];
 }
 
-template <int BITS>
+template <int BITS, bool LITE = false>
 static void launch_scan_bits(int nc, dim3 grid, hipStream_t s, const ScanArgs &a) {
+#define RSLM_SCAN_NC(NCV) \
+  hipLaunchKernelGGL((k_scan<BITS, NCV, LITE>), grid, dim3(kScanThreads), 0, s, a)
   switch (nc) {
-    case 1: hipLaunchKernelGGL((k_scan<BITS, 1>), grid, dim3(kScanThreads), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((k_scan<BITS, 2>), grid, dim3(kScanThreads), 0, s, a); break;
-    case 3: hipLaunchKernelGGL((k_scan<BITS, 3>), grid, dim3(kScanThreads), 0, s, a); break;
-    case 4: hipLaunchKernelGGL((k_scan<BITS, 4>), grid, dim3(kScanThreads), 0, s, a); break;
-    case 6: hipLaunchKernelGGL((k_scan<BITS, 6>), grid, dim3(kScanThreads), 0, s, a); break;
-    case 8: hipLaunchKernelGGL((k_scan<BITS, 8>), grid, dim3(kScanThreads), 0, s, a); break;
-    case 12: hipLaunchKernelGGL((k_scan<BITS, 12>), grid, dim3(kScanThreads), 0, s, a); break;
-    case 16: hipLaunchKernelGGL((k_scan<BITS, 16>), grid, dim3(kScanThreads), 0, s, a); break;
-    case 24: hipLaunchKernelGGL((k_scan<BITS, 24>), grid, dim3(kScanThreads), 0, s, a); break;
-    default: hipLaunchKernelGGL((k_scan<BITS, 32>), grid, dim3(kScanThreads), 0, s, a); break;
+    case 1: RSLM_SCAN_NC(1); break;
+    case 2: RSLM_SCAN_NC(2); break;
+    case 3: RSLM_SCAN_NC(3); break;
+    case 4: RSLM_SCAN_NC(4); break;
+    case 6: RSLM_SCAN_NC(6); break;
+    case 8: RSLM_SCAN_NC(8); break;
+    case 12: RSLM_SCAN_NC(12); break;
+    case 16: RSLM_SCAN_NC(16); break;
+    case 24: RSLM_SCAN_NC(24); break;
+    default: RSLM_SCAN_NC(32); break;
   }
+#undef RSLM_SCAN_NC
 }
 
 }  // namespace rslm
@@ -865,10 +923,9 @@ int rslm_scan_topk(const rslm_plan *p, const rslm_index *idx, const float *q_rot
   if (Q == 0) return RSLM_OK;
   if (Q > 65535) return RSLM_ERR_INVALID_ARG;   // gridDim.y of the top-k kernel
   if (!q_rot || !probe_ids || !probe_dots || !out_scores || !out_ids || !idx->list_offsets ||
-      !idx->list_sizes || !idx->ids || !idx->codes || !idx->scales)
+      !idx->list_sizes || !idx->ids || !idx->codes || (!idx->scales && p->codec.lead == 0))
     return RSLM_ERR_INVALID_ARG;
   if (p->codec.n_chunks > 32) return RSLM_ERR_UNSUPPORTED;   // D > 1024
-  if (p->codec.lead > 0) return RSLM_ERR_UNSUPPORTED;         // Rslm4Lite: rslm_score only
   const size_t need = rslm_scan_topk_workspace(p, idx, Q, nprobe, k);
   if (!ws || ws_bytes < need) return RSLM_ERR_WORKSPACE;
   const int nlist = idx->nlist;
@@ -923,11 +980,17 @@ int rslm_scan_topk(const rslm_plan *p, const rslm_index *idx, const float *q_rot
   a.tile_bytes = p->codec.tile_bytes;
   a.lane_units = p->codec.lane_bytes / 16;
   a.max_list = idx->max_list_size;
+  a.lead = p->codec.lead;
+  a.global = p->codec.global;
+  for (int i = 0; i < 8; ++i) a.cb_lead[i] = p->codec.cb_lead[i];
   const int wg_per_cu = (p->codec.bits == 4) ? 2 : 4;
   const dim3 grid(unsigned(cu_count() * wg_per_cu));
   if ((st = record_timer(0, 0, s))) return st;
   switch (p->codec.bits) {
-    case 4: launch_scan_bits<4>(a.n_chunks, grid, s, a); break;
+    case 4:
+      if (a.lead > 0) launch_scan_bits<4, true>(a.n_chunks, grid, s, a);
+      else launch_scan_bits<4>(a.n_chunks, grid, s, a);
+      break;
     case 3: launch_scan_bits<3>(a.n_chunks, grid, s, a); break;
     case 2: launch_scan_bits<2>(a.n_chunks, grid, s, a); break;
     default: launch_scan_bits<1>(a.n_chunks, grid, s, a); break;

@@ -156,18 +156,16 @@ def test_score_parity(R, D, bits, mode, lite, n_pool, n, Q):
         assert np.all(np.abs(got[i, 3:] - ref[i][sel]) <= tol)
 
 
-def test_lite_plan_is_rejected_by_the_ivf_scan(R):
+def test_lite_plan_is_rejected_by_the_rslm_rescoring_codec(R):
+    """A Lite plan as the rescoring codec is not supported (status, no launch)."""
     from paper_2608_30384_amd import _lib as L
-    plan = R.Plan(256, 4, passes=1, scale_mode="local", lite=True)
-    n = 32
-    codes = torch.zeros(plan.code_bytes(n), dtype=torch.uint8, device=DEV)
-    index = R.Index(_t(np.array([0], np.int64)), _t(np.array([n], np.int32)),
-                    _t(np.arange(n, dtype=np.int32)), codes,
-                    torch.zeros(n, dtype=torch.int32, device=DEV))
+    plan = R.Plan(256, 4, passes=0, scale_mode="global", lite=True)
+    codes2 = torch.zeros((4, plan.canon_bytes), dtype=torch.uint8, device=DEV)
+    scales2 = torch.zeros(4, dtype=torch.int32, device=DEV)
     q = torch.zeros((1, 256), dtype=torch.float32, device=DEV)
     with pytest.raises(L.RslmError):
-        R.rslm_scan_topk(plan, index, q, torch.zeros((1, 1), dtype=torch.int32, device=DEV),
-                         torch.zeros((1, 1), dtype=torch.float32, device=DEV), 5)
+        R.rslm_rescore_rslm(plan, codes2, scales2, q, torch.zeros((1, 2), device=DEV),
+                            torch.zeros((1, 2), dtype=torch.int32, device=DEV), 1)
 
 
 DECODE_CASES = [(768, 4, 2, "global", False), (96, 4, 2, "local", False), (101, 3, 2, "global", False),
@@ -203,3 +201,55 @@ def test_decode_parity(R, D, bits, passes, mode, lite):
     scale = np.maximum(np.linalg.norm(ref, axis=1), np.linalg.norm(cen[assign], axis=1))
     err = np.abs(got - ref).max(1)
     assert np.all(err <= 5e-6 * scale), (err / scale).max()
+
+
+@pytest.mark.parametrize("D,passes,mode,k", [(768, 2, "global", 100), (256, 1, "local", 10),
+                                             (128, 1, "global", 25)])
+def test_lite_ivf_scan_parity(R, D, passes, mode, k):
+    """The IVF scan over Rslm4Lite records (scales read from the codes; no
+    scales array) against the oracle's IVF search with the K = 8 leading
+    codebook."""
+    n, nlist, Q, nprobe = 2500, 9, 20, 3
+    x = synth.aniso(n, D, seed=D + 11)
+    cen = oracle.kmeans(x[:600], nlist, iters=4, seed=1)
+    assign, _ = oracle.assign_l2(x, cen)
+    Rm = H.rot(D, passes)
+    C16, C8 = synth.codebook(4), synth.codebook(3)
+    lead = oracle.lite_lead(mode)
+    enc = oracle.encode(x, Rm, C16, 4, centroids=cen[assign], scale_mode=mode, C_lead=C8)
+    # records of the lists, padded to whole tiles, codes with the embedded scales
+    recs = oracle.pack_records(enc["codes"], enc["s_code"], enc["g_code"], 4, mode, lite=True)
+    counts = np.bincount(assign, minlength=nlist)
+    padded = (counts + 15) // 16 * 16
+    offsets = np.concatenate([[0], np.cumsum(padded)[:-1]]).astype(np.int64)
+    total = int(padded.sum())
+    canon = np.zeros((total, recs.shape[1]), dtype=np.uint8)
+    ids = np.full(total, -1, dtype=np.int32)
+    fill = offsets.copy()
+    for row in range(n):
+        L = assign[row]
+        canon[fill[L]] = recs[row]
+        ids[fill[L]] = row
+        fill[L] += 1
+    plan = R.Plan(D, 4, passes=passes, scale_mode=mode, lite=True)
+    tiles = R.rslm_pack_codes(plan, _t(canon), total)
+    index = R.Index(_t(offsets), _t(counts.astype(np.int32)), _t(ids), tiles,
+                    torch.zeros(1, dtype=torch.int32, device=DEV))
+    sh, gh = H.dec_scales(enc["s_code"].astype(np.uint32) | (enc["g_code"].astype(np.uint32) << 16))
+    lists = {L: {"ids": np.where(assign == L)[0], "codes": enc["codes"][assign == L],
+                 "s_hat": sh[assign == L], "g_hat": gh[assign == L]} for L in range(nlist)}
+    q = synth.queries_like("aniso", Q, D, data_seed=D + 11, query_seed=3)
+    qr = q.astype(np.float64) @ Rm.T
+    ref_s, ref_i, pid = oracle.ivf_search(q, qr, cen, lists, C16, nprobe, k, C8, lead)
+    pdot = (q.astype(np.float64) @ cen.T)[np.arange(Q)[:, None], pid]
+    gs, gi = R.rslm_scan_topk(plan, index, _t(qr.astype(np.float32)), _t(pid, torch.int32),
+                              _t(pdot.astype(np.float32)), k)
+    gs, gi = gs.cpu().numpy(), gi.cpu().numpy()
+    xt = oracle.reconstruct(enc["codes"], enc["s_code"], enc["g_code"], C16, Rm, cen[assign], C8,
+                            lead)
+    xn = np.linalg.norm(xt, axis=1).max()
+    diffs = 0
+    for i in range(Q):
+        tol = H.score_tol(ref_s[i], np.linalg.norm(q[i]), xn)
+        diffs += H.check_topk(gs[i], gi[i], ref_s[i], ref_i[i], np.where(np.isfinite(tol), tol, 0))
+    assert diffs <= max(1, Q // 10)

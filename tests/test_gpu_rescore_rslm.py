@@ -176,8 +176,9 @@ def test_rescore_rslm_parity(R, D, bits2, k_in, k_out):
         H.check_topk(gs[i], gi[i], ref_s[i], ref_i[i], np.where(np.isfinite(tol), tol, 0))
 
 
-@pytest.mark.parametrize("D,passes,n", [(768, 2, 500), (256, 1, 300), (96, 2, 333)])
-def test_encode_sq8_parity(R, D, passes, n):
+@pytest.mark.parametrize("D,passes,n,lite", [(768, 2, 500, False), (256, 1, 300, False),
+                                             (96, 2, 333, False), (768, 2, 400, True)])
+def test_encode_sq8_parity(R, D, passes, n, lite):
     """rslm_encode_sq8: SQ8 codes of the rotated second residual written in the
     encoding pass, against the oracle's residual R x - R a quantised with the
     same float32 ranges; rows whose first stage agrees must match except at
@@ -188,13 +189,16 @@ def test_encode_sq8_parity(R, D, passes, n):
     assign, _ = oracle.assign_l2(x, cen)
     Rm = H.rot(D, passes)
     C = synth.codebook(4)
-    ref = oracle.encode(x, Rm, C, 4, centroids=cen[assign], scale_mode="global")
-    ra = oracle.first_stage_rotated(ref["codes"], ref["s_code"], ref["g_code"], C, Rm, cen[assign])
+    C8 = synth.codebook(3) if lite else None
+    lead = oracle.lite_lead("global") if lite else 0
+    ref = oracle.encode(x, Rm, C, 4, centroids=cen[assign], scale_mode="global", C_lead=C8)
+    ra = oracle.first_stage_rotated(ref["codes"], ref["s_code"], ref["g_code"], C, Rm, cen[assign],
+                                    C8, lead)
     r2 = x.astype(np.float64) @ Rm.T - ra
     lo, hi = oracle.sq8_fit(r2)
     lo32, hi32 = lo.astype(np.float32), hi.astype(np.float32)
     ref2 = oracle.sq8_encode(r2, lo32.astype(np.float64), hi32.astype(np.float64))
-    plan = R.Plan(D, 4, passes=passes, scale_mode="global")
+    plan = R.Plan(D, 4, passes=passes, scale_mode="global", lite=lite)
     xt, ct = _t(x), _t(cen.astype(np.float32))
     crot = R.rslm_fwht(plan, ct)
     codes = torch.zeros(plan.code_bytes(n), dtype=torch.uint8, device=DEV)
@@ -203,6 +207,8 @@ def test_encode_sq8_parity(R, D, passes, n):
     R.rslm_encode_sq8(plan, xt, codes, scales, _t(lo32), _t(hi32), codes2,
                       rec_list=_t(assign, torch.int32), centroids=ct, centroids_rot=crot)
     g1 = oracle.unpack_canonical(R.rslm_unpack_codes(plan, codes, n).cpu().numpy(), 4, D)
+    if lite:
+        g1[:, :lead] &= 7   # drop the embedded scale bits
     sc = scales.cpu().numpy().astype(np.uint32)
     same = ((g1 == ref["codes"]).all(1) & ((sc & 0xFFFF) == ref["s_code"]) &
             ((sc >> 16) == ref["g_code"]))
