@@ -154,7 +154,7 @@ def counter_summary(a_csv, b_csv, n_steps=5):
     kern = [("k_scan<", "scan (a3+a4)"), ("k_topk_stream", "top-k (a5)"),
             ("k_dots_direct", "probe dots (a2)"), ("k_probe_select_reg", "probe selection (a2)"),
             ("k_rotate_reg", "query rotation (a1)"), ("k_rescore_sq8", "rescore (a6)"),
-            ("k_encode_rows", "encode (a7)")]
+            ("k_encode_rows<6, 4, 2,", "encode with SQ8 codes (a7)")]
 
     def avg(d, part):
         ds = [v for (i, n), v in d.items() if part in n][-n_steps:]
@@ -185,7 +185,7 @@ def counter_summary(a_csv, b_csv, n_steps=5):
         mfma = b["SQ_VALU_MFMA_BUSY_CYCLES"] / 1024 / cyc
         lds_conf = a["SQ_LDS_BANK_CONFLICT"] / max(b["SQ_ACTIVE_INST_LDS"], 1)
         wait = a["SQ_WAIT_INST_ANY"] / max(a["SQ_WAVE_CYCLES"], 1)
-        out.append(f"| {label} `{part.rstrip('<')}` | {cyc:,.0f} | {waves:,.0f} | "
+        out.append(f"| {label} `{part.split('<')[0]}` | {cyc:,.0f} | {waves:,.0f} | "
                    f"{a['SQ_INSTS_VALU'] / waves:,.0f} | {100 * valu_busy:.0f}% | "
                    f"{100 * lane_use:.0f}% | {100 * mfma:.0f}% | "
                    f"{a['SQ_INSTS_LDS'] / waves:,.0f} | {100 * lds_conf:.1f}% | {100 * wait:.0f}% |")
