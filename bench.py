@@ -603,6 +603,27 @@ def main():
         "GBps": b2 / (t2 * 1e-3) / 1e9,
         "record_bytes": [rec_bytes, plan2.canon_bytes + 4],
     }
+    # quality of what the step returns, outside the timed region: recall@10
+    # of the rescored top-k_out and of the scan's own first k_out, against
+    # exact float32 MIPS over the raw vectors (torch matmul on the device:
+    # the reference of a quality figure, not of a kernel)
+    hits_final = hits_scan = nq_rec = 0
+    for b in range(min(2, len(batches))):
+        qb = batches[b]
+        qrot = R.rslm_fwht(plan, qb)
+        pid, pdot = R.ivf_assign_probe(qb, cen, args.nprobe, R.IVF_PROBE_IP)
+        s1, i1 = R.rslm_scan_topk(plan, index, qrot, pid, pdot, args.k, ws=ws_scan)
+        _, i2 = R.rslm_rescore(codes2, lo, hi, qrot, s1, i1, args.k_out)
+        ex = torch.topk(torch.matmul(qb, x.T), args.k_out, dim=1).indices.int()
+        hits_final += int((i2[:, :, None] == ex[:, None, :]).any(2).sum().item())
+        hits_scan += int((i1[:, :args.k_out, None] == ex[:, None, :]).any(2).sum().item())
+        nq_rec += qb.shape[0]
+    out["quality"] = {
+        "queries": nq_rec,
+        f"recall_at_{args.k_out}": hits_final / (nq_rec * args.k_out),
+        f"recall_at_{args.k_out}_scan_only": hits_scan / (nq_rec * args.k_out),
+        "reference": "exact float32 inner products over the raw vectors (torch matmul)",
+    }
     if not args.no_cpu_baseline and not args.lite:
         log("CPU oracle baseline")
         qb = batches[0]
@@ -675,7 +696,8 @@ def run_capacity(args):
     cen = ivf.kmeans(sample, nlist, iters=args.kmeans_iters, seed=0)
     del sample
     torch.cuda.synchronize()
-    log(f"k-means done at {time.time() - t_setup:.0f} s; assigning {N} rows")
+    t_km = time.time()
+    log(f"k-means done at {t_km - t_setup:.0f} s; assigning {N} rows")
     assign = torch.empty(N, dtype=torch.int32, device=dev)
     for b in range(nblk):
         xs = block(b)
@@ -684,7 +706,8 @@ def run_capacity(args):
             torch.cuda.synchronize()
             log(f"  assigned {min(N, (b + 1) * BLK)} rows at {time.time() - t_setup:.0f} s")
     torch.cuda.synchronize()
-    log(f"assignment done at {time.time() - t_setup:.0f} s")
+    t_as = time.time()
+    log(f"assignment done at {t_as - t_setup:.0f} s")
     crot = R.rslm_fwht(plan, cen)
     offsets, sizes, src_row, rec_list, ids, total = ivf.layout(assign, nlist)
     del assign
@@ -705,7 +728,8 @@ def run_capacity(args):
     index = R.Index(offsets, sizes, ids, codes, scales)
     resident = (codes.numel() + scales.numel() * 4 + codes2.numel() + scales2.numel() * 4 +
                 ids.numel() * 4)
-    log(f"index built at {time.time() - t_setup:.0f} s: {total} records, max list "
+    t_built = time.time()
+    log(f"index built at {t_built - t_setup:.0f} s: {total} records, max list "
         f"{index.max_list_size}, {resident / 1e9:.1f} GB resident")
 
     # bulk two-stage encode rate on one device-resident block (records = rows)
@@ -787,7 +811,12 @@ def run_capacity(args):
         "encode_two_stage": {"vectors": BLK, "ms": t_enc, "vectors_per_s": BLK / (t_enc * 1e-3),
                              "GBps": BLK * (4 * D + rec_bytes + plan2.canon_bytes + 4) /
                              (t_enc * 1e-3) / 1e9},
-        "build_s": time.time() - t_setup,
+        "build_s": t_built - t_setup,
+        "build_phases_s": {
+            "kmeans": t_km - t_setup, "assign": t_as - t_km, "layout_and_encode": t_built - t_as,
+            "kmeans_rows": min(N, 256 * nlist), "kmeans_iters": args.kmeans_iters,
+            "assign_TFLOPs": 2.0 * N * D * nlist / (t_as - t_km) / 1e12,
+        },
         "kernel_sources": csrc_hash(),
     }
     print(json.dumps(out), flush=True)

@@ -3,12 +3,12 @@
 // (paper, Section "End-to-End Comparison", Setup: Euclidean partitions,
 // routing by the dot product with the centres).
 //
-// Both modes are a dense [n x D] x [D x nlist] contraction in float32.
-// Probing runs it on the matrix cores (v_mfma_f32_16x16x4_f32, 32 x 32 output
-// tiles), writes the dots and selects the top-nprobe per row.  Assignment
-// uses a 64 x 64 tile with 4 x 4 outputs per thread and keeps a running
-// (distance, id) minimum per row across all column tiles, never writing the
-// product.
+// Both modes are a dense [n x D] x [D x nlist] contraction in float32 on the
+// matrix cores (v_mfma_f32_16x16x4_f32).  Probing writes the dots (32 x 32
+// output tiles) and selects the top-nprobe per row.  Assignment keeps a
+// running (distance, id) minimum per row across all centre tiles (128 x 128
+// output tiles), never writing the product; rows that are not whole 16-byte
+// runs take a vector-ALU tile (64 x 64, 4 x 4 outputs per thread) instead.
 #include "rslm_internal.h"
 #include "select_dev.h"
 
@@ -192,6 +192,189 @@ __global__ void __launch_bounds__(256) k_dots_mfma(const float *__restrict__ x, 
     const int c = c0 + wc + ml;
     if (r < n && c < nlist) dots[r * nlist + c] = acc[i];
   }
+}
+
+// Assignment on the matrix cores (v_mfma_f32_16x16x4f32, full float32) for
+// D a multiple of 4 and 16-byte aligned operands.  A workgroup owns 128 rows
+// and walks the centres in tiles of 128, in increasing order; each of its
+// four wavefronts computes a 64 x 64 block of the product as 4 x 4 MFMA tiles.
+// The reduction index is staged through LDS in slabs of 32 (rows padded to 36
+// floats, so that the 16-byte operand reads of eight consecutive lanes fall
+// on distinct banks) and the next slab is fetched into registers while the
+// current one is multiplied.  Within a half slab of 16 both operands use the
+// same permutation of k: lane (m, h) (m = lane % 16, h = lane / 16) supplies
+// k = 4 h + t to MFMA step t, so one 16-byte read covers four steps.  After
+// each centre tile the distances ||c||^2 - 2 <x, c> update a (distance, id)
+// minimum per row and lane (centres visited in increasing order with a
+// strict comparison, so the smallest id wins a tie); lanes and the two
+// wavefronts sharing a row are merged lexicographically at the end.
+constexpr int kAM = 128, kAN = 128, kAK = 32, kAS = kAK + 4;
+
+__device__ __forceinline__ float4 ld4_or_zero(const float *p, bool in) {
+  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (in) v = *reinterpret_cast<const float4 *>(p);
+  return v;
+}
+
+__global__ void __launch_bounds__(256) k_assign_mfma(const float *__restrict__ x, int64_t n,
+                                                     int D, const float *__restrict__ cen,
+                                                     int nlist, const float *__restrict__ cnorm,
+                                                     int32_t *__restrict__ out_ids,
+                                                     float *__restrict__ out_d) {
+  __shared__ float As[kAM][kAS];
+  __shared__ float Bs[kAN][kAS];
+  __shared__ float red_v[kAM];
+  __shared__ int32_t red_i[kAM];
+  __shared__ float xx_s[kAM];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wr = (wave >> 1) * 64, wc = (wave & 1) * 64;
+  const int m = lane & 15, h = lane >> 4;
+  const int64_t r0 = int64_t(blockIdx.x) * kAM;
+  // staging: thread t moves the float4s (row t / 8 + 32 u, column 4 (t % 8)),
+  // u = 0..3, of a 128 x 32 slab; rows past the end are clamped (their
+  // products are computed and never used)
+  const int srow = tid >> 3, scol = (tid & 7) * 4;
+  int64_t aoff[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int64_t r = r0 + srow + 32 * u;
+    aoff[u] = (r < n ? r : n - 1) * D + scol;
+  }
+  float best[16];
+  int32_t bid[16];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    best[r] = 3.4e38f;
+    bid[r] = 0x7fffffff;
+  }
+  const int nslab = (D + kAK - 1) / kAK;
+  for (int c0 = 0; c0 < nlist; c0 += kAN) {
+    int64_t boff[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) boff[u] = int64_t(min(c0 + srow + 32 * u, nlist - 1)) * D + scol;
+    floatx4_t acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+    float4 pa[4], pb[4];
+    const bool in0 = scol < D;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      pa[u] = ld4_or_zero(x + aoff[u], in0);
+      pb[u] = ld4_or_zero(cen + boff[u], in0);
+    }
+    for (int sl = 0; sl < nslab; ++sl) {
+      __syncthreads();   // the previous slab's operand reads are done
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        *reinterpret_cast<float4 *>(&As[srow + 32 * u][scol]) = pa[u];
+        *reinterpret_cast<float4 *>(&Bs[srow + 32 * u][scol]) = pb[u];
+      }
+      __syncthreads();
+      if (sl + 1 < nslab) {
+        const int kn = (sl + 1) * kAK;
+        const bool in = kn + scol < D;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          pa[u] = ld4_or_zero(x + aoff[u] + kn, in);
+          pb[u] = ld4_or_zero(cen + boff[u] + kn, in);
+        }
+      }
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        float4 a4[4], b4[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          a4[i] = *reinterpret_cast<const float4 *>(&As[wr + 16 * i + m][16 * s + 4 * h]);
+          b4[i] = *reinterpret_cast<const float4 *>(&Bs[wc + 16 * i + m][16 * s + 4 * h]);
+        }
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const float av = t == 0 ? a4[i].x : t == 1 ? a4[i].y : t == 2 ? a4[i].z : a4[i].w;
+              const float bv = t == 0 ? b4[j].x : t == 1 ? b4[j].y : t == 2 ? b4[j].z : b4[j].w;
+              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc[i][j], 0, 0, 0);
+            }
+      }
+    }
+    // lane holds C[4 h + e][m] of each 16 x 16 tile: row wr + 16 i + 4 h + e,
+    // centre c0 + wc + 16 j + m
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int c = c0 + wc + 16 * j + m;
+      const float cn = c < nlist ? cnorm[c] : __builtin_inff();
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float v = cn - 2.f * acc[i][j][e];   // ||c||^2 - 2 <x, c>
+          if (v < best[4 * i + e]) {
+            best[4 * i + e] = v;
+            bid[4 * i + e] = c;
+          }
+        }
+    }
+  }
+  // merge the 16 lanes (m) holding the same rows: lexicographic (value, id)
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    for (int off = 1; off < 16; off <<= 1) {
+      const float ov = __shfl_xor(best[r], off, 64);
+      const int oi = __shfl_xor(bid[r], off, 64);
+      if (ov < best[r] || (ov == best[r] && oi < bid[r])) {
+        best[r] = ov;
+        bid[r] = oi;
+      }
+    }
+  }
+  if (wc && m == 0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        red_v[wr + 16 * i + 4 * h + e] = best[4 * i + e];
+        red_i[wr + 16 * i + 4 * h + e] = bid[4 * i + e];
+      }
+  }
+  if (out_d) {   // ||x||^2 of the workgroup's rows: 32 rows per wavefront
+    for (int rr = 0; rr < 32; ++rr) {
+      const int rl = wave * 32 + rr;
+      const int64_t row = r0 + rl < n ? r0 + rl : n - 1;
+      float s = 0.f;
+      for (int k = 4 * lane; k < D; k += 256) {
+        const float4 v = *reinterpret_cast<const float4 *>(x + row * D + k);
+        s += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+      }
+      s = wave_sum(s);
+      if (lane == 0) xx_s[rl] = s;
+    }
+  }
+  __syncthreads();
+  if (wc || m) return;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int rl = wr + 16 * i + 4 * h + e;
+      float v = best[4 * i + e];
+      int32_t id = bid[4 * i + e];
+      const float ov = red_v[rl];
+      const int32_t oi = red_i[rl];
+      if (ov < v || (ov == v && oi < id)) {
+        v = ov;
+        id = oi;
+      }
+      const int64_t r = r0 + rl;
+      if (r < n) {
+        out_ids[r] = id;
+        if (out_d) out_d[r] = xx_s[rl] + v;
+      }
+    }
 }
 
 struct IdentityId {
@@ -429,6 +612,15 @@ int ivf_assign_probe(const float *x, int64_t n, int32_t dim, const float *centro
                        dim, cnorm);
     int st = check_launch();
     if (st) return st;
+    const bool aligned16 = (reinterpret_cast<uintptr_t>(x) % 16 == 0) &&
+                           (reinterpret_cast<uintptr_t>(centroids) % 16 == 0);
+    if (dim % 4 == 0 && aligned16) {   // rows are whole, aligned float4 runs
+      const int64_t grid = (n + kAM - 1) / kAM;
+      if (grid > 0x7fffffff) return RSLM_ERR_INVALID_ARG;
+      hipLaunchKernelGGL(k_assign_mfma, dim3(unsigned(grid)), dim3(256), 0, s, x, n, dim,
+                         centroids, nlist, cnorm, out_ids, out_scores);
+      return check_launch();
+    }
     const int64_t grid = (n + kTM - 1) / kTM;
     if (grid > 0x7fffffff) return RSLM_ERR_INVALID_ARG;
     hipLaunchKernelGGL(k_assign, dim3(unsigned(grid)), dim3(256), 0, s, x, n, dim, centroids,

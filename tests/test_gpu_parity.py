@@ -179,12 +179,26 @@ def test_encode_zero_residual_and_padding_records(R):
 
 
 # ------------------------------------------------------------------ routing
-@pytest.mark.parametrize("D,nlist,n", [(96, 100, 700), (768, 257, 300), (128, 16, 1000)])
-def test_assign_parity(R, D, nlist, n):
+def _unaligned(a):
+    """A device copy of a float32 matrix whose base is 4 bytes past a
+    16-byte boundary (selects the kernel without 16-byte operand loads)."""
+    flat = torch.empty(a.size + 1, dtype=torch.float32, device=DEV)
+    flat[1:] = torch.from_numpy(np.ascontiguousarray(a).reshape(-1)).to(DEV)
+    return flat[1:].view(a.shape)
+
+
+# D % 4 == 0 with aligned rows runs the matrix-core kernel (128-row blocks,
+# centre tiles of 128, k slabs of 32); other shapes the vector-ALU one
+@pytest.mark.parametrize("D,nlist,n", [(96, 100, 700), (768, 257, 300), (128, 16, 1000),
+                                       (36, 300, 1000), (4, 129, 131), (33, 70, 200),
+                                       (100, 250, 700)])
+@pytest.mark.parametrize("aligned", [True, False])
+def test_assign_parity(R, D, nlist, n, aligned):
     rng = np.random.default_rng(D)
     x = synth.gmix(n, D, 32, seed=D)
     cen = x[rng.choice(n, nlist, replace=False)] + 0.01 * rng.standard_normal((nlist, D)).astype(np.float32)
-    ids, dist = R.ivf_assign_probe(_t(x), _t(cen.astype(np.float32)), 1, R.IVF_ASSIGN_L2)
+    xt = _t(x) if aligned else _unaligned(x)
+    ids, dist = R.ivf_assign_probe(xt, _t(cen.astype(np.float32)), 1, R.IVF_ASSIGN_L2)
     ids = ids.cpu().numpy()
     dist = dist.cpu().numpy()
     ref, best = oracle.assign_l2(x, cen.astype(np.float32))
@@ -192,6 +206,28 @@ def test_assign_parity(R, D, nlist, n):
     assert np.all((ids == ref) | (d_gpu_choice - best <= 1e-5 * (1 + best)))
     assert np.mean(ids == ref) > 0.99
     assert np.all(np.abs(dist - best) <= 1e-4 * (1 + np.abs(best)) + 1e-4 * (x * x).sum(1))
+
+
+@pytest.mark.parametrize("D", [64, 33])
+def test_assign_ties_take_the_lowest_id(R, D):
+    """Exact duplicates of every centre (placed in other centre tiles and in
+    the other half of a tile) give bit-identical distances: the lower id
+    must win, as in the oracle's argmin."""
+    rng = np.random.default_rng(5)
+    base = rng.standard_normal((100, D)).astype(np.float32)
+    perm = rng.permutation(300)
+    cen = np.concatenate([base, base, base])[perm]
+    x = synth.gmix(777, D, 16, seed=3)
+    ids, _ = R.ivf_assign_probe(_t(x), _t(cen), 1, R.IVF_ASSIGN_L2)
+    ids = ids.cpu().numpy()
+    ref, best = oracle.assign_l2(x, cen)
+    # the chosen centre's base row, and no duplicate of it with a lower id
+    src = perm % 100
+    for i, c in enumerate(ids):
+        same = np.flatnonzero(src == src[c])
+        assert c == same.min()
+    d_gpu_choice = ((x.astype(np.float64) - cen[ids]) ** 2).sum(1)
+    assert np.all((ids == ref) | (d_gpu_choice - best <= 1e-5 * (1 + best)))
 
 
 @pytest.mark.parametrize("D,nlist,nprobe,Q", [(96, 300, 32, 50), (768, 4096, 64, 20), (128, 16, 4, 100),
