@@ -1,4 +1,5 @@
 // Plan objects, status handling and the E_max constant.
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 #include <new>
@@ -8,6 +9,30 @@
 namespace rslm {
 
 static thread_local int g_last_hip = 0;
+
+// Uniform bucket grid over sorted 1-D decision thresholds (quant_bucket):
+// the smallest of 128, 256 or 512 buckets over +-1.0625 max |t| that puts
+// every threshold in a bucket of its own; none (qn = 0) if even 512 do not.
+static void quant_grid(const float *thr, int n, float &qs, float &qo, int &qn) {
+  qs = qo = 0.0f;
+  qn = 0;
+  if (n < 1) return;
+  float R = 0.0f;
+  for (int k = 0; k < n; ++k) R = std::max(R, std::fabs(thr[k]));
+  if (!(R > 0.0f) || !std::isfinite(R)) R = 1.0f;
+  for (int cand = 128; cand <= 512; cand *= 2) {
+    const float s = float(cand) / (2.125f * R), o = float(cand / 2);
+    bool ok = true;
+    for (int k = 1; k < n && ok; ++k)
+      ok = quant_bucket(thr[k], s, o, cand) > quant_bucket(thr[k - 1], s, o, cand);
+    if (ok) {
+      qs = s;
+      qo = o;
+      qn = cand;
+      return;
+    }
+  }
+}
 
 int set_hip_error(hipError_t e) {
   g_last_hip = int(e);
@@ -173,6 +198,8 @@ int rslm_plan_create(const rslm_plan_desc *d, rslm_plan **out) {
   for (int k = 0; k < 16; ++k)
     c.thr_lead[k] = (d->lite && k < 7) ? 0.5f * (d->codebook_lead[k] + d->codebook_lead[k + 1])
                                        : __builtin_inff();
+  quant_grid(c.thr, g == 1 ? K - 1 : 0, c.qs, c.qo, c.qn);
+  quant_grid(c.thr_lead, d->lite ? 7 : 0, c.qs_lead, c.qo_lead, c.qn_lead);
 
   // --- device tables: signs, intra-block permutation, compact decode table
   float s1f[256];

@@ -182,8 +182,52 @@ __device__ __forceinline__ float row_max16(float v) {
   return v;
 }
 
+// The four lane stages of the 8 elements z[o..o+7] of one block, each a DPP
+// multiply-add v_fmac_f32_dpp (z += sg[k] * z of the partner lane: lane r ^ 1,
+// r ^ 2, r ^ 4, r ^ 8 of the 16-lane row; r ^ 4 as a half-mirror move then a
+// quad reversal).  The compiler does not fold a DPP move into the multiplied
+// operand of a multiply-add, so the stages are written out here.  A DPP
+// operand must not have been written by the two preceding VALU instructions:
+// the block opens and closes with two wait states, and inside it every DPP
+// read is at least seven instructions after the write of its register.
+#define RSLM_DPP_FMAC(I, SG, SRC, CTRL) \
+  "v_fmac_f32_dpp %" #I ", %" #SRC ", %" #SG " " CTRL " row_mask:0xf bank_mask:0xf bound_ctrl:1\n\t"
+#define RSLM_DPP_STAGE(SG, CTRL)                                                           \
+  RSLM_DPP_FMAC(0, SG, 0, CTRL) RSLM_DPP_FMAC(1, SG, 1, CTRL) RSLM_DPP_FMAC(2, SG, 2, CTRL) \
+  RSLM_DPP_FMAC(3, SG, 3, CTRL) RSLM_DPP_FMAC(4, SG, 4, CTRL) RSLM_DPP_FMAC(5, SG, 5, CTRL) \
+  RSLM_DPP_FMAC(6, SG, 6, CTRL) RSLM_DPP_FMAC(7, SG, 7, CTRL)
+#define RSLM_DPP_MIRROR(T, I) \
+  "v_mov_b32_dpp %" #T ", %" #I " row_half_mirror row_mask:0xf bank_mask:0xf bound_ctrl:1\n\t"
+__device__ __forceinline__ void lane_stages8(float *z, int o, const float (&sg)[4]) {
+  float t0, t1, t2, t3, t4, t5, t6, t7;   // half-mirrored copies (stage r ^ 4)
+  asm volatile(
+      "s_nop 1\n\t"
+      RSLM_DPP_STAGE(16, "quad_perm:[1,0,3,2]")
+      RSLM_DPP_STAGE(17, "quad_perm:[2,3,0,1]")
+      RSLM_DPP_MIRROR(8, 0) RSLM_DPP_MIRROR(9, 1) RSLM_DPP_MIRROR(10, 2) RSLM_DPP_MIRROR(11, 3)
+      RSLM_DPP_MIRROR(12, 4) RSLM_DPP_MIRROR(13, 5) RSLM_DPP_MIRROR(14, 6) RSLM_DPP_MIRROR(15, 7)
+      RSLM_DPP_FMAC(0, 18, 8, "quad_perm:[3,2,1,0]") RSLM_DPP_FMAC(1, 18, 9, "quad_perm:[3,2,1,0]")
+      RSLM_DPP_FMAC(2, 18, 10, "quad_perm:[3,2,1,0]") RSLM_DPP_FMAC(3, 18, 11, "quad_perm:[3,2,1,0]")
+      RSLM_DPP_FMAC(4, 18, 12, "quad_perm:[3,2,1,0]") RSLM_DPP_FMAC(5, 18, 13, "quad_perm:[3,2,1,0]")
+      RSLM_DPP_FMAC(6, 18, 14, "quad_perm:[3,2,1,0]") RSLM_DPP_FMAC(7, 18, 15, "quad_perm:[3,2,1,0]")
+      RSLM_DPP_STAGE(19, "row_ror:8")
+      "s_nop 1"
+      : "+v"(z[o + 0]), "+v"(z[o + 1]), "+v"(z[o + 2]), "+v"(z[o + 3]), "+v"(z[o + 4]),
+        "+v"(z[o + 5]), "+v"(z[o + 6]), "+v"(z[o + 7]), "=&v"(t0), "=&v"(t1), "=&v"(t2),
+        "=&v"(t3), "=&v"(t4), "=&v"(t5), "=&v"(t6), "=&v"(t7)
+      : "v"(sg[0]), "v"(sg[1]), "v"(sg[2]), "v"(sg[3]));
+}
+#undef RSLM_DPP_MIRROR
+#undef RSLM_DPP_STAGE
+#undef RSLM_DPP_FMAC
+
 // Unnormalised FWHT of every 128-block of the row's vector; sg[k] = -1 where
-// bit k of r is set (that lane computes partner - own).
+// bit k of r is set.  A lane stage computes own + sg[k] partner, so the
+// exchanged value is the multiplied operand and the exchange folds into the
+// multiply-add (one DPP multiply-add per element and stage).  In a lane with
+// bit k set that is partner - own, the negative of the butterfly's
+// difference: after the four lane stages lane r holds (-1)^popcount(r) times
+// the transform, which the caller folds into a later sign or scale.
 template <int E>
 __device__ __forceinline__ void fwht_rows(float (&z)[E], const float (&sg)[4]) {
 #pragma unroll
@@ -199,20 +243,9 @@ __device__ __forceinline__ void fwht_rows(float (&z)[E], const float (&sg)[4]) {
       }
     }
   }
-  // lane stages, one block at a time: the scheduling barrier keeps the
-  // compiler from batching every exchange of a stage (48 live temporaries)
+  // lane stages, one block at a time
 #pragma unroll
-  for (int b = 0; b < E / 8; ++b) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) z[8 * b + i] = fmaf(sg[0], z[8 * b + i], dppf<kDppQuadXor1>(z[8 * b + i]));
-#pragma unroll
-    for (int i = 0; i < 8; ++i) z[8 * b + i] = fmaf(sg[1], z[8 * b + i], dppf<kDppQuadXor2>(z[8 * b + i]));
-#pragma unroll
-    for (int i = 0; i < 8; ++i) z[8 * b + i] = fmaf(sg[2], z[8 * b + i], dpp_xor4(z[8 * b + i]));
-#pragma unroll
-    for (int i = 0; i < 8; ++i) z[8 * b + i] = fmaf(sg[3], z[8 * b + i], dppf<kDppRowRor8>(z[8 * b + i]));
-    __builtin_amdgcn_sched_barrier(0);
-  }
+  for (int b = 0; b < E / 8; ++b) lane_stages8(z, 8 * b, sg);
 }
 
 // sign bit (bit 31) of coordinate 128 b + 8 r + i from the lane's 16-bit
@@ -220,6 +253,9 @@ __device__ __forceinline__ void fwht_rows(float (&z)[E], const float (&sg)[4]) {
 __device__ __forceinline__ uint32_t sgnbit(uint32_t m, int b, int i) {
   return ((m >> (8 * (b & 1) + i)) & 1u) << 31;
 }
+
+// Stand-in centre rows (zeros) for records encoded without a centre.
+__device__ __align__(16) const float kZeroRow[1024] = {};
 
 // S2 selects the output of the second residual R x - g^ (R c + s^ c^):
 //   0: float32 rows (resid, when given);
@@ -250,6 +286,13 @@ __global__ void __launch_bounds__(256) k_encode_rows(
   __shared__ float cb8[16], thr8[16];   // Rslm4Lite: K = 8 codebook of the leading lanes
   __shared__ float cb2[16], cb2y[16];   // second codebook, first and second coordinates
   __shared__ uint32_t rmask[16];
+  // per lane r: bit 8 b + i (word b / 4) = sign of element (b, i) after the
+  // transpose: S2 of the target coordinate times the lane sign (-1)^popcount
+  // that the first pass left on its source coordinate
+  __shared__ uint32_t tmask[16][2];
+  // quantiser grids: thresholds below each bucket (cp.qn, cp.qn_lead <= 512)
+  __shared__ uint8_t qtab[512];
+  __shared__ uint8_t qtab8[LITE ? 512 : 1];
   __shared__ uint16_t ts[D];
   const int lane = threadIdx.x & 63;
   const int wid = threadIdx.x >> 6;
@@ -266,17 +309,43 @@ __global__ void __launch_bounds__(256) k_encode_rows(
     cbs[threadIdx.x] = cp.cb[threadIdx.x];
     // sorted decision thresholds, padded with +inf for the binary search
     thr[threadIdx.x] = (int(threadIdx.x) + 1 < K) ? cp.thr[threadIdx.x] : __builtin_inff();
-    // S1 (low half) and S2 (high half) sign bits of coordinates 128 p + 8 t + i
+    // S1 sign bits of coordinates 128 p + 8 t + i (p < 2: the signs repeat
+    // every 256 coordinates)
     uint32_t m = 0;
     for (int pi = 0; pi < 16; ++pi) {
       const int c = 128 * (pi >> 3) + 8 * int(threadIdx.x) + (pi & 7);
       m |= sign_bit(rp.s1mask, c) << pi;
-      m |= sign_bit(rp.s1mask, c + 127) << (16 + pi);
     }
     rmask[threadIdx.x] = m;
+    if (rp.passes == 2) {
+      uint32_t tm[2] = {0u, 0u};
+      for (int b = 0; b < NB; ++b)
+        for (int i = 0; i < 8; ++i) {
+          const int o = 128 * b + 8 * int(threadIdx.x) + i;
+          const int src_lane = (rp.tsrc[o] >> 3) & 15;
+          const uint32_t bit = sign_bit(rp.s1mask, o + 127) ^ (__popc(src_lane) & 1u);
+          tm[b >> 2] |= bit << (8 * (b & 3) + i);
+        }
+      tmask[threadIdx.x][0] = tm[0];
+      tmask[threadIdx.x][1] = tm[1];
+    }
   }
   if (rp.passes == 2)
     for (int k = threadIdx.x; k < D; k += blockDim.x) ts[k] = uint16_t(4 * rp.tsrc[k]);
+  for (int j = threadIdx.x; j < cp.qn; j += blockDim.x) {
+    int cnt = 0;
+#pragma unroll
+    for (int k = 0; k + 1 < K; ++k) cnt += quant_bucket(cp.thr[k], cp.qs, cp.qo, cp.qn) < j;
+    qtab[j] = uint8_t(cnt);
+  }
+  if (LITE)
+    for (int j = threadIdx.x; j < cp.qn_lead; j += blockDim.x) {
+      int cnt = 0;
+#pragma unroll
+      for (int k = 0; k < 7; ++k)
+        cnt += quant_bucket(cp.thr_lead[k], cp.qs_lead, cp.qo_lead, cp.qn_lead) < j;
+      qtab8[j] = uint8_t(cnt);
+    }
   __syncthreads();
   const int64_t rec = (int64_t(blockIdx.x) * (blockDim.x >> 6) + wid) * 4 + rho;
   int64_t row = -1;
@@ -292,14 +361,13 @@ __global__ void __launch_bounds__(256) k_encode_rows(
   // A row without a vector leaves; rows never exchange data, and no
   // workgroup barrier follows.
   if (row < 0) return;
-  const uint32_t m1 = rmask[r] & 0xffffu, m2 = rmask[r] >> 16;
+  const uint32_t m1 = rmask[r];
   const float sg[4] = {(r & 1) ? -1.f : 1.f, (r & 2) ? -1.f : 1.f, (r & 4) ? -1.f : 1.f,
                        (r & 8) ? -1.f : 1.f};
 
   // residual r = x - c, its sums, and S1
   const float *xr = x + row * D + 8 * r;
-  const float *cr = (L >= 0) ? cen + int64_t(L) * D + 8 * r : xr;   // weight 0 without c
-  const float cw = (L >= 0) ? 1.f : 0.f;
+  const float *cr = ((L >= 0) ? cen + int64_t(L) * D : kZeroRow) + 8 * r;
   float z[E];
   float xx = 0.f, rr = 0.f, cc = 0.f;
 #pragma unroll
@@ -309,7 +377,7 @@ __global__ void __launch_bounds__(256) k_encode_rows(
       const float4 xv = *reinterpret_cast<const float4 *>(xr + 128 * b + 4 * h);
       const float4 cv4 = *reinterpret_cast<const float4 *>(cr + 128 * b + 4 * h);
       const float xa[4] = {xv.x, xv.y, xv.z, xv.w};
-      const float ca[4] = {cv4.x * cw, cv4.y * cw, cv4.z * cw, cv4.w * cw};
+      const float ca[4] = {cv4.x, cv4.y, cv4.z, cv4.w};
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
         const int i = 4 * h + t;
@@ -343,6 +411,7 @@ __global__ void __launch_bounds__(256) k_encode_rows(
               make_float4(z[8 * b + 4 * h], z[8 * b + 4 * h + 1], z[8 * b + 4 * h + 2],
                           z[8 * b + 4 * h + 3]);
       wave_sync_r();
+      const uint32_t tm[2] = {tmask[r][0], tmask[r][1]};
 #pragma unroll
       for (int b = 0; b < NB; ++b) {
         const uint4 t8 = *reinterpret_cast<const uint4 *>(ts + 128 * b + 8 * r);
@@ -350,13 +419,15 @@ __global__ void __launch_bounds__(256) k_encode_rows(
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
           const uint32_t off = (tw[i >> 1] >> (16 * (i & 1))) & 0xffffu;
-          z[8 * b + i] = __uint_as_float(__float_as_uint(lds_at(vb, off)) ^ sgnbit(m2, b, i));
+          const uint32_t sb = ((tm[b >> 2] >> (8 * (b & 3) + i)) & 1u) << 31;
+          z[8 * b + i] = __uint_as_float(__float_as_uint(lds_at(vb, off)) ^ sb);
         }
       }
       wave_sync_r();
       fwht_rows<E>(z, sg);
       scale = rp.inv_sqrt_b * rp.inv_sqrt_b;
     }
+    if (__popc(r) & 1) scale = -scale;   // the lane sign of the last pass
   }
   float m = 0.f;
 #pragma unroll
@@ -368,43 +439,51 @@ __global__ void __launch_bounds__(256) k_encode_rows(
   const float inv_s0 = (m > 0.f) ? cp.emax / m : 0.f;
 
   // nearest centroid of the sorted 1-D codebook = number of thresholds below
-  // u, by an unrolled binary search (c4 = 4 x code, the LDS byte offset).
-  // Only the packed words are kept; centroid values are looked up again
-  // where needed (registers, not recomputation, bound this kernel).
+  // u: the count below u's bucket on the quantiser grid plus one comparison
+  // with the next threshold (the grid has at most one per bucket).  Only the
+  // packed words are kept; centroid values are looked up again where needed
+  // (registers, not recomputation, bound this kernel).  ||c^||^2 and
+  // <R c, c^> accumulate here, the rotated centre streamed one block ahead.
+  const bool has_rc = L >= 0 && cen_rot;
+  const float *rcr = (has_rc ? cen_rot + int64_t(L) * D : kZeroRow) + 8 * r;
   uint32_t word[NB];
-  float cn2 = 0.f;
+  float cn2 = 0.f, rcd = 0.f;
   const bool lead_lane = LITE && r < cp.lead / 8;   // block 0 of these lanes is on cb8
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
-    float *tb = (LITE && b == 0 && lead_lane) ? thr8 : thr;
-    float *cbb = (LITE && b == 0 && lead_lane) ? cb8 : cbs;
-    uint32_t c4[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
+    const bool lb = LITE && b == 0 && lead_lane;
+    float *tb = lb ? thr8 : thr;
+    float *cbb = lb ? cb8 : cbs;
+    const uint8_t *qt = lb ? qtab8 : qtab;
+    const float qs = lb ? cp.qs_lead : cp.qs, qo = lb ? cp.qo_lead : cp.qo;
+    const int qn = lb ? cp.qn_lead : cp.qn;
+    uint32_t code[8];
 #pragma unroll
-    for (int half = K >> 1; half >= 1; half >>= 1)
-#pragma unroll
-      for (int i = 0; i < 8; ++i)
-        c4[i] += (z[8 * b + i] * inv_s0 > lds_at(tb, c4[i] + 4u * (half - 1))) ? 4u * half : 0u;
+    for (int i = 0; i < 8; ++i) {
+      const float u = z[8 * b + i] * inv_s0;
+      const uint32_t base = qt[quant_bucket(u, qs, qo, qn)];
+      code[i] = base + ((u > tb[base]) ? 1u : 0u);
+    }
     word[b] = 0u;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      const uint32_t c = (m > 0.f) ? (c4[i] >> 2) : 0u;
-      word[b] |= c << (BITS * i);
-      const float v = lds_at(cbb, 4u * c);
+      word[b] |= code[i] << (BITS * i);
+      const float v = cbb[code[i]];
       cn2 = fmaf(v, v, cn2);
     }
     __builtin_amdgcn_sched_barrier(0);
   }
+  // a zero residual has codes 0 (its cn2 and rcd are multiplied by s^ = 0)
+  if (!(m > 0.f))
+#pragma unroll
+    for (int b = 0; b < NB; ++b) word[b] = 0u;
   cn2 = row_sum16(cn2);
-  auto centroid = [&](int b, int i) {   // code 0 of a zero residual decodes to 0
+  // centroid value of a code (a zero residual has codes 0 and s^ = 0, so the
+  // value its codes decode to is always multiplied by 0)
+  auto centroid = [&](int b, int i) {
     float *cbb = (LITE && b == 0 && lead_lane) ? cb8 : cbs;
-    const float v = lds_at(cbb, 4u * ((word[b] >> (BITS * i)) & uint32_t(K - 1)));
-    return (m > 0.f) ? v : 0.f;
+    return lds_at(cbb, 4u * ((word[b] >> (BITS * i)) & uint32_t(K - 1)));
   };
-  // <R c, c^> with the rotated centre (read again for the residual output)
-  const bool has_rc = L >= 0 && cen_rot;
-  const float *rcr = has_rc ? cen_rot + int64_t(L) * D + 8 * r : xr;
-  const float rcw = has_rc ? 1.f : 0.f;
-  float rcd = 0.f;
 #pragma unroll
   for (int b = 0; b < NB; ++b)
 #pragma unroll
@@ -412,7 +491,7 @@ __global__ void __launch_bounds__(256) k_encode_rows(
       const float4 v = *reinterpret_cast<const float4 *>(rcr + 128 * b + 4 * h);
       const float va[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-      for (int t = 0; t < 4; ++t) rcd = fmaf(va[t] * rcw, centroid(b, 4 * h + t), rcd);
+      for (int t = 0; t < 4; ++t) rcd = fmaf(va[t], centroid(b, 4 * h + t), rcd);
     }
   rcd = row_sum16(rcd);
   const float s = (m > 0.f && cn2 > 0.f) ? sqrtf(rr / cn2) : 0.f;
@@ -464,7 +543,7 @@ __global__ void __launch_bounds__(256) k_encode_rows(
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const float4 v = *reinterpret_cast<const float4 *>(rcr + off1 + 128 * b + 4 * h);
-        const float va[4] = {v.x * rcw, v.y * rcw, v.z * rcw, v.w * rcw};
+        const float va[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
           const int e = 8 * b + 4 * h + t;
@@ -509,8 +588,7 @@ __global__ void __launch_bounds__(256) k_encode_rows(
           best[k2] = fminf(best[k2], d);
         }
       }
-      const float rcv[8] = {ra.x * rcw, ra.y * rcw, ra.z * rcw, ra.w * rcw,
-                            rb.x * rcw, rb.y * rcw, rb.z * rcw, rb.w * rcw};
+      const float rcv[8] = {ra.x, ra.y, ra.z, ra.w, rb.x, rb.y, rb.z, rb.w};
       uint32_t wb = word[b];   // first-stage codes, looked up again
       asm volatile("" : "+v"(wb));
       w2[b] = 0u;
@@ -558,7 +636,7 @@ __global__ void __launch_bounds__(256) k_encode_rows(
         const float4 v = *reinterpret_cast<const float4 *>(rcr + 128 * b + 4 * h);
         const float4 l4 = *reinterpret_cast<const float4 *>(lo_r + 128 * b + 4 * h);
         const float4 h4 = *reinterpret_cast<const float4 *>(hi_r + 128 * b + 4 * h);
-        const float va[4] = {v.x * rcw, v.y * rcw, v.z * rcw, v.w * rcw};
+        const float va[4] = {v.x, v.y, v.z, v.w};
         const float la[4] = {l4.x, l4.y, l4.z, l4.w}, ha[4] = {h4.x, h4.y, h4.z, h4.w};
         uint32_t wv = 0u;
 #pragma unroll
@@ -580,7 +658,7 @@ __global__ void __launch_bounds__(256) k_encode_rows(
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const float4 v = *reinterpret_cast<const float4 *>(rcr + 128 * b + 4 * h);
-        const float va[4] = {v.x * rcw, v.y * rcw, v.z * rcw, v.w * rcw};
+        const float va[4] = {v.x, v.y, v.z, v.w};
         float o[4];
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
@@ -641,6 +719,8 @@ bool launch_encode_reg(const rslm_plan *p, const rslm_plan *p2, const float *x, 
   if (s2 != 0 && p->codec.bits != 4) return false;
   const bool lite = p->codec.lead > 0;
   if (lite && s2 == 1) return false;   // Lite with an RSLM second stage: general path
+  // codebooks whose thresholds no quantiser grid separates: general path
+  if (p->codec.qn == 0 || (lite && p->codec.qn_lead == 0)) return false;
   // 16-byte vector loads and stores of every row
   if ((reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(cen) |
        reinterpret_cast<uintptr_t>(cen_rot) | reinterpret_cast<uintptr_t>(resid) |

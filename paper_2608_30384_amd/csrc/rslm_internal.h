@@ -75,7 +75,26 @@ struct CodecParams {
   int record_bytes;           // packed record: canon_bytes + scale suffix (Lite: none)
   float cb_lead[8];           // Rslm4Lite: K = 8 codebook of the leading coordinates
   float thr_lead[16];         // its 7 thresholds, padded with +inf
+  // 1-D quantiser grids (quant_bucket) over the thresholds of cb / cb_lead:
+  // each bucket holds at most one threshold; qn = 0: no such grid
+  float qs, qo, qs_lead, qo_lead;
+  int qn, qn_lead;
 };
+
+// Bucket of u on a uniform grid of qn buckets: floor(clamp(u qs + qo, 0,
+// qn - 1)), one fused multiply-add.  Non-decreasing in u, so with at most one
+// decision threshold per bucket the number of thresholds below u is the
+// number whose bucket is lower, plus one comparison with the next threshold.
+// The plan (host) and the encoders (device) evaluate the same expression.
+__host__ __device__ inline int quant_bucket(float u, float qs, float qo, int qn) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  // the same clamp as one median-of-three (equal for every non-NaN value; a
+  // NaN bucket is one of the bounds or converts to 0)
+  return int(__builtin_amdgcn_fmed3f(fmaf(u, qs, qo), 0.0f, float(qn - 1)));
+#else
+  return int(fminf(fmaxf(fmaf(u, qs, qo), 0.0f), float(qn - 1)));
+#endif
+}
 
 }  // namespace rslm
 
@@ -167,13 +186,19 @@ __device__ __forceinline__ float dec_ue4m12(uint32_t u) {
 }
 
 // SQ8 code of v for the range [lo, hi]: clamp(rne((v - lo) / step), 0, 255)
-// with step = (hi - lo) / 255, evaluated as (v - lo) * (255 / (hi - lo)) with
-// the hardware reciprocal (1 ulp); an empty range gives 0.
-__device__ __forceinline__ uint32_t sq8_code(float v, float lo, float hi) {
+// with step = (hi - lo) / 255, evaluated as (v - lo) * inv, inv = 255 / (hi -
+// lo) with the hardware reciprocal (1 ulp); an empty range has inv = 0, which
+// gives code 0 (a NaN product is clamped to 0 as well).  Encoders that code
+// many rows against the same ranges compute inv once per coordinate.
+__device__ __forceinline__ float sq8_inv(float lo, float hi) {
   const float w = hi - lo;
-  if (!(w > 0.0f)) return 0u;
-  const float inv = __builtin_amdgcn_rcpf(w) * 255.0f;
+  return (w > 0.0f) ? __builtin_amdgcn_rcpf(w) * 255.0f : 0.0f;
+}
+__device__ __forceinline__ uint32_t sq8_code_inv(float v, float lo, float inv) {
   return uint32_t(fminf(fmaxf(rintf((v - lo) * inv), 0.0f), 255.0f));
+}
+__device__ __forceinline__ uint32_t sq8_code(float v, float lo, float hi) {
+  return sq8_code_inv(v, lo, sq8_inv(lo, hi));
 }
 
 // Float -> uint32 whose unsigned order equals the float order.
