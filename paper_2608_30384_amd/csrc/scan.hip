@@ -99,12 +99,11 @@ static ScanWs scan_ws_layout(void *base, int Q, int nprobe, int nlist, int d_pad
 // ------------------------------------------------------------- query prep
 // q_rot (Q x D) -> per-query power-of-two scale so that max |q| * scale lies
 // in [2^14, 2^15), then float16 hi = rne(q * scale), lo = rne(q * scale - hi).
-__global__ void k_prep_queries(const float *__restrict__ q, int Q, int D, int d_pad,
-                               _Float16 *__restrict__ qh, _Float16 *__restrict__ ql,
-                               float *__restrict__ qinv) {
+// One wavefront per query.
+__device__ __forceinline__ void prep_query(const float *__restrict__ q, int row, int D, int d_pad,
+                                           _Float16 *__restrict__ qh, _Float16 *__restrict__ ql,
+                                           float *__restrict__ qinv) {
   const int lane = threadIdx.x & 63;
-  const int row = blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
-  if (row >= Q) return;
   const float *qr = q + int64_t(row) * D;
   float m = 0.f;
   for (int i = lane; i < D; i += 64) m = fmaxf(m, fabsf(qr[i]));
@@ -125,26 +124,20 @@ __global__ void k_prep_queries(const float *__restrict__ q, int Q, int D, int d_
 }
 
 // ------------------------------------------------------------- planning
-__global__ void k_fill_i32(int32_t *a, int n, int32_t v) {
-  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) a[i] = v;
-}
-
-__global__ void k_plan_count(const int32_t *__restrict__ probe_ids, int npairs, int nlist,
-                             int32_t *__restrict__ counts) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= npairs) return;
-  const int L = probe_ids[i];
-  if (L >= 0 && L < nlist) atomicAdd(&counts[L], 1);
-}
+// Two kernels.  The first prepares the queries and, per query, the exclusive
+// prefix of its probed list sizes (where its scores go); its last workgroup
+// counts the (query, list) pairs per list, scans the counts into pair_off and
+// places each list's work items in an order by decreasing item size.  The
+// second groups the pairs by list and writes the work item descriptors.
 
 // One wavefront per query: exclusive prefix over its probes of the (clamped)
 // probed list sizes.
-__global__ void k_plan_prefix(const int32_t *__restrict__ probe_ids, int Q, int nprobe, int nlist,
-                              const int32_t *__restrict__ sizes, int max_list,
-                              int32_t *__restrict__ prefix, int32_t *__restrict__ totals) {
+__device__ __forceinline__ void query_prefix(const int32_t *__restrict__ probe_ids, int q,
+                                             int nprobe, int nlist,
+                                             const int32_t *__restrict__ sizes, int max_list,
+                                             int32_t *__restrict__ prefix,
+                                             int32_t *__restrict__ totals) {
   const int lane = threadIdx.x & 63;
-  const int q = blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
-  if (q >= Q) return;
   int carry = 0;
   for (int p0 = 0; p0 < nprobe; p0 += 64) {
     const int p = p0 + lane;
@@ -173,98 +166,135 @@ __device__ __forceinline__ int item_cands(int sz) {
   return ((sz + nch - 1) / nch + 15) & ~15;
 }
 constexpr int kSizeClasses = kChunkCands / 16;   // item size class = cands / 16 - 1
+constexpr int kPlanThreads = 256;
+constexpr int kPlanRange = 8192;                 // lists counted per pass in LDS
 
-// Single workgroup: exclusive scan over lists of the pair counts, and the
-// position of each list's work items (groups of <= 8 queries x chunks) in an
-// order by decreasing item size, so that the scan hands out its largest
-// items first and finishes on the smallest (counting sort over size classes;
-// the order within a class is immaterial: every item writes its own scores).
-// Also resets the scan's work counter.
-__global__ void __launch_bounds__(1024) k_plan_lists(const int32_t *__restrict__ counts,
-                                                     const int32_t *__restrict__ sizes, int nlist,
-                                                     int max_list,
-                                                     int32_t *__restrict__ pair_off,
-                                                     int32_t *__restrict__ item_off,
-                                                     int32_t *__restrict__ cursor,
-                                                     int32_t *__restrict__ work) {
-  __shared__ int32_t s_pairs[1024];
-  __shared__ int32_t s_hist[kSizeClasses], s_start[kSizeClasses];
-  __shared__ int32_t carry;
+// Work items of list L (groups of <= 8 queries x chunks) and their size class.
+__device__ __forceinline__ int list_items(int cp, int size, int max_list, int &cls) {
+  const int sz = max(0, min(size, max_list));
+  if (cp <= 0 || sz <= 0) return 0;
+  const int ic = item_cands(sz);
+  cls = ic / 16 - 1;
+  return ((cp + kGroupQ - 1) / kGroupQ) * ((sz + ic - 1) / ic);
+}
+
+struct PlanSmem {
+  int32_t cnt[kPlanRange];
+  int32_t part[kPlanThreads];
+  int32_t hist[kSizeClasses], start[kSizeClasses];
+};
+
+// The planning workgroup: pair counts per list (LDS histogram, lists in
+// passes of kPlanRange), their exclusive scan (pair_off), cursor = 0, and
+// each list's first work item in an order by decreasing item size (counting
+// sort over size classes; the order within a class is immaterial: every item
+// writes its own scores).  Also resets the scan's work counter.
+__device__ void plan_lists(PlanSmem &sm, const int32_t *__restrict__ probe_ids, int npairs,
+                           const int32_t *__restrict__ sizes, int nlist, int max_list,
+                           int32_t *__restrict__ counts, int32_t *__restrict__ pair_off,
+                           int32_t *__restrict__ item_off, int32_t *__restrict__ cursor,
+                           int32_t *__restrict__ work) {
   const int t = threadIdx.x;
-  if (t == 0) carry = 0;
-  if (t < kSizeClasses) s_hist[t] = 0;
-  __syncthreads();
-  auto list_items = [&](int L, int &cls) {
-    const int cp = counts[L];
-    const int sz = max(0, min(sizes[L], max_list));
-    if (cp <= 0 || sz <= 0) return 0;
-    const int ic = item_cands(sz);
-    cls = ic / 16 - 1;
-    return ((cp + kGroupQ - 1) / kGroupQ) * ((sz + ic - 1) / ic);
-  };
-  for (int base = 0; base < nlist; base += 1024) {
-    const int L = base + t;
-    int cp = 0;
-    if (L < nlist) {
-      cp = counts[L];
-      cursor[L] = 0;
+  if (t < kSizeClasses) sm.hist[t] = 0;
+  int carry = 0;   // uniform: pairs of the lists before this pass
+  for (int L0 = 0; L0 < nlist; L0 += kPlanRange) {
+    const int nr = min(kPlanRange, nlist - L0);
+    for (int i = t; i < nr; i += kPlanThreads) sm.cnt[i] = 0;
+    __syncthreads();
+    for (int i = t; i < npairs; i += kPlanThreads) {
+      const int L = probe_ids[i];
+      if (L >= L0 && L < L0 + nr) atomicAdd(&sm.cnt[L - L0], 1);
+    }
+    __syncthreads();
+    // thread t owns the consecutive lists [t * per, (t + 1) * per) of the pass
+    const int per = (nr + kPlanThreads - 1) / kPlanThreads;
+    const int a = min(nr, t * per), b = min(nr, a + per);
+    int sum = 0;
+    for (int i = a; i < b; ++i) {
+      const int cp = sm.cnt[i];
+      sum += cp;
       int cls = 0;
-      const int ni = list_items(L, cls);
-      if (ni > 0) atomicAdd(&s_hist[cls], ni);
+      const int ni = list_items(cp, sizes[L0 + i], max_list, cls);
+      if (ni > 0) atomicAdd(&sm.hist[cls], ni);
     }
-    s_pairs[t] = cp;
+    sm.part[t] = sum;
     __syncthreads();
-    for (int off = 1; off < 1024; off <<= 1) {  // Hillis-Steele inclusive scan
-      const int a = (t >= off) ? s_pairs[t - off] : 0;
+    for (int off = 1; off < kPlanThreads; off <<= 1) {   // inclusive scan of the parts
+      const int v = (t >= off) ? sm.part[t - off] : 0;
       __syncthreads();
-      s_pairs[t] += a;
+      sm.part[t] += v;
       __syncthreads();
     }
-    if (L < nlist) pair_off[L] = carry + s_pairs[t] - cp;
-    __syncthreads();
-    if (t == 1023) carry += s_pairs[1023];
+    int run = carry + sm.part[t] - sum;
+    for (int i = a; i < b; ++i) {
+      const int cp = sm.cnt[i];
+      counts[L0 + i] = cp;
+      cursor[L0 + i] = 0;
+      pair_off[L0 + i] = run;
+      run += cp;
+    }
+    carry += sm.part[kPlanThreads - 1];
     __syncthreads();
   }
   if (t == 0) {
     int run = 0;
     for (int c = kSizeClasses - 1; c >= 0; --c) {
-      s_start[c] = run;
-      run += s_hist[c];
+      sm.start[c] = run;
+      run += sm.hist[c];
     }
     pair_off[nlist] = carry;
     item_off[nlist] = run;
     *work = 0;
   }
-  __syncthreads();
-  for (int L = t; L < nlist; L += 1024) {
+  __syncthreads();   // the counts written above are read back by this workgroup
+  for (int L = t; L < nlist; L += kPlanThreads) {
     int cls = 0;
-    const int ni = list_items(L, cls);
-    item_off[L] = ni > 0 ? atomicAdd(&s_start[cls], ni) : 0;
+    const int ni = list_items(counts[L], sizes[L], max_list, cls);
+    item_off[L] = ni > 0 ? atomicAdd(&sm.start[cls], ni) : 0;
   }
 }
 
-__global__ void k_plan_fill(const int32_t *__restrict__ probe_ids, int npairs, int nlist,
-                            const int32_t *__restrict__ pair_off, int32_t *__restrict__ cursor,
-                            int32_t *__restrict__ pairs) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= npairs) return;
-  const int L = probe_ids[i];
-  if (L < 0 || L >= nlist) return;
-  const int pos = atomicAdd(&cursor[L], 1);
-  pairs[pair_off[L] + pos] = i;
+// Blocks [0, n_qblocks): four queries each (prep + prefix); the last block
+// plans the lists.
+__global__ void __launch_bounds__(kPlanThreads) k_plan_a(
+    const float *__restrict__ q_rot, int Q, int D, int d_pad, _Float16 *__restrict__ qh,
+    _Float16 *__restrict__ ql, float *__restrict__ qinv, const int32_t *__restrict__ probe_ids,
+    int nprobe, int nlist, const int32_t *__restrict__ sizes, int max_list,
+    int32_t *__restrict__ prefix, int32_t *__restrict__ totals, int32_t *__restrict__ counts,
+    int32_t *__restrict__ pair_off, int32_t *__restrict__ item_off, int32_t *__restrict__ cursor,
+    int32_t *__restrict__ work) {
+  __shared__ PlanSmem sm;
+  const int n_qblocks = (Q + 3) / 4;
+  if (int(blockIdx.x) == n_qblocks) {
+    plan_lists(sm, probe_ids, Q * nprobe, sizes, nlist, max_list, counts, pair_off, item_off,
+               cursor, work);
+    return;
+  }
+  const int q = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (q >= Q) return;
+  prep_query(q_rot, q, D, d_pad, qh, ql, qinv);
+  query_prefix(probe_ids, q, nprobe, nlist, sizes, max_list, prefix, totals);
 }
 
-// One thread per list: the descriptors of the list's work items, from
-// item_off[L] on.  Item = (group of <= 8 consecutive probing pairs, chunk of
-// item_cands(size) candidates):
+// Threads [0, npairs): pair i joins its list's group (pairs[] grouped by
+// list, slots from a per-list cursor).  Threads [0, nlist) also write the
+// descriptors of list L's work items from item_off[L] on.  Item = (group of
+// <= 8 consecutive pairs of the list, chunk of item_cands(size) candidates):
 //   d0 = {list, first candidate, candidate count, first pair (in pairs[])}
 //   d1 = {queries in the group, first record (low, high word), 0}
-__global__ void k_plan_items(const int32_t *__restrict__ counts, const int32_t *__restrict__ sizes,
-                             const int64_t *__restrict__ list_offsets, int nlist, int max_list,
-                             const int32_t *__restrict__ pair_off,
-                             const int32_t *__restrict__ item_off, int4 *__restrict__ items) {
-  const int L = blockIdx.x * blockDim.x + threadIdx.x;
-  if (L >= nlist) return;
+__global__ void __launch_bounds__(kPlanThreads) k_plan_b(
+    const int32_t *__restrict__ probe_ids, int npairs, int nlist,
+    const int32_t *__restrict__ counts, const int32_t *__restrict__ sizes,
+    const int64_t *__restrict__ list_offsets, int max_list, const int32_t *__restrict__ pair_off,
+    const int32_t *__restrict__ item_off, int32_t *__restrict__ cursor,
+    int32_t *__restrict__ pairs, int4 *__restrict__ items) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < npairs) {
+    const int L = probe_ids[i];
+    if (L >= 0 && L < nlist) pairs[pair_off[L] + atomicAdd(&cursor[L], 1)] = i;
+  }
+  if (i >= nlist) return;
+  const int L = i;
   const int c = counts[L];
   const int sz = max(0, min(sizes[L], max_list));
   if (c <= 0 || sz <= 0) return;
@@ -934,26 +964,15 @@ int rslm_scan_topk(const rslm_plan *p, const rslm_index *idx, const float *q_rot
   hipStream_t s = as_stream(stream);
   const int npairs = Q * nprobe;
   int st;
-  hipLaunchKernelGGL(k_prep_queries, dim3((Q + 3) / 4), dim3(256), 0, s, q_rot, Q, p->rot.D, d_pad,
-                     w.qh, w.ql, w.qinv);
+  hipLaunchKernelGGL(k_plan_a, dim3((Q + 3) / 4 + 1), dim3(kPlanThreads), 0, s, q_rot, Q,
+                     p->rot.D, d_pad, w.qh, w.ql, w.qinv, probe_ids, nprobe, nlist,
+                     idx->list_sizes, idx->max_list_size, w.prefix, w.totals, w.counts,
+                     w.pair_off, w.item_off, w.cursor, w.work);
   if ((st = check_launch())) return st;
-  hipLaunchKernelGGL(k_fill_i32, dim3((nlist + 255) / 256), dim3(256), 0, s, w.counts, nlist, 0);
-  if ((st = check_launch())) return st;
-  hipLaunchKernelGGL(k_plan_count, dim3((npairs + 255) / 256), dim3(256), 0, s, probe_ids, npairs,
-                     nlist, w.counts);
-  if ((st = check_launch())) return st;
-  hipLaunchKernelGGL(k_plan_prefix, dim3((Q + 3) / 4), dim3(256), 0, s, probe_ids, Q, nprobe,
-                     nlist, idx->list_sizes, idx->max_list_size, w.prefix, w.totals);
-  if ((st = check_launch())) return st;
-  hipLaunchKernelGGL(k_plan_lists, dim3(1), dim3(1024), 0, s, w.counts, idx->list_sizes, nlist,
-                     idx->max_list_size, w.pair_off, w.item_off, w.cursor, w.work);
-  if ((st = check_launch())) return st;
-  hipLaunchKernelGGL(k_plan_fill, dim3((npairs + 255) / 256), dim3(256), 0, s, probe_ids, npairs,
-                     nlist, w.pair_off, w.cursor, w.pairs);
-  if ((st = check_launch())) return st;
-  hipLaunchKernelGGL(k_plan_items, dim3((nlist + 255) / 256), dim3(256), 0, s, w.counts,
-                     idx->list_sizes, idx->list_offsets, nlist, idx->max_list_size, w.pair_off,
-                     w.item_off, w.items);
+  hipLaunchKernelGGL(k_plan_b, dim3((std::max(npairs, nlist) + kPlanThreads - 1) / kPlanThreads),
+                     dim3(kPlanThreads), 0, s, probe_ids, npairs, nlist, w.counts,
+                     idx->list_sizes, idx->list_offsets, idx->max_list_size, w.pair_off,
+                     w.item_off, w.cursor, w.pairs, w.items);
   if ((st = check_launch())) return st;
 
   ScanArgs a;
