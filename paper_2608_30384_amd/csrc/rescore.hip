@@ -107,20 +107,22 @@ __device__ __forceinline__ uint64_t score_key(float s, int32_t id) {
   return (uint64_t(order_key(s)) << 32) | uint64_t(0xffffffffu - uint32_t(id));
 }
 
-__global__ void __launch_bounds__(kRescoreThreads) k_rescore_sq8(
+constexpr int kSq8Threads = 1024;   // 64 candidates in flight per workgroup
+
+__global__ void __launch_bounds__(kSq8Threads) k_rescore_sq8(
     const uint8_t *__restrict__ codes, int64_t n_vec, int dim, const float *__restrict__ lo,
     const float *__restrict__ hi, const float *__restrict__ q_rot,
     const float *__restrict__ cand_s, const int32_t *__restrict__ cand_i, int k_in, int k_out,
     float *__restrict__ out_s, int32_t *__restrict__ out_i) {
   extern __shared__ float qs[];   // dim floats: q_d * step_d
   __shared__ uint64_t buf[kMaxK];
-  __shared__ float red[kRescoreThreads / 64];
+  __shared__ float red[kSq8Threads / 64];
   __shared__ uint32_t count;
   const int q = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const float *qr = q_rot + int64_t(q) * dim;
   float part = 0.f;
-  for (int d = tid; d < dim; d += kRescoreThreads) {
+  for (int d = tid; d < dim; d += kSq8Threads) {
     const float step = (hi[d] - lo[d]) / 255.f;
     qs[d] = qr[d] * step;
     part += qr[d] * lo[d];
@@ -130,13 +132,15 @@ __global__ void __launch_bounds__(kRescoreThreads) k_rescore_sq8(
   if (tid == 0) count = 0;
   __syncthreads();
   float qlo = 0.f;
-  for (int w = 0; w < kRescoreThreads / 64; ++w) qlo += red[w];
+  for (int w = 0; w < kSq8Threads / 64; ++w) qlo += red[w];
   // 16 lanes per candidate, four candidates per wavefront; lane j of a group
-  // takes dwords j, j + 16, ... of the candidate's codes.
+  // takes the 16-byte units j, j + 16, ... of the candidate's codes (dwords
+  // when rows are not whole aligned 16-byte runs), all loads of a candidate
+  // issued before its products.
   __syncthreads();   // qs complete
   const int grp = lane >> 4, gl = lane & 15;
-  const int ngroups = (kRescoreThreads / 64) * 4;
-  const int nd4 = dim >> 2;
+  const int ngroups = (kSq8Threads / 64) * 4;
+  const bool wide = (dim & 15) == 0 && (reinterpret_cast<uintptr_t>(codes) & 15) == 0;
   for (int j0 = wave * 4; j0 < k_in; j0 += ngroups) {
     const int j = j0 + grp;
     int32_t id = -1;
@@ -145,15 +149,25 @@ __global__ void __launch_bounds__(kRescoreThreads) k_rescore_sq8(
     float dot = 0.f;
     if (valid) {
       const uint8_t *cr = codes + int64_t(id) * dim;
-      if ((dim & 3) == 0) {
-        const uint32_t *cw = reinterpret_cast<const uint32_t *>(cr);
+      auto dot4 = [&](uint32_t w, int d) {
+        const float4 qv = *reinterpret_cast<const float4 *>(qs + d);
+        return qv.x * float(w & 0xffu) + qv.y * float((w >> 8) & 0xffu) +
+               qv.z * float((w >> 16) & 0xffu) + qv.w * float(w >> 24);
+      };
+      if (wide) {
+        const uint4 *cw = reinterpret_cast<const uint4 *>(cr);
+        const int nd16 = dim >> 4;
 #pragma unroll 4
-        for (int d4 = gl; d4 < nd4; d4 += 16) {
-          const uint32_t w = cw[d4];
-          const float4 qv = *reinterpret_cast<const float4 *>(qs + 4 * d4);
-          dot += qv.x * float(w & 0xffu) + qv.y * float((w >> 8) & 0xffu) +
-                 qv.z * float((w >> 16) & 0xffu) + qv.w * float(w >> 24);
+        for (int d16 = gl; d16 < nd16; d16 += 16) {
+          const uint4 w = cw[d16];
+          dot += dot4(w.x, 16 * d16) + dot4(w.y, 16 * d16 + 4) + dot4(w.z, 16 * d16 + 8) +
+                 dot4(w.w, 16 * d16 + 12);
         }
+      } else if ((dim & 3) == 0) {
+        const uint32_t *cw = reinterpret_cast<const uint32_t *>(cr);
+        const int nd4 = dim >> 2;
+#pragma unroll 4
+        for (int d4 = gl; d4 < nd4; d4 += 16) dot += dot4(cw[d4], 4 * d4);
       } else {
         for (int d = gl; d < dim; d += 16) dot += qs[d] * float(cr[d]);
       }
@@ -496,7 +510,7 @@ int rslm_rescore(const rslm_rescore_codec *c, const float *q_rot, int32_t Q,
   hipStream_t s = as_stream(stream);
   if (c->kind == RSLM_RESCORE_SQ8) {
     if (!c->lo || !c->hi) return RSLM_ERR_INVALID_ARG;
-    hipLaunchKernelGGL(k_rescore_sq8, dim3(unsigned(Q)), dim3(kRescoreThreads),
+    hipLaunchKernelGGL(k_rescore_sq8, dim3(unsigned(Q)), dim3(kSq8Threads),
                        size_t(c->dim) * sizeof(float), s, c->codes, c->n_vectors, c->dim, c->lo,
                        c->hi, q_rot, cand_scores, cand_ids, k_in, k_out, out_scores, out_ids);
     return check_launch();

@@ -791,10 +791,10 @@ __global__ void __launch_bounds__(kStreamThreads) k_topk_stream(
   __syncthreads();
   int cur = 0, cnt = n0;
   uint32_t T = 0;
+  // candidates kept after a threshold raise: a tight target raises T early,
+  // so that later rounds add few candidates and rarely trigger another raise
+  const int keep = min(kStreamSoft / 2, max(256, 2 * k));
   if (n > n0) {
-    T = stream_threshold(sm, cur, cnt, k, kStreamSoft / 2);
-    cnt = stream_compact(sm, cur, cnt, T);
-    cur ^= 1;
     // the rest, 16 scores per thread per round (four 16-byte loads); the
     // next round's loads are issued before the current round is filtered
     constexpr int kRound = kStreamThreads * 16;
@@ -829,13 +829,16 @@ __global__ void __launch_bounds__(kStreamThreads) k_topk_stream(
       if (sm.overflow) return false;
       cnt = int(sm.count[cur]);
       if (cnt > kStreamSoft) {
-        T = stream_threshold(sm, cur, cnt, k, kStreamSoft / 2);
+        T = stream_threshold(sm, cur, cnt, k, keep);
         cnt = stream_compact(sm, cur, cnt, T);
         cur ^= 1;
       }
       return true;
     };
     float4 va[4], vb[4];
+    T = stream_threshold(sm, cur, cnt, k, keep);
+    cnt = stream_compact(sm, cur, cnt, T);
+    cur ^= 1;
     load_round(va, n0);
     for (int base = n0; base < n;) {
       load_round(vb, base + kRound);
