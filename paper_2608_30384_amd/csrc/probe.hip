@@ -4,7 +4,7 @@
 // routing by the dot product with the centres).
 //
 // Both modes are a dense [n x D] x [D x nlist] contraction in float32 on the
-// matrix cores (v_mfma_f32_16x16x4_f32).  Probing writes the dots (32 x 32
+// matrix cores (v_mfma_f32_16x16x4_f32).  Probing writes the dots (64 x 64
 // output tiles) and selects the top-nprobe per row.  Assignment keeps a
 // running (distance, id) minimum per row across all centre tiles (128 x 128
 // output tiles), never writing the product; rows that are not whole 16-byte
@@ -377,90 +377,98 @@ __global__ void __launch_bounds__(256) k_assign_mfma(const float *__restrict__ x
     }
 }
 
-struct IdentityId {
-  __device__ int32_t operator()(int i) const { return i; }
-};
+// Probe dots for D a multiple of 4 and 16-byte aligned operands: a 64 x 64
+// output tile per workgroup, each of the four wavefronts a 32 x 32 block as
+// 2 x 2 MFMA tiles; k staged through LDS in slabs of 32 with the next slab
+// prefetched into registers, the same permuted k within half slabs as the
+// assignment kernel.  Every centre row is read from L2 by n / 64 workgroups.
+constexpr int kPT = 64;
 
-// Probe dots without operand staging (D a multiple of 16): a 32 x 32 output
-// tile is computed by two wavefronts, each over one half of the slabs of 16
-// reduction indices, as 2 x 2 v_mfma_f32_16x16x4f32 tiles with operands read
-// straight from L2 in 16-byte runs.  The reduction index is permuted the same
-// way for both operands: within a slab, lane (m, h) (m = lane % 16, h = lane /
-// 16) supplies k = 4 h + t to MFMA step t, so one float4 per row covers four
-// steps; the next slab is loaded while the current one is multiplied.  The
-// second half's accumulators are added through LDS (one addition of two
-// partial sums: the result does not depend on the order of the waves).
-constexpr int kDTiles = 2;   // output tiles per workgroup (consecutive columns)
-
-__global__ void __launch_bounds__(128 * kDTiles) k_dots_direct(const float *__restrict__ x, int n,
-                                                               int D, const float *__restrict__ cen,
-                                                               int nlist, float *__restrict__ dots) {
-  __shared__ floatx4_t part[kDTiles][4][64];
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int tile = wave >> 1, half = wave & 1;
-  const int r0 = blockIdx.y * 32;
-  const int c0 = (blockIdx.x * kDTiles + tile) * 32;
+__global__ void __launch_bounds__(256) k_dots_tiled(const float *__restrict__ x, int n, int D,
+                                                    const float *__restrict__ cen, int nlist,
+                                                    float *__restrict__ dots) {
+  __shared__ float As[kPT][kAS];
+  __shared__ float Bs[kPT][kAS];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wr = (wave >> 1) * 32, wc = (wave & 1) * 32;
   const int m = lane & 15, h = lane >> 4;
-  // clamped rows / columns: their products are computed and never written
-  const float *a0 = x + int64_t(min(r0 + m, n - 1)) * D + 4 * h;
-  const float *a1 = x + int64_t(min(r0 + 16 + m, n - 1)) * D + 4 * h;
-  const float *b0 = cen + int64_t(min(c0 + m, nlist - 1)) * D + 4 * h;
-  const float *b1 = cen + int64_t(min(c0 + 16 + m, nlist - 1)) * D + 4 * h;
-  const int nslab = D / 16;
-  const int s_lo = half ? nslab / 2 : 0, s_hi = half ? nslab : nslab / 2;
+  const int r0 = blockIdx.y * kPT, c0 = blockIdx.x * kPT;
+  // staging: thread t moves the float4s (row t / 8 + 32 u, column 4 (t % 8)),
+  // u = 0, 1, of a 64 x 32 slab; rows past the end are clamped
+  const int srow = tid >> 3, scol = (tid & 7) * 4;
+  int64_t aoff[2], boff[2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    aoff[u] = int64_t(min(r0 + srow + 32 * u, n - 1)) * D + scol;
+    boff[u] = int64_t(min(c0 + srow + 32 * u, nlist - 1)) * D + scol;
+  }
   floatx4_t acc[2][2];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
-  if (s_lo < s_hi) {
-    int k0 = 16 * s_lo;
-    float4 A0 = *reinterpret_cast<const float4 *>(a0 + k0), A1 = *reinterpret_cast<const float4 *>(a1 + k0);
-    float4 B0 = *reinterpret_cast<const float4 *>(b0 + k0), B1 = *reinterpret_cast<const float4 *>(b1 + k0);
-    for (int sl = s_lo; sl < s_hi; ++sl, k0 += 16) {
-      const int kn = (sl + 1 < s_hi) ? k0 + 16 : k0;   // last slab: reload (no read past the row)
-      const float4 nA0 = *reinterpret_cast<const float4 *>(a0 + kn);
-      const float4 nA1 = *reinterpret_cast<const float4 *>(a1 + kn);
-      const float4 nB0 = *reinterpret_cast<const float4 *>(b0 + kn);
-      const float4 nB1 = *reinterpret_cast<const float4 *>(b1 + kn);
-      const float av[2][4] = {{A0.x, A0.y, A0.z, A0.w}, {A1.x, A1.y, A1.z, A1.w}};
-      const float bv[2][4] = {{B0.x, B0.y, B0.z, B0.w}, {B1.x, B1.y, B1.z, B1.w}};
+  const int nslab = (D + kAK - 1) / kAK;
+  float4 pa[2], pb[2];
+  const bool in0 = scol < D;
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    pa[u] = ld4_or_zero(x + aoff[u], in0);
+    pb[u] = ld4_or_zero(cen + boff[u], in0);
+  }
+  for (int sl = 0; sl < nslab; ++sl) {
+    __syncthreads();   // the previous slab's operand reads are done
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      *reinterpret_cast<float4 *>(&As[srow + 32 * u][scol]) = pa[u];
+      *reinterpret_cast<float4 *>(&Bs[srow + 32 * u][scol]) = pb[u];
+    }
+    __syncthreads();
+    if (sl + 1 < nslab) {
+      const int kn = (sl + 1) * kAK;
+      const bool in = kn + scol < D;
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        pa[u] = ld4_or_zero(x + aoff[u] + kn, in);
+        pb[u] = ld4_or_zero(cen + boff[u] + kn, in);
+      }
+    }
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      float4 a4[2], b4[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        a4[i] = *reinterpret_cast<const float4 *>(&As[wr + 16 * i + m][16 * s + 4 * h]);
+        b4[i] = *reinterpret_cast<const float4 *>(&Bs[wc + 16 * i + m][16 * s + 4 * h]);
+      }
 #pragma unroll
       for (int t = 0; t < 4; ++t)
 #pragma unroll
         for (int i = 0; i < 2; ++i)
 #pragma unroll
-          for (int j = 0; j < 2; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i][t], bv[j][t], acc[i][j], 0, 0, 0);
-      A0 = nA0;
-      A1 = nA1;
-      B0 = nB0;
-      B1 = nB1;
+          for (int j = 0; j < 2; ++j) {
+            const float av = t == 0 ? a4[i].x : t == 1 ? a4[i].y : t == 2 ? a4[i].z : a4[i].w;
+            const float bv = t == 0 ? b4[j].x : t == 1 ? b4[j].y : t == 2 ? b4[j].z : b4[j].w;
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc[i][j], 0, 0, 0);
+          }
     }
   }
-  if (half) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) part[tile][2 * i + j][lane] = acc[i][j];
-  }
-  __syncthreads();
-  if (half || c0 >= nlist) return;
-  // lane holds C[4 (lane / 16) + e][lane % 16] of each 16 x 16 tile
+  // lane holds C[4 h + e][m] of each 16 x 16 tile
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const floatx4_t sum = acc[i][j] + part[tile][2 * i + j][lane];
+    for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const int r = r0 + 16 * i + 4 * h + e;
-        const int c = c0 + 16 * j + m;
-        if (r < n && c < nlist) dots[int64_t(r) * nlist + c] = sum[e];
+        const int r = r0 + wr + 16 * i + 4 * h + e;
+        const int c = c0 + wc + 16 * j + m;
+        if (r < n && c < nlist) dots[int64_t(r) * nlist + c] = acc[i][j][e];
       }
-    }
 }
+
+struct IdentityId {
+  __device__ int32_t operator()(int i) const { return i; }
+};
 
 // Top-nprobe of one row of dots (nlist <= 16,384): 1,024 threads hold the
 // row in registers.  The dots are binned linearly over [min, max] of the row
@@ -634,10 +642,10 @@ int ivf_assign_probe(const float *x, int64_t n, int32_t dim, const float *centro
   int st;
   const bool aligned16 = (reinterpret_cast<uintptr_t>(x) % 16 == 0) &&
                          (reinterpret_cast<uintptr_t>(centroids) % 16 == 0);
-  if (dim % 16 == 0 && aligned16) {   // rows are whole, aligned float4 runs
-    const unsigned gx = unsigned((nlist + 32 * kDTiles - 1) / (32 * kDTiles));
-    hipLaunchKernelGGL(k_dots_direct, dim3(gx, unsigned(gy32)), dim3(128 * kDTiles), 0, s, x, int(n),
-                       dim, centroids, nlist, dots);
+  if (dim % 4 == 0 && aligned16) {   // rows are whole, aligned float4 runs
+    hipLaunchKernelGGL(k_dots_tiled, dim3(unsigned((nlist + kPT - 1) / kPT),
+                                          unsigned((n + kPT - 1) / kPT)),
+                       dim3(256), 0, s, x, int(n), dim, centroids, nlist, dots);
   } else {
     hipLaunchKernelGGL(k_dots_mfma, dim3((nlist + kMT - 1) / kMT, unsigned(gy32)), dim3(256), 0, s,
                        x, n, dim, centroids, nlist, dots);
