@@ -152,7 +152,8 @@ def counter_summary(a_csv, b_csv, n_steps=5):
         return d
     da, db = load(a_csv), load(b_csv)
     kern = [("k_scan<", "scan (a3+a4)"), ("k_topk_stream", "top-k (a5)"),
-            ("k_dots_direct", "probe dots (a2)"), ("k_probe_select_reg", "probe selection (a2)"),
+            ("k_plan_a", "planning, queries (a3-a5)"), ("k_plan_b", "planning, items (a3-a5)"),
+            ("k_dots_tiled", "probe dots (a2)"), ("k_probe_select_reg", "probe selection (a2)"),
             ("k_rotate_reg", "query rotation (a1)"), ("k_rescore_sq8", "rescore (a6)"),
             ("k_encode_rows<6, 4, 2,", "encode with SQ8 codes (a7)")]
 
@@ -165,7 +166,8 @@ def counter_summary(a_csv, b_csv, n_steps=5):
            "(10M x 768, 4-bit)", "",
            "Commands (run from /tmp on one MI355X; `$REPO` is the repository root):", "",
            "```", PROFILE_CMDS["sq_a"], PROFILE_CMDS["sq_b"], "```", "",
-           f"Kernel sources hash: `{csrc_hash()}`.  Averages over the 5 timed steps.  Chip cycles "
+           f"Kernel sources hash: `{csrc_hash()}`.  Averages over the last 5 dispatches of each "
+           "kernel (steps of the same workload).  Chip cycles "
            "= GRBM_GUI_ACTIVE / 8; VALU busy = 4 x SQ_ACTIVE_INST_VALU / 1,024 SIMDs / chip "
            "cycles; VALU lane use = SQ_THREAD_CYCLES_VALU / (64 x SQ_ACTIVE_INST_VALU); MFMA busy = "
            "SQ_VALU_MFMA_BUSY_CYCLES / 1,024 / chip cycles; LDS bank-conflict share = "
@@ -208,9 +210,10 @@ def traffic_summary(fetch_csv, write_csv, cf_csv, cw_csv, bench_json):
     cw = max(_pmc_per_dispatch(cw_csv, "", "WRITE_SIZE"))
     calib = 1 << 30
     ff, wf = calib / (cf * 1024), calib / (cw * 1024)
-    # the scan's launches of the timed steps (the last ones of the run)
-    n = b["steps"]
-    fk, wk = sum(fetch[-n:]) / n, sum(write[-n:]) / n
+    # the scan's launches of the timed steps: after the warm-up launches (the
+    # stage-breakdown and recall passes follow them)
+    n, w0 = b["steps"], b["warmup"]
+    fk, wk = sum(fetch[w0:w0 + n]) / n, sum(write[w0:w0 + n]) / n
     rd, wr = fk * 1024 * ff, wk * 1024 * wf
     return {
         "kernel": b["roofline"]["kernel"],

@@ -166,10 +166,12 @@ __device__ __forceinline__ int item_cands(int sz) {
   return ((sz + nch - 1) / nch + 15) & ~15;
 }
 constexpr int kSizeClasses = kChunkCands / 16;   // item size class = cands / 16 - 1
-constexpr int kPlanThreads = 256;
-constexpr int kPlanRange = 8192;                 // lists counted per pass in LDS
+constexpr int kPlanThreads = 1024;
+constexpr int kPlanQueries = kPlanThreads / 64;   // queries per preparing workgroup
+constexpr int kPlanRange = 8192;                  // lists counted per pass in LDS
 
-// Work items of list L (groups of <= 8 queries x chunks) and their size class.
+// Work items of a list with cp pairs and `size` candidates (groups of <= 8
+// queries x chunks) and their size class.
 __device__ __forceinline__ int list_items(int cp, int size, int max_list, int &cls) {
   const int sz = max(0, min(size, max_list));
   if (cp <= 0 || sz <= 0) return 0;
@@ -188,7 +190,8 @@ struct PlanSmem {
 // passes of kPlanRange), their exclusive scan (pair_off), cursor = 0, and
 // each list's first work item in an order by decreasing item size (counting
 // sort over size classes; the order within a class is immaterial: every item
-// writes its own scores).  Also resets the scan's work counter.
+// writes its own scores).  Also resets the scan's work counter.  Until the
+// class starts are known, item_off[L] holds the list's item count.
 __device__ void plan_lists(PlanSmem &sm, const int32_t *__restrict__ probe_ids, int npairs,
                            const int32_t *__restrict__ sizes, int nlist, int max_list,
                            int32_t *__restrict__ counts, int32_t *__restrict__ pair_off,
@@ -206,7 +209,7 @@ __device__ void plan_lists(PlanSmem &sm, const int32_t *__restrict__ probe_ids, 
       if (L >= L0 && L < L0 + nr) atomicAdd(&sm.cnt[L - L0], 1);
     }
     __syncthreads();
-    // thread t owns the consecutive lists [t * per, (t + 1) * per) of the pass
+    // thread t owns the consecutive lists [a, b) of the pass
     const int per = (nr + kPlanThreads - 1) / kPlanThreads;
     const int a = min(nr, t * per), b = min(nr, a + per);
     int sum = 0;
@@ -216,6 +219,7 @@ __device__ void plan_lists(PlanSmem &sm, const int32_t *__restrict__ probe_ids, 
       int cls = 0;
       const int ni = list_items(cp, sizes[L0 + i], max_list, cls);
       if (ni > 0) atomicAdd(&sm.hist[cls], ni);
+      item_off[L0 + i] = ni;
     }
     sm.part[t] = sum;
     __syncthreads();
@@ -246,16 +250,17 @@ __device__ void plan_lists(PlanSmem &sm, const int32_t *__restrict__ probe_ids, 
     item_off[nlist] = run;
     *work = 0;
   }
-  __syncthreads();   // the counts written above are read back by this workgroup
+  __syncthreads();   // item_off[L] written above is read back by this workgroup
   for (int L = t; L < nlist; L += kPlanThreads) {
+    const int ni = item_off[L];
     int cls = 0;
-    const int ni = list_items(counts[L], sizes[L], max_list, cls);
+    if (ni > 0) (void)list_items(1, sizes[L], max_list, cls);
     item_off[L] = ni > 0 ? atomicAdd(&sm.start[cls], ni) : 0;
   }
 }
 
-// Blocks [0, n_qblocks): four queries each (prep + prefix); the last block
-// plans the lists.
+// Blocks [0, n_qblocks): kPlanQueries queries each (prep + prefix); the last
+// block plans the lists.
 __global__ void __launch_bounds__(kPlanThreads) k_plan_a(
     const float *__restrict__ q_rot, int Q, int D, int d_pad, _Float16 *__restrict__ qh,
     _Float16 *__restrict__ ql, float *__restrict__ qinv, const int32_t *__restrict__ probe_ids,
@@ -264,25 +269,28 @@ __global__ void __launch_bounds__(kPlanThreads) k_plan_a(
     int32_t *__restrict__ pair_off, int32_t *__restrict__ item_off, int32_t *__restrict__ cursor,
     int32_t *__restrict__ work) {
   __shared__ PlanSmem sm;
-  const int n_qblocks = (Q + 3) / 4;
+  const int n_qblocks = (Q + kPlanQueries - 1) / kPlanQueries;
   if (int(blockIdx.x) == n_qblocks) {
     plan_lists(sm, probe_ids, Q * nprobe, sizes, nlist, max_list, counts, pair_off, item_off,
                cursor, work);
     return;
   }
-  const int q = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int q = blockIdx.x * kPlanQueries + (threadIdx.x >> 6);
   if (q >= Q) return;
   prep_query(q_rot, q, D, d_pad, qh, ql, qinv);
   query_prefix(probe_ids, q, nprobe, nlist, sizes, max_list, prefix, totals);
 }
 
 // Threads [0, npairs): pair i joins its list's group (pairs[] grouped by
-// list, slots from a per-list cursor).  Threads [0, nlist) also write the
-// descriptors of list L's work items from item_off[L] on.  Item = (group of
-// <= 8 consecutive pairs of the list, chunk of item_cands(size) candidates):
+// list, slots from a per-list cursor).  Wavefront L (< nlist) writes the
+// descriptors of list L's work items from item_off[L] on, one item per lane.
+// Item = (group of <= 8 consecutive pairs of the list, chunk of
+// item_cands(size) candidates):
 //   d0 = {list, first candidate, candidate count, first pair (in pairs[])}
 //   d1 = {queries in the group, first record (low, high word), 0}
-__global__ void __launch_bounds__(kPlanThreads) k_plan_b(
+constexpr int kPlanBThreads = 256;
+
+__global__ void __launch_bounds__(kPlanBThreads) k_plan_b(
     const int32_t *__restrict__ probe_ids, int npairs, int nlist,
     const int32_t *__restrict__ counts, const int32_t *__restrict__ sizes,
     const int64_t *__restrict__ list_offsets, int max_list, const int32_t *__restrict__ pair_off,
@@ -293,23 +301,24 @@ __global__ void __launch_bounds__(kPlanThreads) k_plan_b(
     const int L = probe_ids[i];
     if (L >= 0 && L < nlist) pairs[pair_off[L] + atomicAdd(&cursor[L], 1)] = i;
   }
-  if (i >= nlist) return;
-  const int L = i;
+  const int L = i >> 6, lane = i & 63;
+  if (L >= nlist) return;
   const int c = counts[L];
   const int sz = max(0, min(sizes[L], max_list));
   if (c <= 0 || sz <= 0) return;
   const int ic = item_cands(sz);
   const int nch = (sz + ic - 1) / ic;
   const int ngr = (c + kGroupQ - 1) / kGroupQ;
-  int it = item_off[L];
-  for (int g = 0; g < ngr; ++g) {
-    for (int ch = 0; ch < nch; ++ch, ++it) {
-      const int cand0 = ch * ic;
-      const int64_t rec0 = list_offsets[L] + cand0;
-      items[2 * int64_t(it)] = make_int4(L, cand0, min(sz - cand0, ic), pair_off[L] + g * kGroupQ);
-      items[2 * int64_t(it) + 1] = make_int4(min(kGroupQ, c - g * kGroupQ), int(uint32_t(rec0)),
-                                             int(uint32_t(uint64_t(rec0) >> 32)), 0);
-    }
+  const int it0 = item_off[L];
+  const int64_t lo = list_offsets[L];
+  for (int t = lane; t < ngr * nch; t += 64) {
+    const int g = t / nch, ch = t - g * nch;
+    const int cand0 = ch * ic;
+    const int64_t rec0 = lo + cand0;
+    const int64_t it = it0 + t;
+    items[2 * it] = make_int4(L, cand0, min(sz - cand0, ic), pair_off[L] + g * kGroupQ);
+    items[2 * it + 1] = make_int4(min(kGroupQ, c - g * kGroupQ), int(uint32_t(rec0)),
+                                  int(uint32_t(uint64_t(rec0) >> 32)), 0);
   }
 }
 
@@ -967,13 +976,15 @@ int rslm_scan_topk(const rslm_plan *p, const rslm_index *idx, const float *q_rot
   hipStream_t s = as_stream(stream);
   const int npairs = Q * nprobe;
   int st;
-  hipLaunchKernelGGL(k_plan_a, dim3((Q + 3) / 4 + 1), dim3(kPlanThreads), 0, s, q_rot, Q,
+  hipLaunchKernelGGL(k_plan_a, dim3((Q + kPlanQueries - 1) / kPlanQueries + 1), dim3(kPlanThreads),
+                     0, s, q_rot, Q,
                      p->rot.D, d_pad, w.qh, w.ql, w.qinv, probe_ids, nprobe, nlist,
                      idx->list_sizes, idx->max_list_size, w.prefix, w.totals, w.counts,
                      w.pair_off, w.item_off, w.cursor, w.work);
   if ((st = check_launch())) return st;
-  hipLaunchKernelGGL(k_plan_b, dim3((std::max(npairs, nlist) + kPlanThreads - 1) / kPlanThreads),
-                     dim3(kPlanThreads), 0, s, probe_ids, npairs, nlist, w.counts,
+  const int64_t planb_threads = std::max<int64_t>(npairs, int64_t(nlist) * 64);
+  hipLaunchKernelGGL(k_plan_b, dim3(unsigned((planb_threads + kPlanBThreads - 1) / kPlanBThreads)),
+                     dim3(kPlanBThreads), 0, s, probe_ids, npairs, nlist, w.counts,
                      idx->list_sizes, idx->list_offsets, idx->max_list_size, w.pair_off,
                      w.item_off, w.cursor, w.pairs, w.items);
   if ((st = check_launch())) return st;
