@@ -690,7 +690,6 @@ def run_capacity(args):
     N, D, nlist, nprobe, B = 100_000_000, 768, 16384, 128, 1024
     nq, k, k_out = 100_000, 100, 10
     BLK = synth.TORCH_BLOCK
-    nblk = (N + BLK - 1) // BLK
     t_setup = time.time()
     plan = R.Plan(D, 4, passes=-1, scale_mode="global")
     plan2 = R.Plan(D, 2, passes=0, scale_mode="global")
@@ -708,38 +707,20 @@ def run_capacity(args):
     torch.cuda.synchronize()
     t_km = time.time()
     log(f"k-means done at {t_km - t_setup:.0f} s; assigning {N} rows")
-    assign = torch.empty(N, dtype=torch.int32, device=dev)
-    for b in range(nblk):
-        xs = block(b)
-        R.ivf_assign_probe(xs, cen, 1, R.IVF_ASSIGN_L2, out_ids=assign[b * BLK:b * BLK + len(xs)])
-        if b % 6 == 5:
-            torch.cuda.synchronize()
-            log(f"  assigned {min(N, (b + 1) * BLK)} rows at {time.time() - t_setup:.0f} s")
+    t_as = None
+
+    def assigned():
+        nonlocal t_as
+        torch.cuda.synchronize()
+        t_as = time.time()
+        log(f"assignment done at {t_as - t_setup:.0f} s")
+    index, codes2, scales2, crot = ivf.build_two_stage_blocked(plan, plan2, block, N, BLK, cen,
+                                                               on_assigned=assigned)
     torch.cuda.synchronize()
-    t_as = time.time()
-    log(f"assignment done at {t_as - t_setup:.0f} s")
-    crot = R.rslm_fwht(plan, cen)
-    offsets, sizes, src_row, rec_list, ids, total = ivf.layout(assign, nlist)
-    del assign
-    codes = torch.zeros(plan.code_bytes(total), dtype=torch.uint8, device=dev)
-    scales = torch.zeros(total, dtype=torch.int32, device=dev)
-    codes2 = torch.zeros((N, plan2.canon_bytes), dtype=torch.uint8, device=dev)
-    scales2 = torch.zeros(N, dtype=torch.int32, device=dev)
-    for b in range(nblk):
-        xs = block(b)
-        lo = b * BLK
-        src_local = src_row - lo    # records of other blocks fall outside [0, rows): skipped
-        R.rslm_encode_two_stage(plan, plan2, xs, codes, scales, codes2[lo:lo + len(xs)],
-                                scales2[lo:lo + len(xs)], n_records=total, src_row=src_local,
-                                rec_list=rec_list, centroids=cen, centroids_rot=crot)
-        del src_local
-    torch.cuda.synchronize()
-    del src_row
-    index = R.Index(offsets, sizes, ids, codes, scales)
-    resident = (codes.numel() + scales.numel() * 4 + codes2.numel() + scales2.numel() * 4 +
-                ids.numel() * 4)
+    resident = (index.codes.numel() + index.scales.numel() * 4 + codes2.numel() +
+                scales2.numel() * 4 + index.ids.numel() * 4)
     t_built = time.time()
-    log(f"index built at {t_built - t_setup:.0f} s: {total} records, max list "
+    log(f"index built at {t_built - t_setup:.0f} s: {index.ids.numel()} records, max list "
         f"{index.max_list_size}, {resident / 1e9:.1f} GB resident")
 
     # bulk two-stage encode rate on one device-resident block (records = rows)
@@ -765,7 +746,7 @@ def run_capacity(args):
     q_all = torch.from_numpy(synth.queries_like("aniso", nq, D, data_seed=100,
                                                 query_seed=200)).to(dev)
     batches = [q_all[i:i + B].contiguous() for i in range(0, nq, B)]
-    work = _streamed(torch, R, cen, batches, nprobe, sizes.long(), nlist)
+    work = _streamed(torch, R, cen, batches, nprobe, index.list_sizes.long(), nlist)
     ws = torch.empty(R.rslm_scan_topk_workspace(plan, index, B, nprobe, k), dtype=torch.uint8,
                      device=dev)
     log(f"setup {time.time() - t_setup:.0f} s; scan workspace {ws.numel() / 1e9:.1f} GB")

@@ -11,7 +11,8 @@ sample of about 256 points per centre.
 import torch
 
 from . import _lib as L
-from .api import Index, ivf_assign_probe, rslm_encode, rslm_fwht, rslm_sq8_encode, rslm_sq8_fit
+from .api import (Index, ivf_assign_probe, rslm_encode, rslm_encode_two_stage, rslm_fwht,
+                  rslm_sq8_encode, rslm_sq8_fit)
 
 
 def kmeans(x, nlist, iters=10, seed=0, sample=None):
@@ -80,3 +81,43 @@ def build_sq8(resid_rot):
     lo, hi = rslm_sq8_fit(resid_rot)
     codes2 = rslm_sq8_encode(resid_rot, lo, hi)
     return codes2, lo, hi
+
+
+def build_two_stage_blocked(plan, plan2, block, n, block_rows, centroids, on_assigned=None,
+                            on_block=None):
+    """Index a collection too large to hold as float32: ``block(b)`` returns
+    rows [b * block_rows, ...) on the device (regenerated on demand).  Rows
+    are assigned block by block, laid out, then encoded block by block into
+    scan records (``plan``) and RSLM rescoring records (``plan2``, indexed by
+    row) with ``rslm_encode_two_stage``: records of other blocks fall outside
+    a block's row range and are skipped.  ``on_assigned()`` runs after the
+    assignment pass and ``on_block(b, rows)`` after each block's encode.
+    Returns (Index, codes2, scales2, R c)."""
+    dev = centroids.device
+    nlist = centroids.shape[0]
+    nblk = (n + block_rows - 1) // block_rows
+    assign = torch.empty(n, dtype=torch.int32, device=dev)
+    for b in range(nblk):
+        xs = block(b)
+        ivf_assign_probe(xs, centroids, 1, L.IVF_ASSIGN_L2,
+                         out_ids=assign[b * block_rows:b * block_rows + len(xs)])
+    if on_assigned is not None:
+        on_assigned()
+    crot = rslm_fwht(plan, centroids)
+    offsets, sizes, src_row, rec_list, ids, total = layout(assign, nlist)
+    del assign
+    codes = torch.zeros(plan.code_bytes(total), dtype=torch.uint8, device=dev)
+    scales = torch.zeros(total, dtype=torch.int32, device=dev)
+    codes2 = torch.zeros((n, plan2.canon_bytes), dtype=torch.uint8, device=dev)
+    scales2 = torch.zeros(n, dtype=torch.int32, device=dev)
+    for b in range(nblk):
+        xs = block(b)
+        lo = b * block_rows
+        src_local = src_row - lo
+        rslm_encode_two_stage(plan, plan2, xs, codes, scales, codes2[lo:lo + len(xs)],
+                              scales2[lo:lo + len(xs)], n_records=total, src_row=src_local,
+                              rec_list=rec_list, centroids=centroids, centroids_rot=crot)
+        del src_local
+        if on_block is not None:
+            on_block(b, xs)
+    return Index(offsets, sizes, ids, codes, scales), codes2, scales2, crot
