@@ -691,7 +691,7 @@ constexpr int kStreamSoft = 2048;
 struct StreamSmem {
   uint64_t buf[2][kStreamCap];
   uint32_t hist[4096];
-  uint32_t bcast[4];
+  uint32_t bcast[4 + kStreamThreads / 64];   // results, then per-wavefront totals
   uint32_t count[2];
   uint32_t overflow;
   int32_t spre[kMaxNprobe], sprobe[kMaxNprobe];
@@ -699,52 +699,92 @@ struct StreamSmem {
 
 // The highest bin bb of hist[0..nb) with above + sum(hist[bb..nb)) >= k, and
 // the count strictly above it, into bcast[0..1].  Every thread must call it.
+// Thread t sums the bins [t per, (t + 1) per); a suffix scan over the threads
+// (within each wavefront by shuffles, then over the wavefronts' totals)
+// gives every thread the count above its bins, and the one thread whose
+// bins hold the boundary walks them (at most four).
 __device__ __forceinline__ void stream_boundary(StreamSmem &sm, int nb, uint32_t above,
                                                 uint32_t k) {
   __syncthreads();
-  if (threadIdx.x < 64) {
-    const int lane = threadIdx.x;
-    const int per = nb / 64;
-    const int hi = nb - lane * per;   // lane 0 owns the highest bins
-    uint32_t sum = 0;
-    for (int b = hi - per; b < hi; ++b) sum += sm.hist[b];
-    uint32_t incl = sum;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int nt = blockDim.x;
+  const int per = nb >= nt ? nb / nt : 1;       // nb and nt are powers of two
+  const int lo = t * per;
+  const bool active = lo < nb;
+  uint32_t sum = 0;
+  if (active)
+    for (int b = lo; b < lo + per; ++b) sum += sm.hist[b];
+  // inclusive suffix scan within the wavefront (higher threads hold higher bins)
+  uint32_t incl = sum;
 #pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const uint32_t t = __shfl_up(incl, off, 64);
-      if (lane >= off) incl += t;
-    }
-    const uint32_t excl = incl - sum;
-    const uint64_t mask = __ballot(above + excl < k && above + incl >= k);
-    const int owner = mask ? __ffsll((unsigned long long)mask) - 1 : 63;
-    if (lane == owner) {
-      uint32_t acc = above + excl;
-      int bb = hi - per;
-      for (int b = hi - 1; b >= hi - per; --b) {
-        if (acc + sm.hist[b] >= k) {
-          bb = b;
-          break;
-        }
-        acc += sm.hist[b];
+  for (int off = 1; off < 64; off <<= 1) {
+    const uint32_t v = __shfl_down(incl, off, 64);
+    if (lane + off < 64) incl += v;
+  }
+  uint32_t *wsum = sm.bcast + 4;   // per-wavefront totals (kStreamThreads / 64 of them)
+  if (lane == 0) wsum[wave] = incl;
+  if (t == 0) {
+    sm.bcast[0] = 0u;
+    sm.bcast[1] = above;
+  }
+  __syncthreads();
+  uint32_t after = 0;   // counts of the wavefronts above this one
+  for (int w = wave + 1; w < nt / 64; ++w) after += wsum[w];
+  incl += after + above;
+  const uint32_t excl = incl - sum;
+  if (active && excl < k && incl >= k) {
+    uint32_t acc = excl;
+    int bb = lo;
+    for (int b = lo + per - 1; b >= lo; --b) {
+      if (acc + sm.hist[b] >= k) {
+        bb = b;
+        break;
       }
-      sm.bcast[0] = uint32_t(bb);
-      sm.bcast[1] = acc;
+      acc += sm.hist[b];
     }
+    sm.bcast[0] = uint32_t(bb);
+    sm.bcast[1] = acc;
   }
   __syncthreads();
 }
 
 // Raises the threshold over the cnt >= k candidates of buffer `cur`: radix
-// passes (12, 12, 8 bits) narrow the bin holding the k-th largest key until
-// at most `target` candidates are at or above its lower edge; returns that
-// edge (never above the k-th largest key).
+// passes of up to 12 bits, starting below the leading bits every candidate
+// shares, narrow the bin holding the k-th largest key until at most `target`
+// candidates are at or above its lower edge; returns that edge (never above
+// the k-th largest key).
 __device__ uint32_t stream_threshold(StreamSmem &sm, int cur, int cnt, int k, int target) {
-  const int tid = threadIdx.x, nt = blockDim.x;
-  uint32_t prefix = 0, above = 0, edge = 0;
-  int pbits = 0;
-  const int digits[3] = {12, 12, 8};
-  for (int di = 0; di < 3; ++di) {
-    const int d = digits[di], nb = 1 << d, shift = 32 - pbits - d;
+  const int tid = threadIdx.x, nt = blockDim.x, lane = tid & 63, wave = tid >> 6;
+  // the leading bits all candidates share: the first digit starts below them
+  uint32_t kmin = 0xffffffffu, kmax = 0u;
+  for (int i = tid; i < cnt; i += nt) {
+    const uint32_t key = uint32_t(sm.buf[cur][i] >> 32);
+    kmin = min(kmin, key);
+    kmax = max(kmax, key);
+  }
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    kmin = min(kmin, uint32_t(__shfl_xor(int(kmin), off, 64)));
+    kmax = max(kmax, uint32_t(__shfl_xor(int(kmax), off, 64)));
+  }
+  __syncthreads();   // hist is free: the previous use of it is complete
+  if (lane == 0) {
+    sm.hist[2 * wave] = kmin;
+    sm.hist[2 * wave + 1] = kmax;
+  }
+  __syncthreads();
+  for (int w = 0; w < nt / 64; ++w) {
+    kmin = min(kmin, sm.hist[2 * w]);
+    kmax = max(kmax, sm.hist[2 * w + 1]);
+  }
+  const uint32_t diff = kmin ^ kmax;
+  if (diff == 0u) return kmin;   // every candidate has the same key
+  int pbits = __clz(diff);
+  uint32_t prefix = pbits ? kmax >> (32 - pbits) : 0u;
+  uint32_t above = 0, edge = 0;
+  while (pbits < 32) {
+    const int d = min(12, 32 - pbits), nb = 1 << d, shift = 32 - pbits - d;
+    __syncthreads();   // the reads of hist above (or of the previous pass) are done
     for (int b = tid; b < nb; b += nt) sm.hist[b] = 0;
     __syncthreads();
     for (int i = tid; i < cnt; i += nt) {
@@ -759,9 +799,9 @@ __device__ uint32_t stream_threshold(StreamSmem &sm, int cur, int cnt, int k, in
     prefix = (prefix << d) | bb;
     pbits += d;
     edge = prefix << (32 - pbits);
-    __syncthreads();
     if (above + in_bin <= uint32_t(target)) break;
   }
+  __syncthreads();
   return edge;
 }
 
