@@ -26,43 +26,54 @@ struct SelectSmem {
     uint64_t buf[kSelCap];
   };
   uint32_t bcast[8];
+  uint32_t wsum[16];   // per-wavefront totals of find_boundary (<= 1,024 threads)
   uint32_t count;
 };
 
 // Find, in hist[0..nb), the highest bin bb with above + sum(hist[bb..]) >= k.
 // Writes bb and the count strictly above it (plus `above`) to sm.bcast[0..1].
+// Thread t sums the bins [t per, (t + 1) per); a suffix scan over the threads
+// (within each wavefront by shuffles, then over the wavefronts' totals)
+// gives every thread the count above its bins, and the one thread whose
+// bins hold the boundary walks them.  nb and blockDim.x are powers of two.
 __device__ __forceinline__ void find_boundary(SelectSmem &sm, int nb, uint32_t above, uint32_t k) {
   __syncthreads();
-  if (threadIdx.x < 64) {
-    const int lane = threadIdx.x;
-    const int per = nb / 64;
-    // lane 0 owns the highest bins
-    const int hi = nb - lane * per;  // bins [hi - per, hi)
-    uint32_t s = 0;
-    for (int b = hi - per; b < hi; ++b) s += sm.hist[b];
-    // inclusive prefix over lanes (from the top)
-    uint32_t incl = s;
-    for (int off = 1; off < 64; off <<= 1) {
-      uint32_t t = __shfl_up(incl, off, 64);
-      if (lane >= off) incl += t;
-    }
-    const uint32_t excl = incl - s;
-    const bool crosses = (above + excl < k) && (above + incl >= k);
-    const uint64_t mask = __ballot(crosses);
-    int owner = mask ? __ffsll((unsigned long long)mask) - 1 : 63;
-    if (lane == owner) {
-      uint32_t acc = above + excl;
-      int bb = hi - per;
-      for (int b = hi - 1; b >= hi - per; --b) {
-        if (acc + sm.hist[b] >= k) {
-          bb = b;
-          break;
-        }
-        acc += sm.hist[b];
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int nt = blockDim.x;
+  const int per = nb >= nt ? nb / nt : 1;
+  const int lo = t * per;
+  const bool active = lo < nb;
+  uint32_t sum = 0;
+  if (active)
+    for (int b = lo; b < lo + per; ++b) sum += sm.hist[b];
+  uint32_t incl = sum;   // inclusive suffix scan (higher threads hold higher bins)
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const uint32_t v = __shfl_down(incl, off, 64);
+    if (lane + off < 64) incl += v;
+  }
+  if (lane == 0) sm.wsum[wave] = incl;
+  if (t == 0) {
+    sm.bcast[0] = 0u;
+    sm.bcast[1] = above;
+  }
+  __syncthreads();
+  uint32_t after = 0;
+  for (int w = wave + 1; w < (nt + 63) / 64; ++w) after += sm.wsum[w];
+  incl += after + above;
+  const uint32_t excl = incl - sum;
+  if (active && excl < k && incl >= k) {
+    uint32_t acc = excl;
+    int bb = lo;
+    for (int b = lo + per - 1; b >= lo; --b) {
+      if (acc + sm.hist[b] >= k) {
+        bb = b;
+        break;
       }
-      sm.bcast[0] = uint32_t(bb);
-      sm.bcast[1] = acc;  // count strictly above bin bb
+      acc += sm.hist[b];
     }
+    sm.bcast[0] = uint32_t(bb);
+    sm.bcast[1] = acc;  // count strictly above bin bb
   }
   __syncthreads();
 }
