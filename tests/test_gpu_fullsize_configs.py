@@ -3,9 +3,10 @@ through the entry points the benchmark uses.
 
 * Mid-size, non-power-of-two dimension: 1,000,000 x 96 unit-norm Gaussian
   mixture rows (1,024 components), 1,024 lists, 4-bit RSLM with global
-  scaling (one rotation pass: the block-wise cascade with an overlapping
-  block), SQ8 rescoring codes; a batch of 256 queries, nprobe = 32, top-100
-  from the scan, top-10 after rescoring.
+  scaling and both rotation passes (the workload exercises the block-wise
+  cascade: overlapping blocks, permutation and strided transpose), SQ8
+  rescoring codes; a batch of 256 queries, nprobe = 32, top-100 from the
+  scan, top-10 after rescoring.
 * Bit-width sweep: 10,000,000 x 1,024 unit-norm anisotropic rows, 4,096
   lists, codes at 1, 2, 3 and 4 bits of the same data (global scaling, two
   passes); a batch of 256 queries, nprobe = 64, top-10.
@@ -47,8 +48,7 @@ def mid():
     gen = torch.Generator(device=dev)
     gen.manual_seed(5)
     cen = x[torch.randperm(MN, generator=gen, device=dev)[:MNLIST]].clone()
-    plan = R.Plan(MD, 4, passes=-1, scale_mode="global")
-    assert plan.passes == 1
+    plan = R.Plan(MD, 4, passes=2, scale_mode="global")
     resid = torch.empty_like(x)
     index, _, assign = ivf.build_index(plan, x, cen, resid_rot=resid)
     codes2, lo, hi = ivf.build_sq8(resid)
@@ -64,7 +64,7 @@ def mid():
                index=index, assign=assign.cpu().numpy(), pos=F.record_positions(torch, index, MN),
                qrot=qrot.cpu().numpy(), pid=pid.cpu().numpy(), pdot=pdot.cpu().numpy(),
                s1=s1.cpu().numpy(), i1=i1.cpu().numpy(), s2=s2.cpu().numpy(),
-               i2=i2.cpu().numpy(), Rm=H.rot(MD, 1), C=synth.codebook(4))
+               i2=i2.cpu().numpy(), Rm=H.rot(MD, 2), C=synth.codebook(4))
     yield out
     del out
     torch.cuda.empty_cache()
