@@ -196,14 +196,7 @@ __global__ void __launch_bounds__(256) k_dots_mfma(const float *__restrict__ x, 
 
 // Assignment on the matrix cores (v_mfma_f32_16x16x4f32, full float32) for
 // D a multiple of 4 and 16-byte aligned operands.  A workgroup owns 128 rows
-// and walks the centres in tiles of 128, in increasing order; each of its
-// four wavefronts computes a 64 x 64 block of the product as 4 x 4 MFMA tiles.
-// The reduction index is staged through LDS in slabs of 32 (rows padded to 36
-// floats, so that the 16-byte operand reads of eight consecutive lanes fall
-// on distinct banks) and the next slab is fetched into registers while the
-// current one is multiplied.  Within a half slab of 16 both operands use the
-// same permutation of k: lane (m, h) (m = lane % 16, h = lane / 16) supplies
-// k = 4 h + t to MFMA step t, so one 16-byte read covers four steps.  After
+// and walks the centres in tiles of 128 (tile128), in increasing order.  After
 // each centre tile the distances ||c||^2 - 2 <x, c> update a (distance, id)
 // minimum per row and lane (centres visited in increasing order with a
 // strict comparison, so the smallest id wins a tie); lanes and the two
@@ -214,6 +207,78 @@ __device__ __forceinline__ float4 ld4_or_zero(const float *p, bool in) {
   float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
   if (in) v = *reinterpret_cast<const float4 *>(p);
   return v;
+}
+
+// The 128 x 128 product tile of rows (staging offsets aoff, four per thread)
+// and centres [c0, c0 + 128) on the matrix cores: four wavefronts of 4 x 4
+// v_mfma_f32_16x16x4f32 tiles, k staged through LDS in slabs of 32 (rows
+// padded to 36 floats, so that the 16-byte operand reads of eight consecutive
+// lanes fall on distinct banks) with the next slab prefetched into registers.
+// Within a half slab of 16 both operands use the same permutation of k: lane
+// (m, h) supplies k = 4 h + t to MFMA step t, so one 16-byte read covers four
+// steps.  Lane (m, h) of wavefront (wr, wc) ends with C[4 h + e][m] of tile
+// (i, j): row wr + 16 i + 4 h + e, centre c0 + wc + 16 j + m.
+__device__ __forceinline__ void tile128(const float *__restrict__ x, const int64_t (&aoff)[4],
+                                        int D, const float *__restrict__ cen, int nlist, int c0,
+                                        float (*As)[kAS], float (*Bs)[kAS],
+                                        floatx4_t (&acc)[4][4]) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wr = (wave >> 1) * 64, wc = (wave & 1) * 64;
+  const int m = lane & 15, h = lane >> 4;
+  const int srow = tid >> 3, scol = (tid & 7) * 4;
+  const int nslab = (D + kAK - 1) / kAK;
+  int64_t boff[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) boff[u] = int64_t(min(c0 + srow + 32 * u, nlist - 1)) * D + scol;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  float4 pa[4], pb[4];
+  const bool in0 = scol < D;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    pa[u] = ld4_or_zero(x + aoff[u], in0);
+    pb[u] = ld4_or_zero(cen + boff[u], in0);
+  }
+  for (int sl = 0; sl < nslab; ++sl) {
+    __syncthreads();   // the previous slab's operand reads are done
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      *reinterpret_cast<float4 *>(&As[srow + 32 * u][scol]) = pa[u];
+      *reinterpret_cast<float4 *>(&Bs[srow + 32 * u][scol]) = pb[u];
+    }
+    __syncthreads();
+    if (sl + 1 < nslab) {
+      const int kn = (sl + 1) * kAK;
+      const bool in = kn + scol < D;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        pa[u] = ld4_or_zero(x + aoff[u] + kn, in);
+        pb[u] = ld4_or_zero(cen + boff[u] + kn, in);
+      }
+    }
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      float4 a4[4], b4[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        a4[i] = *reinterpret_cast<const float4 *>(&As[wr + 16 * i + m][16 * s + 4 * h]);
+        b4[i] = *reinterpret_cast<const float4 *>(&Bs[wc + 16 * i + m][16 * s + 4 * h]);
+      }
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const float av = t == 0 ? a4[i].x : t == 1 ? a4[i].y : t == 2 ? a4[i].z : a4[i].w;
+            const float bv = t == 0 ? b4[j].x : t == 1 ? b4[j].y : t == 2 ? b4[j].z : b4[j].w;
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc[i][j], 0, 0, 0);
+          }
+    }
+  }
 }
 
 __global__ void __launch_bounds__(256) k_assign_mfma(const float *__restrict__ x, int64_t n,
@@ -248,60 +313,9 @@ __global__ void __launch_bounds__(256) k_assign_mfma(const float *__restrict__ x
     best[r] = 3.4e38f;
     bid[r] = 0x7fffffff;
   }
-  const int nslab = (D + kAK - 1) / kAK;
   for (int c0 = 0; c0 < nlist; c0 += kAN) {
-    int64_t boff[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) boff[u] = int64_t(min(c0 + srow + 32 * u, nlist - 1)) * D + scol;
     floatx4_t acc[4][4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
-    float4 pa[4], pb[4];
-    const bool in0 = scol < D;
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      pa[u] = ld4_or_zero(x + aoff[u], in0);
-      pb[u] = ld4_or_zero(cen + boff[u], in0);
-    }
-    for (int sl = 0; sl < nslab; ++sl) {
-      __syncthreads();   // the previous slab's operand reads are done
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        *reinterpret_cast<float4 *>(&As[srow + 32 * u][scol]) = pa[u];
-        *reinterpret_cast<float4 *>(&Bs[srow + 32 * u][scol]) = pb[u];
-      }
-      __syncthreads();
-      if (sl + 1 < nslab) {
-        const int kn = (sl + 1) * kAK;
-        const bool in = kn + scol < D;
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          pa[u] = ld4_or_zero(x + aoff[u] + kn, in);
-          pb[u] = ld4_or_zero(cen + boff[u] + kn, in);
-        }
-      }
-#pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        float4 a4[4], b4[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          a4[i] = *reinterpret_cast<const float4 *>(&As[wr + 16 * i + m][16 * s + 4 * h]);
-          b4[i] = *reinterpret_cast<const float4 *>(&Bs[wc + 16 * i + m][16 * s + 4 * h]);
-        }
-#pragma unroll
-        for (int t = 0; t < 4; ++t)
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              const float av = t == 0 ? a4[i].x : t == 1 ? a4[i].y : t == 2 ? a4[i].z : a4[i].w;
-              const float bv = t == 0 ? b4[j].x : t == 1 ? b4[j].y : t == 2 ? b4[j].z : b4[j].w;
-              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc[i][j], 0, 0, 0);
-            }
-      }
-    }
+    tile128(x, aoff, D, cen, nlist, c0, As, Bs, acc);
     // lane holds C[4 h + e][m] of each 16 x 16 tile: row wr + 16 i + 4 h + e,
     // centre c0 + wc + 16 j + m
 #pragma unroll
@@ -375,6 +389,36 @@ __global__ void __launch_bounds__(256) k_assign_mfma(const float *__restrict__ x
         if (out_d) out_d[r] = xx_s[rl] + v;
       }
     }
+}
+
+// Probe dots for many rows (D a multiple of 4, 16-byte aligned operands): one
+// 128 x 128 tile (tile128) per workgroup, written out.
+__global__ void __launch_bounds__(256) k_dots_big(const float *__restrict__ x, int n, int D,
+                                                  const float *__restrict__ cen, int nlist,
+                                                  float *__restrict__ dots) {
+  __shared__ float As[kAM][kAS];
+  __shared__ float Bs[kAN][kAS];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wr = (wave >> 1) * 64, wc = (wave & 1) * 64;
+  const int m = lane & 15, h = lane >> 4;
+  const int r0 = blockIdx.y * kAM, c0 = blockIdx.x * kAN;
+  const int srow = tid >> 3, scol = (tid & 7) * 4;
+  int64_t aoff[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) aoff[u] = int64_t(min(r0 + srow + 32 * u, n - 1)) * D + scol;
+  floatx4_t acc[4][4];
+  tile128(x, aoff, D, cen, nlist, c0, As, Bs, acc);
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int r = r0 + wr + 16 * i + 4 * h + e;
+        const int c = c0 + wc + 16 * j + m;
+        if (r < n && c < nlist) dots[int64_t(r) * nlist + c] = acc[i][j][e];
+      }
 }
 
 // Probe dots for D a multiple of 4 and 16-byte aligned operands: a 64 x 64
@@ -642,7 +686,12 @@ int ivf_assign_probe(const float *x, int64_t n, int32_t dim, const float *centro
   int st;
   const bool aligned16 = (reinterpret_cast<uintptr_t>(x) % 16 == 0) &&
                          (reinterpret_cast<uintptr_t>(centroids) % 16 == 0);
-  if (dim % 4 == 0 && aligned16) {   // rows are whole, aligned float4 runs
+  const int64_t big_tiles = ((n + kAM - 1) / kAM) * ((nlist + kAN - 1) / kAN);
+  if (dim % 4 == 0 && aligned16 && big_tiles >= 1024) {   // enough 128 x 128 tiles
+    hipLaunchKernelGGL(k_dots_big, dim3(unsigned((nlist + kAN - 1) / kAN),
+                                        unsigned((n + kAM - 1) / kAM)),
+                       dim3(256), 0, s, x, int(n), dim, centroids, nlist, dots);
+  } else if (dim % 4 == 0 && aligned16) {   // rows are whole, aligned float4 runs
     hipLaunchKernelGGL(k_dots_tiled, dim3(unsigned((nlist + kPT - 1) / kPT),
                                           unsigned((n + kPT - 1) / kPT)),
                        dim3(256), 0, s, x, int(n), dim, centroids, nlist, dots);

@@ -168,7 +168,7 @@ __device__ __forceinline__ int item_cands(int sz) {
 constexpr int kSizeClasses = kChunkCands / 16;   // item size class = cands / 16 - 1
 constexpr int kPlanThreads = 1024;
 constexpr int kPlanQueries = kPlanThreads / 64;   // queries per preparing workgroup
-constexpr int kPlanRange = 8192;                  // lists counted per pass in LDS
+constexpr int kPlanRange = 16384;                 // lists counted per pass in LDS
 
 // Work items of a list with cp pairs and `size` candidates (groups of <= 8
 // queries x chunks) and their size class.

@@ -235,7 +235,10 @@ def test_assign_ties_take_the_lowest_id(R, D):
                                               # D not a multiple of 16; nlist above the
                                               # register-resident selection (16,384)
                                               (100, 700, 50, 9), (33, 40, 7, 5),
-                                              (128, 20000, 128, 3)])
+                                              (128, 20000, 128, 3),
+                                              # >= 1,024 tiles of 128 x 128: the large-batch
+                                              # kernel, ragged rows, centres and k slab
+                                              (36, 16500, 40, 1000)])
 def test_probe_parity(R, D, nlist, nprobe, Q):
     rng = np.random.default_rng(nlist)
     cen = rng.standard_normal((nlist, D)).astype(np.float32)
