@@ -112,7 +112,12 @@ def test_capacity_two_stage_encode_sampled(cap):
     sc2 = f["scales2"][t].cpu().numpy().astype(np.uint32)
     sub = {k: (v[ok1] if isinstance(v, np.ndarray) and len(v) == len(ok1) else v)
            for k, v in enc2.items()}
-    assert F.check_codes(g2[ok1], sc2[ok1], sub, f["C2"]).mean() > 0.98
+    # the second stage codes x - a: its windows widen by ||x|| / ||x - a||
+    ra = oracle.first_stage_rotated(enc1["codes"], enc1["s_code"], enc1["g_code"], f["C1"],
+                                    f["Rm"], f["cen"][a[keep]])
+    xk = xs[keep]
+    amp = np.linalg.norm(xk, axis=1) / np.linalg.norm(xk @ f["Rm"].T - ra, axis=1)
+    assert F.check_codes(g2[ok1], sc2[ok1], sub, f["C2"], amp=amp[ok1]).mean() > 0.98
 
 
 @pytest.mark.parametrize("i", [0, 777])
