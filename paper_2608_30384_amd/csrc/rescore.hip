@@ -121,10 +121,15 @@ __global__ void __launch_bounds__(kSq8Threads) k_rescore_sq8(
   const int q = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const float *qr = q_rot + int64_t(q) * dim;
+  const bool wide = (dim & 15) == 0 && (reinterpret_cast<uintptr_t>(codes) & 15) == 0;
+  // wide rows: float4 f of qs is stored at f ^ ((f >> 4) & 3), so that the
+  // 16 lanes of a candidate, reading float4s 4 j + c (j = lane, c fixed),
+  // touch 16 distinct 16-byte bank groups
+  auto slot = [&](int d) { return wide ? (d ^ (((d >> 6) & 3) << 2)) : d; };
   float part = 0.f;
   for (int d = tid; d < dim; d += kSq8Threads) {
     const float step = (hi[d] - lo[d]) / 255.f;
-    qs[d] = qr[d] * step;
+    qs[slot(d)] = qr[d] * step;
     part += qr[d] * lo[d];
   }
   part = wave_sum(part);
@@ -140,7 +145,6 @@ __global__ void __launch_bounds__(kSq8Threads) k_rescore_sq8(
   __syncthreads();   // qs complete
   const int grp = lane >> 4, gl = lane & 15;
   const int ngroups = (kSq8Threads / 64) * 4;
-  const bool wide = (dim & 15) == 0 && (reinterpret_cast<uintptr_t>(codes) & 15) == 0;
   for (int j0 = wave * 4; j0 < k_in; j0 += ngroups) {
     const int j = j0 + grp;
     int32_t id = -1;
@@ -160,8 +164,8 @@ __global__ void __launch_bounds__(kSq8Threads) k_rescore_sq8(
 #pragma unroll 4
         for (int d16 = gl; d16 < nd16; d16 += 16) {
           const uint4 w = cw[d16];
-          dot += dot4(w.x, 16 * d16) + dot4(w.y, 16 * d16 + 4) + dot4(w.z, 16 * d16 + 8) +
-                 dot4(w.w, 16 * d16 + 12);
+          dot += dot4(w.x, slot(16 * d16)) + dot4(w.y, slot(16 * d16 + 4)) +
+                 dot4(w.z, slot(16 * d16 + 8)) + dot4(w.w, slot(16 * d16 + 12));
         }
       } else if ((dim & 3) == 0) {
         const uint32_t *cw = reinterpret_cast<const uint32_t *>(cr);
