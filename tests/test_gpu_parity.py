@@ -338,6 +338,8 @@ SCAN_CASES = [
     (1024, 3, 2, "global", 900, 6, 12, 2, 10, False),
     (1024, 1, 2, "global", 900, 6, 12, 6, 1, False),
     (256, 2, 2, "local", 1500, 30, 50, 30, 1000, False),   # k larger than most candidate sets
+    (64, 4, 1, "global", 30000, 20000, 8, 50, 10, True),   # > 16,384 lists: planned in two
+                                                           # passes, many lists empty
 ]
 
 
