@@ -265,9 +265,10 @@ __device__ __align__(16) const float kZeroRow[1024] = {};
 //      consecutive bits of the canonical record at byte 32 b + 2 r;
 //   2: SQ8 codes with the ranges sq8_lo / sq8_hi, 8 bytes per lane and block.
 // LITE (Rslm4Lite): the lanes holding the first cp.lead coordinates (block 0,
-// r < cp.lead / 8) search the K = 8 thresholds (padded with +inf, so the same
-// four-step search yields codes 0..7) and decode with the K = 8 codebook;
-// their stored code words carry the scale bits in bit 3 of each nibble.
+// r < cp.lead / 8) quantise on the K = 8 codebook's bucket grid and
+// thresholds (padded with +inf, so codes stay 0..7) and decode with that
+// codebook; their stored code words carry the scale bits in bit 3 of each
+// nibble.
 template <int NB, int BITS, int S2, bool LITE = false>
 __global__ void __launch_bounds__(256) k_encode_rows(
     const float *__restrict__ x, int64_t n_rows, const int64_t *__restrict__ src_row,
@@ -307,7 +308,8 @@ __global__ void __launch_bounds__(256) k_encode_rows(
   }
   if (threadIdx.x < 16) {
     cbs[threadIdx.x] = cp.cb[threadIdx.x];
-    // sorted decision thresholds, padded with +inf for the binary search
+    // sorted decision thresholds, padded with +inf (the comparison after the
+    // bucket lookup never passes beyond the last one)
     thr[threadIdx.x] = (int(threadIdx.x) + 1 < K) ? cp.thr[threadIdx.x] : __builtin_inff();
     // S1 sign bits of coordinates 128 p + 8 t + i (p < 2: the signs repeat
     // every 256 coordinates)
