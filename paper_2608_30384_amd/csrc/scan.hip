@@ -169,6 +169,7 @@ constexpr int kSizeClasses = kChunkCands / 16;   // item size class = cands / 16
 constexpr int kPlanThreads = 1024;
 constexpr int kPlanQueries = kPlanThreads / 64;   // queries per preparing workgroup
 constexpr int kPlanRange = 16384;                 // lists counted per pass in LDS
+static_assert(kPlanRange / kPlanThreads == 16, "per-thread list batch");
 
 // Work items of a list with cp pairs and `size` candidates (groups of <= 8
 // queries x chunks) and their size class.
@@ -204,22 +205,36 @@ __device__ void plan_lists(PlanSmem &sm, const int32_t *__restrict__ probe_ids, 
     const int nr = min(kPlanRange, nlist - L0);
     for (int i = t; i < nr; i += kPlanThreads) sm.cnt[i] = 0;
     __syncthreads();
-    for (int i = t; i < npairs; i += kPlanThreads) {
-      const int L = probe_ids[i];
-      if (L >= L0 && L < L0 + nr) atomicAdd(&sm.cnt[L - L0], 1);
+    // batches of 16 pairs per thread: all loads issued before the atomics
+    for (int base = 0; base < npairs; base += 16 * kPlanThreads) {
+      int Ls[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const int i = base + u * kPlanThreads + t;
+        Ls[u] = i < npairs ? probe_ids[i] : -1;
+      }
+#pragma unroll
+      for (int u = 0; u < 16; ++u)
+        if (Ls[u] >= L0 && Ls[u] < L0 + nr) atomicAdd(&sm.cnt[Ls[u] - L0], 1);
     }
     __syncthreads();
-    // thread t owns the consecutive lists [a, b) of the pass
+    // thread t owns the consecutive lists [a, b) of the pass (at most
+    // kPlanRange / kPlanThreads = 16); their sizes are loaded first
     const int per = (nr + kPlanThreads - 1) / kPlanThreads;
     const int a = min(nr, t * per), b = min(nr, a + per);
+    int szv[kPlanRange / kPlanThreads];
+#pragma unroll
+    for (int u = 0; u < kPlanRange / kPlanThreads; ++u) szv[u] = a + u < b ? sizes[L0 + a + u] : 0;
     int sum = 0;
-    for (int i = a; i < b; ++i) {
-      const int cp = sm.cnt[i];
+#pragma unroll
+    for (int u = 0; u < kPlanRange / kPlanThreads; ++u) {
+      if (a + u >= b) break;
+      const int cp = sm.cnt[a + u];
       sum += cp;
       int cls = 0;
-      const int ni = list_items(cp, sizes[L0 + i], max_list, cls);
+      const int ni = list_items(cp, szv[u], max_list, cls);
       if (ni > 0) atomicAdd(&sm.hist[cls], ni);
-      item_off[L0 + i] = ni;
+      item_off[L0 + a + u] = ni;
     }
     sm.part[t] = sum;
     __syncthreads();
@@ -251,11 +266,22 @@ __device__ void plan_lists(PlanSmem &sm, const int32_t *__restrict__ probe_ids, 
     *work = 0;
   }
   __syncthreads();   // item_off[L] written above is read back by this workgroup
-  for (int L = t; L < nlist; L += kPlanThreads) {
-    const int ni = item_off[L];
-    int cls = 0;
-    if (ni > 0) (void)list_items(1, sizes[L], max_list, cls);
-    item_off[L] = ni > 0 ? atomicAdd(&sm.start[cls], ni) : 0;
+  for (int base = 0; base < nlist; base += 16 * kPlanThreads) {   // loads first
+    int niv[16], szv[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const int L = base + u * kPlanThreads + t;
+      niv[u] = L < nlist ? item_off[L] : 0;
+      szv[u] = L < nlist ? sizes[L] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const int L = base + u * kPlanThreads + t;
+      if (L >= nlist) break;
+      int cls = 0;
+      if (niv[u] > 0) (void)list_items(1, szv[u], max_list, cls);
+      item_off[L] = niv[u] > 0 ? atomicAdd(&sm.start[cls], niv[u]) : 0;
+    }
   }
 }
 
