@@ -9,6 +9,7 @@ whose answer is known in advance.
 """
 
 import math
+import os
 
 import numpy as np
 import pytest
@@ -78,12 +79,17 @@ def test_ue7m9_rounding_and_range():
 
 # --- codebooks ---------------------------------------------------------------
 
-MAX_1960 = {   # positive output levels and distortion for N(0,1), J. Max (1960)
-    2: ([0.7980], 0.3634),
-    4: ([0.4528, 1.510], 0.1175),
-    8: ([0.2451, 0.7560, 1.344, 2.152], 0.03454),
-    16: ([0.1284, 0.3881, 0.6568, 0.9424, 1.256, 1.618, 2.069, 2.733], 0.009497),
-}
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def _golden_rows(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return [ln.split() for ln in f if ln.strip() and not ln.startswith("#")]
+
+
+# positive output levels and distortion of the N(0,1) Lloyd-Max quantizers
+MAX_1960 = {int(r[0]): ([float(v) for v in r[2:]], float(r[1]))
+            for r in _golden_rows("lloyd_max_gaussian.txt")}
 
 
 def _mse_1d(c):
@@ -147,11 +153,36 @@ def test_multidim_codebook_lloyd_conditions(bits, scalar_mse):
 # --- packing -----------------------------------------------------------------
 
 def test_packed_sizes_from_paper():
-    assert oracle.canonical_code_bytes(100, 1) == 13        # glove, Rslm1: 13 B + 2
-    assert oracle.canonical_code_bytes(1536, 1) == 192      # openai, Rslm1: 192 B + 2
-    assert oracle.canonical_code_bytes(256, 4) == 128       # Rslm4 at D=256
     assert oracle.canonical_code_bytes(768, 4) == 384
     assert oracle.canonical_code_bytes(1024, 3) == 384
+    rows = _golden_rows("record_sizes.txt")
+    assert len(rows) == 6
+    for _, D, codec, mode, nbytes, lines in rows:
+        bits = int(codec[4])
+        got = oracle.record_bytes(int(D), bits, mode, lite=codec.endswith("Lite"))
+        assert got == int(nbytes), (D, codec, mode)
+        if lines != "-":
+            assert -(-got // 64) == int(lines)
+
+
+def test_codec_table_from_paper():
+    rows = _golden_rows("codec_specs.txt")
+    assert [r[0] for r in rows] == ["Rslm1", "Rslm2", "Rslm3", "Rslm4", "Rslm4Lite"]
+    for codec, bits, g, K, scale in rows:
+        bits, g = int(bits), int(g)
+        if scale == "embedded":
+            k_main, k_lead = (int(v) for v in K.split("/"))
+            assert oracle.codec_shape(bits) == (k_main, g)
+            assert synth.codebook(3).shape == (k_lead, 1)    # the K = 8 lead codebook
+            assert oracle.lite_lead("local") == 16
+            for D in (64, 100, 256, 768):
+                assert oracle.record_bytes(D, bits, "local", lite=True) == -(-D // 2)
+            continue
+        assert oracle.codec_shape(bits) == (int(K), g)
+        assert synth.codebook(bits).shape == (int(K), g)
+        assert scale == "suffix2"
+        for D in (64, 100, 768, 1536):
+            assert oracle.record_bytes(D, bits, "local") == oracle.canonical_code_bytes(D, bits) + 2
 
 
 def test_pack_bit_positions():
