@@ -284,7 +284,9 @@ typedef struct rslm_index {
  * with <q, c_p> = probe_dots; then the k best by (score desc, id asc),
  * padded with (-inf, -1).
  *   q_rot: Q x D rotated queries (rslm_fwht); probe_ids / probe_dots:
- *   Q x nprobe; out_scores / out_ids: Q x k.  1 <= k <= 1024, Q <= 65535.
+ *   Q x nprobe; out_scores / out_ids: Q x k.  1 <= k <= 1024, Q <= 65535,
+ *   nprobe * index->max_list_size < 2^30 (a query's scores are addressed
+ *   with 32-bit byte offsets), else RSLM_ERR_INVALID_ARG.
  *   D <= 1024.  With a Lite plan the scales are read from the codes (the
  *   index's scales array is not used and may be NULL).
  * ------------------------------------------------------------------------ */

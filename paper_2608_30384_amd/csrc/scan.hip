@@ -1027,7 +1027,8 @@ int rslm_scan_topk(const rslm_plan *p, const rslm_index *idx, const float *q_rot
     return RSLM_ERR_INVALID_ARG;
   if (idx->nlist < 1 || idx->nlist > 65536 || nprobe > idx->nlist || idx->max_list_size < 0)
     return RSLM_ERR_INVALID_ARG;
-  if (int64_t(nprobe) * idx->max_list_size >= (int64_t(1) << 31)) return RSLM_ERR_INVALID_ARG;
+  // a query's score region is read through 32-bit byte offsets
+  if (int64_t(nprobe) * idx->max_list_size >= (int64_t(1) << 30)) return RSLM_ERR_INVALID_ARG;
   if (Q == 0) return RSLM_OK;
   if (Q > 65535) return RSLM_ERR_INVALID_ARG;   // gridDim.y of the top-k kernel
   if (!q_rot || !probe_ids || !probe_dots || !out_scores || !out_ids || !idx->list_offsets ||

@@ -253,3 +253,26 @@ def test_lite_ivf_scan_parity(R, D, passes, mode, k):
         tol = H.score_tol(ref_s[i], np.linalg.norm(q[i]), xn)
         diffs += H.check_topk(gs[i], gi[i], ref_s[i], ref_i[i], np.where(np.isfinite(tol), tol, 0))
     assert diffs <= max(1, Q // 10)
+
+
+def test_scan_rejects_oversized_score_regions(R):
+    """nprobe * max_list_size must stay below 2^30 (a query's score region is
+    read with 32-bit byte offsets): at the limit the call returns
+    INVALID_ARG, one below it gets as far as the workspace check; neither
+    launches anything."""
+    import ctypes as C
+    from paper_2608_30384_amd import _lib as L
+    plan = R.Plan(64, 4, passes=0, scale_mode="global")
+    nlist, nprobe, Q, k = 64, 64, 1, 10
+    buf = torch.zeros(4096, dtype=torch.int64, device=DEV)
+    p = buf.data_ptr()
+    q = torch.zeros((Q, 64), dtype=torch.float32, device=DEV)
+    pid = torch.zeros((Q, nprobe), dtype=torch.int32, device=DEV)
+    out = torch.zeros((Q, k), dtype=torch.float32, device=DEV)
+    for max_list, want in (((1 << 30) // nprobe, 1), ((1 << 30) // nprobe - 1, 4)):
+        idx = L.Index(nlist, max_list, p, p, p, p, p)
+        st = L.lib().rslm_scan_topk(plan.handle, C.byref(idx), q.data_ptr(), Q, pid.data_ptr(),
+                                    out.data_ptr(), nprobe, k, out.data_ptr(), pid.data_ptr(),
+                                    p, 0, None)
+        assert st == want, (max_list, st)
+    torch.cuda.synchronize()
