@@ -532,7 +532,7 @@ __device__ __forceinline__ void score_tile(const uint32_t (&tw)[W], uint32_t sc,
 }
 
 template <int BITS, int NC, bool LITE = false>
-__global__ void __launch_bounds__(kScanThreads) k_scan(ScanArgs a) {
+__global__ void __launch_bounds__(kScanThreads, 2) k_scan(ScanArgs a) {
   using T = DecodeTab<BITS>;
   __shared__ uint32_t dtab[T::kEntries * 64 * T::kWords];
   __shared__ uint32_t ltab[LITE ? 256 : 1];
