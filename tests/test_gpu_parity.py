@@ -335,6 +335,7 @@ SCAN_CASES = [
     (768, 4, 2, "local", 1200, 5, 9, 5, 17, False),
     (100, 1, 2, "global", 2000, 10, 25, 4, 10, False),
     (101, 3, 2, "global", 2000, 10, 25, 4, 10, False),
+    (1024, 4, 2, "global", 900, 6, 12, 3, 10, False),     # 32 chunks at 4 bits: 256 VGPRs
     (1024, 3, 2, "global", 900, 6, 12, 2, 10, False),
     (1024, 1, 2, "global", 900, 6, 12, 6, 1, False),
     (256, 2, 2, "local", 1500, 30, 50, 30, 1000, False),   # k larger than most candidate sets

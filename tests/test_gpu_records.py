@@ -204,7 +204,7 @@ def test_decode_parity(R, D, bits, passes, mode, lite):
 
 
 @pytest.mark.parametrize("D,passes,mode,k", [(768, 2, "global", 100), (256, 1, "local", 10),
-                                             (128, 1, "global", 25)])
+                                             (128, 1, "global", 25), (1024, 2, "global", 10)])
 def test_lite_ivf_scan_parity(R, D, passes, mode, k):
     """The IVF scan over Rslm4Lite records (scales read from the codes; no
     scales array) against the oracle's IVF search with the K = 8 leading
