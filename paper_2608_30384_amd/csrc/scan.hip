@@ -942,14 +942,20 @@ __global__ void __launch_bounds__(kStreamThreads) k_topk_stream(
       out[i] = composite(uint32_t(e >> 32), f(int(e & 0xffffffffu)));
     }
     __syncthreads();
+    float *os = out_s + int64_t(q) * k;
+    int32_t *oi = out_i + int64_t(q) * k;
+    if (cnt <= nt) {
+      rank_emit(out, cnt, k, os, oi);
+      return;
+    }
     sort_desc_buf(out, cnt);
     for (int j = tid; j < k; j += nt) {
       if (j < cnt) {
-        out_s[int64_t(q) * k + j] = key_to_float(uint32_t(out[j] >> 32));
-        out_i[int64_t(q) * k + j] = int32_t(0xffffffffu - uint32_t(out[j] & 0xffffffffu));
+        os[j] = key_to_float(uint32_t(out[j] >> 32));
+        oi[j] = int32_t(0xffffffffu - uint32_t(out[j] & 0xffffffffu));
       } else {
-        out_s[int64_t(q) * k + j] = -__builtin_inff();
-        out_i[int64_t(q) * k + j] = -1;
+        os[j] = -__builtin_inff();
+        oi[j] = -1;
       }
     }
     return;

@@ -129,8 +129,38 @@ __device__ __forceinline__ void for_each_key(const float *__restrict__ vals, int
 }
 
 // Sorts the collected survivors and writes the k best (padding when fewer).
+// The k best of buf[0..cnt) (cnt <= blockDim.x, composites as above) in
+// (score desc, id asc) order, (-inf, -1) padded: one entry per thread, whose
+// rank is the number of entries ahead of it (equal composites ordered by
+// slot).  One pass instead of a sort's barrier-separated stages.
+__device__ __forceinline__ void rank_emit(const uint64_t *buf, int cnt, int k,
+                                          float *__restrict__ out_s, int32_t *__restrict__ out_i) {
+  const int t = threadIdx.x;
+  if (t < cnt) {
+    const uint64_t e = buf[t];
+    int r = 0;
+    for (int j = 0; j < cnt; ++j) {
+      const uint64_t v = buf[j];
+      r += (v > e) || (v == e && j < t);
+    }
+    if (r < k) {
+      out_s[r] = key_to_float(uint32_t(e >> 32));
+      out_i[r] = int32_t(0xffffffffu - uint32_t(e & 0xffffffffu));
+    }
+  }
+  for (int j = cnt + t; j < k; j += blockDim.x) {
+    out_s[j] = -__builtin_inff();
+    out_i[j] = -1;
+  }
+}
+
 __device__ __forceinline__ void emit_sorted(SelectSmem &sm, int cnt, int k, float *__restrict__ out_s,
                                             int32_t *__restrict__ out_i) {
+  if (cnt <= int(blockDim.x)) {
+    __syncthreads();   // the entries written by other threads are visible
+    rank_emit(sm.buf, cnt, k, out_s, out_i);
+    return;
+  }
   sort_desc(sm, cnt);
   for (int j = threadIdx.x; j < k; j += blockDim.x) {
     if (j < cnt) {
