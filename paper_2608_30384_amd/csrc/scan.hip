@@ -183,7 +183,7 @@ __device__ __forceinline__ int list_items(int cp, int size, int max_list, int &c
 
 struct PlanSmem {
   int32_t cnt[kPlanRange];
-  int32_t part[kPlanThreads];
+  int32_t part[kPlanThreads / 64];   // per-wavefront totals
   int32_t hist[kSizeClasses], start[kSizeClasses];
 };
 
@@ -236,15 +236,24 @@ __device__ void plan_lists(PlanSmem &sm, const int32_t *__restrict__ probe_ids, 
       if (ni > 0) atomicAdd(&sm.hist[cls], ni);
       item_off[L0 + a + u] = ni;
     }
-    sm.part[t] = sum;
-    __syncthreads();
-    for (int off = 1; off < kPlanThreads; off <<= 1) {   // inclusive scan of the parts
-      const int v = (t >= off) ? sm.part[t - off] : 0;
-      __syncthreads();
-      sm.part[t] += v;
-      __syncthreads();
+    // exclusive prefix of the threads' sums: an inclusive scan within each
+    // wavefront by shuffles, then the totals of the wavefronts before it
+    const int lane = t & 63, wv = t >> 6;
+    int incl = sum;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int v = __shfl_up(incl, off, 64);
+      if (lane >= off) incl += v;
     }
-    int run = carry + sm.part[t] - sum;
+    if (lane == 63) sm.part[wv] = incl;
+    __syncthreads();
+    int before = 0, total = 0;
+    for (int w = 0; w < kPlanThreads / 64; ++w) {
+      const int v = sm.part[w];
+      before += w < wv ? v : 0;
+      total += v;
+    }
+    int run = carry + before + incl - sum;
     for (int i = a; i < b; ++i) {
       const int cp = sm.cnt[i];
       counts[L0 + i] = cp;
@@ -252,7 +261,7 @@ __device__ void plan_lists(PlanSmem &sm, const int32_t *__restrict__ probe_ids, 
       pair_off[L0 + i] = run;
       run += cp;
     }
-    carry += sm.part[kPlanThreads - 1];
+    carry += total;
     __syncthreads();
   }
   if (t == 0) {
