@@ -383,7 +383,7 @@ def main():
         print(json.dumps(traffic_summary(*args.traffic_summary), indent=1))
         return
     if args.gpus != 1:
-        print(json.dumps({"error": "this build measures one GPU only; run with --gpus 1"}))
+        print(json.dumps({"error": "the benchmark runs on one GPU only (the scan has no multi-GPU path); run with --gpus 1"}))
         sys.exit(2)
     if args.workload == "capacity":
         return run_capacity(args)

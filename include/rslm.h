@@ -37,7 +37,7 @@ extern "C" {
 typedef enum rslm_status {
   RSLM_OK = 0,
   RSLM_ERR_INVALID_ARG = 1,   /* null pointer, size or enum out of range */
-  RSLM_ERR_UNSUPPORTED = 2,   /* valid request this build does not implement */
+  RSLM_ERR_UNSUPPORTED = 2,   /* valid request the library does not implement */
   RSLM_ERR_HIP = 3,           /* a HIP launch or runtime call failed */
   RSLM_ERR_WORKSPACE = 4,     /* ws_bytes smaller than the *_workspace size */
   RSLM_ERR_NO_DEVICE = 5      /* no usable gfx950 device is current */
