@@ -10,6 +10,7 @@
 // candidates (16 lanes per candidate, dword loads across coordinates) and
 // sorts them in LDS.
 #include "rslm_internal.h"
+#include "select_dev.h"
 
 namespace rslm {
 
@@ -73,6 +74,10 @@ constexpr int kRescoreThreads = 256;
 __device__ void sort_emit(uint64_t *buf, int n, int q, int k_out, float *__restrict__ out_s,
                           int32_t *__restrict__ out_i) {
   const int tid = threadIdx.x;
+  if (n <= int(blockDim.x)) {   // one candidate per thread: order by rank counting
+    rank_emit(buf, n, k_out, out_s + int64_t(q) * k_out, out_i + int64_t(q) * k_out);
+    return;
+  }
   int p2 = 1;
   while (p2 < n) p2 <<= 1;
   for (int i = n + tid; i < p2; i += blockDim.x) buf[i] = 0ull;
