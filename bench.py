@@ -31,6 +31,10 @@ sys.path.insert(0, ROOT)
 
 METRIC = "scored candidates/sec + achieved HBM GB/s, 4-bit d=768 IVF scan, 1 GPU"
 HBM_PEAK_GBPS = 8000.0
+# The scan's arithmetic: decoded centroids (exact in float16) times the
+# rotated query split into two float16 halves (hi + lo, about 22 significant
+# bits) on the matrix cores, products exact, accumulated in float32.
+SCAN_DTYPE = "split-f16 mfma, f32 accumulate"
 
 
 def log(*a):
@@ -53,13 +57,14 @@ def parse():
     ap.add_argument("--bits", type=int, default=4)
     ap.add_argument("--kmeans-iters", type=int, default=10)
     ap.add_argument("--encode-chunk", type=int, default=65536)
-    ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--lite", action="store_true",
                     help="text768 workload with Rslm4Lite records (scales in the codes)")
-    ap.add_argument("--workload", choices=("text768", "capacity", "sweep", "onetomany"),
+    ap.add_argument("--workload", choices=("text768", "mid", "capacity", "sweep", "onetomany"),
                     default="text768",
-                    help="text768 (default): the metric's configuration; capacity: 100M x 768 "
+                    help="text768 (default): the metric's configuration; mid: 1M x 96 unit-norm "
+                         "Gaussian mixture (1,024 components), nlist 1,024, 4-bit two-pass RSLM "
+                         "+ SQ8 rescoring, nprobe 32; capacity: 100M x 768 "
                          "at nlist 16,384 with 2-bit RSLM rescoring records; sweep: 10M x 1,024 "
                          "unit-norm at 1, 2, 3 and 4 bits with recall@10; onetomany: the paper's "
                          "codec microbenchmarks (OneToMany scoring at D = 256, contiguous and "
@@ -75,7 +80,11 @@ def parse():
                              "BENCH_JSON"),
                     help="print the scan kernel's HBM traffic per launch from rocprofv3 "
                          "FETCH_SIZE / WRITE_SIZE runs and a copy calibration, and exit")
-    return ap.parse_args()
+    args = ap.parse_args()
+    if args.workload == "mid":
+        # the mid-size, non-power-of-two configuration (both rotation passes)
+        args.n, args.dim, args.nlist, args.nprobe = 1_000_000, 96, 1024, 32
+    return args
 
 
 # ------------------------------------------------------------------ profile summaries
@@ -301,73 +310,129 @@ _CPU = {}
 
 
 def _cpu_query(i):
+    """One query of the batch through the oracle: its probed lists' canonical
+    records are unpacked and their scales decoded (input preparation, timed
+    apart), then the LUT-route scan and the top-k (timed)."""
     import oracle
     d = _CPU
-    i = i % len(d["pid"])
     t0 = time.perf_counter()
+    lists = []
+    for L in d["pid"][i]:
+        o, n = int(d["offs"][L]), int(d["sizes"][L])
+        if n == 0:
+            continue
+        sc = d["scales"][o:o + n]
+        lists.append((oracle.unpack_canonical(d["canon"][o:o + n], d["bits"], d["n_sub"]),
+                      np.array([oracle.dec_ue7m9(int(v) & 0xFFFF) for v in sc]),
+                      np.array([oracle.dec_ue4m12(int(v) >> 16) for v in sc]),
+                      d["ids"][o:o + n]))
+    t1 = time.perf_counter()
     all_s, all_i = [], []
     pairs = 0
-    for j, L in enumerate(d["pid"][i]):
-        rec = d["lists"][L]
-        s = oracle.scan_scores_lut(d["qrot"][i], d["pdot"][i, j], rec["codes"], rec["s_hat"],
-                                   rec["g_hat"], d["C"])
+    j = 0
+    for jj, L in enumerate(d["pid"][i]):
+        if int(d["sizes"][L]) == 0:
+            continue
+        codes, sh, gh, ids = lists[j]
+        j += 1
+        s = oracle.scan_scores_lut(d["qrot"][i], d["pdot"][i, jj], codes, sh, gh, d["C"])
         all_s.append(s)
-        all_i.append(rec["ids"])
+        all_i.append(ids)
         pairs += len(s)
-    oracle.topk(np.concatenate(all_s), np.concatenate(all_i), d["k"])
-    return pairs, time.perf_counter() - t0
+    if all_s:
+        oracle.topk(np.concatenate(all_s), np.concatenate(all_i), d["k"])
+    return pairs, time.perf_counter() - t1, t1 - t0, os.getpid()
 
 
-def cpu_baseline(R, plan, index, qrot, pid, pdot, k, budget_s):
-    """The oracle's LUT-route scan + top-k on the host cores, bounded sample."""
+def _cpu_encode(lo_hi):
+    """Rows [lo, hi) of the encode sample through the oracle: codes and
+    scales, the rotated second residual and its SQ8 codes."""
+    import oracle
+    d = _CPU
+    lo, hi = lo_hi
+    t0 = time.perf_counter()
+    xs = d["xe"][lo:hi]
+    cen = d["cen"][d["ae"][lo:hi]]
+    enc = oracle.encode(xs, d["Rm"], d["C"], d["bits"], centroids=cen, scale_mode="global")
+    ra = oracle.first_stage_rotated(enc["codes"], enc["s_code"], enc["g_code"], d["C"], d["Rm"],
+                                    cen)
+    r2 = xs @ d["Rm"].T - ra
+    oracle.sq8_encode(r2, d["sq8_lo"], d["sq8_hi"])
+    return hi - lo, time.perf_counter() - t0, os.getpid()
+
+
+def _per_worker_wall(res, t_index, pid_index):
+    """The busiest worker's summed time: the wall time of the timed parts."""
+    tot = {}
+    for r in res:
+        tot[r[pid_index]] = tot.get(r[pid_index], 0.0) + r[t_index]
+    return max(tot.values())
+
+
+def cpu_baseline(R, plan, index, qrot, pid, pdot, k, xe_rows, cen, n_encode=1 << 17):
+    """The oracle on the host cores, on bounded samples of the workload:
+    (1) the LUT-route scan + top-k of every query of the first batch over its
+    probed lists (the index's records unpacked to the oracle's canonical
+    codes); (2) the encode of the first n_encode collection vectors (codes,
+    scales, rotated second residual, SQ8 codes), against the oracle's own
+    assignment of them, computed beforehand."""
     import multiprocessing as mp
 
     import oracle
     import synth
 
     workers = max(1, min(16, os.cpu_count() or 1))
-    nq_max = min(qrot.shape[0], 8)      # queries whose probed lists are unpacked to the host
-    pid_h = pid[:nq_max].cpu().numpy()
-    need = sorted(set(pid_h.reshape(-1).tolist()))
-    offs = index.list_offsets.cpu().numpy()
-    sizes = index.list_sizes.cpu().numpy()
-    ids_all = index.ids
     K, g = oracle.codec_shape(plan.bits)
     n_sub = -(-plan.dim // g)
-    lists = {}
-    for L in need:
-        o, s = int(offs[L]), int(sizes[L])
-        if s == 0:
-            lists[L] = {"codes": np.zeros((0, n_sub), np.uint8), "s_hat": np.zeros(0),
-                        "g_hat": np.zeros(0), "ids": np.zeros(0, np.int64)}
-            continue
-        tiles = index.codes[(o // 16) * plan.tile_bytes:(o // 16 + (s + 15) // 16) * plan.tile_bytes]
-        canon = R.rslm_unpack_codes(plan, tiles.contiguous(), s).cpu().numpy()
-        sc = index.scales[o:o + s].cpu().numpy().astype(np.uint32)
-        lists[L] = {"codes": oracle.unpack_canonical(canon, plan.bits, n_sub).astype(np.uint8),
-                    "s_hat": np.array([oracle.dec_ue7m9(int(v) & 0xFFFF) for v in sc]),
-                    "g_hat": np.array([oracle.dec_ue4m12(int(v) >> 16) for v in sc]),
-                    "ids": ids_all[o:o + s].cpu().numpy().astype(np.int64)}
-    _CPU.update(pid=pid_h, pdot=pdot[:nq_max].cpu().numpy().astype(np.float64),
-                qrot=qrot[:nq_max].cpu().numpy().astype(np.float64), lists=lists,
-                C=synth.codebook(plan.bits), k=k)
-    # calibrate on one query, then size the sample to ~budget_s of wall time;
-    # the tasks cycle over the unpacked queries
-    p1, t1 = _cpu_query(0)
-    nq = int(workers * max(1, budget_s // max(t1, 1e-3)))
+    total = index.ids.numel()
+    canon = R.rslm_unpack_codes(plan, index.codes, total).cpu().numpy()
+    Rm = oracle.rotation_matrix(plan.dim, plan.passes, synth.sign_table(),
+                                synth.permutation_table())
+    xe = xe_rows.cpu().numpy().astype(np.float64)
+    cen_h = cen.cpu().numpy().astype(np.float64)
+    ae, _ = oracle.assign_l2_expanded(xe, cen_h)
+    # SQ8 ranges of the sample's own second residuals (oracle), as fitted ranges
+    enc0 = oracle.encode(xe[:4096], Rm, synth.codebook(plan.bits), plan.bits,
+                         centroids=cen_h[ae[:4096]], scale_mode="global")
+    ra0 = oracle.first_stage_rotated(enc0["codes"], enc0["s_code"], enc0["g_code"],
+                                     synth.codebook(plan.bits), Rm, cen_h[ae[:4096]])
+    sq8_lo, sq8_hi = oracle.sq8_fit(xe[:4096] @ Rm.T - ra0)
+    _CPU.update(pid=pid.cpu().numpy(), pdot=pdot.cpu().numpy().astype(np.float64),
+                qrot=qrot.cpu().numpy().astype(np.float64), canon=canon,
+                scales=index.scales.cpu().numpy().astype(np.uint32),
+                ids=index.ids.cpu().numpy().astype(np.int64),
+                offs=index.list_offsets.cpu().numpy(), sizes=index.list_sizes.cpu().numpy(),
+                bits=plan.bits, n_sub=n_sub, C=synth.codebook(plan.bits), k=k, xe=xe,
+                cen=cen_h, ae=ae, Rm=Rm, sq8_lo=sq8_lo, sq8_hi=sq8_hi)
     os.environ.setdefault("OMP_NUM_THREADS", "1")
     ctx = mp.get_context("fork")
-    t0 = time.perf_counter()
+    nq = qrot.shape[0]
     with ctx.Pool(workers) as pool:
+        t0 = time.perf_counter()
         res = pool.map(_cpu_query, range(nq), chunksize=1)
-    wall = time.perf_counter() - t0
+        wall_q = time.perf_counter() - t0
+        chunk = 2048
+        t0 = time.perf_counter()
+        res_e = pool.map(_cpu_encode, [(a, min(len(xe), a + chunk))
+                                       for a in range(0, len(xe), chunk)], chunksize=1)
+        wall_e = time.perf_counter() - t0
     pairs = sum(r[0] for r in res)
-    return {"value": pairs / wall, "unit": "scored candidates/s", "cores": workers,
+    scan_wall = _per_worker_wall(res, 1, 3)
+    enc_wall = _per_worker_wall(res_e, 1, 2)
+    _CPU.clear()
+    return {"value": pairs / scan_wall, "unit": "scored candidates/s", "cores": workers,
             "kind": "oracle",
-            "sample": (f"oracle LUT-route scan + top-{k} (float64 NumPy), {nq} query scans cycling "
-                       f"over the first {nq_max} queries of the first batch and their probed "
-                       f"{plan.dim}-d {plan.bits}-bit lists ({pairs} pairs, {wall:.1f} s wall, "
-                       f"{workers} worker processes)")}
+            "sample": (f"oracle LUT-route scan + top-{k} (float64 NumPy) of all {nq} queries of "
+                       f"the first batch over their probed {plan.dim}-d {plan.bits}-bit lists "
+                       f"({pairs} pairs); rate = pairs / the busiest of {workers} worker "
+                       f"processes' summed scan time ({scan_wall:.1f} s; {wall_q:.1f} s wall "
+                       f"including the per-query unpacking of canonical records)"),
+            "encode": {"value": len(xe) / enc_wall, "unit": "vectors/s", "cores": workers,
+                       "sample": (f"oracle encode (codes, UE7M9/UE4M12 scales, rotated second "
+                                  f"residual, SQ8 codes; float64 NumPy, dense rotation) of the "
+                                  f"first {len(xe)} collection vectors against the oracle's own "
+                                  f"assignment, {workers} worker processes, {enc_wall:.1f} s "
+                                  f"(busiest worker), {wall_e:.1f} s wall")}}
 
 
 # ------------------------------------------------------------------ main
@@ -411,18 +476,26 @@ def main():
         return
 
     N, D, nlist = args.n, args.dim, args.nlist
+    mid = args.workload == "mid"
     t_setup = time.time()
-    log(f"generating {N} x {D} vectors on device")
-    x = synth.aniso_torch(N, D, alpha=1.0, seed=100, device=dev)
-    q_all = torch.from_numpy(synth.queries_like("aniso", args.nq, D, data_seed=100,
-                                                query_seed=200)).to(dev)
+    log(f"generating {N} x {D} vectors")
+    if mid:
+        # unit-norm Gaussian mixture of 1,024 components (host generator)
+        x = torch.from_numpy(synth.gmix(N, D, 1024, seed=100)).to(dev)
+        q_all = torch.from_numpy(synth.queries_like("gmix", args.nq, D, data_seed=100,
+                                                    query_seed=200, n_comp=1024)).to(dev)
+    else:
+        x = synth.aniso_torch(N, D, alpha=1.0, seed=100, device=dev)
+        q_all = torch.from_numpy(synth.queries_like("aniso", args.nq, D, data_seed=100,
+                                                    query_seed=200)).to(dev)
     torch.cuda.synchronize()
     log(f"k-means: {nlist} lists, {args.kmeans_iters} iterations on {min(N, 256 * nlist)} points")
     t0 = time.time()
     cen = ivf.kmeans(x, nlist, iters=args.kmeans_iters, seed=0, sample=256 * nlist)
     torch.cuda.synchronize()
     log(f"k-means done in {time.time() - t0:.1f} s")
-    plan = R.Plan(D, args.bits, passes=-1, scale_mode="global", lite=args.lite)
+    # the mid-size configuration exercises the block-wise cascade: two passes
+    plan = R.Plan(D, args.bits, passes=2 if mid else -1, scale_mode="global", lite=args.lite)
     resid = torch.empty_like(x)
     t0 = time.time()
     index, crot, assign = ivf.build_index(plan, x, cen, resid_rot=resid)
@@ -433,7 +506,11 @@ def main():
     del resid
     torch.cuda.synchronize()
     # a chunk of new vectors for the per-step encode (row a7)
-    xe = synth.aniso_torch(args.encode_chunk, D, alpha=1.0, seed=300, device=dev)
+    if mid:
+        xe = torch.from_numpy(synth.gmix(args.encode_chunk, D, 1024, seed=300,
+                                         mean_seed=100)).to(dev)
+    else:
+        xe = synth.aniso_torch(args.encode_chunk, D, alpha=1.0, seed=300, device=dev)
     ae, _ = R.ivf_assign_probe(xe, cen, 1, R.IVF_ASSIGN_L2)
     codes_e = torch.empty(plan.code_bytes(args.encode_chunk), dtype=torch.uint8, device=dev)
     scales_e = torch.empty(args.encode_chunk, dtype=torch.int32, device=dev)
@@ -456,7 +533,8 @@ def main():
         m = torch.bincount(pl, minlength=nlist)
         groups = (m + 7) // 8
         streamed = int((groups * sizes).sum().item())
-        work.append((pairs, streamed))
+        distinct = int(sizes[m > 0].sum().item())     # records of the lists probed at all
+        work.append((pairs, streamed, distinct))
 
     ws_scan = torch.empty(R.rslm_scan_topk_workspace(plan, index, args.batch, args.nprobe, args.k),
                           dtype=torch.uint8, device=dev)
@@ -522,11 +600,12 @@ def main():
     steps_b = [(args.warmup + s) % len(batches) for s in range(args.steps)]
     pairs_total = sum(work[b][0] for b in steps_b)
     streamed_avg = sum(work[b][1] for b in steps_b) / args.steps
+    distinct_avg = sum(work[b][2] for b in steps_b) / args.steps
     pairs_avg = pairs_total / args.steps
     ms_per_step = wall * 1e3 / args.steps
     value = pairs_total / wall
     achieved = streamed_avg * rec_bytes / (t_scan * 1e-3) / 1e9
-    traffic = traffic_from_profiles(streamed_avg)
+    traffic = None if (mid or args.lite) else traffic_from_profiles(streamed_avg)
     enc_ms = stage["encode"] / args.steps
     enc_bytes = args.encode_chunk * (4 * D + rec_bytes + D)
 
@@ -541,13 +620,15 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": SCAN_DTYPE,
         "data": "synthetic",
         "config": {
-            "workload": (f"text-embedding shaped IVF scan: N={N:,} x d={D} anisotropic Gaussian "
-                         f"(power-law spectrum, exponent 1, mean offset, unnormalised), "
+            "workload": ((f"mid-size IVF scan: N={N:,} x d={D} unit-norm Gaussian mixture "
+                          f"(1,024 components, sigma 0.3), " if mid else
+                          f"text-embedding shaped IVF scan: N={N:,} x d={D} anisotropic Gaussian "
+                          f"(power-law spectrum, exponent 1, mean offset, unnormalised), ") +
                          f"nlist={nlist}, {args.bits}-bit RSLM{'4Lite' if args.lite else ''} "
-                         f"global scale + SQ8 rescore, "
+                         f"global scale ({plan.passes} rotation passes) + SQ8 rescore, "
                          f"batches of {args.batch} queries, nprobe={args.nprobe}, "
                          f"top-{args.k} -> top-{args.k_out}; each step also encodes "
                          f"{args.encode_chunk:,} vectors"),
@@ -568,6 +649,12 @@ def main():
             "stream_read_GBps_measured": stream_read_GBps,
             "stream_read_kernel": stream_read_cfg,
             "frac_of_measured_stream": achieved / stream_read_GBps,
+            # the same kernel time under the two other byte models: every
+            # scored (query, candidate) pair reading its record, and every
+            # record of a list the batch probes read once
+            "frac_pair_equivalent": pairs_avg * rec_bytes / (t_scan * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+            "frac_min_bytes": distinct_avg * rec_bytes / (t_scan * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+            "min_bytes_per_launch": distinct_avg * rec_bytes,
         },
         "scan": {
             "pairs_per_step": pairs_avg,
@@ -636,11 +723,12 @@ def main():
     }
     if not args.no_cpu_baseline and not args.lite:
         log("CPU oracle baseline")
-        qb = batches[0]
         qrot, pid, pdot = step(0, None)
         torch.cuda.synchronize()
+        del codes2
+        torch.cuda.empty_cache()
         out["cpu_baseline"] = cpu_baseline(R, plan, index, qrot, pid, pdot, args.k,
-                                           args.cpu_seconds)
+                                           x[:min(N, 1 << 17)], cen)
     print(json.dumps(out), flush=True)
 
 
@@ -783,7 +871,7 @@ def run_capacity(args):
         "n_gpus": 1, "steps": len(batches), "warmup": args.warmup,
         "ms_per_step": wall * 1e3 / len(batches),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "f32", "data": "synthetic",
+        "dtype": SCAN_DTYPE, "data": "synthetic",
         "config": {"workload": ("capacity: N=100,000,000 x d=768 anisotropic Gaussian, "
                                 "nlist=16384, 4-bit RSLM global + 2-bit RSLM global rescoring "
                                 "records resident, 100,000 queries in batches of 1,024, "
@@ -899,7 +987,7 @@ def run_sweep(args):
         "value": res["4"]["scored_candidates_per_s"], "unit": "scored candidates/s",
         "n_gpus": 1, "steps": len(batches), "warmup": args.warmup,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "f32", "data": "synthetic",
+        "dtype": SCAN_DTYPE, "data": "synthetic",
         "config": {"workload": ("bit-width sweep: N=10,000,000 x d=1024 anisotropic Gaussian, "
                                 "unit norm, nlist=4096, RSLM 1/2/3/4-bit global, 10,000 queries "
                                 "in batches of 256, nprobe=64, top-10"),

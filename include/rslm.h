@@ -260,6 +260,22 @@ int ivf_assign_probe(const float *x, int64_t n, int32_t dim,
                      size_t ws_bytes, void *stream);
 
 /* ------------------------------------------------------------------------
+ * ivf_kmeans_update -- the centre update of one Lloyd iteration of the
+ * Euclidean k-means that partitions the collection (Section "End-to-End
+ * Comparison", Setup): given each point's centre (IVF_ASSIGN_L2),
+ *   centroids[p] = mean of the rows x_i with assign[i] == p,
+ * evaluated as float64 sums rounded once to float32; a centre with no points
+ * keeps its value.  Assignments outside [0, nlist) are ignored.
+ *   x: n x dim float32; assign: n int32; centroids: nlist x dim float32,
+ *   read and written in place.  n < 2^31, nlist <= 65536, dim <= 2^20; all
+ *   arrays 4-byte aligned, else RSLM_ERR_INVALID_ARG.
+ * ------------------------------------------------------------------------ */
+size_t ivf_kmeans_update_workspace(int64_t n, int32_t nlist);
+int ivf_kmeans_update(const float *x, int64_t n, int32_t dim, const int32_t *assign,
+                      int32_t nlist, float *centroids, void *ws, size_t ws_bytes,
+                      void *stream);
+
+/* ------------------------------------------------------------------------
  * IVF index of RSLM records (caller-owned device arrays).  List L holds
  * list_sizes[L] records starting at record list_offsets[L] (a multiple of
  * 16, the tile size); record r has id ids[r], packed codes in tile r/16 and
@@ -286,8 +302,9 @@ typedef struct rslm_index {
  *   q_rot: Q x D rotated queries (rslm_fwht); probe_ids / probe_dots:
  *   Q x nprobe; out_scores / out_ids: Q x k.  1 <= k <= 1024, Q <= 65535,
  *   nprobe * index->max_list_size < 2^30 (a query's scores are addressed
- *   with 32-bit byte offsets), else RSLM_ERR_INVALID_ARG.
- *   D <= 1024.  With a Lite plan the scales are read from the codes (the
+ *   with 32-bit byte offsets), else RSLM_ERR_INVALID_ARG.  Alignment:
+ *   index->codes 16 bytes, list_offsets 8 bytes, every other array 4 bytes,
+ *   else RSLM_ERR_INVALID_ARG.  D <= 1024.  With a Lite plan the scales are read from the codes (the
  *   index's scales array is not used and may be NULL).
  * ------------------------------------------------------------------------ */
 size_t rslm_scan_topk_workspace(const rslm_plan *plan, const rslm_index *index,
@@ -352,12 +369,13 @@ int rslm_rescore(const rslm_rescore_codec *codec, const float *q_rot,
                  int32_t *out_ids, void *stream);
 
 /* ------------------------------------------------------------------------
- * Profiling hook (not part of the method): later rslm_scan_topk calls record
- * ev_begin / ev_end (hipEvent_t passed as void*, created by the caller) on
- * their stream immediately before and after one of their kernels:
+ * Profiling hook (not part of the method): later rslm_scan_topk calls made
+ * by the calling host thread record ev_begin / ev_end (hipEvent_t passed as
+ * void*, created by the caller) on their stream immediately before and after
+ * one of their kernels:
  *   RSLM_TIMER_SCAN: the scan kernel;  RSLM_TIMER_TOPK: the top-k kernel.
- * Both NULL disables.  The setting is process-wide and not synchronised:
- * set it from one thread while no rslm_scan_topk call is in flight.
+ * Both NULL disables.  The setting belongs to the calling thread (thread-
+ * local), so calls from other threads are unaffected and never timed by it.
  * ------------------------------------------------------------------------ */
 #define RSLM_TIMER_SCAN 0
 #define RSLM_TIMER_TOPK 1

@@ -29,7 +29,8 @@ from .codec import (
 )
 from .search import (
     assign_l2, assign_l2_expanded, probe_ip, kmeans, scan_scores_lut, scan_scores_dense, topk,
-    ivf_search, sq8_fit, sq8_encode, sq8_decode, rescore_sq8, rescore_rslm, brute_force_mips,
+    ivf_candidates, ivf_search, sq8_fit, sq8_encode, sq8_decode, rescore_sq8, rescore_sq8_scores,
+    rescore_rslm, rescore_rslm_scores, brute_force_mips,
 )
 
 __all__ = [n for n in dir() if not n.startswith("_")]

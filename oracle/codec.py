@@ -161,16 +161,20 @@ def encode(x, R, C, bits, centroids=None, scale_mode="global", chunk=512, C_lead
         chat = chat[:, :D]
         rn = np.linalg.norm(r, axis=1)
         cn = np.linalg.norm(chat, axis=1)
+        sh = np.zeros(hi - lo)
         for i in range(hi - lo):
             row = lo + i
             s = rn[i] / cn[i] if (nz[i] and cn[i] > 0) else 0.0
             su = enc_ue7m9(s)
             s_pre[row], s_code[row] = s, su
-            if scale_mode == "global":
-                a = cen[row] + (dec_ue7m9(su) * chat[i]) @ R   # c + R^T (s^ c^)
-                an = np.linalg.norm(a)
-                gv = np.linalg.norm(x[row]) / an if an > 0 else 0.0
-                g_pre[row], g_code[row] = gv, enc_ue4m12(gv)
+            sh[i] = dec_ue7m9(su)
+        if scale_mode == "global":
+            a = cen[lo:hi] + (sh[:, None] * chat) @ R        # c + R^T (s^ c^), row-wise
+            an = np.linalg.norm(a, axis=1)
+            xn = np.linalg.norm(x[lo:hi], axis=1)
+            for i in range(hi - lo):
+                gv = xn[i] / an[i] if an[i] > 0 else 0.0
+                g_pre[lo + i], g_code[lo + i] = gv, enc_ue4m12(gv)
         codes[lo:hi] = cd
         u_all[lo:hi] = u
     return {"codes": codes, "s_code": s_code, "g_code": g_code,

@@ -82,11 +82,18 @@ def probe_ip(q, centroids, nprobe):
     return ids, vals, dots
 
 
-def kmeans(x, nlist, iters=10, seed=0):
-    """Euclidean k-means (Lloyd): random distinct-point init, fixed iterations."""
+def kmeans(x, nlist, iters=10, seed=0, init=None):
+    """Euclidean k-means (Lloyd): random distinct-point init (or the given
+    initial centres), fixed iterations; each iteration assigns every point to
+    its nearest centre (lowest id on ties) and moves each centre to the mean
+    of its points, an empty cluster keeping its centre."""
     x = np.asarray(x, dtype=np.float64)
-    rng = np.random.default_rng(seed)
-    c = x[rng.choice(len(x), nlist, replace=False)].copy()
+    if init is None:
+        rng = np.random.default_rng(seed)
+        c = x[rng.choice(len(x), nlist, replace=False)].copy()
+    else:
+        c = np.array(init, dtype=np.float64)
+        assert c.shape == (nlist, x.shape[1])
     for _ in range(iters):
         a, _ = assign_l2(x, c)
         for p in range(nlist):
@@ -134,28 +141,40 @@ def topk(scores, ids, k):
     return out_s, out_i
 
 
-def ivf_search(q, q_rot, centroids, lists, C, nprobe, k, C_lead=None, lead=0):
-    """Route, scan (LUT route) and select for a batch of queries.
+def ivf_candidates(q, q_rot, centroids, lists, C, nprobe, C_lead=None, lead=0):
+    """Route and scan (LUT route): every candidate of every probed list.
 
     ``lists[p]`` = dict(ids, codes (n_p, n_sub), s_hat (n_p,), g_hat (n_p,)).
     Rslm4Lite: the first ``lead`` codes look up C_lead.
-    Returns (scores (Q, k), ids (Q, k), probe ids (Q, nprobe)).
+    Returns (probe ids (Q, nprobe), per query a pair (scores, ids) over the
+    members of its probed lists, in probe order).
     """
     pid, pdot, _ = probe_ip(q, centroids, nprobe)
-    Q = len(q)
-    out_s = np.full((Q, k), -np.inf)
-    out_i = np.full((Q, k), -1, dtype=np.int64)
-    for i in range(Q):
-        all_s, all_i = [], []
+    out = []
+    for i in range(len(q)):
+        all_s, all_i = [np.zeros(0)], [np.zeros(0, dtype=np.int64)]
         for j in range(nprobe):
             L = lists[int(pid[i, j])]
             if len(L["ids"]) == 0:
                 continue
             all_s.append(scan_scores_lut(q_rot[i], pdot[i, j], L["codes"],
                                          L["s_hat"], L["g_hat"], C, C_lead, lead))
-            all_i.append(L["ids"])
-        if all_s:
-            out_s[i], out_i[i] = topk(np.concatenate(all_s), np.concatenate(all_i), k)
+            all_i.append(np.asarray(L["ids"], dtype=np.int64))
+        out.append((np.concatenate(all_s), np.concatenate(all_i)))
+    return pid, out
+
+
+def ivf_search(q, q_rot, centroids, lists, C, nprobe, k, C_lead=None, lead=0):
+    """Route, scan (LUT route) and select for a batch of queries.
+
+    Returns (scores (Q, k), ids (Q, k), probe ids (Q, nprobe)).
+    """
+    pid, cands = ivf_candidates(q, q_rot, centroids, lists, C, nprobe, C_lead, lead)
+    Q = len(q)
+    out_s = np.full((Q, k), -np.inf)
+    out_i = np.full((Q, k), -1, dtype=np.int64)
+    for i, (s, ids) in enumerate(cands):
+        out_s[i], out_i[i] = topk(s, ids, k)
     return out_s, out_i, pid
 
 
@@ -178,22 +197,29 @@ def sq8_decode(codes, lo, hi):
     return lo + codes.astype(np.float64) * step
 
 
-def rescore_sq8(q_rot, cand_scores, cand_ids, codes2, lo, hi, k_out):
-    """score2 = score1 + <q_rot, r~2> over the shortlist, then top-k_out.
+def rescore_sq8_scores(q_rot, cand_scores, cand_ids, codes2, lo, hi):
+    """score2 = score1 + <q_rot, r~2> of every shortlisted candidate.
 
     q_rot: (Q, D); cand_*: (Q, k_in), ids < 0 are empty slots; codes2 (N, D)
-    uint8 indexed by id.
+    uint8 indexed by id.  Returns per query a pair (score2, ids).
     """
+    out = []
+    for i in range(cand_ids.shape[0]):
+        ok = cand_ids[i] >= 0
+        ids = np.asarray(cand_ids[i][ok], dtype=np.int64)
+        r2 = sq8_decode(codes2[ids], lo, hi)
+        s2 = np.asarray(cand_scores[i][ok], dtype=np.float64) + r2 @ q_rot[i]
+        out.append((s2, ids))
+    return out
+
+
+def rescore_sq8(q_rot, cand_scores, cand_ids, codes2, lo, hi, k_out):
+    """score2 = score1 + <q_rot, r~2> over the shortlist, then top-k_out."""
     Q, _ = cand_ids.shape
     out_s = np.full((Q, k_out), -np.inf)
     out_i = np.full((Q, k_out), -1, dtype=np.int64)
-    for i in range(Q):
-        ok = cand_ids[i] >= 0
-        ids = cand_ids[i][ok]
-        if len(ids) == 0:
-            continue
-        r2 = sq8_decode(codes2[ids], lo, hi)
-        s2 = np.asarray(cand_scores[i][ok], dtype=np.float64) + r2 @ q_rot[i]
+    for i, (s2, ids) in enumerate(rescore_sq8_scores(q_rot, cand_scores, cand_ids, codes2,
+                                                     lo, hi)):
         out_s[i], out_i[i] = topk(s2, ids, k_out)
     return out_s, out_i
 
@@ -208,19 +234,28 @@ def rescore_rslm(q_rot, cand_scores, cand_ids, codes2, s2_code, g2_code, C2, k_o
     cand_* are (Q, k_in) with ids < 0 for empty slots.
     """
     Q, _ = cand_ids.shape
-    sh = np.array([dec_ue7m9(u) for u in s2_code])
-    gh = np.array([dec_ue4m12(u) for u in g2_code])
     out_s = np.full((Q, k_out), -np.inf)
     out_i = np.full((Q, k_out), -1, dtype=np.int64)
-    for i in range(Q):
-        ok = cand_ids[i] >= 0
-        ids = cand_ids[i][ok]
-        if len(ids) == 0:
-            continue
-        s1 = np.asarray(cand_scores[i][ok], dtype=np.float64)
-        s2 = scan_scores_lut(q_rot[i], s1, codes2[ids], sh[ids], gh[ids], C2)
+    for i, (s2, ids) in enumerate(rescore_rslm_scores(q_rot, cand_scores, cand_ids, codes2,
+                                                      s2_code, g2_code, C2)):
         out_s[i], out_i[i] = topk(s2, ids, k_out)
     return out_s, out_i
+
+
+def rescore_rslm_scores(q_rot, cand_scores, cand_ids, codes2, s2_code, g2_code, C2):
+    """score2 of every shortlisted candidate under the RSLM rescoring codec
+    (see ``rescore_rslm``); per query a pair (score2, ids)."""
+    sh = np.array([dec_ue7m9(u) for u in s2_code])
+    gh = np.array([dec_ue4m12(u) for u in g2_code])
+    out = []
+    for i in range(cand_ids.shape[0]):
+        ok = cand_ids[i] >= 0
+        ids = np.asarray(cand_ids[i][ok], dtype=np.int64)
+        s1 = np.asarray(cand_scores[i][ok], dtype=np.float64)
+        s2 = scan_scores_lut(q_rot[i], s1, codes2[ids], sh[ids], gh[ids], C2) if len(ids) \
+            else np.zeros(0)
+        out.append((s2, ids))
+    return out
 
 
 def brute_force_mips(q, x, k):

@@ -35,16 +35,23 @@ def _need(t, dtype, name):
 
 
 class _Workspace:
-    """Grow-only scratch buffer per device and purpose."""
+    """Grow-only scratch buffer per device, stream and purpose.
+
+    Keyed by stream as well: calls on different streams never share a buffer
+    (they would race), and a buffer is allocated while its stream is current,
+    so torch's caching allocator ties it to that stream and does not hand its
+    memory to another stream while a kernel there may still use it."""
 
     def __init__(self):
         self._bufs = {}
 
-    def get(self, nbytes, device, key):
-        k = (str(device), key)
+    def get(self, nbytes, device, key, stream=None):
+        s = stream if stream is not None else torch.cuda.current_stream(device)
+        k = (str(device), s.cuda_stream, key)
         b = self._bufs.get(k)
         if b is None or b.numel() < nbytes:
-            b = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+            with torch.cuda.stream(s):
+                b = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
             self._bufs[k] = b
         return b
 
@@ -270,11 +277,29 @@ def ivf_assign_probe(x, centroids, nprobe=1, mode=L.IVF_ASSIGN_L2, out_ids=None,
     if out_scores is None:
         out_scores = torch.empty(shape, dtype=torch.float32, device=x.device)
     nb = L.lib().ivf_assign_probe_workspace(n, dim, nlist, nprobe, mode)
-    ws = _WS.get(nb, x.device, "probe")
+    ws = _WS.get(nb, x.device, "probe", stream)
     L.check("ivf_assign_probe", L.lib().ivf_assign_probe(
         _ptr(x), n, dim, _ptr(centroids), nlist, nprobe, mode, _ptr(out_ids),
         _ptr(out_scores), _ptr(ws), ws.numel(), _stream(stream)))
     return out_ids, out_scores
+
+
+def ivf_kmeans_update(x, assign, centroids, stream=None):
+    """One Lloyd centre update in place: centroids[p] = mean of the rows of x
+    assigned to p (an empty centre keeps its value)."""
+    _need(x, torch.float32, "x")
+    _need(assign, torch.int32, "assign")
+    _need(centroids, torch.float32, "centroids")
+    n, dim = x.shape
+    if assign.numel() != n or centroids.dim() != 2 or centroids.shape[1] != dim:
+        raise ValueError("assign must have n entries and centroids nlist x dim")
+    nlist = centroids.shape[0]
+    nb = L.lib().ivf_kmeans_update_workspace(n, nlist)
+    ws = _WS.get(nb, x.device, "kmeans", stream)
+    L.check("ivf_kmeans_update", L.lib().ivf_kmeans_update(
+        _ptr(x), n, dim, _ptr(assign), nlist, _ptr(centroids), _ptr(ws), ws.numel(),
+        _stream(stream)))
+    return centroids
 
 
 class Index:
@@ -315,7 +340,7 @@ def rslm_scan_topk(plan, index, q_rot, probe_ids, probe_dots, k, out_scores=None
     cs = index.c_struct()
     nb = L.lib().rslm_scan_topk_workspace(plan.handle, C.byref(cs), Q, nprobe, k)
     if ws is None:
-        ws = _WS.get(nb, q_rot.device, "scan")
+        ws = _WS.get(nb, q_rot.device, "scan", stream)
     L.check("rslm_scan_topk", L.lib().rslm_scan_topk(
         plan.handle, C.byref(cs), _ptr(q_rot), Q, _ptr(probe_ids), _ptr(probe_dots), nprobe, k,
         _ptr(out_scores), _ptr(out_ids), _ptr(ws), ws.numel(), _stream(stream)))

@@ -884,7 +884,10 @@ __global__ void __launch_bounds__(kStreamThreads) k_topk_stream(
     constexpr int kRound = kStreamThreads * 16;
     // range-checked loads (unconditional, zeros past the region): the range
     // is n rounded up to whole 16-byte groups, inside the region's stride
-    const __amdgpu_buffer_rsrc_t rr = make_rsrc(row, uint32_t((n + 3) & ~3) * 4u);
+    // (computed in 64 bits: a region of 2^30 - 3 or more scores would wrap)
+    const uint64_t rbytes = uint64_t((int64_t(n) + 3) & ~int64_t(3)) * 4u;
+    const __amdgpu_buffer_rsrc_t rr =
+        make_rsrc(row, uint32_t(rbytes < 0xFFFFFFF0ull ? rbytes : 0xFFFFFFF0ull));
     auto load_round = [&](float4 (&v)[4], int base) {
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
@@ -977,8 +980,9 @@ __global__ void __launch_bounds__(kStreamThreads) k_topk_stream(
 }
 
 // Profiling hook: events recorded around the scan kernel (0) and the top-k
-// kernel (1) of later rslm_scan_topk calls.
-static void *g_timer[2][2] = {{nullptr, nullptr}, {nullptr, nullptr}};
+// kernel (1) of later rslm_scan_topk calls made by the same host thread (the
+// setting is per thread, so calls from other threads are never timed by it).
+static thread_local void *g_timer[2][2] = {{nullptr, nullptr}, {nullptr, nullptr}};
 
 static int record_timer(int which, int end, hipStream_t s) {
   void *ev = g_timer[which][end];
@@ -1048,6 +1052,14 @@ int rslm_scan_topk(const rslm_plan *p, const rslm_index *idx, const float *q_rot
   if (Q > 65535) return RSLM_ERR_INVALID_ARG;   // gridDim.y of the top-k kernel
   if (!q_rot || !probe_ids || !probe_dots || !out_scores || !out_ids || !idx->list_offsets ||
       !idx->list_sizes || !idx->ids || !idx->codes || (!idx->scales && p->codec.lead == 0))
+    return RSLM_ERR_INVALID_ARG;
+  // the tile loads are 16-byte buffer loads; scales, ids and sizes are
+  // read as 4-byte words, offsets as 8-byte words
+  if ((reinterpret_cast<uintptr_t>(idx->codes) & 15) || (reinterpret_cast<uintptr_t>(idx->scales) & 3) ||
+      (reinterpret_cast<uintptr_t>(idx->ids) & 3) || (reinterpret_cast<uintptr_t>(idx->list_sizes) & 3) ||
+      (reinterpret_cast<uintptr_t>(idx->list_offsets) & 7) || (reinterpret_cast<uintptr_t>(q_rot) & 3) ||
+      (reinterpret_cast<uintptr_t>(probe_ids) & 3) || (reinterpret_cast<uintptr_t>(probe_dots) & 3) ||
+      (reinterpret_cast<uintptr_t>(out_scores) & 3) || (reinterpret_cast<uintptr_t>(out_ids) & 3))
     return RSLM_ERR_INVALID_ARG;
   if (p->codec.n_chunks > 32) return RSLM_ERR_UNSUPPORTED;   // D > 1024
   const size_t need = rslm_scan_topk_workspace(p, idx, Q, nprobe, k);

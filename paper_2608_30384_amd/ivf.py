@@ -1,9 +1,10 @@
 """IVF index construction around the librslm kernels.
 
-Build-time bookkeeping (partition training, the record layout of the
-inverted lists) uses torch tensor operations for counting, sorting and
-means; every step of the codec itself (assignment, rotation, encoding, SQ8)
-runs in librslm.  The paper's partitioning (Section "End-to-End
+Partition training runs in librslm (assignment by ``ivf_assign_probe``,
+the centre update by ``ivf_kmeans_update``); the record layout of the
+inverted lists is build-time bookkeeping done with torch tensor operations
+(counting and sorting); every step of the codec itself (rotation, encoding,
+SQ8) runs in librslm.  The paper's partitioning (Section "End-to-End
 Comparison", Setup) is Euclidean k-means with random initialisation on a
 sample of about 256 points per centre.
 """
@@ -11,12 +12,16 @@ sample of about 256 points per centre.
 import torch
 
 from . import _lib as L
-from .api import (Index, ivf_assign_probe, rslm_encode, rslm_encode_two_stage, rslm_fwht,
-                  rslm_sq8_encode, rslm_sq8_fit)
+from .api import (Index, ivf_assign_probe, ivf_kmeans_update, rslm_encode,
+                  rslm_encode_two_stage, rslm_fwht, rslm_sq8_encode, rslm_sq8_fit)
 
 
-def kmeans(x, nlist, iters=10, seed=0, sample=None):
-    """Euclidean k-means on device; assignment by ``ivf_assign_probe``."""
+def kmeans(x, nlist, iters=10, seed=0, sample=None, init=None):
+    """Euclidean k-means (Lloyd) on device: each iteration assigns every point
+    to its nearest centre (``ivf_assign_probe``) and moves each centre to the
+    mean of its points (``ivf_kmeans_update``; an empty centre stays).  The
+    initial centres are ``init`` (nlist x dim) or nlist distinct points drawn
+    with torch's generator seeded by ``seed``."""
     n = x.shape[0]
     gen = torch.Generator(device=x.device)
     gen.manual_seed(int(seed))
@@ -24,14 +29,14 @@ def kmeans(x, nlist, iters=10, seed=0, sample=None):
         xs = x[torch.randperm(n, generator=gen, device=x.device)[:sample]].contiguous()
     else:
         xs = x
-    c = xs[torch.randperm(xs.shape[0], generator=gen, device=x.device)[:nlist]].clone()
+    if init is None:
+        c = xs[torch.randperm(xs.shape[0], generator=gen, device=x.device)[:nlist]].clone()
+    else:
+        c = init.to(device=x.device, dtype=torch.float32).clone().contiguous()
+    a = torch.empty(xs.shape[0], dtype=torch.int32, device=x.device)
     for _ in range(iters):
-        a, _ = ivf_assign_probe(xs, c, 1, L.IVF_ASSIGN_L2)
-        a = a.long()
-        sums = torch.zeros_like(c).index_add_(0, a, xs)
-        cnt = torch.bincount(a, minlength=nlist).to(c.dtype)
-        nz = cnt > 0
-        c[nz] = sums[nz] / cnt[nz, None]
+        ivf_assign_probe(xs, c, 1, L.IVF_ASSIGN_L2, out_ids=a)
+        ivf_kmeans_update(xs, a, c)
     return c.contiguous()
 
 

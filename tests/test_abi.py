@@ -70,6 +70,14 @@ def test_calls_validate_arguments_without_device():
     assert lib.ivf_assign_probe(null, 4, 8, null, 16, 17, 1, null, null, null, 0, null) == 1
     assert lib.rslm_sq8_fit(null, 4, 0, null, null, 0, null) == 1
     assert lib.rslm_encode(null, null, 0, null, null, 0, null, null, 0, null, null, null, null) == 1
+    assert lib.ivf_kmeans_update(null, 4, 8, null, 0, null, null, 0, null) == 1      # nlist 0
+    assert lib.ivf_kmeans_update(null, 4, 8, null, 16, null, null, 0, null) == 1     # no centres
+    assert lib.ivf_kmeans_update(null, 4, 0, null, 16, C.c_void_p(256), null, 0, null) == 1
+    assert lib.ivf_kmeans_update(C.c_void_p(0x1002), 4, 8, C.c_void_p(256), 16, C.c_void_p(256),
+                                 C.c_void_p(256), 1 << 20, null) == 1              # misaligned
+    assert lib.ivf_kmeans_update(C.c_void_p(256), 4, 8, C.c_void_p(256), 16, C.c_void_p(256),
+                                 C.c_void_p(256), 16, null) == 4                   # workspace
+    assert lib.ivf_kmeans_update(null, 0, 8, null, 16, C.c_void_p(256), null, 0, null) == 0
     codec = L.RescoreCodec(7, 8, 10, 0, 0, 0)
     assert lib.rslm_rescore(C.byref(codec), null, 1, null, null, 10, 10, null, null, null) == 2
     codec = L.RescoreCodec(0, 8, 10, 0, 0, 0)
@@ -80,3 +88,4 @@ def test_workspace_sizes_are_host_side():
     lib = L.lib()
     assert lib.ivf_assign_probe_workspace(256, 768, 4096, 64, 1) >= 256 * 4096 * 4
     assert lib.ivf_assign_probe_workspace(256, 768, 4096, 1, 0) >= 4096 * 4
+    assert lib.ivf_kmeans_update_workspace(1000, 16) >= 1000 * 4 + 3 * 16 * 4

@@ -11,11 +11,18 @@ can compute one by one:
 
 * the rotated queries and the probe lists of the whole batch;
 * assignment, codes and scale codes of 1,500 sampled vectors;
-* for two queries, every returned top-100 score, and completeness over the
-  query's best probed list (every member the oracle scores above the GPU's
-  k-th score must have been returned);
-* rescoring: the rescored ids come from the scan's shortlist, in order, and
-  bring the scores much closer to the exact inner products.
+* for two queries, over every member of the query's 64 probed lists (about
+  135,000 rows each, encoded by the oracle against their lists' centres):
+  each returned id's score against the oracle's score of that id, and
+  completeness (every member the oracle scores above the returned k-th
+  score must have been returned); only rows in an encoding near-tie window
+  may differ;
+* rescoring: the SQ8 records of the shortlist against the oracle's second
+  residual of those rows (within half a quantisation step plus the measured
+  float32 error of the residual), the rescored scores against the SQ8
+  decode of the stored records (score1 + <q_rot, lo + code * step>), with
+  the (score desc, id asc) order and ids of that definition, and the
+  rescored scores closer to the exact inner products than the scan's.
 
 Oracle inputs are the seeded data (generated on the device by torch's
 generator and copied to the host) and centres chosen as a seeded sample of
@@ -27,6 +34,7 @@ import pytest
 
 import oracle
 import synth
+from tests import fullsize_common as F
 from tests import helpers as H
 
 torch = pytest.importorskip("torch")
@@ -65,7 +73,8 @@ def full():
     pos[ids_rec[valid]] = torch.arange(ids_rec.numel(), device=dev)[valid]
     canon = R.rslm_unpack_codes(plan, index.codes, ids_rec.numel())
     out = dict(R=R, plan=plan, x=x, cen=cen.cpu().numpy().astype(np.float64), q=q, index=index,
-               assign=assign, pos=pos, canon=canon, qrot=qrot.cpu().numpy(),
+               cen_t=cen, crot=R.rslm_fwht(plan, cen), codes2=codes2, lo=lo.cpu().numpy(),
+               hi=hi.cpu().numpy(), assign=assign, pos=pos, canon=canon, qrot=qrot.cpu().numpy(),
                pid=pid.cpu().numpy(), pdot=pdot.cpu().numpy(), s1=s1.cpu().numpy(),
                i1=i1.cpu().numpy(), s2=s2.cpu().numpy(), i2=i2.cpu().numpy(),
                Rm=H.rot(D, 2), C=synth.codebook(BITS))
@@ -89,17 +98,6 @@ def _gpu_records(f, ids):
     codes = oracle.unpack_canonical(canon, BITS, D)
     sh, gh = H.dec_scales(sc)
     return codes, sc.astype(np.uint32), sh, gh
-
-
-def _oracle_scores(f, i, ids):
-    """Oracle assignment, encoding and exact scan score of vectors `ids` for
-    query i (dense route)."""
-    xs = _rows(f, ids)
-    a, _ = oracle.assign_l2_expanded(xs, f["cen"])
-    enc = oracle.encode(xs, f["Rm"], f["C"], BITS, centroids=f["cen"][a], scale_mode="global")
-    xt = oracle.reconstruct(enc["codes"], enc["s_code"], enc["g_code"], f["C"], f["Rm"],
-                            f["cen"][a])
-    return a, enc, xt @ f["q"][i].astype(np.float64), np.linalg.norm(xt, axis=1), xs
 
 
 def test_rotation_and_probe_full_batch(full):
@@ -150,44 +148,52 @@ def test_assign_and_encode_sampled(full):
 def test_scan_topk_sampled(full, i):
     f = full
     gi, gs = f["i1"][i], f["s1"][i]
-    assert np.all(gi >= 0) and len(set(gi.tolist())) == K
-    assert all(gs[j] > gs[j + 1] or (gs[j] == gs[j + 1] and gi[j] < gi[j + 1]) for j in range(K - 1))
+    F.check_topk_order(gs, gi, K)
     qn = np.linalg.norm(f["q"][i])
-    probed = set(f["pid"][i].tolist())
-    # every returned score against the oracle's own encoding of that vector
-    a, enc, exact, xn, _ = _oracle_scores(f, i, gi)
-    assert np.mean([L in probed for L in a]) >= 0.99
-    tol = H.score_tol(exact, qn, xn)
-    viol = np.abs(gs - exact) > tol
-    assert viol.sum() <= 2, (gs[viol], exact[viol])
-    kth = gs[-1]
-    # completeness over the query's best probed list
-    L = int(f["pid"][i][0])
-    o = int(f["index"].list_offsets[L].item())
-    n_l = int(f["index"].list_sizes[L].item())
-    members = f["index"].ids[o:o + n_l].cpu().numpy().astype(np.int64)
-    am, _, sm, xnm, _ = _oracle_scores(f, i, members)
-    same = am == L
-    assert same.mean() >= 0.99
-    tolm = H.score_tol(sm, qn, xnm)
-    returned = set(gi.tolist())
-    missed = [v for v, s, t, ok in zip(members, sm, tolm, same)
-              if ok and s > kth + t and int(v) not in returned]
-    assert len(missed) <= 1, missed
+    members, lst = F.members_of(torch, f["index"], f["pid"][i])
+    xs = _rows(f, members)
+    # the oracle's own assignment agrees on the best probed list's members
+    best = lst == f["pid"][i][0]
+    a, _ = oracle.assign_l2_expanded(xs[best], f["cen"])
+    assert (a == f["pid"][i][0]).mean() >= 0.99
+    sm, xnm, near, _ = F.oracle_member_scores(xs, lst, f["cen"], f["q"][i], f["Rm"], f["C"], BITS)
+    F.check_probed(gs, gi, members, sm, H.score_tol(sm, qn, xnm), near)
 
 
 @pytest.mark.parametrize("i", [0, 137])
 def test_rescore_sampled(full, i):
     f = full
     ri, rs = f["i2"][i], f["s2"][i]
-    assert set(ri.tolist()) <= set(f["i1"][i].tolist())
-    assert all(rs[j] > rs[j + 1] or (rs[j] == rs[j + 1] and ri[j] < ri[j + 1])
-               for j in range(K_OUT - 1))
-    # the rescored scores approach the exact inner products: over the
-    # shortlist, SQ8 of the second residual must cut the first stage's error
-    cand = f["i1"][i]
-    exact = _rows(f, cand) @ f["q"][i].astype(np.float64)
-    err1 = np.abs(f["s1"][i] - exact)
+    cand, s1 = f["i1"][i], f["s1"][i].astype(np.float64)
+    assert set(ri.tolist()) <= set(cand.tolist())
+    F.check_topk_order(rs, ri, K_OUT)
+    qr = f["q"][i].astype(np.float64) @ f["Rm"].T
+    lo, hi = f["lo"].astype(np.float64), f["hi"].astype(np.float64)
+    step = (hi - lo) / 255.0
+    t = torch.from_numpy(cand.astype(np.int64)).to(f["codes2"].device)
+    c2 = f["codes2"][t].cpu().numpy()
+    # the stored SQ8 records against the oracle's second residual of the rows
+    xs = _rows(f, cand)
+    a, _ = oracle.assign_l2_expanded(xs, f["cen"])
+    enc1 = oracle.encode(xs, f["Rm"], f["C"], BITS, centroids=f["cen"][a], scale_mode="global")
+    err, r2, same, _ = F.r2_error(f["R"], torch, f["plan"], xs, a, f["cen_t"], f["crot"], f["Rm"],
+                               enc1, f["C"], f["cen"])
+    same &= f["assign"][t].cpu().numpy() == a      # the stored records used the same list
+    assert same.mean() >= 0.95
+    bound = F.r2_bound(xs, f["cen"][a])
+    assert np.all(err[same] <= bound[same]), (err / bound).max()
+    assert np.all(r2[same] >= lo - err[same, None]) and np.all(r2[same] <= hi + err[same, None])
+    dec = lo + c2 * step
+    slack = 0.5 * step * (1 + 1e-4) + err[:, None]
+    assert np.all(np.abs(dec - r2)[same] <= slack[same])
+    # the rescoring kernel against the SQ8 decode of the stored records
+    s2 = s1 + dec @ qr
+    ref_s, ref_i = oracle.topk(s2, cand, K_OUT)
+    tol = 1e-5 * (np.abs(s2).max() + np.linalg.norm(qr))
+    H.check_topk(rs, ri, ref_s, ref_i, lambda v: np.full(np.shape(v), tol), s2, cand)
+    # and it brings the scores closer to the exact inner products
+    exact = xs @ f["q"][i].astype(np.float64)
+    err1 = np.abs(s1 - exact)
     sel = np.array([np.nonzero(cand == v)[0][0] for v in ri])
     err2 = np.abs(rs - exact[sel])
     assert np.median(err2) < 0.25 * np.median(err1[sel])

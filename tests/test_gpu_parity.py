@@ -100,6 +100,12 @@ ENC_CASES = [
     (1024, 3, 2, "global"),
     (256, 2, 2, "global"),
     (64, 4, 0, "global"),      # no rotation
+    # above the register path: the paper's odd-D Compress shape (block-wise
+    # cascade with the overlap block) and the 1,536-d text-embedding width
+    (2049, 4, 2, "local"),
+    (2049, 3, 2, "global"),
+    (1536, 1, 2, "global"),
+    (1536, 4, 2, "global"),
 ]
 
 
@@ -354,6 +360,7 @@ def test_scan_topk_parity(R, D, bits, passes, mode, n, nlist, Q, nprobe, k, skew
     qr = q.astype(np.float64) @ Rm.T
     lists = _oracle_lists(enc, assign, nlist)
     ref_s, ref_i, pid = oracle.ivf_search(q, qr, cen, lists, C, nprobe, k)
+    _, cands = oracle.ivf_candidates(q, qr, cen, lists, C, nprobe)
     pdot = (q.astype(np.float64) @ cen.T)[np.arange(Q)[:, None], pid]
     gs, gi = R.rslm_scan_topk(plan, index, _t(qr.astype(np.float32)), _t(pid, torch.int32),
                               _t(pdot.astype(np.float32)), k)
@@ -362,9 +369,9 @@ def test_scan_topk_parity(R, D, bits, passes, mode, n, nlist, Q, nprobe, k, skew
     xn = np.linalg.norm(xt, axis=1).max()
     diffs = 0
     for i in range(Q):
-        tol = H.score_tol(ref_s[i][ref_i[i] >= 0], np.linalg.norm(q[i]), xn)
-        tol = np.concatenate([tol, np.zeros(k - len(tol))])
-        diffs += H.check_topk(gs[i], gi[i], ref_s[i], ref_i[i], tol)
+        qn = np.linalg.norm(q[i])
+        diffs += H.check_topk(gs[i], gi[i], ref_s[i], ref_i[i],
+                              lambda s, qn=qn: H.score_tol(s, qn, xn), *cands[i])
     assert diffs <= max(1, Q // 10)
 
 
@@ -401,13 +408,14 @@ def test_rescore_parity(R, D, k_in, k_out):
     cand[0, 3:] = -1                              # a short shortlist
     s1 = rng.standard_normal((Q, k_in)).astype(np.float32)
     ref_s, ref_i = oracle.rescore_sq8(qr.astype(np.float64), s1, cand, codes2, lo, hi, k_out)
+    cands = oracle.rescore_sq8_scores(qr.astype(np.float64), s1, cand, codes2, lo, hi)
     gs, gi = R.rslm_rescore(_t(codes2), _t(lo.astype(np.float32)), _t(hi.astype(np.float32)),
                             _t(qr), _t(s1), _t(cand), k_out)
     gs, gi = gs.cpu().numpy(), gi.cpu().numpy()
     for i in range(Q):
-        tol = 1e-5 * (np.abs(ref_s[i][np.isfinite(ref_s[i])]).max() + np.linalg.norm(qr[i]))
-        tol = np.full(k_out, tol)
-        H.check_topk(gs[i], gi[i], ref_s[i], ref_i[i], tol)
+        t = 1e-5 * (np.abs(ref_s[i][np.isfinite(ref_s[i])]).max() + np.linalg.norm(qr[i]))
+        H.check_topk(gs[i], gi[i], ref_s[i], ref_i[i], lambda s, t=t: np.full(np.shape(s), t),
+                     *cands[i])
 
 
 # ------------------------------------------------------------------ end to end, tiny config
@@ -465,10 +473,11 @@ def _scan_vs_oracle(R, D, bits, passes, x, cen, assign, q, nprobe, k):
     qr = q.astype(np.float64) @ Rm.T
     lists = _oracle_lists(enc, assign, nlist)
     ref_s, ref_i, pid = oracle.ivf_search(q, qr, cen, lists, C, nprobe, k)
+    _, cands = oracle.ivf_candidates(q, qr, cen, lists, C, nprobe)
     pdot = (q.astype(np.float64) @ cen.T)[np.arange(len(q))[:, None], pid]
     gs, gi = R.rslm_scan_topk(plan, index, _t(qr.astype(np.float32)), _t(pid, torch.int32),
                               _t(pdot.astype(np.float32)), k)
-    return gs.cpu().numpy(), gi.cpu().numpy(), ref_s, ref_i, enc, Rm, C
+    return gs.cpu().numpy(), gi.cpu().numpy(), ref_s, ref_i, enc, Rm, C, cands
 
 
 def test_scan_topk_large_candidate_sets(R):
@@ -479,11 +488,15 @@ def test_scan_topk_large_candidate_sets(R):
     cen = x[rng.choice(n, nlist, replace=False)].astype(np.float64)
     assign, _ = oracle.assign_l2(x, cen)
     q = synth.queries_like("gmix", Q, D, data_seed=77, n_comp=12)
-    gs, gi, ref_s, ref_i, enc, Rm, C = _scan_vs_oracle(R, D, bits, 2, x, cen, assign, q, nprobe, k)
+    gs, gi, ref_s, ref_i, enc, Rm, C, cands = _scan_vs_oracle(R, D, bits, 2, x, cen, assign, q,
+                                                              nprobe, k)
     xt = oracle.reconstruct(enc["codes"], enc["s_code"], enc["g_code"], C, Rm, cen[assign])
     xn = np.linalg.norm(xt, axis=1).max()
-    diffs = sum(H.check_topk(gs[i], gi[i], ref_s[i], ref_i[i],
-                             H.score_tol(ref_s[i], np.linalg.norm(q[i]), xn)) for i in range(Q))
+    diffs = 0
+    for i in range(Q):
+        qn = np.linalg.norm(q[i])
+        diffs += H.check_topk(gs[i], gi[i], ref_s[i], ref_i[i],
+                              lambda s, qn=qn: H.score_tol(s, qn, xn), *cands[i])
     assert diffs <= 1
 
 
@@ -502,7 +515,14 @@ def test_scan_topk_exact_ties(R):
     rng = np.random.default_rng(91)
     cen = np.vstack([x[rng.choice(N, nlist - 1, replace=False)], star[None]]).astype(np.float64)
     assign, _ = oracle.assign_l2(x, cen)
-    gs, gi, ref_s, ref_i, *_ = _scan_vs_oracle(R, D, bits, 2, x, cen, assign, q, nprobe, k)
+    gs, gi, ref_s, ref_i, enc, Rm, C, cands = _scan_vs_oracle(R, D, bits, 2, x, cen, assign, q,
+                                                              nprobe, k)
     assert np.array_equal(gi[0], np.sort(dup)[:k])
     assert np.array_equal(ref_i[0], gi[0])
     assert np.all(gs[0] == gs[0][0])
+    xt = oracle.reconstruct(enc["codes"], enc["s_code"], enc["g_code"], C, Rm, cen[assign])
+    xn = np.linalg.norm(xt, axis=1).max()
+    for i in range(Q):
+        qn = np.linalg.norm(q[i])
+        H.check_topk(gs[i], gi[i], ref_s[i], ref_i[i], lambda s, qn=qn: H.score_tol(s, qn, xn),
+                     *cands[i])

@@ -241,6 +241,7 @@ def test_lite_ivf_scan_parity(R, D, passes, mode, k):
     q = synth.queries_like("aniso", Q, D, data_seed=D + 11, query_seed=3)
     qr = q.astype(np.float64) @ Rm.T
     ref_s, ref_i, pid = oracle.ivf_search(q, qr, cen, lists, C16, nprobe, k, C8, lead)
+    _, cands = oracle.ivf_candidates(q, qr, cen, lists, C16, nprobe, C8, lead)
     pdot = (q.astype(np.float64) @ cen.T)[np.arange(Q)[:, None], pid]
     gs, gi = R.rslm_scan_topk(plan, index, _t(qr.astype(np.float32)), _t(pid, torch.int32),
                               _t(pdot.astype(np.float32)), k)
@@ -250,8 +251,9 @@ def test_lite_ivf_scan_parity(R, D, passes, mode, k):
     xn = np.linalg.norm(xt, axis=1).max()
     diffs = 0
     for i in range(Q):
-        tol = H.score_tol(ref_s[i], np.linalg.norm(q[i]), xn)
-        diffs += H.check_topk(gs[i], gi[i], ref_s[i], ref_i[i], np.where(np.isfinite(tol), tol, 0))
+        qn = np.linalg.norm(q[i])
+        diffs += H.check_topk(gs[i], gi[i], ref_s[i], ref_i[i],
+                              lambda s, qn=qn: H.score_tol(s, qn, xn), *cands[i])
     assert diffs <= max(1, Q // 10)
 
 
@@ -275,4 +277,26 @@ def test_scan_rejects_oversized_score_regions(R):
                                     out.data_ptr(), nprobe, k, out.data_ptr(), pid.data_ptr(),
                                     p, 0, None)
         assert st == want, (max_list, st)
+    torch.cuda.synchronize()
+
+
+def test_scan_rejects_misaligned_arrays(R):
+    """Codes must be 16-byte aligned, list offsets 8-byte, the other arrays
+    4-byte aligned: a misaligned pointer returns INVALID_ARG before any
+    launch (pointers are only inspected, never dereferenced)."""
+    import ctypes as C
+    from paper_2608_30384_amd import _lib as L
+    plan = R.Plan(64, 4, passes=0, scale_mode="global")
+    nlist, nprobe, Q, k = 4, 2, 1, 10
+    buf = torch.zeros(4096, dtype=torch.int64, device=DEV)
+    p = buf.data_ptr()
+    q = torch.zeros((Q, 64), dtype=torch.float32, device=DEV)
+    pid = torch.zeros((Q, nprobe), dtype=torch.int32, device=DEV)
+    out = torch.zeros((Q, k), dtype=torch.float32, device=DEV)
+    for codes, scales, offs in ((p + 4, p, p), (p, p + 2, p), (p, p, p + 4)):
+        idx = L.Index(nlist, 16, offs, p, p, codes, scales)
+        st = L.lib().rslm_scan_topk(plan.handle, C.byref(idx), q.data_ptr(), Q, pid.data_ptr(),
+                                    out.data_ptr(), nprobe, k, out.data_ptr(), pid.data_ptr(),
+                                    p, 0, None)   # (a missed check stops at the workspace: 4)
+        assert st == 1, (codes - p, scales - p, offs - p, st)
     torch.cuda.synchronize()

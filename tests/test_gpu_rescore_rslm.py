@@ -46,6 +46,8 @@ TWO_CASES = [
     (128, 2, 1, 4, "global", 300),    # 2-D first stage, 1-D second stage
     (101, 3, 2, 1, "local", 300),     # ragged 4-D second stage, local scale
     (768, 4, 2, 3, "global", 200),    # 3-bit second stage: general path
+    (2049, 4, 2, 2, "global", 150),   # odd D above 1,024: general path, overlap block
+    (1536, 4, 2, 2, "local", 160),
 ]
 
 
@@ -163,6 +165,8 @@ def test_rescore_rslm_parity(R, D, bits2, k_in, k_out):
     s1 = s1.astype(np.float32)
     ref_s, ref_i = oracle.rescore_rslm(qr.astype(np.float64), s1, cand, enc2["codes"],
                                        enc2["s_code"], enc2["g_code"], C2, k_out)
+    cands = oracle.rescore_rslm_scores(qr.astype(np.float64), s1, cand, enc2["codes"],
+                                       enc2["s_code"], enc2["g_code"], C2)
     plan2 = R.Plan(D, bits2, passes=0, scale_mode="global")
     assert plan2.canon_bytes == canon.shape[1]
     gs, gi = R.rslm_rescore_rslm(plan2, _t(canon), _t(sc2.view(np.int32)), _t(qr), _t(s1),
@@ -172,8 +176,9 @@ def test_rescore_rslm_parity(R, D, bits2, k_in, k_out):
     xt2 = oracle.reconstruct(enc2["codes"], enc2["s_code"], enc2["g_code"], C2, np.eye(D), base)
     xn = np.linalg.norm(xt2, axis=1).max()
     for i in range(Q):
-        tol = H.score_tol(ref_s[i], np.linalg.norm(qr[i]), xn)
-        H.check_topk(gs[i], gi[i], ref_s[i], ref_i[i], np.where(np.isfinite(tol), tol, 0))
+        qn = np.linalg.norm(qr[i])
+        H.check_topk(gs[i], gi[i], ref_s[i], ref_i[i], lambda s, qn=qn: H.score_tol(s, qn, xn),
+                     *cands[i])
 
 
 @pytest.mark.parametrize("D,passes,n,lite", [(768, 2, 500, False), (256, 1, 300, False),

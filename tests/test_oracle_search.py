@@ -6,7 +6,10 @@ inputs (exhaustive probing equals exhaustive scoring), explicit min/max for
 SQ8, and hand-made tie cases for the ordering rules.
 """
 
+import os
+
 import numpy as np
+import pytest
 
 import oracle
 import synth
@@ -46,10 +49,15 @@ def test_probe_is_sorted_dots():
     for i in range(5):
         ref = sorted(range(50), key=lambda p: (-dots[i, p], p))[:7]
         assert ids[i].tolist() == ref
-    # ties go to the lower list id
-    c2 = np.vstack([c[:3], c[:3]])
-    ids2, _, _ = oracle.probe_ip(c[:1], c2, 2)
-    assert ids2[0].tolist() == [0, 3] or ids2[0].tolist()[0] == 0
+    # ties go to the lower list id: small integers make every dot product
+    # exact, so duplicated centres tie bit for bit
+    ci = rng.integers(-3, 4, (3, 16)).astype(np.float64)
+    c2 = np.vstack([ci, ci, ci])
+    ids2, vals2, _ = oracle.probe_ip(ci[:1], c2, 4)
+    assert vals2[0, 0] == vals2[0, 1] == vals2[0, 2]
+    order = sorted(range(9), key=lambda p: (-float(ci[0] @ c2[p]), p))
+    assert ids2[0].tolist() == order[:4]
+    assert ids2[0].tolist()[:3] == [0, 3, 6]
 
 
 def test_assign_lowest_on_tie():
@@ -157,3 +165,26 @@ def test_kmeans_objective_decreases():
         _, d = oracle.assign_l2(x, c)
         assert d.mean() <= prev + 1e-12
         prev = d.mean()
+
+
+def _read_kmeans_golden():
+    path = os.path.join(os.path.dirname(__file__), "golden", "kmeans_hand.txt")
+    cases = []
+    for line in open(path):
+        line = line.split("#")[0].strip()
+        if not line:
+            continue
+        pts, init, it, want = [f.strip() for f in line.split("|")]
+        cases.append(([float(v) for v in pts.split()], [float(v) for v in init.split()], int(it),
+                      [eval(v, {}) for v in want.split()]))
+    return cases
+
+
+@pytest.mark.parametrize("pts,init,iters,want", _read_kmeans_golden())
+def test_kmeans_hand_computed(pts, init, iters, want):
+    """Lloyd iterations worked by hand (tests/golden/kmeans_hand.txt): the
+    lowest-id tie rule of the assignment, the mean update and the empty
+    cluster keeping its centre."""
+    x = np.array(pts)[:, None]
+    c = oracle.kmeans(x, len(init), iters=iters, init=np.array(init)[:, None])
+    assert np.allclose(c[:, 0], want, rtol=0, atol=1e-12)
