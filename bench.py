@@ -323,9 +323,7 @@ def _cpu_query(i):
             continue
         sc = d["scales"][o:o + n]
         lists.append((oracle.unpack_canonical(d["canon"][o:o + n], d["bits"], d["n_sub"]),
-                      np.array([oracle.dec_ue7m9(int(v) & 0xFFFF) for v in sc]),
-                      np.array([oracle.dec_ue4m12(int(v) >> 16) for v in sc]),
-                      d["ids"][o:o + n]))
+                      d["dec_s"][sc & 0xFFFF], d["dec_g"][sc >> 16], d["ids"][o:o + n]))
     t1 = time.perf_counter()
     all_s, all_i = [], []
     pairs = 0
@@ -403,6 +401,9 @@ def cpu_baseline(R, plan, index, qrot, pid, pdot, k, xe_rows, cen, n_encode=1 <<
                 ids=index.ids.cpu().numpy().astype(np.int64),
                 offs=index.list_offsets.cpu().numpy(), sizes=index.list_sizes.cpu().numpy(),
                 bits=plan.bits, n_sub=n_sub, C=synth.codebook(plan.bits), k=k, xe=xe,
+                # the oracle's scale decoders tabulated over all 2^16 codes
+                dec_s=np.array([oracle.dec_ue7m9(u) for u in range(1 << 16)]),
+                dec_g=np.array([oracle.dec_ue4m12(u) for u in range(1 << 16)]),
                 cen=cen_h, ae=ae, Rm=Rm, sq8_lo=sq8_lo, sq8_hi=sq8_hi)
     os.environ.setdefault("OMP_NUM_THREADS", "1")
     ctx = mp.get_context("fork")
