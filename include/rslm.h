@@ -260,6 +260,28 @@ int ivf_assign_probe(const float *x, int64_t n, int32_t dim,
                      size_t ws_bytes, void *stream);
 
 /* ------------------------------------------------------------------------
+ * ivf_assign_probe_noalloc -- ivf_assign_probe for callers that cannot
+ * allocate memory or hand in a workspace: code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc.  The same kernels
+ * and results as ivf_assign_probe; the scratch is a fixed device array of
+ * ivf_assign_probe_noalloc_limit() bytes (64 MiB + 256 KiB) that the library
+ * holds once per GPU it runs on until the process ends.  This call allocates
+ * nothing (no hipMalloc / hipFree, no allocating library routine); the
+ * caller passes inputs and outputs as for ivf_assign_probe.
+ *   Sizes whose workspace (ivf_assign_probe_workspace) exceeds the limit --
+ *   probing needs n * nlist * 4 bytes plus 4 * nlist rounded to 256 -- return
+ *   RSLM_ERR_WORKSPACE before any launch.
+ *   Every call on one GPU shares that GPU's scratch: calls that overlap in
+ *   time on one GPU (different streams, threads or processes' graphs) race
+ *   and must be serialised by the caller.  Nothing in the scratch needs to
+ *   start at zero; its contents after a call are unspecified.
+ * ------------------------------------------------------------------------ */
+int ivf_assign_probe_noalloc(const float *x, int64_t n, int32_t dim,
+                             const float *centroids, int32_t nlist, int32_t nprobe,
+                             int mode, int32_t *out_ids, float *out_scores, void *stream);
+size_t ivf_assign_probe_noalloc_limit(void);
+
+/* ------------------------------------------------------------------------
  * ivf_kmeans_update -- the centre update of one Lloyd iteration of the
  * Euclidean k-means that partitions the collection (Section "End-to-End
  * Comparison", Setup): given each point's centre (IVF_ASSIGN_L2),

@@ -23,7 +23,8 @@ EXPORTS = [
     "rslm_plan_create", "rslm_plan_destroy", "rslm_plan_get_info",
     "rslm_fwht", "rslm_encode", "rslm_encode_two_stage", "rslm_encode_sq8", "rslm_pack_codes",
     "rslm_pack_records", "rslm_score", "rslm_decode", "rslm_unpack_codes",
-    "ivf_assign_probe_workspace", "ivf_assign_probe", "ivf_kmeans_update_workspace",
+    "ivf_assign_probe_workspace", "ivf_assign_probe", "ivf_assign_probe_noalloc",
+    "ivf_assign_probe_noalloc_limit", "ivf_kmeans_update_workspace",
     "ivf_kmeans_update",
     "rslm_scan_topk_workspace", "rslm_scan_topk",
     "rslm_sq8_fit", "rslm_sq8_encode", "rslm_rescore", "rslm_set_timer", "rslm_calibrate_read",
@@ -86,6 +87,8 @@ def _declare(lib):
         "rslm_unpack_codes": (C.c_int, [P, P, I64, P, P]),
         "ivf_assign_probe_workspace": (SZ, [I64, I32, I32, I32, C.c_int]),
         "ivf_assign_probe": (C.c_int, [P, I64, I32, P, I32, I32, C.c_int, P, P, P, SZ, P]),
+        "ivf_assign_probe_noalloc": (C.c_int, [P, I64, I32, P, I32, I32, C.c_int, P, P, P]),
+        "ivf_assign_probe_noalloc_limit": (SZ, []),
         "ivf_kmeans_update_workspace": (SZ, [I64, I32]),
         "ivf_kmeans_update": (C.c_int, [P, I64, I32, P, I32, P, P, SZ, P]),
         "rslm_scan_topk_workspace": (SZ, [P, C.POINTER(Index), I32, I32, I32]),

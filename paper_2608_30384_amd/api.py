@@ -284,6 +284,20 @@ def ivf_assign_probe(x, centroids, nprobe=1, mode=L.IVF_ASSIGN_L2, out_ids=None,
     return out_ids, out_scores
 
 
+def ivf_assign_probe_noalloc(x, centroids, nprobe, mode, out_ids, out_scores, stream=None):
+    """``ivf_assign_probe`` through the entry point that allocates nothing
+    (fixed per-GPU scratch); the caller provides the outputs."""
+    _need(x, torch.float32, "x")
+    _need(centroids, torch.float32, "centroids")
+    _need(out_ids, torch.int32, "out_ids")
+    _need(out_scores, torch.float32, "out_scores")
+    n, dim = x.shape
+    L.check("ivf_assign_probe_noalloc", L.lib().ivf_assign_probe_noalloc(
+        _ptr(x), n, dim, _ptr(centroids), centroids.shape[0], nprobe, mode, _ptr(out_ids),
+        _ptr(out_scores), _stream(stream)))
+    return out_ids, out_scores
+
+
 def ivf_kmeans_update(x, assign, centroids, stream=None):
     """One Lloyd centre update in place: centroids[p] = mean of the rows of x
     assigned to p (an empty centre keeps its value)."""

@@ -9,6 +9,8 @@
 // running (distance, id) minimum per row across all centre tiles (128 x 128
 // output tiles), never writing the product; rows that are not whole 16-byte
 // runs take a vector-ALU tile (64 x 64, 4 x 4 outputs per thread) instead.
+#include <mutex>
+
 #include "rslm_internal.h"
 #include "select_dev.h"
 
@@ -627,6 +629,45 @@ __global__ void __launch_bounds__(kSelThreads) k_probe_select(const float *__res
              out_ids + row * nprobe, sm);
 }
 
+// ------------------------------------------------------------- fixed scratch
+// Scratch of ivf_assign_probe_noalloc: a static device array, one per GPU
+// the library runs on, held until the process ends.  Host code never uses
+// its name as an address: the device address is looked up once per device
+// (hipGetSymbolAddress, with that device current) and kept in g_scratch_ptr.
+constexpr size_t kProbeScratchBytes = (size_t(64) << 20) + (size_t(256) << 10);
+static __device__ __align__(256) unsigned char scratch[kProbeScratchBytes];
+
+constexpr int kMaxDevices = 64;
+static void *g_scratch_ptr[kMaxDevices] = {nullptr};
+static std::mutex g_scratch_mu;
+
+// Device address of this GPU's scratch (looked up on first use); nullptr
+// with *status set when the lookup fails.
+static void *scratch_of_current_device(int *status) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) {
+    *status = set_hip_error(e);
+    return nullptr;
+  }
+  if (dev < 0 || dev >= kMaxDevices) {
+    *status = RSLM_ERR_UNSUPPORTED;
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr) {
+      *status = set_hip_error(e != hipSuccess ? e : hipErrorInvalidSymbol);
+      return nullptr;
+    }
+    g_scratch_ptr[dev] = ptr;
+  }
+  *status = RSLM_OK;
+  return g_scratch_ptr[dev];
+}
+
 }  // namespace rslm
 
 using namespace rslm;
@@ -709,5 +750,32 @@ int ivf_assign_probe(const float *x, int64_t n, int32_t dim, const float *centro
                        nprobe, out_ids, out_scores);
   return check_launch();
 }
+
+}  // extern "C"
+
+extern "C" {
+
+int ivf_assign_probe_noalloc(const float *x, int64_t n, int32_t dim, const float *centroids,
+                             int32_t nlist, int32_t nprobe, int mode, int32_t *out_ids,
+                             float *out_scores, void *stream) {
+  // the same validation as ivf_assign_probe, then the fixed scratch's limit
+  if (n < 0 || dim < 1 || nlist < 1 || nlist > 65536) return RSLM_ERR_INVALID_ARG;
+  if (mode != IVF_ASSIGN_L2 && mode != IVF_PROBE_IP) return RSLM_ERR_INVALID_ARG;
+  if (mode == IVF_ASSIGN_L2 && nprobe != 1) return RSLM_ERR_INVALID_ARG;
+  if (mode == IVF_PROBE_IP && (nprobe < 1 || nprobe > nlist || nprobe > kMaxNprobe))
+    return RSLM_ERR_INVALID_ARG;
+  if (n == 0) return RSLM_OK;
+  if (!x || !centroids || !out_ids || (mode == IVF_PROBE_IP && !out_scores))
+    return RSLM_ERR_INVALID_ARG;
+  const size_t need = ivf_assign_probe_workspace(n, dim, nlist, nprobe, mode);
+  if (need > kProbeScratchBytes) return RSLM_ERR_WORKSPACE;
+  int st = RSLM_OK;
+  void *ws = scratch_of_current_device(&st);
+  if (!ws) return st;
+  return ivf_assign_probe(x, n, dim, centroids, nlist, nprobe, mode, out_ids, out_scores, ws,
+                          kProbeScratchBytes, stream);
+}
+
+size_t ivf_assign_probe_noalloc_limit(void) { return kProbeScratchBytes; }
 
 }  // extern "C"
