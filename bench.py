@@ -35,6 +35,9 @@ HBM_PEAK_GBPS = 8000.0
 # rotated query split into two float16 halves (hi + lo, about 22 significant
 # bits) on the matrix cores, products exact, accumulated in float32.
 SCAN_DTYPE = "split-f16 mfma, f32 accumulate"
+# Queries of a batch that probe the same list are scored together, up to
+# this many per work item: a list's records leave HBM once per such group.
+SCAN_GROUP_Q = 8
 
 
 def log(*a):
@@ -532,7 +535,7 @@ def main():
         pl = pid.long().reshape(-1)
         pairs = int(sizes[pl].sum().item())
         m = torch.bincount(pl, minlength=nlist)
-        groups = (m + 7) // 8
+        groups = (m + SCAN_GROUP_Q - 1) // SCAN_GROUP_Q
         streamed = int((groups * sizes).sum().item())
         distinct = int(sizes[m > 0].sum().item())     # records of the lists probed at all
         work.append((pairs, streamed, distinct))
@@ -748,14 +751,16 @@ def _timed_batches(torch, batches, fn, warmup):
 
 
 def _streamed(torch, R, cen, batches, nprobe, sizes, nlist):
-    """Scored pairs and streamed records (lists read once per group of <= 8
-    queries) of each batch, computed outside the timed region."""
+    """Scored pairs and streamed records (lists read once per group of
+    <= SCAN_GROUP_Q queries) of each batch, computed outside the timed
+    region."""
     out = []
     for qb in batches:
         pid, _ = R.ivf_assign_probe(qb, cen, nprobe, R.IVF_PROBE_IP)
         pl = pid.long().reshape(-1)
         m = torch.bincount(pl, minlength=nlist)
-        out.append((int(sizes[pl].sum().item()), int((((m + 7) // 8) * sizes).sum().item())))
+        out.append((int(sizes[pl].sum().item()),
+                    int((((m + SCAN_GROUP_Q - 1) // SCAN_GROUP_Q) * sizes).sum().item())))
     return out
 
 
