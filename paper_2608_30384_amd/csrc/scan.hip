@@ -21,7 +21,7 @@
 // units and a wavefront's load is 1 KiB contiguous.
 //
 // Scheduling.  A work item is (list, group of <= 8 queries, chunk of the
-// list); lists are cut into equal chunks of at most 1,024 candidates and the
+// list); lists are cut into equal chunks of at most 2,048 candidates and the
 // items are ordered by decreasing size.  A persistent grid (two 256-thread
 // workgroups per CU) takes items from an atomic counter, so the launch ends
 // on the smallest items.  Within an item each wavefront scores every fourth
@@ -41,10 +41,11 @@ typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kChunkCands = 1024;   // candidates per work item
+constexpr int kChunkCands = 2048;   // candidates per work item
 constexpr int kGroupQ = 8;          // queries per work item (16 MFMA rows / 2)
 constexpr int kScanThreads = 256;
-static_assert(kChunkCands / 16 <= 4 * 16, "a wave scores at most 16 tiles of an item");
+constexpr int kScaleRegs = kChunkCands / 256;   // scale words per lane: 4 tiles of a wave each
+static_assert(kChunkCands / 16 <= 4 * 4 * kScaleRegs, "scale registers of a wave's tiles");
 
 static size_t align256(size_t b) { return (b + 255) / 256 * 256; }
 
@@ -638,44 +639,57 @@ __global__ void __launch_bounds__(kScanThreads, 2) k_scan(ScanArgs a) {
     // lists start on a tile boundary and cand0 is a multiple of 16
     const uint8_t *tiles = a.codes + (rec0 >> 4) * a.tile_bytes;
     const uint32_t tb = uint32_t(a.tile_bytes);
-    // Scale words of every tile this wave scores (tile lt = wave + 4 j,
-    // j < 16), loaded before any code tile: lane (kq, m) holds candidate m of
-    // tiles j = kq, kq + 4, kq + 8, kq + 12.  Issued first, they never make
-    // the tile loop wait for code tiles still in flight.
+    // Scale words.  Up to 24 chunks: every tile this wave scores (tile lt =
+    // wave + 4 j, j < 32) has its scales loaded before any code tile, lane
+    // (kq, m) holding candidate m of tiles j = kq + 4 r; issued first, they
+    // never make the tile loop wait for code tiles still in flight.  With 32
+    // chunks the registers are short: each tile's scale word is loaded with
+    // its codes instead and shares their wait.
     // (Rslm4Lite: the scales are in the code stream; no scales array read.)
+    constexpr bool kPreload = NC < 32;
     const __amdgpu_buffer_rsrc_t rs =
         make_rsrc(LITE ? static_cast<const void *>(a.codes) : static_cast<const void *>(a.scales + rec0),
                   LITE ? 0u : uint32_t(n_cand) * 4u);
-    uint32_t sreg[4];
+    uint32_t sreg[kPreload ? kScaleRegs : 1];
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
-      sreg[r] = LITE ? 0u : __builtin_amdgcn_raw_buffer_load_b32(
+    for (int r = 0; r < (kPreload ? kScaleRegs : 1); ++r)
+      sreg[r] = (LITE || !kPreload) ? 0u : __builtin_amdgcn_raw_buffer_load_b32(
                                 rs, uint32_t((wave + nwaves * (kq + 4 * r)) * 16 + m) * 4u, 0, 0);
     const bool lead_lane = LITE && kq < a.lead / 8;
     auto scale_of = [&](int j) {   // j is uniform across the wave
       const int r = j >> 2;
-      const uint32_t v = r == 0 ? sreg[0] : r == 1 ? sreg[1] : r == 2 ? sreg[2] : sreg[3];
+      uint32_t v = sreg[0];
+#pragma unroll
+      for (int t = 1; t < (kPreload ? kScaleRegs : 1); ++t) v = r == t ? sreg[t] : v;
       return uint32_t(__shfl(int(v), 16 * (j & 3) + m, 64));
+    };
+    auto load_scale = [&](int t) {
+      return (LITE || kPreload) ? 0u
+                                : __builtin_amdgcn_raw_buffer_load_b32(rs, uint32_t(t * 16 + m) * 4u, 0, 0);
     };
     // Software pipeline, depth 1: the codes of the wave's next tile are in
     // flight while the current tile is decoded and multiplied.  Tiles past
     // the item read as zeros from the buffer range check and are not scored.
     uint32_t bufA[kWordsPerLane], bufB[kWordsPerLane];
+    uint32_t scA, scB = 0u;
     int lt = wave, j = 0;
     const uint32_t voff = uint32_t(lane) * 16u;
     load_tile(bufA, tiles, lt, n_tiles, tb, voff);
+    scA = load_scale(lt);
     while (lt < n_tiles) {
       load_tile(bufB, tiles, lt + nwaves, n_tiles, tb, voff);
-      score_tile<BITS, NC, kWordsPerLane, LITE>(bufA, LITE ? 0u : scale_of(j), av, dtab, lane4, lt,
-                                                n_cand, m, ok, qc, qi, out, ltab, lead_lane,
-                                                a.global);
+      scB = load_scale(lt + nwaves);
+      score_tile<BITS, NC, kWordsPerLane, LITE>(bufA, LITE ? 0u : kPreload ? scale_of(j) : scA, av,
+                                                dtab, lane4, lt, n_cand, m, ok, qc, qi, out, ltab,
+                                                lead_lane, a.global);
       lt += nwaves;
       ++j;
       if (lt >= n_tiles) break;
       load_tile(bufA, tiles, lt + nwaves, n_tiles, tb, voff);
-      score_tile<BITS, NC, kWordsPerLane, LITE>(bufB, LITE ? 0u : scale_of(j), av, dtab, lane4, lt,
-                                                n_cand, m, ok, qc, qi, out, ltab, lead_lane,
-                                                a.global);
+      scA = load_scale(lt + nwaves);
+      score_tile<BITS, NC, kWordsPerLane, LITE>(bufB, LITE ? 0u : kPreload ? scale_of(j) : scB, av,
+                                                dtab, lane4, lt, n_cand, m, ok, qc, qi, out, ltab,
+                                                lead_lane, a.global);
       lt += nwaves;
       ++j;
     }
