@@ -23,8 +23,11 @@
 // Scheduling.  A work item is (list, group of <= 8 queries, chunk of the
 // list); lists are cut into equal chunks of at most 2,048 candidates and the
 // items are ordered by decreasing size.  A persistent grid (two 256-thread
-// workgroups per CU) takes items from an atomic counter, so the launch ends
-// on the smallest items.  Within an item each wavefront scores every fourth
+// workgroups per CU) takes items from atomic counters, so the launch ends on
+// the smallest items.  The counters are per XCD: blocks of consecutive items
+// (the query groups that stream the same chunk of a list are consecutive)
+// go to one XCD's queue, so those groups read the chunk through the same L2;
+// a workgroup whose queue is empty takes items from the others.  Within an item each wavefront scores every fourth
 // tile with the next tile's codes in flight; all loads are range-checked
 // buffer loads, so no load is conditional and the compiler's wait counts
 // stay exact.
@@ -44,7 +47,15 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kChunkCands = 2048;   // candidates per work item
 constexpr int kGroupQ = 8;          // queries per work item (16 MFMA rows / 2)
 constexpr int kScanThreads = 256;
-constexpr int kScaleRegs = kChunkCands / 256;   // scale words per lane: 4 tiles of a wave each
+constexpr int kScaleRegs = kChunkCands / 256;
+// Work queues: one per XCD (accelerator complex die, each with its own L2).
+// Queue x holds the blocks of kQueueBlock consecutive items (in the global
+// order) whose block number is x modulo kQueues; its counter sits in its
+// own 64-byte line of the workspace.
+constexpr int kQueues = 8;
+constexpr int kQueueShift = 4;
+constexpr int kQueueBlock = 1 << kQueueShift;
+constexpr int kQueueStride = 16;   // int32 words between two queue counters   // scale words per lane: 4 tiles of a wave each
 static_assert(kChunkCands / 16 <= 4 * 4 * kScaleRegs, "scale registers of a wave's tiles");
 
 static size_t align256(size_t b) { return (b + 255) / 256 * 256; }
@@ -55,7 +66,7 @@ struct ScanWs {
   int32_t *counts, *cursor, *pair_off, *item_off;
   int32_t *pairs, *prefix, *totals;
   int4 *items;            // two int4 per work item (see k_plan_items)
-  int32_t *work;          // next work item of the scan (dynamic schedule)
+  int32_t *work;          // per-XCD queue counters of the scan (dynamic schedule)
   float *scores;
   int64_t stride;
   size_t bytes;
@@ -81,7 +92,7 @@ static ScanWs scan_ws_layout(void *base, int Q, int nprobe, int nlist, int d_pad
   w.pairs = reinterpret_cast<int32_t *>(take(size_t(Q) * nprobe * 4));
   w.prefix = reinterpret_cast<int32_t *>(take(size_t(Q) * nprobe * 4));
   w.totals = reinterpret_cast<int32_t *>(take(size_t(Q) * 4));
-  w.work = reinterpret_cast<int32_t *>(take(4));
+  w.work = reinterpret_cast<int32_t *>(take(kQueues * kQueueStride * 4));
   {
     // work items <= (groups of <= 8 queries) x (chunks of the longest list);
     // groups <= npairs / 8 + (number of probed lists)
@@ -192,7 +203,7 @@ struct PlanSmem {
 // passes of kPlanRange), their exclusive scan (pair_off), cursor = 0, and
 // each list's first work item in an order by decreasing item size (counting
 // sort over size classes; the order within a class is immaterial: every item
-// writes its own scores).  Also resets the scan's work counter.  Until the
+// writes its own scores).  Also resets the scan's queue counters.  Until the
 // class starts are known, item_off[L] holds the list's item count.
 __device__ void plan_lists(PlanSmem &sm, const int32_t *__restrict__ probe_ids, int npairs,
                            const int32_t *__restrict__ sizes, int nlist, int max_list,
@@ -273,8 +284,8 @@ __device__ void plan_lists(PlanSmem &sm, const int32_t *__restrict__ probe_ids, 
     }
     pair_off[nlist] = carry;
     item_off[nlist] = run;
-    *work = 0;
   }
+  if (t < kQueues) work[t * kQueueStride] = 0;
   __syncthreads();   // item_off[L] written above is read back by this workgroup
   for (int base = 0; base < nlist; base += 16 * kPlanThreads) {   // loads first
     int niv[16], szv[16];
@@ -319,7 +330,9 @@ __global__ void __launch_bounds__(kPlanThreads) k_plan_a(
 
 // Threads [0, npairs): pair i joins its list's group (pairs[] grouped by
 // list, slots from a per-list cursor).  Wavefront L (< nlist) writes the
-// descriptors of list L's work items from item_off[L] on, one item per lane.
+// descriptors of list L's work items from item_off[L] on, one item per lane,
+// chunk-major: the groups that stream the same chunk are consecutive items,
+// so they land in the same XCD queue and their reads share that L2.
 // Item = (group of <= 8 consecutive pairs of the list, chunk of
 // item_cands(size) candidates):
 //   d0 = {list, first candidate, candidate count, first pair (in pairs[])}
@@ -348,7 +361,7 @@ __global__ void __launch_bounds__(kPlanBThreads) k_plan_b(
   const int it0 = item_off[L];
   const int64_t lo = list_offsets[L];
   for (int t = lane; t < ngr * nch; t += 64) {
-    const int g = t / nch, ch = t - g * nch;
+    const int ch = t / ngr, g = t - ch * ngr;
     const int cand0 = ch * ic;
     const int64_t rec0 = lo + cand0;
     const int64_t it = it0 + t;
@@ -359,6 +372,20 @@ __global__ void __launch_bounds__(kPlanBThreads) k_plan_b(
 }
 
 // ------------------------------------------------------------- scan kernel
+// Index of the XCD (0..7) this wavefront runs on, from the hardware register.
+__device__ __forceinline__ int xcd_id() {
+  uint32_t v;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(v));
+  return int(v & uint32_t(kQueues - 1));
+}
+
+// Global item of ticket j of queue x (blocks of kQueueBlock items dealt
+// round-robin over the queues); increasing in j.
+__device__ __forceinline__ int64_t queue_item(int x, uint32_t j) {
+  return (int64_t(j >> kQueueShift) << (kQueueShift + 3)) | (int64_t(x) << kQueueShift) |
+         int64_t(j & uint32_t(kQueueBlock - 1));
+}
+static_assert(kQueues == 8, "queue_item deals blocks over 8 queues");
 struct ScanArgs {
   const int64_t *list_offsets;
   const int32_t *list_sizes;
@@ -574,20 +601,37 @@ __global__ void __launch_bounds__(kScanThreads, 2) k_scan(ScanArgs a) {
   const int n_items = __builtin_amdgcn_readfirstlane(a.item_off[a.nlist]);
   const int m = lane & 15;           // A row / B column of this lane
   const int kq = lane >> 4;          // k-quarter: coordinates 8 kq .. 8 kq + 7 of a chunk
-  // Dynamic schedule: workgroups take items (largest first) from a counter.
-  // The ticket for the next item is drawn when an item starts and published
-  // in LDS after its tiles are scored (by then the atomic has returned), in
-  // one of two slots: a slot is rewritten only two barriers after it was read.
+  // Dynamic schedule: a workgroup takes items (largest first) from the queue
+  // of its XCD, and once that is empty from the other queues in turn (a
+  // queue whose ticket maps past the last item stays empty).  Thread 0 keeps
+  // the queue state.  The ticket for the next item is drawn when an item
+  // starts and published in LDS after its tiles are scored (by then the
+  // atomic has returned), in one of two slots: a slot is rewritten only two
+  // barriers after it was read.
   __shared__ int s_ticket[2];
-  if (tid == 0) s_ticket[0] = atomicAdd(a.work, 1);
+  int q_cur = xcd_id(), q_tried = 0;
+  // atomicInc (not add): left alone by the compiler's wave-aggregation
+  // rewrite, which would wait for the returned value where it is issued
+  auto draw = [&](int x) {
+    return uint32_t(atomicInc(reinterpret_cast<unsigned *>(a.work + x * kQueueStride), 0x7fffffffu));
+  };
+  // item of ticket j of the current queue, moving on to the next queues
+  // while the current one is empty; n_items when every queue is
+  auto resolve = [&](uint32_t j) {
+    int64_t it = queue_item(q_cur, j);
+    while (it >= n_items && ++q_tried < kQueues) {
+      q_cur = (q_cur + 1) & (kQueues - 1);
+      it = queue_item(q_cur, draw(q_cur));
+    }
+    return int(it < n_items ? it : n_items);
+  };
+  if (tid == 0) s_ticket[0] = resolve(draw(q_cur));
   __syncthreads();
   int k_it = 0;
   for (int item = __builtin_amdgcn_readfirstlane(s_ticket[0]); item < n_items;
        ++k_it, item = __builtin_amdgcn_readfirstlane(s_ticket[k_it & 1])) {
-    int next_ticket = 0;
-    // atomicInc (not add): left alone by the compiler's wave-aggregation rewrite,
-    // which would wait for the returned value right here
-    if (tid == 0) next_ticket = int(atomicInc(reinterpret_cast<unsigned *>(a.work), 0x7fffffffu));
+    uint32_t next_ticket = 0;
+    if (tid == 0) next_ticket = draw(q_cur);
     // The descriptor is the same for the whole wavefront: readfirstlane keeps
     // every item-level quantity (and so the buffer resources and the tile
     // loop) in scalar registers.
@@ -697,7 +741,7 @@ __global__ void __launch_bounds__(kScanThreads, 2) k_scan(ScanArgs a) {
     // item, so the loop above always starts with a known set of loads in
     // flight and the compiler keeps its waits partial.
     __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
-    if (tid == 0) s_ticket[(k_it + 1) & 1] = next_ticket;
+    if (tid == 0) s_ticket[(k_it + 1) & 1] = resolve(next_ticket);
     __syncthreads();
   }
 }
