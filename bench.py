@@ -647,7 +647,7 @@ def main():
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBPS,
             "traffic": traffic,
-            "kernel": f"k_scan<{args.bits},{min(32, max(4, -(-plan.d_pad // 32)))}>",
+            "kernel": f"k_scan<{args.bits},{plan.d_pad // 32}>",
             "algorithmic_bytes_per_launch": streamed_avg * rec_bytes,
             "kernel_ms": t_scan,
             "stream_read_GBps_measured": stream_read_GBps,
