@@ -326,8 +326,11 @@ typedef struct rslm_index {
  *   nprobe * index->max_list_size < 2^30 (a query's scores are addressed
  *   with 32-bit byte offsets), else RSLM_ERR_INVALID_ARG.  Alignment:
  *   index->codes 16 bytes, list_offsets 8 bytes, every other array 4 bytes,
- *   else RSLM_ERR_INVALID_ARG.  D <= 1024.  With a Lite plan the scales are read from the codes (the
- *   index's scales array is not used and may be NULL).
+ *   else RSLM_ERR_INVALID_ARG.  Any plan dimension (above D = 1,024 the
+ *   coordinates are scored in passes over equal chunk ranges); a Lite plan
+ *   above D = 1,024 returns RSLM_ERR_UNSUPPORTED.  With a Lite plan the
+ *   scales are read from the codes (the index's scales array is not used
+ *   and may be NULL).
  * ------------------------------------------------------------------------ */
 size_t rslm_scan_topk_workspace(const rslm_plan *plan, const rslm_index *index,
                                 int32_t Q, int32_t nprobe, int32_t k);

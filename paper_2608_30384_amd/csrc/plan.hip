@@ -167,14 +167,27 @@ int rslm_plan_create(const rslm_plan_desc *d, rslm_plan **out) {
   // each); the padded dimension is rounded up to the next one so that the
   // kernel's chunk loop is fully static.  Padding coordinates carry code 0
   // and meet zero query coordinates.
+  // Above 32 chunks the scan runs in passes over equal chunk ranges of 16,
+  // 24 or 32 chunks whose codes start on a 16-byte unit of a lane's stream
+  // (chunks x bits a multiple of 16); the count is the smallest such total.
   {
     static const int kInst[] = {1, 2, 3, 4, 6, 8, 12, 16, 24, 32};
     int nc = (D + 31) / 32;
-    for (int v : kInst)
-      if (v >= nc) {
-        nc = v;
-        break;
+    if (nc <= 32) {
+      for (int v : kInst)
+        if (v >= nc) {
+          nc = v;
+          break;
+        }
+    } else {
+      int best = 0;
+      for (int per : {32, 24, 16}) {
+        if ((per * bits) % 16) continue;
+        const int total = (nc + per - 1) / per * per;
+        if (!best || total < best) best = total;
       }
+      nc = best;
+    }
     c.n_chunks = nc;
     c.d_pad = nc * 32;
   }

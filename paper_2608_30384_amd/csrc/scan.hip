@@ -32,11 +32,18 @@
 // buffer loads, so no load is conditional and the compiler's wait counts
 // stay exact.
 //
+// Above 32 chunks (D > 1,024) the A operands of all chunks no longer fit in
+// registers: an item is scored in passes over equal chunk ranges, each pass
+// adding its part of the residual dot to the candidate's score slot and the
+// last one applying the scales.
+//
 // Scores of every candidate are written to a per-query region of the
 // workspace; a second kernel selects each query's top-k exactly (radix
 // select, then a bitonic sort of the survivors) and maps positions to ids.
 #include "rslm_internal.h"
 #include "select_dev.h"
+
+#include <type_traits>
 
 namespace rslm {
 
@@ -401,6 +408,7 @@ struct ScanArgs {
   float *scores;
   int64_t stride;
   int nlist, nprobe, d_pad, n_chunks, tile_bytes, lane_units, max_list;
+  int n_pass;             // passes over ranges of NC chunks (NC * n_pass = n_chunks)
   int lead;               // Rslm4Lite: leading coordinates on the K = 8 codebook (16 or 32)
   int global;             // Rslm4Lite: the global scale is embedded too
   float cb_lead[8];       // Rslm4Lite: the K = 8 codebook
@@ -525,7 +533,11 @@ __device__ __forceinline__ uint32_t nibble_tops(uint32_t w) {
   return t;
 }
 
-template <int BITS, int NC, int W, bool LITE = false>
+// MODE: 0 one pass over all chunks (score written); above 32 chunks the
+// chunks are scored in passes and the raw residual dot of a candidate is
+// kept in its score slot between them: 1 first pass (dot stored), 2 middle
+// pass (added), 3 last pass (added, then the score written).
+template <int BITS, int NC, int W, bool LITE = false, int MODE = 0>
 __device__ __forceinline__ void score_tile(const uint32_t (&tw)[W], uint32_t sc,
                                            const half8 (&av)[NC], const uint32_t *dtab,
                                            uint32_t lane4, int lt, int n_cand, int m,
@@ -538,6 +550,15 @@ __device__ __forceinline__ void score_tile(const uint32_t (&tw)[W], uint32_t sc,
   // latency of chunk c + 2 overlaps the MFMAs of chunks c and c + 1; even and
   // odd chunks accumulate separately to halve the dependent MFMA chain.
   floatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+  float prev[2] = {0.f, 0.f};     // dot of the earlier passes, loaded before the MFMAs
+  if constexpr (MODE >= 2) {
+    const int c = lt * 16 + m;
+    if (c < n_cand) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        if (ok[i]) prev[i] = out[i][c];
+    }
+  }
   half8 b[3];
   if (LITE) {
     // scales from the code stream: lane (kq, m) holds 8 scale bits of
@@ -561,14 +582,28 @@ __device__ __forceinline__ void score_tile(const uint32_t (&tw)[W], uint32_t sc,
   const floatx4 acc = acc0 + acc1;
   const int cand = lt * 16 + m;   // item-local candidate index
   if (cand < n_cand) {
-    const float sh = dec_ue7m9(sc & 0xffffu);
-    const float gh = dec_ue4m12(sc >> 16);
-    if (ok[0]) out[0][cand] = gh * (qc[0] + sh * ((acc[0] + acc[1]) * qi[0]));
-    if (ok[1]) out[1][cand] = gh * (qc[1] + sh * ((acc[2] + acc[3]) * qi[1]));
+    if (MODE == 0) {
+      const float sh = dec_ue7m9(sc & 0xffffu);
+      const float gh = dec_ue4m12(sc >> 16);
+      if (ok[0]) out[0][cand] = gh * (qc[0] + sh * ((acc[0] + acc[1]) * qi[0]));
+      if (ok[1]) out[1][cand] = gh * (qc[1] + sh * ((acc[2] + acc[3]) * qi[1]));
+    } else {
+      float d[2] = {acc[0] + acc[1], acc[2] + acc[3]};
+      if (MODE >= 2) {
+        d[0] += prev[0];
+        d[1] += prev[1];
+      }
+      const float sh = dec_ue7m9(sc & 0xffffu);
+      const float gh = dec_ue4m12(sc >> 16);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        if (ok[i]) out[i][cand] = (MODE == 3) ? gh * (qc[i] + sh * (d[i] * qi[i])) : d[i];
+    }
   }
 }
 
-template <int BITS, int NC, bool LITE = false>
+// MP: the multi-pass variant (items scored in a.n_pass passes of NC chunks).
+template <int BITS, int NC, bool LITE = false, bool MP = false>
 __global__ void __launch_bounds__(kScanThreads, 2) k_scan(ScanArgs a) {
   using T = DecodeTab<BITS>;
   __shared__ uint32_t dtab[T::kEntries * 64 * T::kWords];
@@ -646,7 +681,7 @@ __global__ void __launch_bounds__(kScanThreads, 2) k_scan(ScanArgs a) {
 
     // A operands: row m = 2 * slot + part (part 0 = hi, 1 = lo)
     half8 av[NC];
-    {
+    if constexpr (!MP) {
       const int slot = m >> 1;
       if (slot < G) {
         const int pr = a.pairs[pbase + slot];
@@ -659,6 +694,20 @@ __global__ void __launch_bounds__(kScanThreads, 2) k_scan(ScanArgs a) {
         for (int c = 0; c < NC; ++c) av[c] = half8{};
       }
     }
+    // multi-pass: the A operands of chunks [c0, c0 + NC), loaded per pass
+    auto load_a = [&](int c0) {
+      const int slot = m >> 1;
+      if (slot < G) {
+        const int pr = a.pairs[pbase + slot];
+        const int q = pr / a.nprobe;
+        const _Float16 *src = ((m & 1) ? a.ql : a.qh) + int64_t(q) * a.d_pad + 32 * c0 + 8 * kq;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) av[c] = *reinterpret_cast<const half8 *>(src + 32 * c);
+      } else {
+#pragma unroll
+        for (int c = 0; c < NC; ++c) av[c] = half8{};
+      }
+    };
     // epilogue parameters of the two query slots this lane outputs
     float qc[2], qi[2];
     int64_t obase[2];
@@ -711,34 +760,83 @@ __global__ void __launch_bounds__(kScanThreads, 2) k_scan(ScanArgs a) {
       return (LITE || kPreload) ? 0u
                                 : __builtin_amdgcn_raw_buffer_load_b32(rs, uint32_t(t * 16 + m) * 4u, 0, 0);
     };
-    // Software pipeline, depth 1: the codes of the wave's next tile are in
-    // flight while the current tile is decoded and multiplied.  Tiles past
-    // the item read as zeros from the buffer range check and are not scored.
-    uint32_t bufA[kWordsPerLane], bufB[kWordsPerLane];
-    uint32_t scA, scB = 0u;
-    int lt = wave, j = 0;
-    const uint32_t voff = uint32_t(lane) * 16u;
-    load_tile(bufA, tiles, lt, n_tiles, tb, voff);
-    scA = load_scale(lt);
-    while (lt < n_tiles) {
-      load_tile(bufB, tiles, lt + nwaves, n_tiles, tb, voff);
-      scB = load_scale(lt + nwaves);
-      score_tile<BITS, NC, kWordsPerLane, LITE>(bufA, LITE ? 0u : kPreload ? scale_of(j) : scA, av,
-                                                dtab, lane4, lt, n_cand, m, ok, qc, qi, out, ltab,
-                                                lead_lane, a.global);
-      lt += nwaves;
-      ++j;
-      if (lt >= n_tiles) break;
-      load_tile(bufA, tiles, lt + nwaves, n_tiles, tb, voff);
-      scA = load_scale(lt + nwaves);
-      score_tile<BITS, NC, kWordsPerLane, LITE>(bufB, LITE ? 0u : kPreload ? scale_of(j) : scB, av,
-                                                dtab, lane4, lt, n_cand, m, ok, qc, qi, out, ltab,
-                                                lead_lane, a.global);
-      lt += nwaves;
-      ++j;
+    if constexpr (!MP) {
+      // Software pipeline, depth 1: the codes of the wave's next tile are in
+      // flight while the current tile is decoded and multiplied.  Tiles past
+      // the item read as zeros from the buffer range check and are not scored.
+      uint32_t bufA[kWordsPerLane], bufB[kWordsPerLane];
+      uint32_t scA, scB = 0u;
+      int lt = wave, j = 0;
+      const uint32_t voff = uint32_t(lane) * 16u;
+      load_tile(bufA, tiles, lt, n_tiles, tb, voff);
+      scA = load_scale(lt);
+      while (lt < n_tiles) {
+        load_tile(bufB, tiles, lt + nwaves, n_tiles, tb, voff);
+        scB = load_scale(lt + nwaves);
+        score_tile<BITS, NC, kWordsPerLane, LITE>(bufA, LITE ? 0u : kPreload ? scale_of(j) : scA, av,
+                                                  dtab, lane4, lt, n_cand, m, ok, qc, qi, out, ltab,
+                                                  lead_lane, a.global);
+        lt += nwaves;
+        ++j;
+        if (lt >= n_tiles) break;
+        load_tile(bufA, tiles, lt + nwaves, n_tiles, tb, voff);
+        scA = load_scale(lt + nwaves);
+        score_tile<BITS, NC, kWordsPerLane, LITE>(bufB, LITE ? 0u : kPreload ? scale_of(j) : scB, av,
+                                                  dtab, lane4, lt, n_cand, m, ok, qc, qi, out, ltab,
+                                                  lead_lane, a.global);
+        lt += nwaves;
+        ++j;
+      }
+    } else {
+      // Software pipeline, depth 1: the codes of the wave's next tile are in
+      // flight while the current tile is decoded and multiplied.  Tiles past
+      // the item read as zeros from the buffer range check and are not scored.
+      // voff: this lane's first 16-byte unit of the pass's chunks.
+      auto run_tiles = [&](auto mode_tag, uint32_t voff) {
+        constexpr int MODE = decltype(mode_tag)::value;
+        uint32_t bufA[kWordsPerLane], bufB[kWordsPerLane];
+        uint32_t scA, scB = 0u;
+        int lt = wave, j = 0;
+        load_tile(bufA, tiles, lt, n_tiles, tb, voff);
+        scA = load_scale(lt);
+        while (lt < n_tiles) {
+          load_tile(bufB, tiles, lt + nwaves, n_tiles, tb, voff);
+          scB = load_scale(lt + nwaves);
+          score_tile<BITS, NC, kWordsPerLane, LITE, MODE>(bufA, LITE ? 0u : kPreload ? scale_of(j) : scA, av,
+                                                    dtab, lane4, lt, n_cand, m, ok, qc, qi, out, ltab,
+                                                    lead_lane, a.global);
+          lt += nwaves;
+          ++j;
+          if (lt >= n_tiles) break;
+          load_tile(bufA, tiles, lt + nwaves, n_tiles, tb, voff);
+          scA = load_scale(lt + nwaves);
+          score_tile<BITS, NC, kWordsPerLane, LITE, MODE>(bufB, LITE ? 0u : kPreload ? scale_of(j) : scB, av,
+                                                    dtab, lane4, lt, n_cand, m, ok, qc, qi, out, ltab,
+                                                    lead_lane, a.global);
+          lt += nwaves;
+          ++j;
+        }
+      };
+      const uint32_t voff0 = uint32_t(lane) * 16u;
+      static_assert(NC >= 16 && !LITE && (NC * BITS) % 16 == 0, "multi-pass configuration");
+      // passes over chunk ranges of NC chunks: NC * BITS bytes of a lane's
+      // stream, a whole number of 16-byte units (the plan's chunk counts
+      // above 32 are multiples of such ranges; the host picks NC)
+      constexpr uint32_t kPassUnits = uint32_t(NC * BITS / 16);
+      for (int pass = 0; pass < a.n_pass; ++pass) {
+        load_a(pass * NC);
+        const uint32_t voff = voff0 + uint32_t(pass) * kPassUnits * 1024u;
+        if (pass == 0) run_tiles(std::integral_constant<int, 1>{}, voff);
+        else if (pass + 1 < a.n_pass) run_tiles(std::integral_constant<int, 2>{}, voff);
+        else run_tiles(std::integral_constant<int, 3>{}, voff);
+        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+        // this lane's dot stores of the pass before the next pass's loads
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+      }
     }
     // Retire the last (out-of-range, zero-traffic) prefetch before the next
-    // item, so the loop above always starts with a known set of loads in
+    // item, so the tile loop always starts with a known set of loads in
     // flight and the compiler keeps its waits partial.
     __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
     if (tid == 0) s_ticket[(k_it + 1) & 1] = resolve(next_ticket);
@@ -1064,9 +1162,20 @@ static int cu_count() {
 }
 
 template <int BITS, bool LITE = false>
-static void launch_scan_bits(int nc, dim3 grid, hipStream_t s, const ScanArgs &a) {
+static void launch_scan_bits(int nc, bool multi, dim3 grid, hipStream_t s, const ScanArgs &a) {
 #define RSLM_SCAN_NC(NCV) \
   hipLaunchKernelGGL((k_scan<BITS, NCV, LITE>), grid, dim3(kScanThreads), 0, s, a)
+#define RSLM_SCAN_MP(NCV) \
+  hipLaunchKernelGGL((k_scan<BITS, NCV, false, true>), grid, dim3(kScanThreads), 0, s, a)
+  if (multi) {
+    // pass ranges of 24 or 16 chunks starting on 16-byte units (ranges of
+    // 32 would spill registers in the pass loop)
+    if constexpr (!LITE) {
+      if (nc == 16) RSLM_SCAN_MP(16);
+      else if constexpr (BITS % 2 == 0) RSLM_SCAN_MP(24);
+    }
+    return;
+  }
   switch (nc) {
     case 1: RSLM_SCAN_NC(1); break;
     case 2: RSLM_SCAN_NC(2); break;
@@ -1079,6 +1188,7 @@ static void launch_scan_bits(int nc, dim3 grid, hipStream_t s, const ScanArgs &a
     case 24: RSLM_SCAN_NC(24); break;
     default: RSLM_SCAN_NC(32); break;
   }
+#undef RSLM_SCAN_MP
 #undef RSLM_SCAN_NC
 }
 
@@ -1119,7 +1229,21 @@ int rslm_scan_topk(const rslm_plan *p, const rslm_index *idx, const float *q_rot
       (reinterpret_cast<uintptr_t>(probe_ids) & 3) || (reinterpret_cast<uintptr_t>(probe_dots) & 3) ||
       (reinterpret_cast<uintptr_t>(out_scores) & 3) || (reinterpret_cast<uintptr_t>(out_ids) & 3))
     return RSLM_ERR_INVALID_ARG;
-  if (p->codec.n_chunks > 32) return RSLM_ERR_UNSUPPORTED;   // D > 1024
+  // above 32 chunks: passes over equal ranges of 24 or 16 chunks that start
+  // on a 16-byte unit of a lane's stream (the plan's chunk counts above 32
+  // are multiples of 16, 24 or 32); Rslm4Lite: one pass only
+  int nc_pass = p->codec.n_chunks, n_pass = 1;
+  if (nc_pass > 32) {
+    if (p->codec.lead > 0) return RSLM_ERR_UNSUPPORTED;
+    n_pass = 0;
+    for (int per : {24, 16})
+      if (p->codec.n_chunks % per == 0 && (per * p->codec.bits) % 16 == 0) {
+        nc_pass = per;
+        n_pass = p->codec.n_chunks / per;
+        break;
+      }
+    if (n_pass == 0) return RSLM_ERR_UNSUPPORTED;
+  }
   const size_t need = rslm_scan_topk_workspace(p, idx, Q, nprobe, k);
   if (!ws || ws_bytes < need) return RSLM_ERR_WORKSPACE;
   const int nlist = idx->nlist;
@@ -1162,6 +1286,7 @@ int rslm_scan_topk(const rslm_plan *p, const rslm_index *idx, const float *q_rot
   a.nprobe = nprobe;
   a.d_pad = d_pad;
   a.n_chunks = p->codec.n_chunks;
+  a.n_pass = n_pass;
   a.tile_bytes = p->codec.tile_bytes;
   a.lane_units = p->codec.lane_bytes / 16;
   a.max_list = idx->max_list_size;
@@ -1173,12 +1298,12 @@ int rslm_scan_topk(const rslm_plan *p, const rslm_index *idx, const float *q_rot
   if ((st = record_timer(0, 0, s))) return st;
   switch (p->codec.bits) {
     case 4:
-      if (a.lead > 0) launch_scan_bits<4, true>(a.n_chunks, grid, s, a);
-      else launch_scan_bits<4>(a.n_chunks, grid, s, a);
+      if (a.lead > 0) launch_scan_bits<4, true>(nc_pass, n_pass > 1, grid, s, a);
+      else launch_scan_bits<4>(nc_pass, n_pass > 1, grid, s, a);
       break;
-    case 3: launch_scan_bits<3>(a.n_chunks, grid, s, a); break;
-    case 2: launch_scan_bits<2>(a.n_chunks, grid, s, a); break;
-    default: launch_scan_bits<1>(a.n_chunks, grid, s, a); break;
+    case 3: launch_scan_bits<3>(nc_pass, n_pass > 1, grid, s, a); break;
+    case 2: launch_scan_bits<2>(nc_pass, n_pass > 1, grid, s, a); break;
+    default: launch_scan_bits<1>(nc_pass, n_pass > 1, grid, s, a); break;
   }
   if ((st = check_launch())) return st;
   if ((st = record_timer(0, 1, s))) return st;

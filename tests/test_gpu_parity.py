@@ -347,6 +347,13 @@ SCAN_CASES = [
     (256, 2, 2, "local", 1500, 30, 50, 30, 1000, False),   # k larger than most candidate sets
     (64, 4, 1, "global", 30000, 20000, 8, 50, 10, True),   # > 16,384 lists: planned in two
                                                            # passes, many lists empty
+    # D > 1,024: the chunks are scored in passes (48 chunks: 2 x 24; 2049 -> 72: 3 x 24;
+    # 3-bit 1100 -> 48: 3 x 16; 2-bit 2048: 4 x 16; 1-bit 3072: 6 x 16)
+    (1536, 4, 2, "global", 900, 6, 12, 3, 10, False),
+    (2049, 4, 2, "local", 700, 5, 10, 2, 17, False),
+    (1100, 3, 2, "global", 700, 5, 10, 2, 10, False),
+    (2048, 2, 2, "global", 600, 5, 10, 3, 10, False),
+    (3072, 1, 2, "global", 500, 4, 8, 2, 10, False),
 ]
 
 

@@ -300,3 +300,24 @@ def test_scan_rejects_misaligned_arrays(R):
                                     p, 0, None)   # (a missed check stops at the workspace: 4)
         assert st == 1, (codes - p, scales - p, offs - p, st)
     torch.cuda.synchronize()
+
+
+def test_lite_scan_above_1024_is_unsupported(R):
+    """A Lite plan scores in one pass only: above D = 1,024 the scan returns
+    UNSUPPORTED before any launch (pointers are only inspected)."""
+    import ctypes as C
+    from paper_2608_30384_amd import _lib as L
+    plan = R.Plan(1152, 4, passes=2, scale_mode="global", lite=True)
+    nlist, nprobe, Q, k = 4, 2, 1, 10
+    buf = torch.zeros(4096, dtype=torch.int64, device=DEV)
+    p = buf.data_ptr()
+    q = torch.zeros((Q, 1152), dtype=torch.float32, device=DEV)
+    pid = torch.zeros((Q, nprobe), dtype=torch.int32, device=DEV)
+    out = torch.zeros((Q, k), dtype=torch.float32, device=DEV)
+    idx = L.Index(nlist, 16, p, p, p, p, p)
+    st = L.lib().rslm_scan_topk(plan.handle, C.byref(idx), q.data_ptr(), Q, pid.data_ptr(),
+                                out.data_ptr(), nprobe, k, out.data_ptr(), pid.data_ptr(), p, 0,
+                                None)
+    assert st == 2, st
+    torch.cuda.synchronize()
+
