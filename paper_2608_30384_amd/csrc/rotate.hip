@@ -30,14 +30,16 @@ __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-template <int R>
+// W: lanes per vector (the encoder gives small vectors fewer lanes); lane is
+// the lane's index among them.
+template <int R, int W = kWave>
 __device__ __forceinline__ void fwht_round(float *v, int off, int nblk, int B, int s,
                                            bool last, float scale, int lane) {
   constexpr int G = 1 << R;
   const int h = 1 << s;
   const int gpb = B >> R;  // groups per block (power of two)
   const int total = nblk * gpb;
-  for (int gi = lane; gi < total; gi += kWave) {
+  for (int gi = lane; gi < total; gi += W) {
     const int blk = gi / gpb;
     const int t = gi - blk * gpb;
     const int low = t & (h - 1);
@@ -68,6 +70,7 @@ __device__ __forceinline__ void fwht_round(float *v, int off, int nblk, int B, i
 
 // Orthonormal FWHT of nblk adjacent blocks of size B starting at off, by the
 // calling wavefront.
+template <int W = kWave>
 __device__ __forceinline__ void fwht_blocks(float *v, int off, int nblk, const RotParams &rp,
                                             int lane) {
   const int B = rp.B, logB = rp.logB;
@@ -75,23 +78,56 @@ __device__ __forceinline__ void fwht_blocks(float *v, int off, int nblk, const R
   for (int s = 0; s < logB; s += 3) {
     const int R = (logB - s) < 3 ? (logB - s) : 3;
     const bool last = (s + R) == logB;
-    if (R == 3) fwht_round<3>(v, off, nblk, B, s, last, rp.inv_sqrt_b, lane);
-    else if (R == 2) fwht_round<2>(v, off, nblk, B, s, last, rp.inv_sqrt_b, lane);
-    else fwht_round<1>(v, off, nblk, B, s, last, rp.inv_sqrt_b, lane);
+    if (R == 3) fwht_round<3, W>(v, off, nblk, B, s, last, rp.inv_sqrt_b, lane);
+    else if (R == 2) fwht_round<2, W>(v, off, nblk, B, s, last, rp.inv_sqrt_b, lane);
+    else fwht_round<1, W>(v, off, nblk, B, s, last, rp.inv_sqrt_b, lane);
     wave_sync();
   }
 }
 
 // One pass of block transforms.  Forward: full blocks, then the overlap
 // block.  Reverse (inverse rotation): overlap block first.
+template <int W = kWave>
 __device__ __forceinline__ void fwht_pass(float *v, const RotParams &rp, int lane, bool reverse) {
   if (!reverse) {
-    if (rp.n_full) fwht_blocks(v, 0, rp.n_full, rp, lane);
-    if (rp.overlap) fwht_blocks(v, rp.D - rp.B, 1, rp, lane);
+    if (rp.n_full) fwht_blocks<W>(v, 0, rp.n_full, rp, lane);
+    if (rp.overlap) fwht_blocks<W>(v, rp.D - rp.B, 1, rp, lane);
   } else {
-    if (rp.overlap) fwht_blocks(v, rp.D - rp.B, 1, rp, lane);
-    if (rp.n_full) fwht_blocks(v, 0, rp.n_full, rp, lane);
+    if (rp.overlap) fwht_blocks<W>(v, rp.D - rp.B, 1, rp, lane);
+    if (rp.n_full) fwht_blocks<W>(v, 0, rp.n_full, rp, lane);
   }
+}
+
+// Sign bits of the elements lane + W t of a vector spread over W lanes, bit t
+// for t < 256 / W (the sign tables repeat every 256 coordinates); x: S1,
+// y: S2 (S1 offset by 127).  W = 64 gives lane_sign_masks.
+template <int W>
+__device__ __forceinline__ uint2 sub_sign_masks(const RotParams &rp, int lane) {
+  static_assert(W >= 8 && W <= kWave && 256 % W == 0, "lanes per vector");
+  uint32_t a = 0, b = 0;
+#pragma unroll
+  for (int t = 0; t < 256 / W; ++t) {
+    a |= sign_bit(rp.s1mask, lane + W * t) << t;
+    b |= sign_bit(rp.s1mask, lane + W * t + 127) << t;
+  }
+  return make_uint2(a, b);
+}
+template <int W>
+__device__ __forceinline__ float flip_w(float v, uint32_t mask, int t) {
+  return __uint_as_float(__float_as_uint(v) ^ (((mask >> (t & (256 / W - 1))) & 1u) << 31));
+}
+// Sum / maximum over the W lanes of a vector (aligned groups of W lanes).
+template <int W>
+__device__ __forceinline__ float sub_sum(float v) {
+#pragma unroll
+  for (int off = W / 2; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+template <int W>
+__device__ __forceinline__ float sub_max(float v) {
+#pragma unroll
+  for (int off = W / 2; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
+  return v;
 }
 
 // Source of output o of the strided transpose; pi is the workgroup's LDS
@@ -113,16 +149,17 @@ __device__ __forceinline__ void load_perm(const RotParams &rp, int16_t *pi) {
 
 // Forward rotation of the vector held in v (already multiplied by S1 when
 // passes > 0; element i at v[px(i)]).  Returns the buffer holding the result.
+template <int W = kWave>
 __device__ float *rotate_forward(float *v, float *w, const RotParams &rp, const int16_t *pi,
                                  uint32_t s2bits, int lane) {
   if (rp.passes == 0) return v;
-  fwht_pass(v, rp, lane, false);
+  fwht_pass<W>(v, rp, lane, false);
   if (rp.passes == 1) return v;
 #pragma unroll 4
-  for (int o = lane, t = 0; o < rp.D; o += kWave, ++t)
-    w[px(o)] = flip(v[px(transpose_src(o, rp, pi))], s2bits, t);
+  for (int o = lane, t = 0; o < rp.D; o += W, ++t)
+    w[px(o)] = flip_w<W>(v[px(transpose_src(o, rp, pi))], s2bits, t);
   wave_sync();
-  fwht_pass(w, rp, lane, false);
+  fwht_pass<W>(w, rp, lane, false);
   return w;
 }
 
@@ -200,6 +237,9 @@ __device__ __forceinline__ void store_group(uint8_t *codes, int64_t rec, int G, 
   }
 }
 
+// VPW vectors per wavefront, W = 64 / VPW lanes each (small D: a wavefront
+// per vector would leave most lanes idle in every butterfly round).
+template <int VPW>
 __global__ void __launch_bounds__(256) k_encode(
     const float *__restrict__ x, int64_t n_rows, const int64_t *__restrict__ src_row,
     const int32_t *__restrict__ rec_list, int64_t n_records, const float *__restrict__ cen,
@@ -210,16 +250,20 @@ __global__ void __launch_bounds__(256) k_encode(
   extern __shared__ float lds[];
   __shared__ float cbs[64], cbs2[64], cbl[8];
   __shared__ int16_t pi[128];
+  constexpr int W = kWave / VPW;
   const int lane = threadIdx.x & 63;
   const int wid = threadIdx.x >> 6;
   const int nw = blockDim.x >> 6;
+  const int sl = lane & (W - 1);            // lane within the vector's W lanes
+  const int vid = wid * VPW + lane / W;     // vector slot of the workgroup
+  const int nv = nw * VPW;
   if (threadIdx.x < 64) {
     cbs[threadIdx.x] = cp.cb[threadIdx.x];
     cbs2[threadIdx.x] = cp2.cb[threadIdx.x];
   }
   if (threadIdx.x < 8) cbl[threadIdx.x] = cp.cb_lead[threadIdx.x];
   load_perm(rp, pi);
-  const int64_t rec = int64_t(blockIdx.x) * nw + wid;
+  const int64_t rec = int64_t(blockIdx.x) * nv + vid;
   int64_t row = -1;
   int L = -1;
   if (rec < n_records) {
@@ -230,15 +274,17 @@ __global__ void __launch_bounds__(256) k_encode(
       if (L < 0 || L >= nlist) row = -1;
     }
   }
-  if (row < 0) return;   // no workgroup barriers below
-  float *v = lds + wid * 2 * dstride;
+  // no workgroup barriers below; the W lanes of a vector leave together and
+  // never exchange data with another vector's lanes
+  if (row < 0) return;
+  float *v = lds + vid * 2 * dstride;
   float *w = v + dstride;
-  uint8_t *cl = reinterpret_cast<uint8_t *>(lds + nw * 2 * dstride) + wid * (dstride / 1);
+  uint8_t *cl = reinterpret_cast<uint8_t *>(lds + nv * 2 * dstride) + vid * dstride;
   // second-stage codes follow the first-stage ones (allocated only with codes2)
-  uint8_t *cl2 = reinterpret_cast<uint8_t *>(lds + nw * 2 * dstride) + (nw + wid) * dstride;
+  uint8_t *cl2 = reinterpret_cast<uint8_t *>(lds + nv * 2 * dstride) + (nv + vid) * dstride;
   const int D = rp.D;
   float xx = 0.f, rr = 0.f, cc = 0.f;
-  const uint2 sm = lane_sign_masks(rp, lane);
+  const uint2 sm = sub_sign_masks<W>(rp, sl);
   const uint32_t s1in = (rp.passes > 0) ? sm.x : 0u;
   {
     const float *xr = x + row * D;
@@ -246,23 +292,23 @@ __global__ void __launch_bounds__(256) k_encode(
     const float *cr = (L >= 0) ? cen + int64_t(L) * D : xr;
     const float cw = (L >= 0) ? 1.f : 0.f;
   #pragma unroll 4
-    for (int i = lane, t = 0; i < D; i += kWave, ++t) {
+    for (int i = sl, t = 0; i < D; i += W, ++t) {
       const float xv = xr[i];
       const float cv = cr[i] * cw;
       const float r = xv - cv;
       xx += xv * xv;
       rr += r * r;
       cc += cv * cv;
-      v[px(i)] = flip(r, s1in, t);
+      v[px(i)] = flip_w<W>(r, s1in, t);
     }
   }
   wave_sync();
-  const float *z = rotate_forward(v, w, rp, pi, sm.y, lane);
+  const float *z = rotate_forward<W>(v, w, rp, pi, sm.y, sl);
 
   float m = 0.f;
 #pragma unroll 4
-  for (int i = lane; i < D; i += kWave) m = fmaxf(m, fabsf(z[px(i)]));
-  m = wave_max(m);
+  for (int i = sl; i < D; i += W) m = fmaxf(m, fabsf(z[px(i)]));
+  m = sub_max<W>(m);
   const float inv_s0 = (m > 0.f) ? cp.emax / m : 0.f;
   const bool has_rc = L >= 0 && cen_rot;
   const float *rc = has_rc ? cen_rot + int64_t(L) * D : x + row * D;   // any valid row
@@ -270,7 +316,7 @@ __global__ void __launch_bounds__(256) k_encode(
   const int g = cp.g;
   float cn2 = 0.f, rcd = 0.f;
 #pragma unroll 4
-  for (int j = lane; j < cp.n_sub; j += kWave) {
+  for (int j = sl; j < cp.n_sub; j += W) {
     int code = 0;
     if (m > 0.f) {
       if (g == 1 && j < cp.lead) {   // Rslm4Lite leading coordinate: K = 8
@@ -313,11 +359,11 @@ __global__ void __launch_bounds__(256) k_encode(
     }
     cl[j] = uint8_t(code);
   }
-  xx = wave_sum(xx);
-  rr = wave_sum(rr);
-  cc = wave_sum(cc);
-  cn2 = wave_sum(cn2);
-  rcd = wave_sum(rcd);
+  xx = sub_sum<W>(xx);
+  rr = sub_sum<W>(rr);
+  cc = sub_sum<W>(cc);
+  cn2 = sub_sum<W>(cn2);
+  rcd = sub_sum<W>(rcd);
   const float s = (m > 0.f && cn2 > 0.f) ? sqrtf(rr / cn2) : 0.f;
   const uint32_t su = enc_ue7m9(s);
   const float sh = dec_ue7m9(su);
@@ -327,7 +373,7 @@ __global__ void __launch_bounds__(256) k_encode(
     const float gv = (den2 > 0.f) ? sqrtf(xx / den2) : 0.f;
     gu = enc_ue4m12(gv);
   }
-  if (lane == 0) scales[rec] = su | (gu << 16);
+  if (sl == 0) scales[rec] = su | (gu << 16);
   __builtin_amdgcn_wave_barrier();  // codes in cl are written by other lanes
   // first-stage centroid value of valid coordinate i (0 for a zero residual)
   auto cval = [&](int i) {
@@ -342,7 +388,7 @@ __global__ void __launch_bounds__(256) k_encode(
     float *r2 = (z == v) ? w : v;   // the buffer the rotation left free
     float m2 = 0.f, rr2 = 0.f;
 #pragma unroll 4
-    for (int i = lane; i < D; i += kWave) {
+    for (int i = sl; i < D; i += W) {
       const float cv = cval(i);
       const float rcv = rc[i] * rcw;
       const float d = z[px(i)] + rcv - gh * (rcv + sh * cv);
@@ -351,13 +397,13 @@ __global__ void __launch_bounds__(256) k_encode(
       rr2 += d * d;
     }
     wave_sync();
-    m2 = wave_max(m2);
-    rr2 = wave_sum(rr2);
+    m2 = sub_max<W>(m2);
+    rr2 = sub_sum<W>(rr2);
     const float inv2 = (m2 > 0.f) ? cp2.emax / m2 : 0.f;
     const int g2 = cp2.g;
     float cn22 = 0.f, rad = 0.f;   // ||c2^||^2 and <R a, c2^> / g^
 #pragma unroll 2
-    for (int j = lane; j < cp2.n_sub; j += kWave) {
+    for (int j = sl; j < cp2.n_sub; j += W) {
       int code = 0;
       if (m2 > 0.f) {
         if (g2 == 1) {
@@ -398,8 +444,8 @@ __global__ void __launch_bounds__(256) k_encode(
       }
       cl2[j] = uint8_t(code);
     }
-    cn22 = wave_sum(cn22);
-    rad = wave_sum(rad) * gh;
+    cn22 = sub_sum<W>(cn22);
+    rad = sub_sum<W>(rad) * gh;
     const float s2 = (m2 > 0.f && cn22 > 0.f) ? sqrtf(rr2 / cn22) : 0.f;
     const uint32_t su2 = enc_ue7m9(s2);
     const float sh2 = dec_ue7m9(su2);
@@ -408,12 +454,12 @@ __global__ void __launch_bounds__(256) k_encode(
       const float dd = gh * gh * den2 + 2.f * sh2 * rad + sh2 * sh2 * cn22;
       gu2 = enc_ue4m12((dd > 0.f) ? sqrtf(xx / dd) : 0.f);
     }
-    if (lane == 0) scales2[row] = su2 | (gu2 << 16);
+    if (sl == 0) scales2[row] = su2 | (gu2 << 16);
     __builtin_amdgcn_wave_barrier();   // cl2 is written by other lanes
     // canonical bit stream: code j at bits [w j, w j + w)
     uint8_t *dst = codes2 + row * int64_t(cp2.canon_bytes);
     const int w2 = cp2.w;
-    for (int t = lane; t < cp2.canon_bytes; t += kWave) {
+    for (int t = sl; t < cp2.canon_bytes; t += W) {
       uint32_t val = 0;
       for (int b = 0; b < 8; ++b) {
         const int p = 8 * t + b;
@@ -427,7 +473,7 @@ __global__ void __launch_bounds__(256) k_encode(
   // pack: group G covers coordinates [8G, 8G + 8) = sub-vectors [8G/g, 8G/g + 8/g)
   const int n_groups = cp.d_pad >> 3;
   const int per = 8 / g;
-  for (int G = lane; G < n_groups; G += kWave) {
+  for (int G = sl; G < n_groups; G += W) {
     uint32_t val = 0;
     for (int t = 0; t < per; ++t) {
       const int j = G * per + t;
@@ -442,7 +488,7 @@ __global__ void __launch_bounds__(256) k_encode(
     // rslm_sq8_encode arithmetic), both indexed by source row
     const float gh = dec_ue4m12(gu);
   #pragma unroll 4
-    for (int i = lane; i < D; i += kWave) {
+    for (int i = sl; i < D; i += W) {
       const float cv = cval(i);
       const float rcv = rc[i] * rcw;
       const float o = z[px(i)] + rcv - gh * (rcv + sh * cv);
@@ -607,18 +653,31 @@ static int encode_impl(const rslm_plan *p, const rslm_plan *p2, const float *x, 
     return check_launch();
   const int D = p->rot.D;
   const int dstride = lds_floats(D);
+  // vectors per wavefront: a butterfly round has D / 8 groups, so give a
+  // vector about that many lanes (1 to 8 vectors per wavefront)
+  int vpw = 1;
+  while (vpw < 8 && D * vpw * 2 <= 512) vpw *= 2;
   // two float buffers plus one byte per sub-vector (<= dstride bytes) per
-  // wave, and another for an RSLM second stage
-  const size_t per_wave = 2 * size_t(dstride) * 4 + size_t(dstride) * (p2 ? 2 : 1);
+  // vector, and another for an RSLM second stage
+  const size_t per_vec = 2 * size_t(dstride) * 4 + size_t(dstride) * (p2 ? 2 : 1);
   int waves = 4;
-  while (waves > 1 && size_t(waves) * per_wave > 65536) waves >>= 1;
-  const size_t shm = size_t(waves) * per_wave;
-  const int64_t grid = (n_records + waves - 1) / waves;
+  while (waves > 1 && size_t(waves) * vpw * per_vec > 65536) waves >>= 1;
+  const size_t shm = size_t(waves) * vpw * per_vec;
+  const int64_t per_wg = int64_t(waves) * vpw;
+  const int64_t grid = (n_records + per_wg - 1) / per_wg;
   if (grid > 0x7fffffff) return RSLM_ERR_INVALID_ARG;
-  hipLaunchKernelGGL(k_encode, dim3(unsigned(grid)), dim3(64 * waves), shm, s, x, n_rows, src_row,
-                     rec_list, n_records, centroids, centroids_rot, nlist, codes, scales,
-                     resid_rot, p->rot, p->codec, dstride, codes2, scales2,
-                     p2 ? p2->codec : p->codec, sq8_lo, sq8_hi);
+#define RSLM_ENCODE_VPW(V)                                                                       \
+  hipLaunchKernelGGL((k_encode<V>), dim3(unsigned(grid)), dim3(64 * waves), shm, s, x, n_rows,      \
+                     src_row, rec_list, n_records, centroids, centroids_rot, nlist, codes, scales, \
+                     resid_rot, p->rot, p->codec, dstride, codes2, scales2,                        \
+                     p2 ? p2->codec : p->codec, sq8_lo, sq8_hi)
+  switch (vpw) {
+    case 8: RSLM_ENCODE_VPW(8); break;
+    case 4: RSLM_ENCODE_VPW(4); break;
+    case 2: RSLM_ENCODE_VPW(2); break;
+    default: RSLM_ENCODE_VPW(1); break;
+  }
+#undef RSLM_ENCODE_VPW
   return check_launch();
 }
 
