@@ -250,6 +250,10 @@ __global__ void __launch_bounds__(256) k_encode(
   extern __shared__ float lds[];
   __shared__ float cbs[64], cbs2[64], cbl[8];
   __shared__ int16_t pi[128];
+  // 1-D quantiser grid (cp.qn > 0): thresholds below each bucket, and the
+  // sorted thresholds padded with +inf
+  __shared__ uint8_t qtab[512];
+  __shared__ float thr_s[16];
   constexpr int W = kWave / VPW;
   const int lane = threadIdx.x & 63;
   const int wid = threadIdx.x >> 6;
@@ -262,7 +266,16 @@ __global__ void __launch_bounds__(256) k_encode(
     cbs2[threadIdx.x] = cp2.cb[threadIdx.x];
   }
   if (threadIdx.x < 8) cbl[threadIdx.x] = cp.cb_lead[threadIdx.x];
-  load_perm(rp, pi);
+  if (cp.g == 1 && cp.qn > 0) {
+    if (threadIdx.x < 16)
+      thr_s[threadIdx.x] = (int(threadIdx.x) + 1 < cp.K) ? cp.thr[threadIdx.x] : __builtin_inff();
+    for (int j = threadIdx.x; j < cp.qn; j += blockDim.x) {
+      int cnt = 0;
+      for (int k = 0; k + 1 < cp.K; ++k) cnt += quant_bucket(cp.thr[k], cp.qs, cp.qo, cp.qn) < j;
+      qtab[j] = uint8_t(cnt);
+    }
+  }
+  load_perm(rp, pi);   // (its barrier also publishes the tables above)
   const int64_t rec = int64_t(blockIdx.x) * nv + vid;
   int64_t row = -1;
   int L = -1;
@@ -323,6 +336,13 @@ __global__ void __launch_bounds__(256) k_encode(
         const float u = z[px(j)] * inv_s0;
 #pragma unroll
         for (int k = 0; k < 7; ++k) code += (u > cp.thr_lead[k]) ? 1 : 0;
+      } else if (g == 1 && cp.qn > 0) {
+        // thresholds below u's bucket, plus one comparison with the next
+        // threshold (the grid has at most one per bucket): the same count
+        // as comparing u with every threshold
+        const float u = z[px(j)] * inv_s0;
+        const int base = qtab[quant_bucket(u, cp.qs, cp.qo, cp.qn)];
+        code = base + ((u > thr_s[base]) ? 1 : 0);
       } else if (g == 1) {
         const float u = z[px(j)] * inv_s0;
 #pragma unroll
