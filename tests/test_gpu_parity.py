@@ -354,6 +354,7 @@ SCAN_CASES = [
     (1100, 3, 2, "global", 700, 5, 10, 2, 10, False),
     (2048, 2, 2, "global", 600, 5, 10, 3, 10, False),
     (3072, 1, 2, "global", 500, 4, 8, 2, 10, False),
+    (1536, 4, 2, "global", 9000, 3, 8, 2, 100, True),      # lists of several chunks, in passes
 ]
 
 
