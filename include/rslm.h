@@ -327,10 +327,9 @@ typedef struct rslm_index {
  *   with 32-bit byte offsets), else RSLM_ERR_INVALID_ARG.  Alignment:
  *   index->codes 16 bytes, list_offsets 8 bytes, every other array 4 bytes,
  *   else RSLM_ERR_INVALID_ARG.  Any plan dimension (above D = 1,024 the
- *   coordinates are scored in passes over equal chunk ranges); a Lite plan
- *   above D = 1,024 returns RSLM_ERR_UNSUPPORTED.  With a Lite plan the
- *   scales are read from the codes (the index's scales array is not used
- *   and may be NULL).
+ *   coordinates are scored in passes over equal chunk ranges).  With a Lite
+ *   plan the scales are read from the codes (the index's scales array is not
+ *   used and may be NULL).
  * ------------------------------------------------------------------------ */
 size_t rslm_scan_topk_workspace(const rslm_plan *plan, const rslm_index *index,
                                 int32_t Q, int32_t nprobe, int32_t k);

@@ -35,7 +35,8 @@
 // Above 32 chunks (D > 1,024) the A operands of all chunks no longer fit in
 // registers: an item is scored in passes over equal chunk ranges, each pass
 // adding its part of the residual dot to the candidate's score slot and the
-// last one applying the scales.
+// last one applying the scales (Rslm4Lite: read again from chunk 0's code
+// word).
 //
 // Scores of every candidate are written to a per-query region of the
 // workspace; a second kernel selects each query's top-k exactly (radix
@@ -537,6 +538,16 @@ __device__ __forceinline__ uint32_t nibble_tops(uint32_t w) {
 // chunks are scored in passes and the raw residual dot of a candidate is
 // kept in its score slot between them: 1 first pass (dot stored), 2 middle
 // pass (added), 3 last pass (added, then the score written).
+// Rslm4Lite: the scale word of candidate m from the chunk-0 code words of
+// the four lanes holding it (bit 3 of each nibble: s^ in kq 0, 1, g^ in kq
+// 2, 3).
+__device__ __forceinline__ uint32_t lite_scales(uint32_t chunk0, int m, int global) {
+  const uint32_t t = nibble_tops(chunk0);
+  const uint32_t t0 = __shfl(int(t), m, 64), t1 = __shfl(int(t), 16 + m, 64);
+  const uint32_t t2 = __shfl(int(t), 32 + m, 64), t3 = __shfl(int(t), 48 + m, 64);
+  return (t0 | (t1 << 8)) | ((global ? (t2 | (t3 << 8)) : 0x7000u) << 16);
+}
+
 template <int BITS, int NC, int W, bool LITE = false, int MODE = 0>
 __device__ __forceinline__ void score_tile(const uint32_t (&tw)[W], uint32_t sc,
                                            const half8 (&av)[NC], const uint32_t *dtab,
@@ -560,13 +571,11 @@ __device__ __forceinline__ void score_tile(const uint32_t (&tw)[W], uint32_t sc,
     }
   }
   half8 b[3];
-  if (LITE) {
+  if (LITE && MODE <= 1) {
     // scales from the code stream: lane (kq, m) holds 8 scale bits of
-    // candidate m in chunk 0 (kq 0, 1: s^; kq 2, 3: g^)
-    const uint32_t t = nibble_tops(chunk_bits<BITS>(tw, 0));
-    const uint32_t t0 = __shfl(int(t), m, 64), t1 = __shfl(int(t), 16 + m, 64);
-    const uint32_t t2 = __shfl(int(t), 32 + m, 64), t3 = __shfl(int(t), 48 + m, 64);
-    sc = (t0 | (t1 << 8)) | ((global ? (t2 | (t3 << 8)) : 0x7000u) << 16);
+    // candidate m in chunk 0 (kq 0, 1: s^; kq 2, 3: g^); in passes the last
+    // one gets them from the caller, which reads chunk 0's word again
+    if (MODE == 0) sc = lite_scales(chunk_bits<BITS>(tw, 0), m, global);
     b[0] = lead_lane ? decode8_lite(ltab, chunk_bits<BITS>(tw, 0))
                      : decode8<BITS>(dtab, chunk_bits<BITS>(tw, 0), lane4);
   } else {
@@ -794,31 +803,47 @@ __global__ void __launch_bounds__(kScanThreads, 2) k_scan(ScanArgs a) {
       // voff: this lane's first 16-byte unit of the pass's chunks.
       auto run_tiles = [&](auto mode_tag, uint32_t voff) {
         constexpr int MODE = decltype(mode_tag)::value;
+        // Rslm4Lite, last pass: the first code word of the lane's stream
+        // (chunk 0, which holds the scale bits), read with each tile
+        constexpr bool kWord0 = LITE && MODE == 3;
+        auto load_word0 = [&](int t) {
+          return kWord0 ? __builtin_amdgcn_raw_buffer_load_b32(
+                              make_rsrc(tiles + int64_t(t) * tb, t < n_tiles ? tb : 0u),
+                              uint32_t(lane) * 16u, 0, 0)
+                        : 0u;
+        };
+        auto sc_of = [&](uint32_t word0, uint32_t sc_reg, int jj) {
+          if (LITE) return kWord0 ? lite_scales(word0, m, a.global) : 0u;
+          return kPreload ? scale_of(jj) : sc_reg;
+        };
         uint32_t bufA[kWordsPerLane], bufB[kWordsPerLane];
-        uint32_t scA, scB = 0u;
+        uint32_t scA, scB = 0u, w0A, w0B = 0u;
         int lt = wave, j = 0;
         load_tile(bufA, tiles, lt, n_tiles, tb, voff);
         scA = load_scale(lt);
+        w0A = load_word0(lt);
         while (lt < n_tiles) {
           load_tile(bufB, tiles, lt + nwaves, n_tiles, tb, voff);
           scB = load_scale(lt + nwaves);
-          score_tile<BITS, NC, kWordsPerLane, LITE, MODE>(bufA, LITE ? 0u : kPreload ? scale_of(j) : scA, av,
-                                                    dtab, lane4, lt, n_cand, m, ok, qc, qi, out, ltab,
-                                                    lead_lane, a.global);
+          w0B = load_word0(lt + nwaves);
+          score_tile<BITS, NC, kWordsPerLane, LITE, MODE>(bufA, sc_of(w0A, scA, j), av, dtab, lane4,
+                                                          lt, n_cand, m, ok, qc, qi, out, ltab,
+                                                          lead_lane, a.global);
           lt += nwaves;
           ++j;
           if (lt >= n_tiles) break;
           load_tile(bufA, tiles, lt + nwaves, n_tiles, tb, voff);
           scA = load_scale(lt + nwaves);
-          score_tile<BITS, NC, kWordsPerLane, LITE, MODE>(bufB, LITE ? 0u : kPreload ? scale_of(j) : scB, av,
-                                                    dtab, lane4, lt, n_cand, m, ok, qc, qi, out, ltab,
-                                                    lead_lane, a.global);
+          w0A = load_word0(lt + nwaves);
+          score_tile<BITS, NC, kWordsPerLane, LITE, MODE>(bufB, sc_of(w0B, scB, j), av, dtab, lane4,
+                                                          lt, n_cand, m, ok, qc, qi, out, ltab,
+                                                          lead_lane, a.global);
           lt += nwaves;
           ++j;
         }
       };
       const uint32_t voff0 = uint32_t(lane) * 16u;
-      static_assert(NC >= 16 && !LITE && (NC * BITS) % 16 == 0, "multi-pass configuration");
+      static_assert(NC >= 16 && (NC * BITS) % 16 == 0, "multi-pass configuration");
       // passes over chunk ranges of NC chunks: NC * BITS bytes of a lane's
       // stream, a whole number of 16-byte units (the plan's chunk counts
       // above 32 are multiples of such ranges; the host picks NC)
@@ -1166,14 +1191,12 @@ static void launch_scan_bits(int nc, bool multi, dim3 grid, hipStream_t s, const
 #define RSLM_SCAN_NC(NCV) \
   hipLaunchKernelGGL((k_scan<BITS, NCV, LITE>), grid, dim3(kScanThreads), 0, s, a)
 #define RSLM_SCAN_MP(NCV) \
-  hipLaunchKernelGGL((k_scan<BITS, NCV, false, true>), grid, dim3(kScanThreads), 0, s, a)
+  hipLaunchKernelGGL((k_scan<BITS, NCV, LITE, true>), grid, dim3(kScanThreads), 0, s, a)
   if (multi) {
     // pass ranges of 24 or 16 chunks starting on 16-byte units (ranges of
     // 32 would spill registers in the pass loop)
-    if constexpr (!LITE) {
-      if (nc == 16) RSLM_SCAN_MP(16);
-      else if constexpr (BITS % 2 == 0) RSLM_SCAN_MP(24);
-    }
+    if (nc == 16) RSLM_SCAN_MP(16);
+    else if constexpr (BITS % 2 == 0) RSLM_SCAN_MP(24);
     return;
   }
   switch (nc) {
@@ -1231,10 +1254,9 @@ int rslm_scan_topk(const rslm_plan *p, const rslm_index *idx, const float *q_rot
     return RSLM_ERR_INVALID_ARG;
   // above 32 chunks: passes over equal ranges of 24 or 16 chunks that start
   // on a 16-byte unit of a lane's stream (the plan's chunk counts above 32
-  // are multiples of 16, 24 or 32); Rslm4Lite: one pass only
+  // are multiples of 16, 24 or 32)
   int nc_pass = p->codec.n_chunks, n_pass = 1;
   if (nc_pass > 32) {
-    if (p->codec.lead > 0) return RSLM_ERR_UNSUPPORTED;
     n_pass = 0;
     for (int per : {24, 16})
       if (p->codec.n_chunks % per == 0 && (per * p->codec.bits) % 16 == 0) {

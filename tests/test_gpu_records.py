@@ -204,7 +204,10 @@ def test_decode_parity(R, D, bits, passes, mode, lite):
 
 
 @pytest.mark.parametrize("D,passes,mode,k", [(768, 2, "global", 100), (256, 1, "local", 10),
-                                             (128, 1, "global", 25), (1024, 2, "global", 10)])
+                                             (128, 1, "global", 25), (1024, 2, "global", 10),
+                                             # above D = 1,024: scored in passes, the scales
+                                             # read again from chunk 0 in the last one
+                                             (1536, 2, "global", 10), (1152, 2, "local", 17)])
 def test_lite_ivf_scan_parity(R, D, passes, mode, k):
     """The IVF scan over Rslm4Lite records (scales read from the codes; no
     scales array) against the oracle's IVF search with the K = 8 leading
@@ -300,24 +303,3 @@ def test_scan_rejects_misaligned_arrays(R):
                                     p, 0, None)   # (a missed check stops at the workspace: 4)
         assert st == 1, (codes - p, scales - p, offs - p, st)
     torch.cuda.synchronize()
-
-
-def test_lite_scan_above_1024_is_unsupported(R):
-    """A Lite plan scores in one pass only: above D = 1,024 the scan returns
-    UNSUPPORTED before any launch (pointers are only inspected)."""
-    import ctypes as C
-    from paper_2608_30384_amd import _lib as L
-    plan = R.Plan(1152, 4, passes=2, scale_mode="global", lite=True)
-    nlist, nprobe, Q, k = 4, 2, 1, 10
-    buf = torch.zeros(4096, dtype=torch.int64, device=DEV)
-    p = buf.data_ptr()
-    q = torch.zeros((Q, 1152), dtype=torch.float32, device=DEV)
-    pid = torch.zeros((Q, nprobe), dtype=torch.int32, device=DEV)
-    out = torch.zeros((Q, k), dtype=torch.float32, device=DEV)
-    idx = L.Index(nlist, 16, p, p, p, p, p)
-    st = L.lib().rslm_scan_topk(plan.handle, C.byref(idx), q.data_ptr(), Q, pid.data_ptr(),
-                                out.data_ptr(), nprobe, k, out.data_ptr(), pid.data_ptr(), p, 0,
-                                None)
-    assert st == 2, st
-    torch.cuda.synchronize()
-
