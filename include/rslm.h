@@ -340,6 +340,27 @@ int rslm_scan_topk(const rslm_plan *plan, const rslm_index *index,
                    size_t ws_bytes, void *stream);
 
 /* ------------------------------------------------------------------------
+ * rslm_workspace_size -- the workspace (bytes) of one call, by call:
+ *   RSLM_WS_SCAN_TOPK      = rslm_scan_topk_workspace(plan, index, n (= Q),
+ *                            nprobe, k)
+ *   RSLM_WS_ASSIGN_L2      = ivf_assign_probe_workspace(n, dim, nlist, 1,
+ *                            IVF_ASSIGN_L2)
+ *   RSLM_WS_PROBE_IP       = ivf_assign_probe_workspace(n, dim, nlist,
+ *                            nprobe, IVF_PROBE_IP)
+ *   RSLM_WS_KMEANS_UPDATE  = ivf_kmeans_update_workspace(n, nlist)
+ * Arguments a call does not use are ignored (plan and index may be NULL
+ * except for RSLM_WS_SCAN_TOPK).  Returns 0 for an unknown call or out-of-
+ * range arguments.  Host arithmetic only; no device is touched.  The calls
+ * not listed need no workspace.
+ * ------------------------------------------------------------------------ */
+#define RSLM_WS_SCAN_TOPK 0
+#define RSLM_WS_ASSIGN_L2 1
+#define RSLM_WS_PROBE_IP 2
+#define RSLM_WS_KMEANS_UPDATE 3
+size_t rslm_workspace_size(int call, const rslm_plan *plan, const rslm_index *index, int64_t n,
+                           int32_t dim, int32_t nlist, int32_t nprobe, int32_t k);
+
+/* ------------------------------------------------------------------------
  * 8-bit rescoring codec: SQ8 (Section "Background and Related Work": scalar
  * quantisation to 2^8 levels with a per-dimension range) applied to the
  * rotated second residual, used relatively with local scaling ("RelApprox-

@@ -26,7 +26,7 @@ EXPORTS = [
     "ivf_assign_probe_workspace", "ivf_assign_probe", "ivf_assign_probe_noalloc",
     "ivf_assign_probe_noalloc_limit", "ivf_kmeans_update_workspace",
     "ivf_kmeans_update",
-    "rslm_scan_topk_workspace", "rslm_scan_topk",
+    "rslm_scan_topk_workspace", "rslm_scan_topk", "rslm_workspace_size",
     "rslm_sq8_fit", "rslm_sq8_encode", "rslm_rescore", "rslm_set_timer", "rslm_calibrate_read",
 ]
 
@@ -92,6 +92,7 @@ def _declare(lib):
         "ivf_kmeans_update_workspace": (SZ, [I64, I32]),
         "ivf_kmeans_update": (C.c_int, [P, I64, I32, P, I32, P, P, SZ, P]),
         "rslm_scan_topk_workspace": (SZ, [P, C.POINTER(Index), I32, I32, I32]),
+        "rslm_workspace_size": (SZ, [C.c_int, P, C.POINTER(Index), I64, I32, I32, I32, I32]),
         "rslm_scan_topk": (C.c_int, [P, C.POINTER(Index), P, I32, P, P, I32, I32, P, P, P,
                                      SZ, P]),
         "rslm_sq8_fit": (C.c_int, [P, I64, I32, P, P, C.c_int, P]),

@@ -101,6 +101,19 @@ int rslm_last_hip_error(void) { return g_last_hip; }
 
 const char *rslm_version(void) { return "0.1.0"; }
 
+size_t rslm_workspace_size(int call, const rslm_plan *plan, const rslm_index *index, int64_t n,
+                           int32_t dim, int32_t nlist, int32_t nprobe, int32_t k) {
+  switch (call) {
+    case RSLM_WS_SCAN_TOPK:
+      if (n < 0 || n > 0x7fffffff) return 0;
+      return rslm_scan_topk_workspace(plan, index, int32_t(n), nprobe, k);
+    case RSLM_WS_ASSIGN_L2: return ivf_assign_probe_workspace(n, dim, nlist, 1, IVF_ASSIGN_L2);
+    case RSLM_WS_PROBE_IP: return ivf_assign_probe_workspace(n, dim, nlist, nprobe, IVF_PROBE_IP);
+    case RSLM_WS_KMEANS_UPDATE: return ivf_kmeans_update_workspace(n, nlist);
+    default: return 0;
+  }
+}
+
 int rslm_plan_create(const rslm_plan_desc *d, rslm_plan **out) {
   if (!d || !out || !d->signs || !d->perm || !d->codebook) return RSLM_ERR_INVALID_ARG;
   if (d->dim < 1 || d->dim > kMaxDim) return RSLM_ERR_INVALID_ARG;

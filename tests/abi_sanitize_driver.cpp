@@ -121,6 +121,10 @@ int main() {
   (void)ivf_kmeans_update_workspace(int64_t(1) << 31, 65536);
   (void)ivf_assign_probe_noalloc_limit();
   (void)rslm_scan_topk_workspace(nullptr, &idx, 65535, 1024, 1024);
+  for (int call = -1; call < 5; ++call) {
+    (void)rslm_workspace_size(call, nullptr, &idx, int64_t(1) << 40, 4096, 65536, 1024, 1024);
+    (void)rslm_workspace_size(call, nullptr, nullptr, -5, -1, 0, 0, 0);
+  }
 
   std::printf("%s (%d failures)\n", failures ? "FAILED" : "ok", failures);
   return failures ? 1 : 0;

@@ -89,3 +89,12 @@ def test_workspace_sizes_are_host_side():
     assert lib.ivf_assign_probe_workspace(256, 768, 4096, 64, 1) >= 256 * 4096 * 4
     assert lib.ivf_assign_probe_workspace(256, 768, 4096, 1, 0) >= 4096 * 4
     assert lib.ivf_kmeans_update_workspace(1000, 16) >= 1000 * 4 + 3 * 16 * 4
+    # the unified query answers as the per-call functions
+    assert lib.rslm_workspace_size(2, None, None, 256, 768, 4096, 64, 0) == \
+        lib.ivf_assign_probe_workspace(256, 768, 4096, 64, 1)
+    assert lib.rslm_workspace_size(1, None, None, 5000, 96, 1024, 7, 0) == \
+        lib.ivf_assign_probe_workspace(5000, 96, 1024, 1, 0)
+    assert lib.rslm_workspace_size(3, None, None, 1000, 0, 16, 0, 0) == \
+        lib.ivf_kmeans_update_workspace(1000, 16)
+    assert lib.rslm_workspace_size(0, None, None, 256, 0, 0, 64, 100) == 0   # no plan
+    assert lib.rslm_workspace_size(9, None, None, 256, 768, 4096, 64, 100) == 0

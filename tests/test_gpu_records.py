@@ -303,3 +303,19 @@ def test_scan_rejects_misaligned_arrays(R):
                                     p, 0, None)   # (a missed check stops at the workspace: 4)
         assert st == 1, (codes - p, scales - p, offs - p, st)
     torch.cuda.synchronize()
+
+
+def test_unified_workspace_size_matches_the_scan_call(R):
+    """rslm_workspace_size(RSLM_WS_SCAN_TOPK, ...) answers as
+    rslm_scan_topk_workspace for a real plan and index."""
+    import ctypes as C
+    from paper_2608_30384_amd import _lib as L
+    plan = R.Plan(768, 4, passes=2, scale_mode="global")
+    buf = torch.zeros(64, dtype=torch.int64, device=DEV)
+    p = buf.data_ptr()
+    for nlist, max_list, Q, nprobe, k in ((4096, 3431, 256, 64, 100), (16, 40, 3, 2, 10)):
+        idx = L.Index(nlist, max_list, p, p, p, p, p)
+        want = L.lib().rslm_scan_topk_workspace(plan.handle, C.byref(idx), Q, nprobe, k)
+        got = L.lib().rslm_workspace_size(0, plan.handle, C.byref(idx), Q, 0, 0, nprobe, k)
+        assert want > 0 and got == want, (got, want)
+
