@@ -1,5 +1,5 @@
 // Register-resident rotation and 1-D encoder for dimensions that are a
-// multiple of the 128-element block (D = 128 NB, NB = 1, 2, 3, 4, 6, 8).
+// multiple of the 128-element block (D = 128 NB, NB = 1, 2, 3, 4, 6, 8, 12, 16).
 //
 // Same arithmetic as the general path (paper, Section "Pre-Quantization
 // Transformations": S1, block FWHT, permutation + strided transpose, S2,
@@ -255,7 +255,7 @@ __device__ __forceinline__ uint32_t sgnbit(uint32_t m, int b, int i) {
 }
 
 // Stand-in centre rows (zeros) for records encoded without a centre.
-__device__ __align__(16) const float kZeroRow[1024] = {};
+__device__ __align__(16) const float kZeroRow[2048] = {};
 
 // S2 selects the output of the second residual R x - g^ (R c + s^ c^):
 //   0: float32 rows (resid, when given);
@@ -290,7 +290,8 @@ __global__ void __launch_bounds__(256) k_encode_rows(
   // per lane r: bit 8 b + i (word b / 4) = sign of element (b, i) after the
   // transpose: S2 of the target coordinate times the lane sign (-1)^popcount
   // that the first pass left on its source coordinate
-  __shared__ uint32_t tmask[16][2];
+  constexpr int kTmWords = (NB + 3) / 4;   // 4 blocks of 8 sign bits per word
+  __shared__ uint32_t tmask[16][kTmWords];
   // quantiser grids: thresholds below each bucket (cp.qn, cp.qn_lead <= 512)
   __shared__ uint8_t qtab[512];
   __shared__ uint8_t qtab8[LITE ? 512 : 1];
@@ -320,7 +321,7 @@ __global__ void __launch_bounds__(256) k_encode_rows(
     }
     rmask[threadIdx.x] = m;
     if (rp.passes == 2) {
-      uint32_t tm[2] = {0u, 0u};
+      uint32_t tm[kTmWords] = {};
       for (int b = 0; b < NB; ++b)
         for (int i = 0; i < 8; ++i) {
           const int o = 128 * b + 8 * int(threadIdx.x) + i;
@@ -328,8 +329,7 @@ __global__ void __launch_bounds__(256) k_encode_rows(
           const uint32_t bit = sign_bit(rp.s1mask, o + 127) ^ (__popc(src_lane) & 1u);
           tm[b >> 2] |= bit << (8 * (b & 3) + i);
         }
-      tmask[threadIdx.x][0] = tm[0];
-      tmask[threadIdx.x][1] = tm[1];
+      for (int t = 0; t < kTmWords; ++t) tmask[threadIdx.x][t] = tm[t];
     }
   }
   if (rp.passes == 2)
@@ -413,7 +413,9 @@ __global__ void __launch_bounds__(256) k_encode_rows(
               make_float4(z[8 * b + 4 * h], z[8 * b + 4 * h + 1], z[8 * b + 4 * h + 2],
                           z[8 * b + 4 * h + 3]);
       wave_sync_r();
-      const uint32_t tm[2] = {tmask[r][0], tmask[r][1]};
+      uint32_t tm[kTmWords];
+#pragma unroll
+      for (int t = 0; t < kTmWords; ++t) tm[t] = tmask[r][t];
 #pragma unroll
       for (int b = 0; b < NB; ++b) {
         const uint4 t8 = *reinterpret_cast<const uint4 *>(ts + 128 * b + 8 * r);
@@ -681,13 +683,15 @@ __global__ void __launch_bounds__(256) k_encode_rows(
     case 4: CALL(8); break;       \
     case 6: CALL(12); break;      \
     case 8: CALL(16); break;      \
+    case 12: CALL(24); break;     \
+    case 16: CALL(32); break;     \
     default: return false;        \
   }
 
 bool reg_path_ok(const RotParams &rp) {
   if (rp.B != 128 || rp.overlap || rp.D % 128) return false;
   const int nb = rp.D / 128;
-  return nb == 1 || nb == 2 || nb == 3 || nb == 4 || nb == 6 || nb == 8;
+  return nb == 1 || nb == 2 || nb == 3 || nb == 4 || nb == 6 || nb == 8 || nb == 12 || nb == 16;
 }
 
 static int reg_dstride(int D) { return (D + (D >> 5) + 4 + 3) / 4 * 4; }

@@ -36,7 +36,8 @@ def _t(a, dtype=None):
 
 
 # ------------------------------------------------------------------ rotation
-@pytest.mark.parametrize("D", [1, 4, 8, 64, 96, 98, 100, 101, 128, 256, 300, 768, 1024, 2049])
+@pytest.mark.parametrize("D", [1, 4, 8, 64, 96, 98, 100, 101, 128, 256, 300, 768, 1024, 1536,
+                               2048, 2049])
 @pytest.mark.parametrize("passes", [0, 1, 2])
 def test_fwht_forward_inverse(R, D, passes):
     plan = R.Plan(D, 4, passes=passes)
@@ -105,7 +106,9 @@ ENC_CASES = [
     (2049, 4, 2, "local"),
     (2049, 3, 2, "global"),
     (1536, 1, 2, "global"),
-    (1536, 4, 2, "global"),
+    (1536, 4, 2, "global"),    # register path, 12 blocks of 128
+    (1536, 3, 2, "local"),
+    (2048, 4, 2, "local"),     # register path, 16 blocks of 128
 ]
 
 

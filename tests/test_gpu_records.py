@@ -39,7 +39,7 @@ def _t(a, dtype=None):
 
 
 LITE_CASES = [(256, 1, "local", 333), (768, 2, "global", 300), (96, 2, "global", 200),
-              (200, 2, "local", 150), (128, 1, "global", 170)]
+              (200, 2, "local", 150), (128, 1, "global", 170), (1536, 2, "global", 150)]
 
 
 @pytest.mark.parametrize("D,passes,mode,n", LITE_CASES)

@@ -47,7 +47,8 @@ TWO_CASES = [
     (101, 3, 2, 1, "local", 300),     # ragged 4-D second stage, local scale
     (768, 4, 2, 3, "global", 200),    # 3-bit second stage: general path
     (2049, 4, 2, 2, "global", 150),   # odd D above 1,024: general path, overlap block
-    (1536, 4, 2, 2, "local", 160),
+    (1536, 4, 2, 2, "local", 160),    # register path, 12 blocks
+    (2048, 4, 2, 2, "global", 120),   # register path, 16 blocks
 ]
 
 
@@ -182,7 +183,8 @@ def test_rescore_rslm_parity(R, D, bits2, k_in, k_out):
 
 
 @pytest.mark.parametrize("D,passes,n,lite", [(768, 2, 500, False), (256, 1, 300, False),
-                                             (96, 2, 333, False), (768, 2, 400, True)])
+                                             (96, 2, 333, False), (768, 2, 400, True),
+                                             (1536, 2, 200, False), (2048, 2, 150, True)])
 def test_encode_sq8_parity(R, D, passes, n, lite):
     """rslm_encode_sq8: SQ8 codes of the rotated second residual written in the
     encoding pass, against the oracle's residual R x - R a quantised with the
