@@ -474,13 +474,15 @@ def test_end_to_end_tiny_config(R):
 
 
 # ------------------------------------------------------------------ large / tied top-k
-def _scan_vs_oracle(R, D, bits, passes, x, cen, assign, q, nprobe, k):
+def _scan_vs_oracle(R, D, bits, passes, x, cen, assign, q, nprobe, k, max_list=None):
     Rm = H.rot(D, passes)
     C = synth.codebook(bits)
     enc = oracle.encode(x, Rm, C, bits, centroids=cen[assign], scale_mode="global")
     nlist = len(cen)
     plan = R.Plan(D, bits, passes=passes, scale_mode="global")
     index = _device_index(R, plan, enc, assign, nlist, bits)
+    if max_list is not None:   # a looser bound: wider score regions, same results
+        index.max_list_size = max(index.max_list_size, max_list)
     qr = q.astype(np.float64) @ Rm.T
     lists = _oracle_lists(enc, assign, nlist)
     ref_s, ref_i, pid = oracle.ivf_search(q, qr, cen, lists, C, nprobe, k)
@@ -491,8 +493,11 @@ def _scan_vs_oracle(R, D, bits, passes, x, cen, assign, q, nprobe, k):
     return gs.cpu().numpy(), gi.cpu().numpy(), ref_s, ref_i, enc, Rm, C, cands
 
 
-def test_scan_topk_large_candidate_sets(R):
-    """~70,000 candidates per query: the sampled-threshold selection."""
+# max_list: a looser bound on the list sizes (wider per-query score regions,
+# the same results)
+@pytest.mark.parametrize("max_list", [None, 100_000])
+def test_scan_topk_large_candidate_sets(R, max_list):
+    """~70,000 candidates per query: the streaming threshold selection."""
     D, bits, n, nlist, Q, nprobe, k = 64, 4, 90000, 9, 6, 7, 100
     x = synth.gmix(n, D, 12, seed=77)
     rng = np.random.default_rng(77)
@@ -500,7 +505,7 @@ def test_scan_topk_large_candidate_sets(R):
     assign, _ = oracle.assign_l2(x, cen)
     q = synth.queries_like("gmix", Q, D, data_seed=77, n_comp=12)
     gs, gi, ref_s, ref_i, enc, Rm, C, cands = _scan_vs_oracle(R, D, bits, 2, x, cen, assign, q,
-                                                              nprobe, k)
+                                                              nprobe, k, max_list)
     xt = oracle.reconstruct(enc["codes"], enc["s_code"], enc["g_code"], C, Rm, cen[assign])
     xn = np.linalg.norm(xt, axis=1).max()
     diffs = 0
@@ -511,7 +516,8 @@ def test_scan_topk_large_candidate_sets(R):
     assert diffs <= 1
 
 
-def test_scan_topk_exact_ties(R):
+@pytest.mark.parametrize("max_list", [None, 150_000])
+def test_scan_topk_exact_ties(R, max_list):
     """60,000 identical top candidates: the k lowest ids must win.  Every
     top-k slice then holds more tied scores than its sort buffer, so the
     radix selection with the id tie-break runs."""
@@ -527,7 +533,7 @@ def test_scan_topk_exact_ties(R):
     cen = np.vstack([x[rng.choice(N, nlist - 1, replace=False)], star[None]]).astype(np.float64)
     assign, _ = oracle.assign_l2(x, cen)
     gs, gi, ref_s, ref_i, enc, Rm, C, cands = _scan_vs_oracle(R, D, bits, 2, x, cen, assign, q,
-                                                              nprobe, k)
+                                                              nprobe, k, max_list)
     assert np.array_equal(gi[0], np.sort(dup)[:k])
     assert np.array_equal(ref_i[0], gi[0])
     assert np.all(gs[0] == gs[0][0])
