@@ -414,10 +414,11 @@ int rslm_rescore(const rslm_rescore_codec *codec, const float *q_rot,
                  int32_t *out_ids, void *stream);
 
 /* ------------------------------------------------------------------------
- * Profiling hook (not part of the method): later rslm_scan_topk calls made
- * by the calling host thread record ev_begin / ev_end (hipEvent_t passed as
- * void*, created by the caller) on their stream immediately before and after
- * one of their kernels:
+ * Profiling hook (not part of the method): in later rslm_scan_topk calls
+ * made by the calling host thread, ev_begin / ev_end (hipEvent_t passed as
+ * void*, created by the caller with timing enabled) take the start and end
+ * times of one of their kernels' dispatch (the events are attached to the
+ * kernel launch itself, so timing adds nothing to the stream):
  *   RSLM_TIMER_SCAN: the scan kernel;  RSLM_TIMER_TOPK: the top-k kernel.
  * Both NULL disables.  The setting belongs to the calling thread (thread-
  * local), so calls from other threads are unaffected and never timed by it.

@@ -44,6 +44,8 @@
 #include "rslm_internal.h"
 #include "select_dev.h"
 
+#include <hip/hip_ext.h>
+
 #include <type_traits>
 
 namespace rslm {
@@ -441,32 +443,20 @@ __device__ __forceinline__ uint32_t chunk_bits(const uint32_t *sw, int c) {
   return uint32_t(v >> sh) & 0xffffffu;
 }
 
+// 4 and 3 bits: eight coordinates from their bits (one chunk of a lane).
 template <int BITS>
 __device__ __forceinline__ half8 decode8(const uint32_t *tab, uint32_t bits, uint32_t lane4) {
   union {
     uint32_t u[4];
     half8 h;
   } r;
-  if (BITS == 4) {
+  if constexpr (BITS == 4) {
     // symbol = byte i; LDS byte address = byte * 256 + lane * 4 (one v_perm)
 #pragma unroll
     for (int i = 0; i < 4; ++i)
       r.u[i] = lds_word(tab, __builtin_amdgcn_perm(bits, lane4, 0x0c0c0400u | ((4u + i) << 8)));
-  } else if (BITS == 2) {
-    const uint32_t t = bits & 0x0f0fu, u = (bits >> 4) & 0x0f0fu;
-    r.u[0] = lds_word(tab, __builtin_amdgcn_perm(t, lane4, 0x0c0c0400u));
-    r.u[1] = lds_word(tab, __builtin_amdgcn_perm(u, lane4, 0x0c0c0400u));
-    r.u[2] = lds_word(tab, __builtin_amdgcn_perm(t, lane4, 0x0c0c0500u));
-    r.u[3] = lds_word(tab, __builtin_amdgcn_perm(u, lane4, 0x0c0c0500u));
-  } else if (BITS == 1) {
-    const uint32_t a0 = __builtin_amdgcn_perm(bits & 0xfu, lane4, 0x0c0c0400u) << 1;
-    const uint32_t a1 = __builtin_amdgcn_perm(bits >> 4, lane4, 0x0c0c0400u) << 1;
-    const uint2 e0 = lds_dword2(tab, a0), e1 = lds_dword2(tab, a1);
-    r.u[0] = e0.x;
-    r.u[1] = e0.y;
-    r.u[2] = e1.x;
-    r.u[3] = e1.y;
   } else {
+    static_assert(BITS == 3, "1 and 2 bits decode in decode_chunk");
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const uint32_t sym = (bits >> (6 * i)) & 63u;
@@ -474,6 +464,48 @@ __device__ __forceinline__ half8 decode8(const uint32_t *tab, uint32_t bits, uin
     }
   }
   return r.h;
+}
+
+// Decode chunk c of this lane's stream words sw.  1 and 2 bits read the
+// codes straight from the stream word: for 1 bit each table address is one
+// bit-field extract and one shift-or (entry of nibble v at v * 512 + lane * 8),
+// for 2 bits the low and high nibbles of a whole word are split into bytes
+// once for the two chunks it holds, and each address is one v_perm.
+template <int BITS, int W>
+__device__ __forceinline__ half8 decode_chunk(const uint32_t *tab, const uint32_t (&sw)[W], int c,
+                                              uint32_t lane4) {
+  if constexpr (BITS == 2) {
+    union {
+      uint32_t u[4];
+      half8 h;
+    } r;
+    const uint32_t w = sw[c >> 1];
+    const uint32_t t = w & 0x0f0f0f0fu, u = (w >> 4) & 0x0f0f0f0fu;
+    const uint32_t b0 = 4u + 2u * uint32_t(c & 1);   // selector of the chunk's first byte
+    r.u[0] = lds_word(tab, __builtin_amdgcn_perm(t, lane4, 0x0c0c0400u | (b0 << 8)));
+    r.u[1] = lds_word(tab, __builtin_amdgcn_perm(u, lane4, 0x0c0c0400u | (b0 << 8)));
+    r.u[2] = lds_word(tab, __builtin_amdgcn_perm(t, lane4, 0x0c0c0400u | ((b0 + 1u) << 8)));
+    r.u[3] = lds_word(tab, __builtin_amdgcn_perm(u, lane4, 0x0c0c0400u | ((b0 + 1u) << 8)));
+    return r.h;
+  } else if constexpr (BITS == 1) {
+    union {
+      uint32_t u[4];
+      half8 h;
+    } r;
+    const uint32_t w = sw[c >> 2];
+    const int s = 8 * (c & 3);
+    const uint32_t lane8 = lane4 << 1;
+    const uint32_t a0 = (((w >> s) & 0xfu) << 9) | lane8;
+    const uint32_t a1 = (((w >> (s + 4)) & 0xfu) << 9) | lane8;
+    const uint2 e0 = lds_dword2(tab, a0), e1 = lds_dword2(tab, a1);
+    r.u[0] = e0.x;
+    r.u[1] = e0.y;
+    r.u[2] = e1.x;
+    r.u[3] = e1.y;
+    return r.h;
+  } else {
+    return decode8<BITS>(tab, chunk_bits<BITS>(sw, c), lane4);
+  }
 }
 
 // Buffer resources (gfx9 format: 48-bit base, stride 0, byte range, data
@@ -577,14 +609,14 @@ __device__ __forceinline__ void score_tile(const uint32_t (&tw)[W], uint32_t sc,
     // one gets them from the caller, which reads chunk 0's word again
     if (MODE == 0) sc = lite_scales(chunk_bits<BITS>(tw, 0), m, global);
     b[0] = lead_lane ? decode8_lite(ltab, chunk_bits<BITS>(tw, 0))
-                     : decode8<BITS>(dtab, chunk_bits<BITS>(tw, 0), lane4);
+                     : decode_chunk<BITS>(dtab, tw, 0, lane4);
   } else {
-    b[0] = decode8<BITS>(dtab, chunk_bits<BITS>(tw, 0), lane4);
+    b[0] = decode_chunk<BITS>(dtab, tw, 0, lane4);
   }
-  if (NC > 1) b[1] = decode8<BITS>(dtab, chunk_bits<BITS>(tw, NC > 1 ? 1 : 0), lane4);
+  if (NC > 1) b[1] = decode_chunk<BITS>(dtab, tw, NC > 1 ? 1 : 0, lane4);
 #pragma unroll
   for (int c = 0; c < NC; ++c) {
-    if (c + 2 < NC) b[(c + 2) % 3] = decode8<BITS>(dtab, chunk_bits<BITS>(tw, c + 2 < NC ? c + 2 : 0), lane4);
+    if (c + 2 < NC) b[(c + 2) % 3] = decode_chunk<BITS>(dtab, tw, c + 2 < NC ? c + 2 : 0, lane4);
     if (c & 1) acc1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(av[c], b[c % 3], acc1, 0, 0, 0);
     else acc0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(av[c], b[c % 3], acc0, 0, 0, 0);
   }
@@ -1160,16 +1192,16 @@ __global__ void __launch_bounds__(kStreamThreads) k_topk_stream(
   block_topk(row, n, k, f, out_s + int64_t(q) * k, out_i + int64_t(q) * k, ss);
 }
 
-// Profiling hook: events recorded around the scan kernel (0) and the top-k
-// kernel (1) of later rslm_scan_topk calls made by the same host thread (the
-// setting is per thread, so calls from other threads are never timed by it).
+// Profiling hook: events that take the start and end times of the scan
+// kernel's (0) and the top-k kernel's (1) own dispatch in later
+// rslm_scan_topk calls made by the same host thread (the setting is per
+// thread, so calls from other threads are never timed by it).  The events
+// ride on the kernels' dispatch packets (hipExtLaunchKernelGGL), so timing
+// adds no packets, and no gaps, to the stream.
 static thread_local void *g_timer[2][2] = {{nullptr, nullptr}, {nullptr, nullptr}};
 
-static int record_timer(int which, int end, hipStream_t s) {
-  void *ev = g_timer[which][end];
-  if (!ev) return RSLM_OK;
-  hipError_t e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev), s);
-  return e == hipSuccess ? RSLM_OK : set_hip_error(e);
+static hipEvent_t timer_event(int which, int end) {
+  return reinterpret_cast<hipEvent_t>(g_timer[which][end]);
 }
 
 static int cu_count() {
@@ -1188,10 +1220,12 @@ static int cu_count() {
 
 template <int BITS, bool LITE = false>
 static void launch_scan_bits(int nc, bool multi, dim3 grid, hipStream_t s, const ScanArgs &a) {
+  const hipEvent_t e0 = timer_event(0, 0), e1 = timer_event(0, 1);
 #define RSLM_SCAN_NC(NCV) \
-  hipLaunchKernelGGL((k_scan<BITS, NCV, LITE>), grid, dim3(kScanThreads), 0, s, a)
-#define RSLM_SCAN_MP(NCV) \
-  hipLaunchKernelGGL((k_scan<BITS, NCV, LITE, true>), grid, dim3(kScanThreads), 0, s, a)
+  hipExtLaunchKernelGGL((k_scan<BITS, NCV, LITE>), grid, dim3(kScanThreads), 0, s, e0, e1, 0, a)
+#define RSLM_SCAN_MP(NCV)                                                                    \
+  hipExtLaunchKernelGGL((k_scan<BITS, NCV, LITE, true>), grid, dim3(kScanThreads), 0, s, e0, e1, \
+                        0, a)
   if (multi) {
     // pass ranges of 24 or 16 chunks starting on 16-byte units (ranges of
     // 32 would spill registers in the pass loop)
@@ -1317,7 +1351,6 @@ int rslm_scan_topk(const rslm_plan *p, const rslm_index *idx, const float *q_rot
   for (int i = 0; i < 8; ++i) a.cb_lead[i] = p->codec.cb_lead[i];
   const int wg_per_cu = (p->codec.bits == 4) ? 2 : 4;
   const dim3 grid(unsigned(cu_count() * wg_per_cu));
-  if ((st = record_timer(0, 0, s))) return st;
   switch (p->codec.bits) {
     case 4:
       if (a.lead > 0) launch_scan_bits<4, true>(nc_pass, n_pass > 1, grid, s, a);
@@ -1328,13 +1361,11 @@ int rslm_scan_topk(const rslm_plan *p, const rslm_index *idx, const float *q_rot
     default: launch_scan_bits<1>(nc_pass, n_pass > 1, grid, s, a); break;
   }
   if ((st = check_launch())) return st;
-  if ((st = record_timer(0, 1, s))) return st;
-  if ((st = record_timer(1, 0, s))) return st;
-  hipLaunchKernelGGL(k_topk_stream, dim3(unsigned(Q)), dim3(kStreamThreads), 0, s, w.scores,
-                     w.stride, w.totals, w.prefix, probe_ids, nprobe, idx->list_offsets, idx->ids,
-                     k, out_scores, out_ids);
-  if ((st = check_launch())) return st;
-  return record_timer(1, 1, s);
+  hipExtLaunchKernelGGL(k_topk_stream, dim3(unsigned(Q)), dim3(kStreamThreads), 0, s,
+                        timer_event(1, 0), timer_event(1, 1), 0, w.scores, w.stride, w.totals,
+                        w.prefix, probe_ids, nprobe, idx->list_offsets, idx->ids, k, out_scores,
+                        out_ids);
+  return check_launch();
 }
 
 int rslm_set_timer(int which, void *ev_begin, void *ev_end) {
