@@ -417,9 +417,26 @@ struct ScanArgs {
   float cb_lead[8];       // Rslm4Lite: the K = 8 codebook
 };
 
-template <int BITS> struct DecodeTab {
-  static constexpr int kEntries = BITS == 4 ? 256 : BITS == 3 ? 64 : 16;
-  static constexpr int kWords = BITS == 1 ? 2 : 1;
+// LDS decode table of a scan instantiation.  The plan ships a compact
+// table: per symbol (a byte = two 4-bit codes; 6 bits = two 3-bit codes; a
+// nibble = one 2-D or 4-D centroid for 2 and 1 bits) its float16 centroid
+// values.  In LDS every entry is replicated once per lane of an LDS pass, so
+// the lanes of a read always hit distinct banks: 64 copies for 32-bit reads.
+// From 24 chunks up (where registers already limit the scan to two
+// workgroups per CU) 2- and 1-bit codes are decoded by whole bytes: a byte
+// of 2-bit codes is four coordinates (a 64-bit read, 32 copies), a byte of
+// 1-bit codes eight (a 128-bit read, 16 copies), built in the kernel from the
+// compact nibble table.  Entry e of copy l sits at byte e * 256 + l * 4 *
+// kWords, so an address is one v_perm (except the nibble tables of 1-bit
+// codes: 64 copies of two words, an entry stride of 512 bytes).
+template <int BITS, int NC> struct DecodeTab {
+  static constexpr bool kByte = BITS <= 2 && NC >= 24;
+  static constexpr int kCompactWords = BITS == 1 ? 2 : 1;   // words per compact entry
+  static constexpr int kCompactEntries = BITS == 4 ? 256 : BITS == 3 ? 64 : 16;
+  static constexpr int kEntries = kByte ? 256 : kCompactEntries;
+  static constexpr int kWords = kByte ? 2 * kCompactWords : kCompactWords;
+  static constexpr int kCopies = kByte ? 64 / kWords : 64;
+  static_assert(!kByte || kCopies * kWords * 4 == 256, "byte tables: entry stride of 256 bytes");
 };
 
 __device__ __forceinline__ uint32_t lds_word(const uint32_t *tab, uint32_t byte_addr) {
@@ -427,6 +444,9 @@ __device__ __forceinline__ uint32_t lds_word(const uint32_t *tab, uint32_t byte_
 }
 __device__ __forceinline__ uint2 lds_dword2(const uint32_t *tab, uint32_t byte_addr) {
   return *reinterpret_cast<const uint2 *>(reinterpret_cast<const char *>(tab) + byte_addr);
+}
+__device__ __forceinline__ uint4 lds_dword4(const uint32_t *tab, uint32_t byte_addr) {
+  return *reinterpret_cast<const uint4 *>(reinterpret_cast<const char *>(tab) + byte_addr);
 }
 
 // Bits of chunk c (8 coordinates of this lane) from the lane's stream words.
@@ -467,18 +487,42 @@ __device__ __forceinline__ half8 decode8(const uint32_t *tab, uint32_t bits, uin
 }
 
 // Decode chunk c of this lane's stream words sw.  1 and 2 bits read the
-// codes straight from the stream word: for 1 bit each table address is one
-// bit-field extract and one shift-or (entry of nibble v at v * 512 + lane * 8),
-// for 2 bits the low and high nibbles of a whole word are split into bytes
-// once for the two chunks it holds, and each address is one v_perm.
-template <int BITS, int W>
+// codes straight from the stream word: with byte tables each address is one
+// v_perm of a code byte; with nibble tables, for 1 bit each address is one
+// bit-field extract and one shift-or (entry of nibble v at v * 512 + lane *
+// 8), for 2 bits the low and high nibbles of a whole word are split into
+// bytes once for the two chunks it holds, and each address is one v_perm.
+template <int BITS, int NC, int W>
 __device__ __forceinline__ half8 decode_chunk(const uint32_t *tab, const uint32_t (&sw)[W], int c,
                                               uint32_t lane4) {
-  if constexpr (BITS == 2) {
-    union {
-      uint32_t u[4];
-      half8 h;
-    } r;
+  union {
+    uint32_t u[4];
+    half8 h;
+  } r;
+  if constexpr (DecodeTab<BITS, NC>::kByte && BITS == 2) {
+    // bytes 2 (c & 1) and 2 (c & 1) + 1 of the word: coordinates 0-3, 4-7
+    const uint32_t w = sw[c >> 1];
+    const uint32_t lo = (lane4 & 124u) << 1;   // copy lane % 32, 8 bytes each
+    const uint32_t b0 = 4u + 2u * uint32_t(c & 1);
+    const uint2 e0 = lds_dword2(tab, __builtin_amdgcn_perm(w, lo, 0x0c0c0400u | (b0 << 8)));
+    const uint2 e1 = lds_dword2(tab, __builtin_amdgcn_perm(w, lo, 0x0c0c0400u | ((b0 + 1u) << 8)));
+    r.u[0] = e0.x;
+    r.u[1] = e0.y;
+    r.u[2] = e1.x;
+    r.u[3] = e1.y;
+    return r.h;
+  } else if constexpr (DecodeTab<BITS, NC>::kByte && BITS == 1) {
+    // byte c & 3 of the word: all eight coordinates
+    const uint32_t w = sw[c >> 2];
+    const uint32_t lo = (lane4 & 60u) << 2;   // copy lane % 16, 16 bytes each
+    const uint4 e = lds_dword4(
+        tab, __builtin_amdgcn_perm(w, lo, 0x0c0c0400u | ((4u + uint32_t(c & 3)) << 8)));
+    r.u[0] = e.x;
+    r.u[1] = e.y;
+    r.u[2] = e.z;
+    r.u[3] = e.w;
+    return r.h;
+  } else if constexpr (BITS == 2) {
     const uint32_t w = sw[c >> 1];
     const uint32_t t = w & 0x0f0f0f0fu, u = (w >> 4) & 0x0f0f0f0fu;
     const uint32_t b0 = 4u + 2u * uint32_t(c & 1);   // selector of the chunk's first byte
@@ -488,10 +532,6 @@ __device__ __forceinline__ half8 decode_chunk(const uint32_t *tab, const uint32_
     r.u[3] = lds_word(tab, __builtin_amdgcn_perm(u, lane4, 0x0c0c0400u | ((b0 + 1u) << 8)));
     return r.h;
   } else if constexpr (BITS == 1) {
-    union {
-      uint32_t u[4];
-      half8 h;
-    } r;
     const uint32_t w = sw[c >> 2];
     const int s = 8 * (c & 3);
     const uint32_t lane8 = lane4 << 1;
@@ -609,14 +649,15 @@ __device__ __forceinline__ void score_tile(const uint32_t (&tw)[W], uint32_t sc,
     // one gets them from the caller, which reads chunk 0's word again
     if (MODE == 0) sc = lite_scales(chunk_bits<BITS>(tw, 0), m, global);
     b[0] = lead_lane ? decode8_lite(ltab, chunk_bits<BITS>(tw, 0))
-                     : decode_chunk<BITS>(dtab, tw, 0, lane4);
+                     : decode_chunk<BITS, NC>(dtab, tw, 0, lane4);
   } else {
-    b[0] = decode_chunk<BITS>(dtab, tw, 0, lane4);
+    b[0] = decode_chunk<BITS, NC>(dtab, tw, 0, lane4);
   }
-  if (NC > 1) b[1] = decode_chunk<BITS>(dtab, tw, NC > 1 ? 1 : 0, lane4);
+  if (NC > 1) b[1] = decode_chunk<BITS, NC>(dtab, tw, NC > 1 ? 1 : 0, lane4);
 #pragma unroll
   for (int c = 0; c < NC; ++c) {
-    if (c + 2 < NC) b[(c + 2) % 3] = decode_chunk<BITS>(dtab, tw, c + 2 < NC ? c + 2 : 0, lane4);
+    if (c + 2 < NC)
+      b[(c + 2) % 3] = decode_chunk<BITS, NC>(dtab, tw, c + 2 < NC ? c + 2 : 0, lane4);
     if (c & 1) acc1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(av[c], b[c % 3], acc1, 0, 0, 0);
     else acc0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(av[c], b[c % 3], acc0, 0, 0, 0);
   }
@@ -646,8 +687,8 @@ __device__ __forceinline__ void score_tile(const uint32_t (&tw)[W], uint32_t sc,
 // MP: the multi-pass variant (items scored in a.n_pass passes of NC chunks).
 template <int BITS, int NC, bool LITE = false, bool MP = false>
 __global__ void __launch_bounds__(kScanThreads, 2) k_scan(ScanArgs a) {
-  using T = DecodeTab<BITS>;
-  __shared__ uint32_t dtab[T::kEntries * 64 * T::kWords];
+  using T = DecodeTab<BITS, NC>;
+  __shared__ uint32_t dtab[T::kEntries * T::kCopies * T::kWords];
   __shared__ uint32_t ltab[LITE ? 256 : 1];
   if (LITE) {   // Rslm4Lite chunk-0 table: byte -> half2(C8[lo & 7], C8[hi & 7])
     const int e = threadIdx.x;   // kScanThreads == 256 entries
@@ -665,12 +706,21 @@ __global__ void __launch_bounds__(kScanThreads, 2) k_scan(ScanArgs a) {
   const int nwaves = kScanThreads / 64;
   const uint32_t lane4 = uint32_t(lane) * 4u;
 
-  // replicate the compact table once per lane: entry e of lane l at
-  // word (e * 64 + l) * kWords
-  for (int idx = tid; idx < T::kEntries * 64; idx += kScanThreads) {
-    const int e = idx >> 6;
+  // replicate the table: entry e of copy l at word (e * kCopies + l) *
+  // kWords; a byte entry is the compact entries of its low and high nibbles
+  for (int idx = tid; idx < T::kEntries * T::kCopies; idx += kScanThreads) {
+    const int e = idx / T::kCopies;
+    if constexpr (T::kByte) {
+      constexpr int cw = T::kCompactWords;
 #pragma unroll
-    for (int w = 0; w < T::kWords; ++w) dtab[idx * T::kWords + w] = a.dtab[e * T::kWords + w];
+      for (int w = 0; w < cw; ++w) {
+        dtab[idx * T::kWords + w] = a.dtab[(e & 15) * cw + w];
+        dtab[idx * T::kWords + cw + w] = a.dtab[(e >> 4) * cw + w];
+      }
+    } else {
+#pragma unroll
+      for (int w = 0; w < T::kWords; ++w) dtab[idx * T::kWords + w] = a.dtab[e * T::kWords + w];
+    }
   }
   __syncthreads();
 
@@ -1349,7 +1399,10 @@ int rslm_scan_topk(const rslm_plan *p, const rslm_index *idx, const float *q_rot
   a.lead = p->codec.lead;
   a.global = p->codec.global;
   for (int i = 0; i < 8; ++i) a.cb_lead[i] = p->codec.cb_lead[i];
-  const int wg_per_cu = (p->codec.bits == 4) ? 2 : 4;
+  // two workgroups per CU where the decode table takes 64 KiB of LDS (4 bits;
+  // byte tables of 2 and 1 bits from 24 chunks up)
+  const bool big_table = p->codec.bits == 4 || (p->codec.bits <= 2 && nc_pass >= 24);
+  const int wg_per_cu = big_table ? 2 : 4;
   const dim3 grid(unsigned(cu_count() * wg_per_cu));
   switch (p->codec.bits) {
     case 4:

@@ -358,6 +358,10 @@ SCAN_CASES = [
     (2048, 2, 2, "global", 600, 5, 10, 3, 10, False),
     (3072, 1, 2, "global", 500, 4, 8, 2, 10, False),
     (1536, 4, 2, "global", 9000, 3, 8, 2, 100, True),      # lists of several chunks, in passes
+    # 1- and 2-bit codes decoded by whole bytes (24 chunks and more, passes of 24)
+    (1024, 2, 2, "global", 900, 6, 12, 3, 10, False),
+    (768, 1, 2, "local", 900, 6, 12, 4, 10, False),
+    (1536, 2, 2, "global", 600, 5, 10, 3, 10, False),
 ]
 
 
