@@ -254,6 +254,11 @@ __device__ __forceinline__ uint32_t sgnbit(uint32_t m, int b, int i) {
   return ((m >> (8 * (b & 1) + i)) & 1u) << 31;
 }
 
+// Quantiser grid buckets the register-path encoder holds in LDS (the plan's
+// grids for the Lloyd-Max codebooks have 128; larger grids take the general
+// path).
+constexpr int kQuantBuckets = 128;
+
 // Stand-in centre rows (zeros) for records encoded without a centre.
 __device__ __align__(16) const float kZeroRow[2048] = {};
 
@@ -284,17 +289,21 @@ __global__ void __launch_bounds__(256) k_encode_rows(
   constexpr int kVecStride = D + 4;   // floats per vector buffer (offset of 4 banks per row)
   __shared__ float buf[16 * kVecStride];
   __shared__ float cbs[16], thr[16];
-  __shared__ float cb8[16], thr8[16];   // Rslm4Lite: K = 8 codebook of the leading lanes
-  __shared__ float cb2[16], cb2y[16];   // second codebook, first and second coordinates
+  // Rslm4Lite: K = 8 codebook of the leading lanes
+  __shared__ float cb8[LITE ? 16 : 1], thr8[LITE ? 16 : 1];
+  // second codebook, first and second coordinates
+  __shared__ float cb2[TWO ? 16 : 1], cb2y[TWO ? 16 : 1];
   __shared__ uint32_t rmask[16];
   // per lane r: bit 8 b + i (word b / 4) = sign of element (b, i) after the
   // transpose: S2 of the target coordinate times the lane sign (-1)^popcount
   // that the first pass left on its source coordinate
   constexpr int kTmWords = (NB + 3) / 4;   // 4 blocks of 8 sign bits per word
   __shared__ uint32_t tmask[16][kTmWords];
-  // quantiser grids: thresholds below each bucket (cp.qn, cp.qn_lead <= 512)
-  __shared__ uint8_t qtab[512];
-  __shared__ uint8_t qtab8[LITE ? 512 : 1];
+  // quantiser grids: thresholds below each bucket (cp.qn, cp.qn_lead <=
+  // kQuantBuckets)
+  __shared__ uint8_t qtab[kQuantBuckets];
+  __shared__ uint8_t qtab8[LITE ? kQuantBuckets : 1];
+
   __shared__ uint16_t ts[D];
   const int lane = threadIdx.x & 63;
   const int wid = threadIdx.x >> 6;
@@ -334,6 +343,7 @@ __global__ void __launch_bounds__(256) k_encode_rows(
   }
   if (rp.passes == 2)
     for (int k = threadIdx.x; k < D; k += blockDim.x) ts[k] = uint16_t(4 * rp.tsrc[k]);
+
   for (int j = threadIdx.x; j < cp.qn; j += blockDim.x) {
     int cnt = 0;
 #pragma unroll
@@ -632,22 +642,70 @@ __global__ void __launch_bounds__(256) k_encode_rows(
     const float gh = dec_ue4m12(gu);
     uint8_t *dst = codes2 + row * D + 8 * r;   // indexed by source row
     const float *lo_r = sq8_lo + 8 * r, *hi_r = sq8_hi + 8 * r;
+    // lo and 255 / (hi - lo) of every dimension (sq8_inv), staged once per
+    // wavefront in its vector buffers (free after the rotation) by the lanes
+    // still running, instead of a reciprocal per coordinate: the four rows
+    // share the dimensions
+    float *sq_inv = buf + 4 * wid * kVecStride, *sq_lo = sq_inv + D;
+    static_assert(2 * D <= 4 * kVecStride, "ranges fit the wavefront's vector buffers");
+    if constexpr (!LITE) {
+      wave_sync_r();   // the wavefront is done with its vector buffers
+      const uint64_t act = __ballot(1);
+      const int n_act = __popcll(act);
+      const int me = __popcll(act & ((uint64_t(1) << lane) - 1u));
+      if (n_act == 64) {
+        // every lane: dimensions lane + 64 j, loads of four j in flight
+#pragma unroll
+        for (int j0 = 0; j0 < D / 64; j0 += 4) {
+          float l4[4], h4[4];
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            l4[t] = sq8_lo[lane + 64 * (j0 + t)];
+            h4[t] = sq8_hi[lane + 64 * (j0 + t)];
+          }
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            sq_inv[lane + 64 * (j0 + t)] = sq8_inv(l4[t], h4[t]);
+            sq_lo[lane + 64 * (j0 + t)] = l4[t];
+          }
+        }
+      } else {
+        for (int d = me; d < D; d += n_act) {
+          sq_inv[d] = sq8_inv(sq8_lo[d], sq8_hi[d]);
+          sq_lo[d] = sq8_lo[d];
+        }
+      }
+      wave_sync_r();
+    }
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
       uint32_t word2[2];
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const float4 v = *reinterpret_cast<const float4 *>(rcr + 128 * b + 4 * h);
-        const float4 l4 = *reinterpret_cast<const float4 *>(lo_r + 128 * b + 4 * h);
-        const float4 h4 = *reinterpret_cast<const float4 *>(hi_r + 128 * b + 4 * h);
+        const float4 l4 = *reinterpret_cast<const float4 *>(
+            (LITE ? lo_r : sq_lo + 8 * r) + 128 * b + 4 * h);
         const float va[4] = {v.x, v.y, v.z, v.w};
-        const float la[4] = {l4.x, l4.y, l4.z, l4.w}, ha[4] = {h4.x, h4.y, h4.z, h4.w};
+        const float la[4] = {l4.x, l4.y, l4.z, l4.w};
+        float ia[4];
+        if constexpr (!LITE) {
+          const float4 i4 = *reinterpret_cast<const float4 *>(sq_inv + 128 * b + 8 * r + 4 * h);
+          ia[0] = i4.x;
+          ia[1] = i4.y;
+          ia[2] = i4.z;
+          ia[3] = i4.w;
+        } else {
+          const float4 h4 = *reinterpret_cast<const float4 *>(hi_r + 128 * b + 4 * h);
+          const float ha[4] = {h4.x, h4.y, h4.z, h4.w};
+#pragma unroll
+          for (int t = 0; t < 4; ++t) ia[t] = sq8_inv(la[t], ha[t]);
+        }
         uint32_t wv = 0u;
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
           const int e = 8 * b + 4 * h + t;
           const float o = z[e] + va[t] - gh * (va[t] + sh * centroid(b, 4 * h + t));
-          wv |= sq8_code(o, la[t], ha[t]) << (8 * t);
+          wv |= sq8_code_inv(o, la[t], ia[t]) << (8 * t);
         }
         word2[h] = wv;
       }
@@ -727,6 +785,7 @@ bool launch_encode_reg(const rslm_plan *p, const rslm_plan *p2, const float *x, 
   if (lite && s2 == 1) return false;   // Lite with an RSLM second stage: general path
   // codebooks whose thresholds no quantiser grid separates: general path
   if (p->codec.qn == 0 || (lite && p->codec.qn_lead == 0)) return false;
+  if (p->codec.qn > kQuantBuckets || (lite && p->codec.qn_lead > kQuantBuckets)) return false;
   // 16-byte vector loads and stores of every row
   if ((reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(cen) |
        reinterpret_cast<uintptr_t>(cen_rot) | reinterpret_cast<uintptr_t>(resid) |

@@ -182,7 +182,10 @@ def test_rescore_rslm_parity(R, D, bits2, k_in, k_out):
                      *cands[i])
 
 
-@pytest.mark.parametrize("D,passes,n,lite", [(768, 2, 500, False), (256, 1, 300, False),
+# 503 rows: the last wavefront holds three rows (its SQ8 ranges are prepared
+# by the lanes that remain)
+@pytest.mark.parametrize("D,passes,n,lite", [(768, 2, 500, False), (768, 2, 503, False),
+                                             (256, 1, 300, False),
                                              (96, 2, 333, False), (768, 2, 400, True),
                                              (1536, 2, 200, False), (2048, 2, 150, True)])
 def test_encode_sq8_parity(R, D, passes, n, lite):
