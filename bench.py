@@ -547,9 +547,10 @@ def main():
     def step(b, timers):
         """One pass of every row over one batch: rotate, probe, scan + top-k,
         rescore, and the encode of new vectors into scan records and SQ8
-        rescoring codes (row a7).  (Running the encode
-        concurrently on a second stream was slower: it takes the CUs the
-        probe and top-k need.)"""
+        rescoring codes (row a7), in this order on one stream.  (The encode
+        on a second stream shortens the step by about 3 %, but its
+        workgroups then share the CUs with the scan, whose own time grows by
+        about 6 %; in order, the scan's figure is the kernel's alone.)"""
         qb = batches[b % len(batches)]
         mark = (lambda i: timers[i].record()) if timers else (lambda i: None)
         mark(0)
