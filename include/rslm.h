@@ -323,8 +323,8 @@ typedef struct rslm_index {
  * padded with (-inf, -1).
  *   q_rot: Q x D rotated queries (rslm_fwht); probe_ids / probe_dots:
  *   Q x nprobe; out_scores / out_ids: Q x k.  1 <= k <= 1024, Q <= 65535,
- *   nprobe * index->max_list_size < 2^30 (a query's scores are addressed
- *   with 32-bit byte offsets), else RSLM_ERR_INVALID_ARG.  Alignment:
+ *   nprobe * index->max_list_size <= 2^30 - 4 (a query's scores are read
+ *   with 32-bit byte ranges), else RSLM_ERR_INVALID_ARG.  Alignment:
  *   index->codes 16 bytes, list_offsets 8 bytes, every other array 4 bytes,
  *   else RSLM_ERR_INVALID_ARG.  Any plan dimension (above D = 1,024 the
  *   coordinates are scored in passes over equal chunk ranges).  With a Lite

@@ -1147,10 +1147,9 @@ __global__ void __launch_bounds__(kStreamThreads) k_topk_stream(
     constexpr int kRound = kStreamThreads * 16;
     // range-checked loads (unconditional, zeros past the region): the range
     // is n rounded up to whole 16-byte groups, inside the region's stride
-    // (computed in 64 bits: a region of 2^30 - 3 or more scores would wrap)
-    const uint64_t rbytes = uint64_t((int64_t(n) + 3) & ~int64_t(3)) * 4u;
-    const __amdgpu_buffer_rsrc_t rr =
-        make_rsrc(row, uint32_t(rbytes < 0xFFFFFFF0ull ? rbytes : 0xFFFFFFF0ull));
+    // (n <= 2^30 - 4, so at most 2^32 - 16 bytes: a 32-bit range)
+    const uint32_t rbytes = uint32_t((int64_t(n) + 3) & ~int64_t(3)) * 4u;
+    const __amdgpu_buffer_rsrc_t rr = make_rsrc(row, rbytes);
     auto load_round = [&](float4 (&v)[4], int base) {
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
@@ -1322,7 +1321,9 @@ int rslm_scan_topk(const rslm_plan *p, const rslm_index *idx, const float *q_rot
   if (idx->nlist < 1 || idx->nlist > 65536 || nprobe > idx->nlist || idx->max_list_size < 0)
     return RSLM_ERR_INVALID_ARG;
   // a query's score region is read through 32-bit byte offsets
-  if (int64_t(nprobe) * idx->max_list_size >= (int64_t(1) << 30)) return RSLM_ERR_INVALID_ARG;
+  // a query's score region is read with 32-bit byte ranges of whole 16-byte
+  // groups: at most 2^30 - 4 scores
+  if (int64_t(nprobe) * idx->max_list_size > (int64_t(1) << 30) - 4) return RSLM_ERR_INVALID_ARG;
   if (Q == 0) return RSLM_OK;
   if (Q > 65535) return RSLM_ERR_INVALID_ARG;   // gridDim.y of the top-k kernel
   if (!q_rot || !probe_ids || !probe_dots || !out_scores || !out_ids || !idx->list_offsets ||

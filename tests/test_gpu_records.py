@@ -261,10 +261,10 @@ def test_lite_ivf_scan_parity(R, D, passes, mode, k):
 
 
 def test_scan_rejects_oversized_score_regions(R):
-    """nprobe * max_list_size must stay below 2^30 (a query's score region is
-    read with 32-bit byte offsets): at the limit the call returns
-    INVALID_ARG, one below it gets as far as the workspace check; neither
-    launches anything."""
+    """nprobe * max_list_size must not exceed 2^30 - 4 (a query's score region
+    is read with 32-bit byte ranges of whole 16-byte groups): above it the
+    call returns INVALID_ARG, at it the call gets as far as the workspace
+    check; neither launches anything."""
     import ctypes as C
     from paper_2608_30384_amd import _lib as L
     plan = R.Plan(64, 4, passes=0, scale_mode="global")
@@ -274,12 +274,14 @@ def test_scan_rejects_oversized_score_regions(R):
     q = torch.zeros((Q, 64), dtype=torch.float32, device=DEV)
     pid = torch.zeros((Q, nprobe), dtype=torch.int32, device=DEV)
     out = torch.zeros((Q, k), dtype=torch.float32, device=DEV)
-    for max_list, want in (((1 << 30) // nprobe, 1), ((1 << 30) // nprobe - 1, 4)):
+    for np_, max_list, want in ((nprobe, (1 << 30) // nprobe, 1),
+                                (nprobe, (1 << 30) // nprobe - 1, 4),
+                                (1, (1 << 30) - 3, 1), (1, (1 << 30) - 4, 4)):
         idx = L.Index(nlist, max_list, p, p, p, p, p)
         st = L.lib().rslm_scan_topk(plan.handle, C.byref(idx), q.data_ptr(), Q, pid.data_ptr(),
-                                    out.data_ptr(), nprobe, k, out.data_ptr(), pid.data_ptr(),
+                                    out.data_ptr(), np_, k, out.data_ptr(), pid.data_ptr(),
                                     p, 0, None)
-        assert st == want, (max_list, st)
+        assert st == want, (np_, max_list, st)
     torch.cuda.synchronize()
 
 
