@@ -2,6 +2,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <limits>
 #include <new>
 
 #include "rslm_internal.h"
@@ -32,6 +33,53 @@ static void quant_grid(const float *thr, int n, float &qs, float &qo, int &qn) {
       return;
     }
   }
+}
+
+// Candidate lists of the 2-D nearest-centroid grid (CodecParams::g2tab).
+// Code k is left out of a cell only if one other code j is nearer by more
+// than kMargin everywhere in the cell widened by kWiden (the device rounds
+// u, the cell index and the distance in float32, far below both margins):
+// with d_k(u) = |C_k|^2 / 2 - <u, C_k>, j beats k on a box when
+// (h_k - h_j) - max_u <u, C_k - C_j> > kMargin, the maximum taken at the
+// box's corner in the direction of C_k - C_j (an unbounded side, the outer
+// cells extend to infinity, only if that component is zero or points away).
+// The nearest code of any point is then in its cell's list, and the device,
+// scanning the list in ascending order with a strict comparison, picks the
+// same code (lowest on ties) as a search over all K.  False if a cell needs
+// more than four codes.
+static bool grid2_lists(const CodecParams &c, uint16_t *tab) {
+  constexpr double kWiden = 1e-4, kMargin = 1e-4;
+  const double inf = std::numeric_limits<double>::infinity();
+  for (int i = 0; i < kGrid2; ++i)
+    for (int j = 0; j < kGrid2; ++j) {
+      double lo[2] = {(i - double(c.g2o)) / c.g2s - kWiden, (j - double(c.g2o)) / c.g2s - kWiden};
+      double hi[2] = {(i + 1 - double(c.g2o)) / c.g2s + kWiden,
+                      (j + 1 - double(c.g2o)) / c.g2s + kWiden};
+      if (i == 0) lo[0] = -inf;
+      if (i == kGrid2 - 1) hi[0] = inf;
+      if (j == 0) lo[1] = -inf;
+      if (j == kGrid2 - 1) hi[1] = inf;
+      int list[16], n = 0;
+      for (int k = 0; k < c.K; ++k) {
+        bool beaten = false;
+        for (int o = 0; o < c.K && !beaten; ++o) {
+          if (o == k) continue;
+          double m = 0.0;   // max over the box of <u, C_k - C_o>
+          for (int d = 0; d < 2; ++d) {
+            const double a = double(c.cb[2 * k + d]) - double(c.cb[2 * o + d]);
+            if (a > 0) m += a * hi[d];
+            else if (a < 0) m += a * lo[d];
+          }
+          beaten = (double(c.cbh[k]) - double(c.cbh[o])) - m > kMargin;
+        }
+        if (!beaten) list[n++] = k;
+      }
+      if (n < 1 || n > 4) return false;
+      uint32_t e = 0;
+      for (int t = 0; t < 4; ++t) e |= uint32_t(list[t < n ? t : n - 1]) << (4 * t);
+      tab[i * kGrid2 + j] = uint16_t(e);   // cell (gx = i, gy = j)
+    }
+  return true;
 }
 
 int set_hip_error(hipError_t e) {
@@ -226,6 +274,12 @@ int rslm_plan_create(const rslm_plan_desc *d, rslm_plan **out) {
                                        : __builtin_inff();
   quant_grid(c.thr, g == 1 ? K - 1 : 0, c.qs, c.qo, c.qn);
   quant_grid(c.thr_lead, d->lite ? 7 : 0, c.qs_lead, c.qo_lead, c.qn_lead);
+  // 2-D codebooks: nearest-centroid grid over [-emax, emax]^2 (|u| <= emax)
+  uint16_t g2[kGrid2 * kGrid2];
+  c.g2s = float(kGrid2) / (2.0f * c.emax);
+  c.g2o = float(kGrid2 / 2);
+  c.g2tab = nullptr;
+  const bool has_g2 = g == 2 && grid2_lists(c, g2);
 
   // --- device tables: signs, intra-block permutation, compact decode table
   float s1f[256];
@@ -301,6 +355,14 @@ int rslm_plan_create(const rslm_plan_desc *d, rslm_plan **out) {
     rslm_plan_destroy(p);
     return set_hip_error(e);
   }
+  if (has_g2) {
+    if ((e = hipMalloc(&p->d_g2tab, sizeof(g2))) != hipSuccess ||
+        (e = hipMemcpy(p->d_g2tab, g2, sizeof(g2), hipMemcpyHostToDevice)) != hipSuccess) {
+      rslm_plan_destroy(p);
+      return set_hip_error(e);
+    }
+    c.g2tab = p->d_g2tab;
+  }
   r.s1 = p->d_s1;
   r.pi = p->d_pi;
   r.tsrc = p->d_tsrc;
@@ -320,6 +382,7 @@ int rslm_plan_destroy(rslm_plan *p) {
   if (p->d_pi) (void)hipFree(p->d_pi);
   if (p->d_dtab) (void)hipFree(p->d_dtab);
   if (p->d_tsrc) (void)hipFree(p->d_tsrc);
+  if (p->d_g2tab) (void)hipFree(p->d_g2tab);
   delete p;
   return RSLM_OK;
 }

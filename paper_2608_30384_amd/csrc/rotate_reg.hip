@@ -291,8 +291,10 @@ __global__ void __launch_bounds__(256) k_encode_rows(
   __shared__ float cbs[16], thr[16];
   // Rslm4Lite: K = 8 codebook of the leading lanes
   __shared__ float cb8[LITE ? 16 : 1], thr8[LITE ? 16 : 1];
-  // second codebook, first and second coordinates
-  __shared__ float cb2[TWO ? 16 : 1], cb2y[TWO ? 16 : 1];
+  // second codebook: (first, second coordinate, |C_k|^2 / 2) per code, and
+  // the candidate lists of its nearest-centroid grid
+  __shared__ float4 cb2[TWO ? 16 : 1];
+  __shared__ uint16_t g2t[TWO ? kGrid2 * kGrid2 : 1];
   __shared__ uint32_t rmask[16];
   // per lane r: bit 8 b + i (word b / 4) = sign of element (b, i) after the
   // transpose: S2 of the target coordinate times the lane sign (-1)^popcount
@@ -308,10 +310,11 @@ __global__ void __launch_bounds__(256) k_encode_rows(
   const int lane = threadIdx.x & 63;
   const int wid = threadIdx.x >> 6;
   const int rho = lane >> 4, r = lane & 15;
-  if (TWO && threadIdx.x < 16) {
-    cb2[threadIdx.x] = cp2.cb[2 * threadIdx.x];
-    cb2y[threadIdx.x] = cp2.cb[2 * threadIdx.x + 1];
-  }
+  if (TWO && threadIdx.x < 16)
+    cb2[threadIdx.x] = make_float4(cp2.cb[2 * threadIdx.x], cp2.cb[2 * threadIdx.x + 1],
+                                   cp2.cbh[threadIdx.x], 0.f);
+  if (TWO)
+    for (int j = threadIdx.x; j < kGrid2 * kGrid2; j += blockDim.x) g2t[j] = cp2.g2tab[j];
   if (LITE && threadIdx.x < 16) {
     cb8[threadIdx.x] = (threadIdx.x < 8) ? cp.cb_lead[threadIdx.x] : 0.f;
     thr8[threadIdx.x] = cp.thr_lead[threadIdx.x];
@@ -571,10 +574,12 @@ __global__ void __launch_bounds__(256) k_encode_rows(
     rr2 = row_sum16(rr2);
     const float inv2 = (m2 > 0.f) ? cp2.emax / m2 : 0.f;
     // Nearest 2-D centroid: argmin_k |c_k|^2 / 2 - <u, c_k> (lower k on
-    // ties); the codebook terms are uniform (kernel arguments, scalar
-    // registers).  With the codes of a block: ||c2^||^2, <c^, c2^> and
-    // <R c, c2^>.  A zero r2 (m2 = 0) gets codes 0 and s2^ = 0, which
-    // removes these sums from g2^, so they need no guard.
+    // ties) over the (at most four) codes listed for u's cell of the grid,
+    // in ascending order with a strict comparison: the same code as a scan
+    // of all K (the lists hold every code that can be nearest in the cell).
+    // With the codes of a block: ||c2^||^2, <c^, c2^> and <R c, c2^>.  A
+    // zero r2 (m2 = 0) gets codes 0 and s2^ = 0, which removes these sums
+    // from g2^, so they need no guard.
     uint32_t w2[NB];
     float cn22 = 0.f, c12 = 0.f, rc2 = 0.f;
     int off2 = 0;
@@ -585,20 +590,26 @@ __global__ void __launch_bounds__(256) k_encode_rows(
       const float4 rb = *reinterpret_cast<const float4 *>(rcr + off2 + 128 * b + 4);
       float nu0[4], nu1[4], best[4];
       uint32_t code[4];
+      uint32_t cell[4];
 #pragma unroll
       for (int k2 = 0; k2 < 4; ++k2) {
-        nu0[k2] = -z[8 * b + 2 * k2] * inv2;
-        nu1[k2] = -z[8 * b + 2 * k2 + 1] * inv2;
+        const float u0 = z[8 * b + 2 * k2] * inv2, u1 = z[8 * b + 2 * k2 + 1] * inv2;
+        nu0[k2] = -u0;
+        nu1[k2] = -u1;
         best[k2] = 3.4e38f;
         code[k2] = 0u;
+        const int gx = int(__builtin_amdgcn_fmed3f(fmaf(u0, cp2.g2s, cp2.g2o), 0.f, float(kGrid2 - 1)));
+        const int gy = int(__builtin_amdgcn_fmed3f(fmaf(u1, cp2.g2s, cp2.g2o), 0.f, float(kGrid2 - 1)));
+        cell[k2] = g2t[gx * kGrid2 + gy];
       }
 #pragma unroll
-      for (int k = 0; k < 16; ++k) {
-        const float c0 = cp2.cb[2 * k], c1 = cp2.cb[2 * k + 1], hk = cp2.cbh[k];
+      for (int t = 0; t < 4; ++t) {
 #pragma unroll
         for (int k2 = 0; k2 < 4; ++k2) {
-          const float d = fmaf(nu1[k2], c1, fmaf(nu0[k2], c0, hk));
-          code[k2] = (d < best[k2]) ? uint32_t(k) : code[k2];
+          const uint32_t k = (cell[k2] >> (4 * t)) & 15u;
+          const float4 ck = cb2[k];
+          const float d = fmaf(nu1[k2], ck.y, fmaf(nu0[k2], ck.x, ck.z));
+          code[k2] = (d < best[k2]) ? k : code[k2];
           best[k2] = fminf(best[k2], d);
         }
       }
@@ -610,7 +621,8 @@ __global__ void __launch_bounds__(256) k_encode_rows(
       for (int k2 = 0; k2 < 4; ++k2) {
         const uint32_t cd = code[k2];
         w2[b] |= cd << (4 * k2);
-        const float c0 = cb2[cd], c1 = cb2y[cd];
+        const float4 cc = cb2[cd];
+        const float c0 = cc.x, c1 = cc.y;
         cn22 = fmaf(c0, c0, fmaf(c1, c1, cn22));
         const float e0 = lds_at(cbs, 4u * ((wb >> (BITS * 2 * k2)) & uint32_t(K - 1)));
         const float e1 = lds_at(cbs, 4u * ((wb >> (BITS * (2 * k2 + 1))) & uint32_t(K - 1)));
@@ -778,7 +790,7 @@ bool launch_encode_reg(const rslm_plan *p, const rslm_plan *p2, const float *x, 
   const int s2 = p2 ? 1 : (sq8_lo ? 2 : 0);
   // the RSLM second stage here is the 2-D K = 16 codec only
   if (s2 == 1 && (p2->codec.g != 2 || p2->codec.K != 16 || p2->codec.n_sub * 2 != p->rot.D ||
-                  p2->codec.canon_bytes * 4 != p->rot.D || resid))
+                  p2->codec.canon_bytes * 4 != p->rot.D || resid || !p2->codec.g2tab))
     return false;
   if (s2 != 0 && p->codec.bits != 4) return false;
   const bool lite = p->codec.lead > 0;

@@ -79,7 +79,16 @@ struct CodecParams {
   // each bucket holds at most one threshold; qn = 0: no such grid
   float qs, qo, qs_lead, qo_lead;
   int qn, qn_lead;
+  // 2-D codebooks: a kGrid2 x kGrid2 grid of cells over [-emax, emax]^2
+  // (cell of u: floor(clamp(u_d g2s + g2o, 0, kGrid2 - 1)) per coordinate),
+  // each cell listing, in ascending order, at most four codes that can be
+  // nearest to some point of it (4 bits each, the last repeated); g2tab is
+  // device memory of the plan, null when some cell needs more than four
+  float g2s, g2o;
+  const uint16_t *g2tab;
 };
+
+constexpr int kGrid2 = 32;
 
 // Bucket of u on a uniform grid of qn buckets: floor(clamp(u qs + qo, 0,
 // qn - 1)), one fused multiply-add.  Non-decreasing in u, so with at most one
@@ -110,6 +119,7 @@ struct rslm_plan {
   int16_t *d_pi = nullptr;
   int16_t *d_tsrc = nullptr;
   uint32_t *d_dtab = nullptr;   // compact decode table (see scan.hip)
+  uint16_t *d_g2tab = nullptr;  // candidate lists of the 2-D nearest-centroid grid
   int dtab_entries = 0;
   int dtab_words = 0;           // 32-bit words per entry
 };
