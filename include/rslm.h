@@ -174,6 +174,29 @@ int rslm_encode_two_stage(const rslm_plan *plan, const rslm_plan *plan2, const f
                           void *stream);
 
 /* ------------------------------------------------------------------------
+ * rslm_grid2_lists -- host utility (no device work, no GPU needed): the
+ * candidate lists with which the encoder finds the nearest centroid of a
+ * 2-D codebook (the second stage of rslm_encode_two_stage) without scoring
+ * all K: a RSLM_GRID2 x RSLM_GRID2 grid of cells over [-emax, emax]^2, the
+ * cell of u being (gx, gy), g_d = floor(clamp(u_d s + o, 0, RSLM_GRID2 - 1)),
+ * whose list holds every code that can be nearest to some point of the cell
+ * (lowest code on ties), so that scanning it in order with a strict
+ * comparison of |C_k|^2 / 2 - <u, C_k> gives the nearest code.  Plans of
+ * 2-D codebooks build the same lists.
+ *   codebook     : K x 2 floats (host), 1 <= K <= 16, finite.
+ *   emax         : > 0, E_max of the plan's dimension (float).
+ *   out          : RSLM_GRID2 * RSLM_GRID2 uint16 (host); cell (gx, gy) at
+ *                  gx * RSLM_GRID2 + gy, four 4-bit codes from the lowest
+ *                  bits up, ascending, the last one repeated.
+ *   scale_offset : 2 floats (host) receiving s and o.
+ * RSLM_ERR_INVALID_ARG for a bad argument, RSLM_ERR_UNSUPPORTED if some cell
+ * needs more than four codes (the encoder then scores all K).
+ * ------------------------------------------------------------------------ */
+#define RSLM_GRID2 32
+int rslm_grid2_lists(const float *codebook, int32_t K, float emax, uint16_t *out,
+                     float *scale_offset);
+
+/* ------------------------------------------------------------------------
  * rslm_encode_sq8 -- rslm_encode with the rotated second residual
  * r2 = R x - g^ (R c + s^ C[code]) written directly as SQ8 codes with given
  * ranges (the RelApprox-SQ8 rescoring records; Sections "Background and

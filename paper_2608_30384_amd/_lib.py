@@ -28,6 +28,7 @@ EXPORTS = [
     "ivf_kmeans_update",
     "rslm_scan_topk_workspace", "rslm_scan_topk", "rslm_workspace_size",
     "rslm_sq8_fit", "rslm_sq8_encode", "rslm_rescore", "rslm_set_timer", "rslm_calibrate_read",
+    "rslm_grid2_lists",
 ]
 
 
@@ -100,6 +101,7 @@ def _declare(lib):
         "rslm_rescore": (C.c_int, [C.POINTER(RescoreCodec), P, I32, P, P, I32, I32, P, P, P]),
         "rslm_set_timer": (C.c_int, [C.c_int, P, P]),
         "rslm_calibrate_read": (C.c_int, [P, I64, P, I32, C.c_int, P]),
+        "rslm_grid2_lists": (C.c_int, [P, I32, C.c_float, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)

@@ -35,6 +35,13 @@ static void quant_grid(const float *thr, int n, float &qs, float &qo, int &qn) {
   }
 }
 
+// |C_k|^2 / 2 of a g-dimensional centroid, in float as the encoders use it.
+static float half_norm2(const float *c, int g) {
+  float h = 0.0f;
+  for (int t = 0; t < g; ++t) h += c[t] * c[t];
+  return 0.5f * h;
+}
+
 // Candidate lists of the 2-D nearest-centroid grid (CodecParams::g2tab).
 // Code k is left out of a cell only if one other code j is nearer by more
 // than kMargin everywhere in the cell widened by kWiden (the device rounds
@@ -47,30 +54,30 @@ static void quant_grid(const float *thr, int n, float &qs, float &qo, int &qn) {
 // scanning the list in ascending order with a strict comparison, picks the
 // same code (lowest on ties) as a search over all K.  False if a cell needs
 // more than four codes.
-static bool grid2_lists(const CodecParams &c, uint16_t *tab) {
+static bool grid2_lists(const float *cb, const float *cbh, int K, float g2s, float g2o,
+                        uint16_t *tab) {
   constexpr double kWiden = 1e-4, kMargin = 1e-4;
   const double inf = std::numeric_limits<double>::infinity();
   for (int i = 0; i < kGrid2; ++i)
     for (int j = 0; j < kGrid2; ++j) {
-      double lo[2] = {(i - double(c.g2o)) / c.g2s - kWiden, (j - double(c.g2o)) / c.g2s - kWiden};
-      double hi[2] = {(i + 1 - double(c.g2o)) / c.g2s + kWiden,
-                      (j + 1 - double(c.g2o)) / c.g2s + kWiden};
+      double lo[2] = {(i - double(g2o)) / g2s - kWiden, (j - double(g2o)) / g2s - kWiden};
+      double hi[2] = {(i + 1 - double(g2o)) / g2s + kWiden, (j + 1 - double(g2o)) / g2s + kWiden};
       if (i == 0) lo[0] = -inf;
       if (i == kGrid2 - 1) hi[0] = inf;
       if (j == 0) lo[1] = -inf;
       if (j == kGrid2 - 1) hi[1] = inf;
       int list[16], n = 0;
-      for (int k = 0; k < c.K; ++k) {
+      for (int k = 0; k < K; ++k) {
         bool beaten = false;
-        for (int o = 0; o < c.K && !beaten; ++o) {
+        for (int o = 0; o < K && !beaten; ++o) {
           if (o == k) continue;
           double m = 0.0;   // max over the box of <u, C_k - C_o>
           for (int d = 0; d < 2; ++d) {
-            const double a = double(c.cb[2 * k + d]) - double(c.cb[2 * o + d]);
+            const double a = double(cb[2 * k + d]) - double(cb[2 * o + d]);
             if (a > 0) m += a * hi[d];
             else if (a < 0) m += a * lo[d];
           }
-          beaten = (double(c.cbh[k]) - double(c.cbh[o])) - m > kMargin;
+          beaten = (double(cbh[k]) - double(cbh[o])) - m > kMargin;
         }
         if (!beaten) list[n++] = k;
       }
@@ -259,11 +266,7 @@ int rslm_plan_create(const rslm_plan_desc *d, rslm_plan **out) {
   p->emax = emax_of(D);
   c.emax = float(p->emax);
   for (int i = 0; i < 64; ++i) c.cb[i] = (i < K * g) ? d->codebook[i] : 0.0f;
-  for (int k = 0; k < 16; ++k) {   // half squared norms of the centroids
-    float h = 0.0f;
-    for (int t = 0; t < g && k < K; ++t) h += d->codebook[k * g + t] * d->codebook[k * g + t];
-    c.cbh[k] = (k < K) ? 0.5f * h : 3.0e38f;
-  }
+  for (int k = 0; k < 16; ++k) c.cbh[k] = (k < K) ? half_norm2(d->codebook + k * g, g) : 3.0e38f;
   for (int k = 0; k < 16; ++k)
     c.thr[k] = (g == 1 && k + 1 < K) ? 0.5f * (d->codebook[k] + d->codebook[k + 1]) : 0.0f;
   c.lead = d->lite ? (d->scale_mode ? 32 : 16) : 0;
@@ -279,7 +282,7 @@ int rslm_plan_create(const rslm_plan_desc *d, rslm_plan **out) {
   c.g2s = float(kGrid2) / (2.0f * c.emax);
   c.g2o = float(kGrid2 / 2);
   c.g2tab = nullptr;
-  const bool has_g2 = g == 2 && grid2_lists(c, g2);
+  const bool has_g2 = g == 2 && grid2_lists(c.cb, c.cbh, K, c.g2s, c.g2o, g2);
 
   // --- device tables: signs, intra-block permutation, compact decode table
   float s1f[256];
@@ -373,6 +376,27 @@ int rslm_plan_create(const rslm_plan_desc *d, rslm_plan **out) {
     r.s1mask[w] = m;
   }
   *out = p;
+  return RSLM_OK;
+}
+
+int rslm_grid2_lists(const float *codebook, int32_t K, float emax, uint16_t *out,
+                     float *scale_offset) {
+  if (!codebook || !out || !scale_offset || K < 1 || K > 16 || !(emax > 0.0f) ||
+      !std::isfinite(emax))
+    return RSLM_ERR_INVALID_ARG;
+  float cb[32], cbh[16];
+  for (int k = 0; k < K; ++k) {
+    cb[2 * k] = codebook[2 * k];
+    cb[2 * k + 1] = codebook[2 * k + 1];
+    if (!std::isfinite(cb[2 * k]) || !std::isfinite(cb[2 * k + 1])) return RSLM_ERR_INVALID_ARG;
+    cbh[k] = half_norm2(cb + 2 * k, 2);
+  }
+  const float s = float(kGrid2) / (2.0f * emax), o = float(kGrid2 / 2);
+  uint16_t tab[kGrid2 * kGrid2];
+  if (!grid2_lists(cb, cbh, K, s, o, tab)) return RSLM_ERR_UNSUPPORTED;
+  std::memcpy(out, tab, sizeof(tab));
+  scale_offset[0] = s;
+  scale_offset[1] = o;
   return RSLM_OK;
 }
 

@@ -88,7 +88,7 @@ struct CodecParams {
   const uint16_t *g2tab;
 };
 
-constexpr int kGrid2 = 32;
+constexpr int kGrid2 = RSLM_GRID2;
 
 // Bucket of u on a uniform grid of qn buckets: floor(clamp(u qs + qo, 0,
 // qn - 1)), one fused multiply-add.  Non-decreasing in u, so with at most one

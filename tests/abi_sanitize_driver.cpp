@@ -5,6 +5,7 @@
 // the status strings, version and workspace-size functions are exercised at
 // the edges of their ranges.  Exit status 0 when every call returned the
 // expected status; the sanitizers abort on any memory or UB error.
+#include <cmath>
 #include <cstdio>
 #include <cstdint>
 #include <cstring>
@@ -114,6 +115,29 @@ int main() {
          RSLM_ERR_INVALID_ARG);
   EXPECT(rslm_set_timer(5, nullptr, nullptr), RSLM_ERR_INVALID_ARG);
   EXPECT(rslm_calibrate_read(nullptr, 16, nullptr, 1, 0, nullptr), RSLM_ERR_INVALID_ARG);
+  // the 2-D nearest-centroid lists: host code, run in full here
+  {
+    float cb2d[32], so[2];
+    uint16_t lists[RSLM_GRID2 * RSLM_GRID2];
+    for (int k = 0; k < 9; ++k) {   // a centre code and a ring of 8 (K = 9)
+      const double a = 6.283185307179586 * k / 8.0, rad = k ? 1.5 : 0.0;
+      cb2d[2 * k] = float(rad * std::cos(a));
+      cb2d[2 * k + 1] = float(rad * std::sin(a));
+    }
+    EXPECT(rslm_grid2_lists(cb2d, 9, 3.36f, lists, so), RSLM_OK);
+    float ring[32];   // 16 codes on one ring: the outer corner cells, which
+    for (int k = 0; k < 16; ++k) {   // extend to infinity over a quarter of the
+      const double a = 6.283185307179586 * k / 16.0;   // directions, need more than four
+      ring[2 * k] = float(1.5 * std::cos(a));
+      ring[2 * k + 1] = float(1.5 * std::sin(a));
+    }
+    EXPECT(rslm_grid2_lists(ring, 16, 3.36f, lists, so), RSLM_ERR_UNSUPPORTED);
+    EXPECT(rslm_grid2_lists(cb2d, 0, 3.36f, lists, so), RSLM_ERR_INVALID_ARG);
+    EXPECT(rslm_grid2_lists(cb2d, 17, 3.36f, lists, so), RSLM_ERR_INVALID_ARG);
+    EXPECT(rslm_grid2_lists(cb2d, 9, -1.0f, lists, so), RSLM_ERR_INVALID_ARG);
+    EXPECT(rslm_grid2_lists(nullptr, 9, 3.36f, lists, so), RSLM_ERR_INVALID_ARG);
+    EXPECT(rslm_grid2_lists(cb2d, 9, 3.36f, nullptr, so), RSLM_ERR_INVALID_ARG);
+  }
 
   // workspace sizes at the edges of their ranges (host arithmetic only)
   (void)ivf_assign_probe_workspace(int64_t(1) << 31, 4096, 65536, 1024, IVF_PROBE_IP);
