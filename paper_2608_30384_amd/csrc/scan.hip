@@ -188,6 +188,7 @@ __device__ __forceinline__ int item_cands(int sz) {
   return ((sz + nch - 1) / nch + 15) & ~15;
 }
 constexpr int kSizeClasses = kChunkCands / 16;   // item size class = cands / 16 - 1
+static_assert(kSizeClasses == 128, "the class-start scan takes two classes per lane");
 constexpr int kPlanThreads = 1024;
 constexpr int kPlanQueries = kPlanThreads / 64;   // queries per preparing workgroup
 constexpr int kPlanRange = 16384;                 // lists counted per pass in LDS
@@ -286,14 +287,23 @@ __device__ void plan_lists(PlanSmem &sm, const int32_t *__restrict__ probe_ids, 
     carry += total;
     __syncthreads();
   }
-  if (t == 0) {
-    int run = 0;
-    for (int c = kSizeClasses - 1; c >= 0; --c) {
-      sm.start[c] = run;
-      run += sm.hist[c];
+  if (t < 64) {
+    // class starts in decreasing class order: lane t takes classes 127 - 2t
+    // and 126 - 2t, an inclusive scan of their sums over the wavefront
+    const int c0 = kSizeClasses - 1 - 2 * t;
+    const int h0 = sm.hist[c0], h1 = sm.hist[c0 - 1];
+    int incl = h0 + h1;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int v = __shfl_up(incl, off, 64);
+      if (t >= off) incl += v;
     }
-    pair_off[nlist] = carry;
-    item_off[nlist] = run;
+    sm.start[c0] = incl - h0 - h1;
+    sm.start[c0 - 1] = incl - h1;
+    if (t == 63) {
+      pair_off[nlist] = carry;
+      item_off[nlist] = incl;
+    }
   }
   if (t < kQueues) work[t * kQueueStride] = 0;
   __syncthreads();   // item_off[L] written above is read back by this workgroup
@@ -309,15 +319,15 @@ __device__ void plan_lists(PlanSmem &sm, const int32_t *__restrict__ probe_ids, 
     for (int u = 0; u < 16; ++u) {
       const int L = base + u * kPlanThreads + t;
       if (L >= nlist) break;
-      int cls = 0;
-      if (niv[u] > 0) (void)list_items(1, szv[u], max_list, cls);
+      // a list with items has 0 < size; its class depends on the size only
+      const int cls = item_cands(max(1, min(szv[u], max_list))) / 16 - 1;
       item_off[L] = niv[u] > 0 ? atomicAdd(&sm.start[cls], niv[u]) : 0;
     }
   }
 }
 
-// Blocks [0, n_qblocks): kPlanQueries queries each (prep + prefix); the last
-// block plans the lists.
+// Block 0 plans the lists (the longest chain, so it is dispatched first);
+// blocks [1, n_qblocks + 1) prepare kPlanQueries queries each (prep + prefix).
 __global__ void __launch_bounds__(kPlanThreads) k_plan_a(
     const float *__restrict__ q_rot, int Q, int D, int d_pad, _Float16 *__restrict__ qh,
     _Float16 *__restrict__ ql, float *__restrict__ qinv, const int32_t *__restrict__ probe_ids,
@@ -326,13 +336,12 @@ __global__ void __launch_bounds__(kPlanThreads) k_plan_a(
     int32_t *__restrict__ pair_off, int32_t *__restrict__ item_off, int32_t *__restrict__ cursor,
     int32_t *__restrict__ work) {
   __shared__ PlanSmem sm;
-  const int n_qblocks = (Q + kPlanQueries - 1) / kPlanQueries;
-  if (int(blockIdx.x) == n_qblocks) {
+  if (blockIdx.x == 0) {
     plan_lists(sm, probe_ids, Q * nprobe, sizes, nlist, max_list, counts, pair_off, item_off,
                cursor, work);
     return;
   }
-  const int q = blockIdx.x * kPlanQueries + (threadIdx.x >> 6);
+  const int q = (blockIdx.x - 1) * kPlanQueries + (threadIdx.x >> 6);
   if (q >= Q) return;
   prep_query(q_rot, q, D, d_pad, qh, ql, qinv);
   query_prefix(probe_ids, q, nprobe, nlist, sizes, max_list, prefix, totals);
