@@ -513,7 +513,8 @@ __global__ void __launch_bounds__(256) k_encode(
       const float rcv = rc[i] * rcw;
       const float o = z[px(i)] + rcv - gh * (rcv + sh * cv);
       if (resid) resid[row * D + i] = o;
-      if (sq8_lo) codes2[row * D + i] = uint8_t(sq8_code(o, sq8_lo[i], sq8_hi[i]));
+      if (sq8_lo)
+        codes2[row * D + i] = uint8_t(sq8_code_put(0u, o, sq8_lo[i], sq8_inv(sq8_lo[i], sq8_hi[i]), 0));
     }
   }
 }

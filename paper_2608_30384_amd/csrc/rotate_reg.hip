@@ -717,7 +717,7 @@ __global__ void __launch_bounds__(256) k_encode_rows(
         for (int t = 0; t < 4; ++t) {
           const int e = 8 * b + 4 * h + t;
           const float o = z[e] + va[t] - gh * (va[t] + sh * centroid(b, 4 * h + t));
-          wv |= sq8_code_inv(o, la[t], ia[t]) << (8 * t);
+          wv = sq8_code_put(wv, o, la[t], ia[t], t);
         }
         word2[h] = wv;
       }

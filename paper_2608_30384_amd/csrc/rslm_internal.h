@@ -210,6 +210,12 @@ __device__ __forceinline__ uint32_t sq8_code_inv(float v, float lo, float inv) {
 __device__ __forceinline__ uint32_t sq8_code(float v, float lo, float hi) {
   return sq8_code_inv(v, lo, sq8_inv(lo, hi));
 }
+// sq8_code_inv(v, lo, inv) written into byte t of w, the other bytes kept:
+// v_cvt_pk_u8_f32 rounds to nearest even and saturates to [0, 255] (NaN gives
+// 0), the rounding and clamp above in one instruction.
+__device__ __forceinline__ uint32_t sq8_code_put(uint32_t w, float v, float lo, float inv, int t) {
+  return __builtin_amdgcn_cvt_pk_u8_f32((v - lo) * inv, uint32_t(t), w);
+}
 
 // Float -> uint32 whose unsigned order equals the float order.
 __device__ __forceinline__ uint32_t order_key(float f) {
