@@ -779,56 +779,7 @@ __global__ void __launch_bounds__(kScanThreads, 2) k_scan(ScanArgs a) {
     const int64_t rec0 = int64_t((uint64_t(uint32_t(__builtin_amdgcn_readfirstlane(d1.z))) << 32) |
                                  uint32_t(__builtin_amdgcn_readfirstlane(d1.y)));
 
-    // A operands: row m = 2 * slot + part (part 0 = hi, 1 = lo)
-    half8 av[NC];
-    if constexpr (!MP) {
-      const int slot = m >> 1;
-      if (slot < G) {
-        const int pr = a.pairs[pbase + slot];
-        const int q = pr / a.nprobe;
-        const _Float16 *src = ((m & 1) ? a.ql : a.qh) + int64_t(q) * a.d_pad + 8 * kq;
-#pragma unroll
-        for (int c = 0; c < NC; ++c) av[c] = *reinterpret_cast<const half8 *>(src + 32 * c);
-      } else {
-#pragma unroll
-        for (int c = 0; c < NC; ++c) av[c] = half8{};
-      }
-    }
-    // multi-pass: the A operands of chunks [c0, c0 + NC), loaded per pass
-    auto load_a = [&](int c0) {
-      const int slot = m >> 1;
-      if (slot < G) {
-        const int pr = a.pairs[pbase + slot];
-        const int q = pr / a.nprobe;
-        const _Float16 *src = ((m & 1) ? a.ql : a.qh) + int64_t(q) * a.d_pad + 32 * c0 + 8 * kq;
-#pragma unroll
-        for (int c = 0; c < NC; ++c) av[c] = *reinterpret_cast<const half8 *>(src + 32 * c);
-      } else {
-#pragma unroll
-        for (int c = 0; c < NC; ++c) av[c] = half8{};
-      }
-    };
-    // epilogue parameters of the two query slots this lane outputs
-    float qc[2], qi[2];
-    int64_t obase[2];
-    bool ok[2];
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int slot = 2 * kq + i;
-      ok[i] = slot < G;
-      qc[i] = 0.f;
-      qi[i] = 0.f;
-      obase[i] = 0;
-      if (ok[i]) {
-        const int pr = a.pairs[pbase + slot];
-        const int q = pr / a.nprobe;
-        qc[i] = a.probe_dots[pr];
-        qi[i] = a.qinv[q];
-        obase[i] = int64_t(q) * a.stride + a.prefix[pr];
-      }
-    }
     const int n_tiles = (n_cand + 15) / 16;
-    float *out[2] = {a.scores + obase[0] + cand0, a.scores + obase[1] + cand0};
     // lists start on a tile boundary and cand0 is a multiple of 16
     const uint8_t *tiles = a.codes + (rec0 >> 4) * a.tile_bytes;
     const uint32_t tb = uint32_t(a.tile_bytes);
@@ -848,6 +799,55 @@ __global__ void __launch_bounds__(kScanThreads, 2) k_scan(ScanArgs a) {
     for (int r = 0; r < (kPreload ? kScaleRegs : 1); ++r)
       sreg[r] = (LITE || !kPreload) ? 0u : __builtin_amdgcn_raw_buffer_load_b32(
                                 rs, uint32_t((wave + nwaves * (kq + 4 * r)) * 16 + m) * 4u, 0, 0);
+    auto load_scale = [&](int t) {
+      return (LITE || kPreload) ? 0u
+                                : __builtin_amdgcn_raw_buffer_load_b32(rs, uint32_t(t * 16 + m) * 4u, 0, 0);
+    };
+    // single pass: the wave's first code tile is issued here, ahead of the
+    // dependent query loads below, so that it arrives while they do
+    uint32_t bufA[MP ? 1 : kWordsPerLane];
+    uint32_t scA = 0u;
+    const uint32_t voff = uint32_t(lane) * 16u;
+    if constexpr (!MP) {
+      load_tile(bufA, tiles, wave, n_tiles, tb, voff);
+      scA = load_scale(wave);
+    }
+
+    // The item's queries, in two dependent rounds of unconditional loads:
+    // the pairs of this lane's A row slot (m / 2) and of its two output slots
+    // (2 kq, 2 kq + 1), then the query rows and epilogue terms.  Slots at or
+    // past G read the item's last pair instead: their A rows only feed MFMA
+    // output rows that are never stored (ok[] below).
+    const int prA = a.pairs[pbase + min(m >> 1, G - 1)];
+    int prs[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) prs[i] = a.pairs[pbase + min(2 * kq + i, G - 1)];
+    const int qA = prA / a.nprobe;
+    // A operands: row m = 2 * slot + part (part 0 = hi, 1 = lo)
+    const _Float16 *asrc = ((m & 1) ? a.ql : a.qh) + int64_t(qA) * a.d_pad + 8 * kq;
+    half8 av[NC];
+    if constexpr (!MP) {
+#pragma unroll
+      for (int c = 0; c < NC; ++c) av[c] = *reinterpret_cast<const half8 *>(asrc + 32 * c);
+    }
+    // multi-pass: the A operands of chunks [c0, c0 + NC), loaded per pass
+    auto load_a = [&](int c0) {
+#pragma unroll
+      for (int c = 0; c < NC; ++c) av[c] = *reinterpret_cast<const half8 *>(asrc + 32 * (c0 + c));
+    };
+    // epilogue parameters of the two query slots this lane outputs
+    float qc[2], qi[2];
+    int64_t obase[2];
+    bool ok[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int q = prs[i] / a.nprobe;
+      ok[i] = 2 * kq + i < G;
+      qc[i] = a.probe_dots[prs[i]];
+      qi[i] = a.qinv[q];
+      obase[i] = int64_t(q) * a.stride + a.prefix[prs[i]];
+    }
+    float *out[2] = {a.scores + obase[0] + cand0, a.scores + obase[1] + cand0};
     const bool lead_lane = LITE && kq < a.lead / 8;
     auto scale_of = [&](int j) {   // j is uniform across the wave
       const int r = j >> 2;
@@ -856,20 +856,14 @@ __global__ void __launch_bounds__(kScanThreads, 2) k_scan(ScanArgs a) {
       for (int t = 1; t < (kPreload ? kScaleRegs : 1); ++t) v = r == t ? sreg[t] : v;
       return uint32_t(__shfl(int(v), 16 * (j & 3) + m, 64));
     };
-    auto load_scale = [&](int t) {
-      return (LITE || kPreload) ? 0u
-                                : __builtin_amdgcn_raw_buffer_load_b32(rs, uint32_t(t * 16 + m) * 4u, 0, 0);
-    };
     if constexpr (!MP) {
       // Software pipeline, depth 1: the codes of the wave's next tile are in
-      // flight while the current tile is decoded and multiplied.  Tiles past
-      // the item read as zeros from the buffer range check and are not scored.
-      uint32_t bufA[kWordsPerLane], bufB[kWordsPerLane];
-      uint32_t scA, scB = 0u;
+      // flight while the current tile is decoded and multiplied (the first
+      // tile, bufA, was issued above).  Tiles past the item read as zeros
+      // from the buffer range check and are not scored.
+      uint32_t bufB[kWordsPerLane];
+      uint32_t scB = 0u;
       int lt = wave, j = 0;
-      const uint32_t voff = uint32_t(lane) * 16u;
-      load_tile(bufA, tiles, lt, n_tiles, tb, voff);
-      scA = load_scale(lt);
       while (lt < n_tiles) {
         load_tile(bufB, tiles, lt + nwaves, n_tiles, tb, voff);
         scB = load_scale(lt + nwaves);
