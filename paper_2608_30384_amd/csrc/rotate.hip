@@ -33,15 +33,15 @@ __device__ __forceinline__ void wave_sync() {
 // W: lanes per vector (the encoder gives small vectors fewer lanes); lane is
 // the lane's index among them.
 template <int R, int W = kWave>
-__device__ __forceinline__ void fwht_round(float *v, int off, int nblk, int B, int s,
+__device__ __forceinline__ void fwht_round(float *v, int off, int nblk, int B, int logB, int s,
                                            bool last, float scale, int lane) {
   constexpr int G = 1 << R;
   const int h = 1 << s;
-  const int gpb = B >> R;  // groups per block (power of two)
-  const int total = nblk * gpb;
+  const int lg = logB - R;   // groups per block: 2^lg
+  const int total = nblk << lg;
   for (int gi = lane; gi < total; gi += W) {
-    const int blk = gi / gpb;
-    const int t = gi - blk * gpb;
+    const int blk = gi >> lg;
+    const int t = gi & ((1 << lg) - 1);
     const int low = t & (h - 1);
     const int high = t >> s;
     const int base = off + blk * B + ((high << (s + R)) | low);
@@ -78,9 +78,9 @@ __device__ __forceinline__ void fwht_blocks(float *v, int off, int nblk, const R
   for (int s = 0; s < logB; s += 3) {
     const int R = (logB - s) < 3 ? (logB - s) : 3;
     const bool last = (s + R) == logB;
-    if (R == 3) fwht_round<3, W>(v, off, nblk, B, s, last, rp.inv_sqrt_b, lane);
-    else if (R == 2) fwht_round<2, W>(v, off, nblk, B, s, last, rp.inv_sqrt_b, lane);
-    else fwht_round<1, W>(v, off, nblk, B, s, last, rp.inv_sqrt_b, lane);
+    if (R == 3) fwht_round<3, W>(v, off, nblk, B, logB, s, last, rp.inv_sqrt_b, lane);
+    else if (R == 2) fwht_round<2, W>(v, off, nblk, B, logB, s, last, rp.inv_sqrt_b, lane);
+    else fwht_round<1, W>(v, off, nblk, B, logB, s, last, rp.inv_sqrt_b, lane);
     wave_sync();
   }
 }
@@ -130,34 +130,24 @@ __device__ __forceinline__ float sub_max(float v) {
   return v;
 }
 
-// Source of output o of the strided transpose; pi is the workgroup's LDS
-// copy of the intra-block permutation.
-__device__ __forceinline__ int transpose_src(int o, const RotParams &rp, const int16_t *pi) {
-  const int MB = rp.n_full * rp.B;
-  if (o >= MB) return o;
-  const int M = rp.n_full;
-  const int k = o / M;
-  const int b = o - k * M;
-  return b * rp.B + int(pi[k]);
-}
-
-// Workgroup prologue: LDS copy of the permutation (all threads must call).
-__device__ __forceinline__ void load_perm(const RotParams &rp, int16_t *pi) {
-  for (int k = threadIdx.x; k < rp.B; k += blockDim.x) pi[k] = rp.pi[k];
-  __syncthreads();
+// Source of output o of the strided transpose, (o mod M) B + P(o / M) below
+// M B (M = n_full), o above: the plan's table of it (a division per element
+// otherwise).
+__device__ __forceinline__ int transpose_src(int o, const RotParams &rp) {
+  return int(rp.tsrc[o]);
 }
 
 // Forward rotation of the vector held in v (already multiplied by S1 when
 // passes > 0; element i at v[px(i)]).  Returns the buffer holding the result.
 template <int W = kWave>
-__device__ float *rotate_forward(float *v, float *w, const RotParams &rp, const int16_t *pi,
+__device__ float *rotate_forward(float *v, float *w, const RotParams &rp,
                                  uint32_t s2bits, int lane) {
   if (rp.passes == 0) return v;
   fwht_pass<W>(v, rp, lane, false);
   if (rp.passes == 1) return v;
 #pragma unroll 4
   for (int o = lane, t = 0; o < rp.D; o += W, ++t)
-    w[px(o)] = flip_w<W>(v[px(transpose_src(o, rp, pi))], s2bits, t);
+    w[px(o)] = flip_w<W>(v[px(transpose_src(o, rp))], s2bits, t);
   wave_sync();
   fwht_pass<W>(w, rp, lane, false);
   return w;
@@ -165,7 +155,7 @@ __device__ float *rotate_forward(float *v, float *w, const RotParams &rp, const 
 
 // Inverse rotation R^T of the vector in v; the result excludes the final S1
 // multiplication, which the caller applies on output.
-__device__ float *rotate_inverse(float *v, float *w, const RotParams &rp, const int16_t *pi,
+__device__ float *rotate_inverse(float *v, float *w, const RotParams &rp,
                                  uint32_t s2bits, int lane) {
   if (rp.passes == 0) return v;
   if (rp.passes == 1) {
@@ -175,7 +165,7 @@ __device__ float *rotate_inverse(float *v, float *w, const RotParams &rp, const 
   fwht_pass(v, rp, lane, true);
 #pragma unroll 4
   for (int o = lane, t = 0; o < rp.D; o += kWave, ++t)
-    w[px(transpose_src(o, rp, pi))] = flip(v[px(o)], s2bits, t);
+    w[px(transpose_src(o, rp))] = flip(v[px(o)], s2bits, t);
   wave_sync();
   fwht_pass(w, rp, lane, true);
   return w;
@@ -185,8 +175,6 @@ __device__ float *rotate_inverse(float *v, float *w, const RotParams &rp, const 
 __global__ void __launch_bounds__(256) k_rotate(const float *__restrict__ x, float *y, int64_t n,
                                                 RotParams rp, int inverse, int dstride) {
   extern __shared__ float lds[];
-  __shared__ int16_t pi[128];
-  load_perm(rp, pi);
   const int lane = threadIdx.x & 63;
   const int wid = threadIdx.x >> 6;
   const int64_t row = int64_t(blockIdx.x) * (blockDim.x >> 6) + wid;
@@ -201,8 +189,8 @@ __global__ void __launch_bounds__(256) k_rotate(const float *__restrict__ x, flo
 #pragma unroll 4
   for (int i = lane, t = 0; i < D; i += kWave, ++t) v[px(i)] = flip(xr[i], s1in, t);
   wave_sync();
-  const float *res = inverse ? rotate_inverse(v, w, rp, pi, sm.y, lane)
-                             : rotate_forward(v, w, rp, pi, sm.y, lane);
+  const float *res = inverse ? rotate_inverse(v, w, rp, sm.y, lane)
+                             : rotate_forward(v, w, rp, sm.y, lane);
   float *yr = y + row * D;
 #pragma unroll 4
   for (int i = lane, t = 0; i < D; i += kWave, ++t) yr[i] = flip(res[px(i)], s1out, t);
@@ -249,7 +237,6 @@ __global__ void __launch_bounds__(256) k_encode(
     CodecParams cp2, const float *__restrict__ sq8_lo, const float *__restrict__ sq8_hi) {
   extern __shared__ float lds[];
   __shared__ float cbs[64], cbs2[64], cbl[8];
-  __shared__ int16_t pi[128];
   // 1-D quantiser grid (cp.qn > 0): thresholds below each bucket, and the
   // sorted thresholds padded with +inf
   __shared__ uint8_t qtab[512];
@@ -275,7 +262,7 @@ __global__ void __launch_bounds__(256) k_encode(
       qtab[j] = uint8_t(cnt);
     }
   }
-  load_perm(rp, pi);   // (its barrier also publishes the tables above)
+  __syncthreads();   // publishes the tables above
   const int64_t rec = int64_t(blockIdx.x) * nv + vid;
   int64_t row = -1;
   int L = -1;
@@ -316,7 +303,7 @@ __global__ void __launch_bounds__(256) k_encode(
     }
   }
   wave_sync();
-  const float *z = rotate_forward<W>(v, w, rp, pi, sm.y, sl);
+  const float *z = rotate_forward<W>(v, w, rp, sm.y, sl);
 
   float m = 0.f;
 #pragma unroll 4
@@ -532,10 +519,9 @@ __global__ void __launch_bounds__(256) k_decode(const uint8_t *__restrict__ code
                                                 CodecParams cp, int dstride) {
   extern __shared__ float lds[];
   __shared__ float cbs[64], cbl[8];
-  __shared__ int16_t pi[128];
   if (threadIdx.x < 64) cbs[threadIdx.x] = cp.cb[threadIdx.x];
   if (threadIdx.x < 8) cbl[threadIdx.x] = cp.cb_lead[threadIdx.x];
-  load_perm(rp, pi);   // includes the barrier that publishes cbs / cbl
+  __syncthreads();   // publishes cbs / cbl
   const int lane = threadIdx.x & 63;
   const int wid = threadIdx.x >> 6;
   const int64_t rec = int64_t(blockIdx.x) * (blockDim.x >> 6) + wid;
@@ -565,7 +551,7 @@ __global__ void __launch_bounds__(256) k_decode(const uint8_t *__restrict__ code
   wave_sync();
   const uint2 sm = lane_sign_masks(rp, lane);
   const uint32_t s1out = (rp.passes > 0) ? sm.x : 0u;
-  const float *res = rotate_inverse(v, w, rp, pi, sm.y, lane);
+  const float *res = rotate_inverse(v, w, rp, sm.y, lane);
   const float *cr = (L >= 0) ? cen + int64_t(L) * D : nullptr;
   float *orow = out + rec * D;
 #pragma unroll 4
