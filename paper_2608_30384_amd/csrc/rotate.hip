@@ -383,9 +383,10 @@ __global__ void __launch_bounds__(256) k_encode(
   if (sl == 0) scales[rec] = su | (gu << 16);
   __builtin_amdgcn_wave_barrier();  // codes in cl are written by other lanes
   // first-stage centroid value of valid coordinate i (0 for a zero residual)
+  const int lg = g >> 1;   // log2 g: sub-vectors of 1, 2 or 4 coordinates
   auto cval = [&](int i) {
     if (!(m > 0.f)) return 0.f;
-    return (i < cp.lead) ? cbl[cl[i]] : cbs[cl[i / g] * g + (i % g)];
+    return (i < cp.lead) ? cbl[cl[i]] : cbs[cl[i >> lg] * g + (i & (g - 1))];
   };
 
   if (codes2 && !sq8_lo) {
@@ -538,14 +539,15 @@ __global__ void __launch_bounds__(256) k_decode(const uint8_t *__restrict__ code
     if (L < 0 || L >= nlist) L = -1;
   }
   const int per = 8 / g;   // sub-vectors per group of 8 coordinates
+  const int lg = g >> 1;   // log2 g: sub-vectors of 1, 2 or 4 coordinates
 #pragma unroll 4
   for (int i = lane; i < D; i += kWave) {
-    const int j = i / g;             // sub-vector
-    const int G = j / per;           // group of 8 coordinates
+    const int j = i >> lg;           // sub-vector
+    const int G = i >> 3;            // group of 8 coordinates
     uint32_t bits = 0;
     for (int b = 0; b < cp.bits; ++b) bits |= uint32_t(codes[tile_byte_addr(rec, G, b, cp)]) << (8 * b);
     const uint32_t code = (bits >> (cp.w * (j - G * per))) & ((1u << cp.w) - 1u);
-    const float c = (j < cp.lead) ? cbl[code & 7u] : cbs[code * g + (i % g)];
+    const float c = (j < cp.lead) ? cbl[code & 7u] : cbs[code * g + (i & (g - 1))];
     v[px(i)] = sh * c;
   }
   wave_sync();
