@@ -224,12 +224,6 @@ __device__ void plan_lists(PlanSmem &sm, const int32_t *__restrict__ probe_ids, 
   const int t = threadIdx.x;
   if (t < kSizeClasses) sm.hist[t] = 0;
   int carry = 0;   // uniform: pairs of the lists before this pass
-  // one pass (nlist <= kPlanRange): each thread keeps its lists' item counts
-  // and classes in registers for the placement below, instead of a round
-  // trip through item_off
-  const bool one_pass = nlist <= kPlanRange;
-  int a = 0, b = 0;
-  int niv_k[kPlanRange / kPlanThreads], cls_k[kPlanRange / kPlanThreads];
   for (int L0 = 0; L0 < nlist; L0 += kPlanRange) {
     const int nr = min(kPlanRange, nlist - L0);
     for (int i = t; i < nr; i += kPlanThreads) sm.cnt[i] = 0;
@@ -250,25 +244,20 @@ __device__ void plan_lists(PlanSmem &sm, const int32_t *__restrict__ probe_ids, 
     // thread t owns the consecutive lists [a, b) of the pass (at most
     // kPlanRange / kPlanThreads = 16); their sizes are loaded first
     const int per = (nr + kPlanThreads - 1) / kPlanThreads;
-    a = min(nr, t * per);
-    b = min(nr, a + per);
+    const int a = min(nr, t * per), b = min(nr, a + per);
     int szv[kPlanRange / kPlanThreads];
 #pragma unroll
     for (int u = 0; u < kPlanRange / kPlanThreads; ++u) szv[u] = a + u < b ? sizes[L0 + a + u] : 0;
     int sum = 0;
 #pragma unroll
     for (int u = 0; u < kPlanRange / kPlanThreads; ++u) {
-      niv_k[u] = 0;
-      cls_k[u] = 0;
-      if (a + u >= b) continue;
+      if (a + u >= b) break;
       const int cp = sm.cnt[a + u];
       sum += cp;
       int cls = 0;
       const int ni = list_items(cp, szv[u], max_list, cls);
       if (ni > 0) atomicAdd(&sm.hist[cls], ni);
-      niv_k[u] = ni;
-      cls_k[u] = cls;
-      if (!one_pass) item_off[L0 + a + u] = ni;
+      item_off[L0 + a + u] = ni;
     }
     // exclusive prefix of the threads' sums: an inclusive scan within each
     // wavefront by shuffles, then the totals of the wavefronts before it
@@ -317,13 +306,7 @@ __device__ void plan_lists(PlanSmem &sm, const int32_t *__restrict__ probe_ids, 
     }
   }
   if (t < kQueues) work[t * kQueueStride] = 0;
-  __syncthreads();   // the class starts (and item_off[L], when written) are read below
-  if (one_pass) {
-#pragma unroll
-    for (int u = 0; u < kPlanRange / kPlanThreads; ++u)
-      if (a + u < b) item_off[a + u] = niv_k[u] > 0 ? atomicAdd(&sm.start[cls_k[u]], niv_k[u]) : 0;
-    return;
-  }
+  __syncthreads();   // item_off[L] written above is read back by this workgroup
   for (int base = 0; base < nlist; base += 16 * kPlanThreads) {   // loads first
     int niv[16], szv[16];
 #pragma unroll
