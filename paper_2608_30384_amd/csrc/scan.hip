@@ -57,7 +57,7 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kChunkCands = 2048;   // candidates per work item
 constexpr int kGroupQ = 8;          // queries per work item (16 MFMA rows / 2)
 constexpr int kScanThreads = 256;
-constexpr int kScaleRegs = kChunkCands / 256;
+constexpr int kScaleRegs = kChunkCands / 256;   // scale words per lane: 4 tiles of a wave each
 // Work queues: one per XCD (accelerator complex die, each with its own L2).
 // Queue x holds the blocks of kQueueBlock consecutive items (in the global
 // order) whose block number is x modulo kQueues; its counter sits in its
@@ -65,7 +65,7 @@ constexpr int kScaleRegs = kChunkCands / 256;
 constexpr int kQueues = 8;
 constexpr int kQueueShift = 4;
 constexpr int kQueueBlock = 1 << kQueueShift;
-constexpr int kQueueStride = 16;   // int32 words between two queue counters   // scale words per lane: 4 tiles of a wave each
+constexpr int kQueueStride = 16;   // int32 words between two queue counters
 static_assert(kChunkCands / 16 <= 4 * 4 * kScaleRegs, "scale registers of a wave's tiles");
 
 static size_t align256(size_t b) { return (b + 255) / 256 * 256; }
