@@ -225,6 +225,47 @@ __device__ __forceinline__ void store_group(uint8_t *codes, int64_t rec, int G, 
   }
 }
 
+// Register rotation for D = 96 on 8 lanes per vector (the plan's blocks of 64:
+// [0, 64) and the overlapping [32, 96)).  Lane l holds elements l + 8 t,
+// t < 12, in e[t]; in a block starting at element 8 t0, bits 0-2 of the
+// in-block index are the lane and bits 3-5 are t - t0.  The butterfly stages
+// run in the order of the LDS rounds (bits 0, 1, 2, then 3, 4, 5; the scale
+// last), so the results are those of the general path bit for bit.
+template <int CTRL>
+__device__ __forceinline__ float dpp8(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xf, 0xf, true));
+}
+// value of lane l ^ m of the 8-lane group (quad_perm for m = 1, 2; for m = 4
+// a half-row mirror, l ^ 7, then a quad reversal, ^ 3)
+template <int M>
+__device__ __forceinline__ float lane_xor8(float v) {
+  if constexpr (M == 1) return dpp8<0xB1>(v);
+  else if constexpr (M == 2) return dpp8<0x4E>(v);
+  else return dpp8<0x1B>(dpp8<0x141>(v));
+}
+template <int M>
+__device__ __forceinline__ void lane_stage8(float (&e)[12], int t0, int sl) {
+  const float sg = (sl & M) ? -1.f : 1.f;   // upper lane: partner - own
+#pragma unroll
+  for (int k = 0; k < 8; ++k) e[t0 + k] = fmaf(e[t0 + k], sg, lane_xor8<M>(e[t0 + k]));
+}
+__device__ __forceinline__ void fwht64_r8(float (&e)[12], int t0, int sl, float scale) {
+  lane_stage8<1>(e, t0, sl);
+  lane_stage8<2>(e, t0, sl);
+  lane_stage8<4>(e, t0, sl);
+#pragma unroll
+  for (int h = 1; h < 8; h <<= 1)
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+      if (!(k & h)) {
+        const float a = e[t0 + k], b = e[t0 + k + h];
+        e[t0 + k] = a + b;
+        e[t0 + k + h] = a - b;
+      }
+#pragma unroll
+  for (int k = 0; k < 8; ++k) e[t0 + k] *= scale;
+}
+
 // VPW vectors per wavefront, W = 64 / VPW lanes each (small D: a wavefront
 // per vector would leave most lanes idle in every butterfly round).
 template <int VPW>
@@ -286,11 +327,44 @@ __global__ void __launch_bounds__(256) k_encode(
   float xx = 0.f, rr = 0.f, cc = 0.f;
   const uint2 sm = sub_sign_masks<W>(rp, sl);
   const uint32_t s1in = (rp.passes > 0) ? sm.x : 0u;
-  {
-    const float *xr = x + row * D;
-    // branch-free loads: without a centre read x's row and weight it by 0
-    const float *cr = (L >= 0) ? cen + int64_t(L) * D : xr;
-    const float cw = (L >= 0) ? 1.f : 0.f;
+  const float *xr = x + row * D;
+  // branch-free loads: without a centre read x's row and weight it by 0
+  const float *cr = (L >= 0) ? cen + int64_t(L) * D : xr;
+  const float cw = (L >= 0) ? 1.f : 0.f;
+  const float *z = v;
+  bool rotated = false;
+  if constexpr (W == 8) {
+    if (D == 96 && rp.B == 64 && rp.passes == 2) {
+      // residual and both passes in registers; the transpose through v
+      float e[12];
+#pragma unroll
+      for (int t = 0; t < 12; ++t) {
+        const int i = sl + 8 * t;
+        const float xv = xr[i];
+        const float cv = cr[i] * cw;
+        const float r = xv - cv;
+        xx += xv * xv;
+        rr += r * r;
+        cc += cv * cv;
+        e[t] = flip_w<W>(r, s1in, t);
+      }
+      fwht64_r8(e, 0, sl, rp.inv_sqrt_b);
+      fwht64_r8(e, 4, sl, rp.inv_sqrt_b);
+#pragma unroll
+      for (int t = 0; t < 12; ++t) v[px(sl + 8 * t)] = e[t];
+      wave_sync();
+#pragma unroll
+      for (int t = 0; t < 12; ++t) e[t] = flip_w<W>(v[px(transpose_src(sl + 8 * t, rp))], sm.y, t);
+      fwht64_r8(e, 0, sl, rp.inv_sqrt_b);
+      fwht64_r8(e, 4, sl, rp.inv_sqrt_b);
+#pragma unroll
+      for (int t = 0; t < 12; ++t) w[px(sl + 8 * t)] = e[t];
+      wave_sync();
+      z = w;
+      rotated = true;
+    }
+  }
+  if (!rotated) {
   #pragma unroll 4
     for (int i = sl, t = 0; i < D; i += W, ++t) {
       const float xv = xr[i];
@@ -301,9 +375,9 @@ __global__ void __launch_bounds__(256) k_encode(
       cc += cv * cv;
       v[px(i)] = flip_w<W>(r, s1in, t);
     }
+    wave_sync();
+    z = rotate_forward<W>(v, w, rp, sm.y, sl);
   }
-  wave_sync();
-  const float *z = rotate_forward<W>(v, w, rp, sm.y, sl);
 
   float m = 0.f;
 #pragma unroll 4
