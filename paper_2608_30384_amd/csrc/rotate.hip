@@ -700,6 +700,38 @@ __global__ void k_pack_records(const uint8_t *__restrict__ tiles, const uint32_t
 
 static int lds_floats(int D) { return (padded_len((D + 31) / 32 * 32) + 3) / 4 * 4; }
 
+// Forward rotation at D = 96 with both passes in registers (fwht64_r8):
+// 8 lanes per row, 32 rows per workgroup, the transpose through one LDS
+// buffer per row.  The same results as k_rotate bit for bit.
+constexpr int kRot96Rows = 32;
+__global__ void __launch_bounds__(256) k_rotate96(const float *__restrict__ x, float *y, int64_t n,
+                                                  RotParams rp, int dstride) {
+  extern __shared__ float lds[];
+  const int sl = threadIdx.x & 7;
+  const int slot = threadIdx.x >> 3;
+  const int64_t row = int64_t(blockIdx.x) * kRot96Rows + slot;
+  if (row >= n) return;   // a row's 8 lanes leave together; no barriers below
+  float *v = lds + slot * dstride;
+  const uint2 sm = sub_sign_masks<8>(rp, sl);
+  const float *xr = x + row * 96;
+  float e[12];
+#pragma unroll
+  for (int t = 0; t < 12; ++t) e[t] = flip_w<8>(xr[sl + 8 * t], sm.x, t);
+  fwht64_r8(e, 0, sl, rp.inv_sqrt_b);
+  fwht64_r8(e, 4, sl, rp.inv_sqrt_b);
+#pragma unroll
+  for (int t = 0; t < 12; ++t) v[px(sl + 8 * t)] = e[t];
+  wave_sync();
+#pragma unroll
+  for (int t = 0; t < 12; ++t) e[t] = flip_w<8>(v[px(transpose_src(sl + 8 * t, rp))], sm.y, t);
+  fwht64_r8(e, 0, sl, rp.inv_sqrt_b);
+  fwht64_r8(e, 4, sl, rp.inv_sqrt_b);
+  float *yr = y + row * 96;
+#pragma unroll
+  for (int t = 0; t < 12; ++t) yr[sl + 8 * t] = e[t];
+}
+
+
 }  // namespace rslm
 
 using namespace rslm;
@@ -714,6 +746,13 @@ int rslm_fwht(const rslm_plan *p, const float *x, float *y, int64_t n, int inver
   if (launch_rotate_reg(p, x, y, n, inverse, as_stream(stream))) return check_launch();
   const int D = p->rot.D;
   const int dstride = lds_floats(D);
+  if (!inverse && D == 96 && p->rot.B == 64 && p->rot.passes == 2) {
+    const int64_t g96 = (n + kRot96Rows - 1) / kRot96Rows;
+    hipLaunchKernelGGL(k_rotate96, dim3(unsigned(g96)), dim3(8 * kRot96Rows),
+                       size_t(kRot96Rows) * dstride * sizeof(float), as_stream(stream), x, y, n,
+                       p->rot, dstride);
+    return check_launch();
+  }
   int waves = 4;
   while (waves > 1 && size_t(waves) * 2 * dstride * 4 > 65536) waves >>= 1;
   const size_t shm = size_t(waves) * 2 * dstride * sizeof(float);
