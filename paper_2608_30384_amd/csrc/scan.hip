@@ -716,7 +716,11 @@ __global__ void __launch_bounds__(kScanThreads, 2) k_scan(ScanArgs a) {
   const uint32_t lane4 = uint32_t(lane) * 4u;
 
   // replicate the table: entry e of copy l at word (e * kCopies + l) *
-  // kWords; a byte entry is the compact entries of its low and high nibbles
+  // kWords; a byte entry is the compact entries of its low and high nibbles.
+  // Unrolled so that a batch of the (cached) table loads is in flight at
+  // once: one load and its wait per iteration made the fill a chain of 64
+  // dependent loads per thread at every launch.
+#pragma unroll 16
   for (int idx = tid; idx < T::kEntries * T::kCopies; idx += kScanThreads) {
     const int e = idx / T::kCopies;
     if constexpr (T::kByte) {
