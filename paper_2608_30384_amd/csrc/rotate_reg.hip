@@ -313,8 +313,14 @@ __global__ void __launch_bounds__(256) k_encode_rows(
   if (TWO && threadIdx.x < 16)
     cb2[threadIdx.x] = make_float4(cp2.cb[2 * threadIdx.x], cp2.cb[2 * threadIdx.x + 1],
                                    cp2.cbh[threadIdx.x], 0.f);
-  if (TWO)
-    for (int j = threadIdx.x; j < kGrid2 * kGrid2; j += blockDim.x) g2t[j] = cp2.g2tab[j];
+  if (TWO) {   // all loads first, then the stores (kGrid2^2 is a multiple of 256)
+    static_assert(kGrid2 * kGrid2 % 256 == 0, "grid table copy");
+    uint16_t gv[TWO ? kGrid2 * kGrid2 / 256 : 1];
+#pragma unroll
+    for (int u = 0; u < (TWO ? kGrid2 * kGrid2 / 256 : 1); ++u) gv[u] = cp2.g2tab[threadIdx.x + 256 * u];
+#pragma unroll
+    for (int u = 0; u < (TWO ? kGrid2 * kGrid2 / 256 : 1); ++u) g2t[threadIdx.x + 256 * u] = gv[u];
+  }
   if (LITE && threadIdx.x < 16) {
     cb8[threadIdx.x] = (threadIdx.x < 8) ? cp.cb_lead[threadIdx.x] : 0.f;
     thr8[threadIdx.x] = cp.thr_lead[threadIdx.x];
@@ -344,8 +350,15 @@ __global__ void __launch_bounds__(256) k_encode_rows(
       for (int t = 0; t < kTmWords; ++t) tmask[threadIdx.x][t] = tm[t];
     }
   }
-  if (rp.passes == 2)
-    for (int k = threadIdx.x; k < D; k += blockDim.x) ts[k] = uint16_t(4 * rp.tsrc[k]);
+  if (rp.passes == 2) {   // all loads first (clamped index), then the stores
+    constexpr int kU = (D + 255) / 256;
+    int16_t tv[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) tv[u] = rp.tsrc[min(int(threadIdx.x) + 256 * u, D - 1)];
+#pragma unroll
+    for (int u = 0; u < kU; ++u)
+      if (int(threadIdx.x) + 256 * u < D) ts[threadIdx.x + 256 * u] = uint16_t(4 * tv[u]);
+  }
 
   for (int j = threadIdx.x; j < cp.qn; j += blockDim.x) {
     int cnt = 0;
