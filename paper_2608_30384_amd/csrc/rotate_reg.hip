@@ -101,10 +101,19 @@ __device__ __forceinline__ void rotate_inv_reg(float (&x)[J], const RotParams &r
 
 // Workgroup prologue: LDS copy of the transpose source table (D entries), as
 // byte offsets into the padded per-wave buffer.
+// D = 64 J entries, 256 threads: all loads first (clamped index), then the
+// stores.
+template <int J>
 __device__ __forceinline__ void load_tsrc_r(const RotParams &rp, uint16_t *ts) {
-  if (rp.passes == 2)
-    for (int k = threadIdx.x; k < rp.D; k += blockDim.x)
-      ts[k] = uint16_t(4 * px_r(rp.tsrc[k]));
+  constexpr int D = 64 * J, kU = (D + 255) / 256;
+  if (rp.passes == 2) {
+    int16_t tv[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) tv[u] = rp.tsrc[min(int(threadIdx.x) + 256 * u, D - 1)];
+#pragma unroll
+    for (int u = 0; u < kU; ++u)
+      if (int(threadIdx.x) + 256 * u < D) ts[threadIdx.x + 256 * u] = uint16_t(4 * px_r(tv[u]));
+  }
   __syncthreads();
 }
 
@@ -114,7 +123,7 @@ __global__ void __launch_bounds__(256) k_rotate_reg(const float *__restrict__ x,
                                                     int dstride) {
   extern __shared__ float lds[];
   __shared__ uint16_t ts[64 * J];
-  load_tsrc_r(rp, ts);
+  load_tsrc_r<J>(rp, ts);
   const int lane = threadIdx.x & 63;
   const int wid = threadIdx.x >> 6;
   const int64_t row = int64_t(blockIdx.x) * (blockDim.x >> 6) + wid;
