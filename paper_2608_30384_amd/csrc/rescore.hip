@@ -153,7 +153,11 @@ __global__ void __launch_bounds__(kSq8Threads) k_rescore_sq8(
   for (int j0 = wave * 4; j0 < k_in; j0 += ngroups) {
     const int j = j0 + grp;
     int32_t id = -1;
-    if (j < k_in) id = cand_i[int64_t(q) * k_in + j];
+    float s1 = 0.f;   // loaded with the id, not after the products
+    if (j < k_in) {
+      id = cand_i[int64_t(q) * k_in + j];
+      s1 = cand_s[int64_t(q) * k_in + j];
+    }
     const bool valid = id >= 0 && id < n_vec;
     float dot = 0.f;
     if (valid) {
@@ -184,7 +188,7 @@ __global__ void __launch_bounds__(kSq8Threads) k_rescore_sq8(
 #pragma unroll
     for (int off = 8; off >= 1; off >>= 1) dot += __shfl_xor(dot, off, 64);
     if (valid && gl == 0) {
-      const float s2 = cand_s[int64_t(q) * k_in + j] + (qlo + dot);
+      const float s2 = s1 + (qlo + dot);
       const uint32_t pos = atomicAdd(&count, 1u);
       buf[pos] = score_key(s2, id);
     }
